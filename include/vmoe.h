@@ -1,0 +1,197 @@
+/*
+ * vmoe.h -- C ABI of libvmoe: one sparse Vision-MoE layer, forward and
+ * backward, on an AMD Instinct MI355X (gfx950).
+ *
+ * The operation. The paper co-adapts V-MoE vision backbones whose blocks
+ * route every token to a few experts out of a shared pool (Sec. 1, Sec. 2.1:
+ * sparse expert routing over expertised MLP blocks; Sec. 2.2: experts of
+ * several models pooled as one parallel expert set, each model keeping its
+ * own router), under per-expert capacity limits (Sec. 2.3), and adapts the
+ * experts by back-propagation (Sec. 3.1-3.2: V-MoE retraining). The paper
+ * does not write the layer out; this library implements V-MoE's definition
+ * as read for this project:
+ *
+ *   logits = x W_r[g]^T (+ bias) (+ noise)       noisy gate, one router per group g
+ *   p      = softmax(logits)                     exact-order fp32, see vmoe_route
+ *   e_1..k = top-k experts of each token         ties to the lower expert index
+ *   priority = p[e_1]; each group's tokens are walked by priority (desc),
+ *   first choices of all tokens before second choices, and an assignment is
+ *   kept while its expert has fewer than C tokens of that group
+ *   (batch-prioritized routing); kept gates are p[e_j], not renormalised
+ *   xe     = kept tokens packed into per-expert buffers
+ *   ye     = W2_e gelu(W1_e xe + b1_e) + b2_e   per expert (exact-erf GELU)
+ *   y[t]   = sum_j gate[t,j] ye[row(t,j)]        dropped tokens give 0
+ * and the gradients of y w.r.t. x, the router and every expert parameter.
+ *
+ * Conventions shared by every entry point
+ * - All tensor pointers are DEVICE pointers owned by the caller, row-major and
+ *   contiguous, 16-byte aligned. The library allocates nothing, keeps no
+ *   state, never synchronises and never reads device data on the host.
+ * - `stream` is a hipStream_t passed as void* (NULL = the null stream). Work
+ *   is enqueued asynchronously on it, in call order.
+ * - Activations and weights use shape.dtype (VMOE_F32 or VMOE_BF16; bf16 is
+ *   stored as raw 16-bit patterns). Gating tensors (logits, probs, gate,
+ *   dgate, noise, bias) and all weight / router / input gradients are f32.
+ * - Sizes: N tokens in G equal routing groups (N_g = N / G), model width d,
+ *   expert hidden width f, E experts, top-k, capacity C per (group, expert)
+ *   from vmoe_capacity. Expert buffers are [E, G*C, width]; expert e's kept
+ *   rows are packed at the front, group by group: rows [0, n_e) with
+ *   n_e = sum_g counts[g, e]. Rows at or beyond n_e are never read.
+ *   row(t, j) = e*G*C + row_base[g, e] + slot[t, j]  for e = expert_idx[t, j].
+ * - Every call overwrites its outputs, except vmoe_route_bwd's dx (+=).
+ * - Errors are status codes, checked before anything is enqueued: a NULL
+ *   required pointer, N % G != 0, k outside [1, E], E > 64, d or f not a
+ *   multiple of 8, a non-positive capacity factor, an unknown dtype or
+ *   misaligned pointer -> VMOE_ERR_INVALID_ARG; a too-small workspace ->
+ *   VMOE_ERR_WORKSPACE; a failed kernel launch -> VMOE_ERR_HIP. Nothing
+ *   throws across the ABI. All entry points are thread-safe (stateless).
+ */
+#ifndef VMOE_H
+#define VMOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define VMOE_ABI_VERSION 1
+
+typedef enum {
+    VMOE_OK = 0,
+    VMOE_ERR_INVALID_ARG = 1,
+    VMOE_ERR_UNSUPPORTED = 2,
+    VMOE_ERR_WORKSPACE = 3,
+    VMOE_ERR_HIP = 4
+} vmoe_status;
+
+typedef enum { VMOE_F32 = 0, VMOE_BF16 = 1 } vmoe_dtype;
+
+/* vmoe_route flags */
+#define VMOE_ROUTE_LOGITS_IN 1 /* skip the router product; `logits` is an input */
+
+typedef struct vmoe_shape {
+    int32_t n_tokens;          /* N >= 0                                        */
+    int32_t n_groups;          /* G >= 1, divides N                             */
+    int32_t d_model;           /* d, multiple of 8                              */
+    int32_t d_ff;              /* f, multiple of 8                              */
+    int32_t n_experts;         /* E in [1, 64]                                  */
+    int32_t k;                 /* top-k in [1, E]                               */
+    double capacity_factor;    /* c > 0                                         */
+    int32_t capacity_rounding; /* 0: round half away from zero, 1: ceil         */
+    int32_t capacity_override; /* > 0: use this C instead of the formula        */
+    int32_t dtype;             /* vmoe_dtype                                    */
+    int32_t reserved;          /* must be 0                                     */
+} vmoe_shape;
+
+/* ABI version of the loaded library (VMOE_ABI_VERSION). */
+int32_t vmoe_abi_version(void);
+
+/* Static description of a status code. */
+const char* vmoe_status_string(int32_t status);
+
+/* Capacity per (group, expert): C = round(k * N_g * c / E), at least 1, the
+ * buffer size of V-MoE's capacity limit (capacity limits, paper Sec. 2.3).
+ * Returns -1 if the shape is invalid. */
+int32_t vmoe_capacity(const vmoe_shape* shape);
+
+/* Bytes of scratch that vmoe_route needs (0 on an invalid shape). */
+size_t vmoe_route_workspace_bytes(const vmoe_shape* shape);
+
+/* Bytes of scratch that vmoe_route_bwd needs (0 on an invalid shape). */
+size_t vmoe_route_bwd_workspace_bytes(const vmoe_shape* shape);
+
+/* Noisy top-k gating with capacity and batch-prioritized routing
+ * (sparse expert routing, paper Sec. 1 and Sec. 2.1; capacity, Sec. 2.3).
+ *   x          [N, d] dtype         tokens (unused with LOGITS_IN)
+ *   w_router   [G, E, d] dtype      router of each group (unused with LOGITS_IN)
+ *   logit_bias [E] f32 or NULL      constant logit offset
+ *   noise      [N, E] f32 or NULL   gating noise drawn by the caller
+ *   logits     [N, E] f32           out: sum_i x[t,i] w_router[g,e,i], summed in
+ *                                   double in increasing i and rounded once to f32
+ *                                   (in with LOGITS_IN)
+ *   probs      [N, E] f32           out: softmax of z = (logits + bias) + noise,
+ *                                   exp by Cody-Waite reduction and a degree-7
+ *                                   polynomial, sum in expert order, IEEE divide
+ *   expert_idx [N, k] i32           out: top-k experts by z, ties to lower index
+ *   slot       [N, k] i32           out: slot in the expert's group buffer, -1 = dropped
+ *   gate       [N, k] f32           out: probs[t, expert_idx[t,j]] if kept, else 0
+ *   order      [N] i32              out: each group's tokens by priority p[e_1]
+ *                                   descending, token index ascending
+ *   counts     [G, E] i32           out: kept assignments per (group, expert) (<= C)
+ *   row_base   [G, E] i32           out: sum_{g' < g} counts[g', e]
+ *   workspace  device scratch of vmoe_route_workspace_bytes(shape) bytes
+ * Given the same fp32 logits, every integer output and probs/gate are
+ * bit-for-bit deterministic. */
+vmoe_status vmoe_route(const vmoe_shape* shape, const void* x, const void* w_router,
+                       const float* logit_bias, const float* noise, int32_t flags, float* logits,
+                       float* probs, int32_t* expert_idx, int32_t* slot, float* gate,
+                       int32_t* order, int32_t* counts, int32_t* row_base, void* workspace,
+                       size_t workspace_bytes, void* stream);
+
+/* Dispatch (permutation) of kept tokens into per-expert buffers:
+ * xe[row(t, j), :] = x[t, :] for every kept (t, j). x [N, d], xe [E, G*C, d]. */
+vmoe_status vmoe_dispatch(const vmoe_shape* shape, const void* x, const int32_t* expert_idx,
+                          const int32_t* slot, const int32_t* row_base, void* xe, void* stream);
+
+/* Expert MLP forward over each expert's n_e packed rows (expertised MLP
+ * blocks, paper Sec. 2.1): H = xe W1_e^T + b1_e, A = gelu(H), ye = A W2_e^T + b2_e.
+ *   xe [E, G*C, d], counts [G, E] (device; n_e = sum_g counts[g, e])
+ *   w1 [E, f, d], b1 [E, f], w2 [E, d, f], b2 [E, d]     (dtype)
+ *   h, a [E, G*C, f] out (saved for the backward), ye [E, G*C, d] out.
+ * bf16 runs on bf16 matrix cores with f32 accumulation; f32 accumulates in f32. */
+vmoe_status vmoe_expert_ffn_fwd(const vmoe_shape* shape, const void* xe, const int32_t* counts,
+                                const void* w1, const void* b1, const void* w2, const void* b2,
+                                void* h, void* a, void* ye, void* stream);
+
+/* Gate-weighted combine: y[t] = sum over kept j (in j order, f32 accumulation)
+ * of gate[t,j] * ye[row(t,j)]; 0 for a token with no kept assignment. y [N, d]. */
+vmoe_status vmoe_combine_fwd(const vmoe_shape* shape, const void* ye, const int32_t* expert_idx,
+                             const int32_t* slot, const int32_t* row_base, const float* gate,
+                             void* y, void* stream);
+
+/* Backward of the combine: dye[row(t,j)] = gate[t,j] * dy[t];
+ * dgate[t,j] = <dy[t], ye[row(t,j)]> (f32) for kept j, 0 for dropped j.
+ * dy [N, d], dye [E, G*C, d], dgate [N, k] f32. */
+vmoe_status vmoe_combine_bwd(const vmoe_shape* shape, const void* dy, const void* ye,
+                             const int32_t* expert_idx, const int32_t* slot,
+                             const int32_t* row_base, const float* gate, void* dye, float* dgate,
+                             void* stream);
+
+/* Backward of the expert MLP (adaptation by back-propagation, paper Sec. 3):
+ *   dH  = (dye W2_e) * gelu'(h)          dh  [E, G*C, f] out (dtype)
+ *   dxe = dH W1_e                        dxe [E, G*C, d] out (dtype)
+ *   dW2 = dye^T a,  db2 = sum_rows dye   dw2 [E, d, f], db2 [E, d]  f32 out
+ *   dW1 = dH^T xe,  db1 = sum_rows dH    dw1 [E, f, d], db1 [E, f]  f32 out
+ * h and a are the forward's saved tensors. Experts with n_e = 0 get zero
+ * weight gradients. */
+vmoe_status vmoe_expert_ffn_bwd(const vmoe_shape* shape, const void* xe, const int32_t* counts,
+                                const void* w1, const void* w2, const void* h, const void* a,
+                                const void* dye, void* dh, void* dxe, float* dw1, float* db1,
+                                float* dw2, float* db2, void* stream);
+
+/* Backward of the dispatch: dx[t] = sum over kept j of dxe[row(t,j)]
+ * (f32, overwritten; 0 for a token with no kept assignment). dx [N, d] f32. */
+vmoe_status vmoe_dispatch_bwd(const vmoe_shape* shape, const void* dxe,
+                              const int32_t* expert_idx, const int32_t* slot,
+                              const int32_t* row_base, float* dx, void* stream);
+
+/* Backward through the gate into the router (the top-k choice, capacity and
+ * priority order are piecewise constant and pass no gradient):
+ *   dp[t,e]  = sum of dgate[t,j] over kept j with expert_idx[t,j] = e
+ *   dz[t,e]  = probs[t,e] * (dp[t,e] - sum_e' probs[t,e'] dp[t,e'])
+ *   dx[t,:] += sum_e dz[t,e] w_router[g,e,:]                    (accumulates)
+ *   dw_router[g,e,:] = sum_{t in g} dz[t,e] x[t,:]  f32 [G,E,d], overwritten;
+ *                      NULL skips it (frozen routers)
+ * workspace: vmoe_route_bwd_workspace_bytes(shape) bytes. */
+vmoe_status vmoe_route_bwd(const vmoe_shape* shape, const void* x, const void* w_router,
+                           const float* probs, const int32_t* expert_idx, const int32_t* slot,
+                           const float* dgate, float* dx, float* dw_router, void* workspace,
+                           size_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* VMOE_H */

@@ -1,0 +1,457 @@
+// Expert MLP forward and backward as grouped GEMMs on gfx950.
+//
+// bf16 path: one templated matrix-core kernel, C[M x N] = sum_k A(m,k) B(n,k),
+// per expert (grid.z). Tiles of 128 x 128 x 64 per 256-thread block, four
+// waves in 2 x 2, each wave 64 x 64 as 4 x 4 blocks of
+// v_mfma_f32_16x16x32_bf16 with f32 accumulation. Both operands are staged
+// in LDS k-contiguous (double buffered, one barrier per k-step); an operand
+// whose k index is strided in HBM (weights read transposed in the backward,
+// the row-reduced weight-gradient GEMMs) is loaded as 4 k-rows x 8 values
+// per thread and transposed in registers on its way into LDS. The operand
+// roles are swapped inside the MFMA so each lane ends up holding 4
+// consecutive output columns of one row, which the fused epilogues (bias,
+// GELU, GELU', bf16 rounding, f32 weight gradients) store directly.
+//
+// Each expert's row count n_e = sum_g counts[g, e] is read on the device:
+// tiles past n_e exit at once (M = n_e GEMMs) or n_e bounds the k loop
+// (weight-gradient GEMMs, which still write zeros for an empty expert).
+//
+// f32 path: a plain LDS-tiled FMA kernel with the same operand and epilogue
+// description (small widths; accuracy path).
+#include "common.h"
+
+namespace vmoe {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+enum Epi { EPI_FWD1 = 0, EPI_BIAS = 1, EPI_GELU_GRAD = 2, EPI_STORE = 3, EPI_F32 = 4 };
+
+// Operand: element (mn, k) of expert e is
+//   k-major : base[e*estride + mn*ld + k]
+//   mn-major: base[e*estride + k*ld + mn]
+struct Operand {
+    const void* base;
+    long long estride;
+    int ld;
+};
+
+struct GemmArgs {
+    Operand a, b;
+    int M, N, K;            // static sizes; M or K is replaced by n_e (see var_k)
+    int var_k;              // 0: M = n_e, 1: K = n_e
+    const int32_t* counts;  // [G, E]
+    int G, E;
+    void* out;              // primary output
+    void* out2;             // EPI_FWD1: activation
+    long long out_estride;
+    int ldo;
+    const void* bias;       // EPI_FWD1 / EPI_BIAS
+    long long bias_estride;
+    const void* aux;        // EPI_GELU_GRAD: saved pre-activation H
+};
+
+__device__ __forceinline__ int expert_rows(const int32_t* counts, int G, int E, int e) {
+    int n = 0;
+    for (int g = 0; g < G; ++g) n += counts[g * E + e];
+    return n;
+}
+
+__device__ __forceinline__ float gelu_f(float h) {
+    return 0.5f * h * (1.0f + erff(h * 0.70710678118654752f));
+}
+
+__device__ __forceinline__ float gelu_grad_f(float h) {
+    return 0.5f * (1.0f + erff(h * 0.70710678118654752f)) +
+           h * 0.39894228040143268f * __expf(-0.5f * h * h);
+}
+
+// ------------------------------------------------------------------ bf16 MFMA
+
+constexpr int BM = 128, BN = 128, BK = 64;
+constexpr int LDK = BK + 8;  // padded LDS row (bf16 elements): 144 B
+
+// Global -> registers for one 128 x 64 operand tile. A masked-off vector is
+// still loaded, from the (always valid) operand base, and then replaced by
+// zeros in registers: no data-dependent address ever points off the operand.
+__device__ __forceinline__ uint4 masked_load(const uint16_t* __restrict__ base, size_t off,
+                                             bool ok) {
+    const uint4 v = *reinterpret_cast<const uint4*>(base + (ok ? off : 0));
+    return ok ? v : make_uint4(0, 0, 0, 0);
+}
+
+template <bool KMAJOR>
+__device__ __forceinline__ void load_tile(const uint16_t* __restrict__ base, int ld, int mn0,
+                                          int mn_lim, int k0, int k_lim, uint4 (&r)[4]) {
+    const int tid = threadIdx.x;
+    if (KMAJOR) {
+        const int kv = (tid & 7) * 8;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int mn = (tid >> 3) + 32 * j;
+            const bool ok = (mn0 + mn < mn_lim) && (k0 + kv < k_lim);
+            r[j] = masked_load(base, static_cast<size_t>(mn0 + mn) * ld + k0 + kv, ok);
+        }
+    } else {
+        const int mv = (tid & 15) * 8;
+        const int kq = (tid >> 4) * 4;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const bool ok = (mn0 + mv < mn_lim) && (k0 + kq + q < k_lim);
+            r[q] = masked_load(base, static_cast<size_t>(k0 + kq + q) * ld + mn0 + mv, ok);
+        }
+    }
+}
+
+__device__ __forceinline__ uint32_t half_of(const uint4& v, int c) {
+    const uint32_t w = (c >> 1) == 0 ? v.x : (c >> 1) == 1 ? v.y : (c >> 1) == 2 ? v.z : v.w;
+    return (c & 1) ? (w >> 16) : (w & 0xFFFFu);
+}
+
+// Registers -> LDS tile [128 mn][LDK] (k contiguous).
+template <bool KMAJOR>
+__device__ __forceinline__ void store_tile(uint16_t (*s)[LDK], const uint4 (&r)[4]) {
+    const int tid = threadIdx.x;
+    if (KMAJOR) {
+        const int kv = (tid & 7) * 8;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) *reinterpret_cast<uint4*>(&s[(tid >> 3) + 32 * j][kv]) = r[j];
+    } else {
+        const int mv = (tid & 15) * 8;
+        const int kq = (tid >> 4) * 4;
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+            uint2 v;
+            v.x = half_of(r[0], c) | (half_of(r[1], c) << 16);
+            v.y = half_of(r[2], c) | (half_of(r[3], c) << 16);
+            *reinterpret_cast<uint2*>(&s[mv + c][kq]) = v;
+        }
+    }
+}
+
+template <bool A_KMAJOR, bool B_KMAJOR, int EPI>
+__global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs p) {
+    __shared__ __attribute__((aligned(16))) uint16_t As[2][BM][LDK];
+    __shared__ __attribute__((aligned(16))) uint16_t Bs[2][BN][LDK];
+
+    const int e = blockIdx.z;
+    const int ne = expert_rows(p.counts, p.G, p.E, e);
+    const int M = p.var_k ? p.M : ne;
+    const int K = p.var_k ? ne : p.K;
+    const int N = p.N;
+    const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+    if (m0 >= M) return;
+
+    const uint16_t* A = static_cast<const uint16_t*>(p.a.base) + e * p.a.estride;
+    const uint16_t* B = static_cast<const uint16_t*>(p.b.base) + e * p.b.estride;
+
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+
+    f32x4 acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    const int nk = (K + BK - 1) / BK;
+    uint4 ra[4], rb[4];
+    load_tile<A_KMAJOR>(A, p.a.ld, m0, M, 0, K, ra);
+    load_tile<B_KMAJOR>(B, p.b.ld, n0, N, 0, K, rb);
+    store_tile<A_KMAJOR>(As[0], ra);
+    store_tile<B_KMAJOR>(Bs[0], rb);
+    __syncthreads();
+
+    for (int kt = 0; kt < nk; ++kt) {
+        const int cur = kt & 1;
+        const bool more = kt + 1 < nk;
+        if (more) {
+            load_tile<A_KMAJOR>(A, p.a.ld, m0, M, (kt + 1) * BK, K, ra);
+            load_tile<B_KMAJOR>(B, p.b.ld, n0, N, (kt + 1) * BK, K, rb);
+        }
+#pragma unroll
+        for (int ks = 0; ks < BK / 32; ++ks) {
+            const int kc = ks * 32 + (lane >> 4) * 8;
+            bf16x8 af[4], bfr[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                af[i] = *reinterpret_cast<const bf16x8*>(&As[cur][wm * 64 + i * 16 + (lane & 15)][kc]);
+                bfr[i] = *reinterpret_cast<const bf16x8*>(&Bs[cur][wn * 64 + i * 16 + (lane & 15)][kc]);
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bfr[j], af[i], acc[i][j], 0,
+                                                                        0, 0);
+        }
+        if (more) {
+            store_tile<A_KMAJOR>(As[cur ^ 1], ra);
+            store_tile<B_KMAJOR>(Bs[cur ^ 1], rb);
+        }
+        __syncthreads();
+    }
+
+    // Epilogue: lane holds C[m][n .. n+3].
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int m = m0 + wm * 64 + i * 16 + (lane & 15);
+        if (m >= M) continue;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int n = n0 + wn * 64 + j * 16 + (lane >> 4) * 4;
+            if (n >= N) continue;
+            const f32x4 v = acc[i][j];
+            const size_t o = e * p.out_estride + static_cast<size_t>(m) * p.ldo + n;
+            if (EPI == EPI_F32) {
+                *reinterpret_cast<float4*>(static_cast<float*>(p.out) + o) =
+                    make_float4(v[0], v[1], v[2], v[3]);
+            } else {
+                float r[4] = {v[0], v[1], v[2], v[3]};
+                if (EPI == EPI_FWD1 || EPI == EPI_BIAS) {
+                    const uint2 bb = *reinterpret_cast<const uint2*>(
+                        static_cast<const uint16_t*>(p.bias) + e * p.bias_estride + n);
+                    r[0] += bf16_to_f32(bb.x & 0xFFFFu);
+                    r[1] += bf16_to_f32(bb.x >> 16);
+                    r[2] += bf16_to_f32(bb.y & 0xFFFFu);
+                    r[3] += bf16_to_f32(bb.y >> 16);
+                }
+                if (EPI == EPI_GELU_GRAD) {
+                    const uint2 hh =
+                        *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(p.aux) + o);
+                    r[0] *= gelu_grad_f(bf16_to_f32(hh.x & 0xFFFFu));
+                    r[1] *= gelu_grad_f(bf16_to_f32(hh.x >> 16));
+                    r[2] *= gelu_grad_f(bf16_to_f32(hh.y & 0xFFFFu));
+                    r[3] *= gelu_grad_f(bf16_to_f32(hh.y >> 16));
+                }
+                uint2 w;
+                w.x = pack_bf16x2(r[0], r[1]);
+                w.y = pack_bf16x2(r[2], r[3]);
+                *reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.out) + o) = w;
+                if (EPI == EPI_FWD1) {
+                    uint2 a;
+                    a.x = pack_bf16x2(gelu_f(r[0]), gelu_f(r[1]));
+                    a.y = pack_bf16x2(gelu_f(r[2]), gelu_f(r[3]));
+                    *reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.out2) + o) = a;
+                }
+            }
+        }
+    }
+}
+
+// ------------------------------------------------------------------ f32 FMA path
+
+constexpr int FT = 64, FK = 16;
+
+template <bool KMAJOR>
+__device__ __forceinline__ float f32_elem(const float* base, int ld, int mn, int k) {
+    return KMAJOR ? base[static_cast<size_t>(mn) * ld + k] : base[static_cast<size_t>(k) * ld + mn];
+}
+
+template <bool A_KMAJOR, bool B_KMAJOR, int EPI>
+__global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs p) {
+    __shared__ float As[FK][FT + 1];
+    __shared__ float Bs[FK][FT + 1];
+    const int e = blockIdx.z;
+    const int ne = expert_rows(p.counts, p.G, p.E, e);
+    const int M = p.var_k ? p.M : ne;
+    const int K = p.var_k ? ne : p.K;
+    const int N = p.N;
+    const int m0 = blockIdx.y * FT, n0 = blockIdx.x * FT;
+    if (m0 >= M) return;
+    const float* A = static_cast<const float*>(p.a.base) + e * p.a.estride;
+    const float* B = static_cast<const float*>(p.b.base) + e * p.b.estride;
+    const int tm = (threadIdx.x >> 4) * 4, tn = (threadIdx.x & 15) * 4;
+    float acc[4][4] = {};
+    for (int k0 = 0; k0 < K; k0 += FK) {
+        for (int q = threadIdx.x; q < FK * FT; q += 256) {
+            const int kk = q / FT, mn = q % FT;
+            As[kk][mn] = (m0 + mn < M && k0 + kk < K)
+                             ? f32_elem<A_KMAJOR>(A, p.a.ld, m0 + mn, k0 + kk) : 0.0f;
+            Bs[kk][mn] = (n0 + mn < N && k0 + kk < K)
+                             ? f32_elem<B_KMAJOR>(B, p.b.ld, n0 + mn, k0 + kk) : 0.0f;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int kk = 0; kk < FK; ++kk)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    acc[i][j] = __builtin_fmaf(As[kk][tm + i], Bs[kk][tn + j], acc[i][j]);
+        __syncthreads();
+    }
+    for (int i = 0; i < 4; ++i) {
+        const int m = m0 + tm + i;
+        if (m >= M) continue;
+        for (int j = 0; j < 4; ++j) {
+            const int n = n0 + tn + j;
+            if (n >= N) continue;
+            const size_t o = e * p.out_estride + static_cast<size_t>(m) * p.ldo + n;
+            float v = acc[i][j];
+            float* out = static_cast<float*>(p.out);
+            if (EPI == EPI_FWD1 || EPI == EPI_BIAS)
+                v += static_cast<const float*>(p.bias)[e * p.bias_estride + n];
+            if (EPI == EPI_GELU_GRAD) v *= gelu_grad_f(static_cast<const float*>(p.aux)[o]);
+            out[o] = v;
+            if (EPI == EPI_FWD1) static_cast<float*>(p.out2)[o] = gelu_f(v);
+        }
+    }
+}
+
+// ------------------------------------------------------------------ bias gradients
+
+// out[e, c] = sum over the n_e rows of src[e, r, c]; 64 columns x 4 row phases
+// per block, phases added in a fixed order.
+template <typename T>
+__global__ __launch_bounds__(256) void colsum_kernel(const T* __restrict__ src,
+                                                     long long estride, int cols,
+                                                     const int32_t* __restrict__ counts, int G,
+                                                     int E, float* __restrict__ out) {
+    __shared__ float part[4][64];
+    const int e = blockIdx.y;
+    const int c = blockIdx.x * 64 + (threadIdx.x & 63);
+    const int ph = threadIdx.x >> 6;
+    const int ne = expert_rows(counts, G, E, e);
+    float s = 0.0f;
+    if (c < cols) {
+        const T* p = src + e * estride + c;
+        for (int r = ph; r < ne; r += 4) s += Elem<T>::load(p, static_cast<size_t>(r) * cols);
+    }
+    part[ph][threadIdx.x & 63] = s;
+    __syncthreads();
+    if (ph == 0 && c < cols)
+        out[static_cast<size_t>(e) * cols + c] = ((part[0][c & 63] + part[1][c & 63]) +
+                                                  part[2][c & 63]) + part[3][c & 63];
+}
+
+template <bool AK, bool BK_, int EPI>
+void launch_gemm(const Dims& D, const GemmArgs& a, int grid_m_rows, hipStream_t st) {
+    if (D.dtype == VMOE_BF16) {
+        dim3 grid(cdiv(a.N, BN), cdiv(grid_m_rows, BM), D.E);
+        gemm_bf16_kernel<AK, BK_, EPI><<<grid, 256, 0, st>>>(a);
+    } else {
+        dim3 grid(cdiv(a.N, FT), cdiv(grid_m_rows, FT), D.E);
+        gemm_f32_kernel<AK, BK_, EPI><<<grid, 256, 0, st>>>(a);
+    }
+}
+
+GemmArgs base_args(const Dims& D, const int32_t* counts) {
+    GemmArgs a{};
+    a.counts = counts;
+    a.G = D.G;
+    a.E = D.E;
+    return a;
+}
+
+size_t esize(const Dims& D) { return D.dtype == VMOE_BF16 ? 2 : 4; }
+
+}  // namespace
+
+vmoe_status ffn_fwd_launch(const Dims& D, const void* xe, const int32_t* counts, const void* w1,
+                           const void* b1, const void* w2, const void* b2, void* h, void* act,
+                           void* ye, hipStream_t st) {
+    const long long rows = D.rows_per_expert();
+    if (rows == 0 || D.E == 0) return VMOE_OK;
+    // H = xe W1^T + b1, A = gelu(H)
+    GemmArgs g1 = base_args(D, counts);
+    g1.a = Operand{xe, rows * D.d, D.d};
+    g1.b = Operand{w1, static_cast<long long>(D.f) * D.d, D.d};
+    g1.M = static_cast<int>(rows);
+    g1.N = D.f;
+    g1.K = D.d;
+    g1.out = h;
+    g1.out2 = act;
+    g1.out_estride = rows * D.f;
+    g1.ldo = D.f;
+    g1.bias = b1;
+    g1.bias_estride = D.f;
+    launch_gemm<true, true, EPI_FWD1>(D, g1, static_cast<int>(rows), st);
+    // ye = A W2^T + b2
+    GemmArgs g2 = base_args(D, counts);
+    g2.a = Operand{act, rows * D.f, D.f};
+    g2.b = Operand{w2, static_cast<long long>(D.d) * D.f, D.f};
+    g2.M = static_cast<int>(rows);
+    g2.N = D.d;
+    g2.K = D.f;
+    g2.out = ye;
+    g2.out_estride = rows * D.d;
+    g2.ldo = D.d;
+    g2.bias = b2;
+    g2.bias_estride = D.d;
+    launch_gemm<true, true, EPI_BIAS>(D, g2, static_cast<int>(rows), st);
+    return launch_status();
+}
+
+vmoe_status ffn_bwd_launch(const Dims& D, const void* xe, const int32_t* counts, const void* w1,
+                           const void* w2, const void* h, const void* act, const void* dye,
+                           void* dh, void* dxe, float* dw1, float* db1, float* dw2, float* db2,
+                           hipStream_t st) {
+    const long long rows = D.rows_per_expert();
+    if (D.E == 0) return VMOE_OK;
+    if (rows > 0) {
+        // dH = (dye W2) * gelu'(H): W2 [d, f] read with k = d strided (mn-major)
+        GemmArgs g = base_args(D, counts);
+        g.a = Operand{dye, rows * D.d, D.d};
+        g.b = Operand{w2, static_cast<long long>(D.d) * D.f, D.f};
+        g.M = static_cast<int>(rows);
+        g.N = D.f;
+        g.K = D.d;
+        g.out = dh;
+        g.out_estride = rows * D.f;
+        g.ldo = D.f;
+        g.aux = h;
+        launch_gemm<true, false, EPI_GELU_GRAD>(D, g, static_cast<int>(rows), st);
+        // dxe = dH W1: W1 [f, d] read with k = f strided
+        GemmArgs x = base_args(D, counts);
+        x.a = Operand{dh, rows * D.f, D.f};
+        x.b = Operand{w1, static_cast<long long>(D.f) * D.d, D.d};
+        x.M = static_cast<int>(rows);
+        x.N = D.d;
+        x.K = D.f;
+        x.out = dxe;
+        x.out_estride = rows * D.d;
+        x.ldo = D.d;
+        launch_gemm<true, false, EPI_STORE>(D, x, static_cast<int>(rows), st);
+    }
+    // dW2 [d, f] = dye^T A, reduced over the n_e rows (k = row, strided)
+    GemmArgs w = base_args(D, counts);
+    w.var_k = 1;
+    w.a = Operand{dye, rows * D.d, D.d};
+    w.b = Operand{act, rows * D.f, D.f};
+    w.M = D.d;
+    w.N = D.f;
+    w.K = 0;
+    w.out = dw2;
+    w.out_estride = static_cast<long long>(D.d) * D.f;
+    w.ldo = D.f;
+    launch_gemm<false, false, EPI_F32>(D, w, D.d, st);
+    // dW1 [f, d] = dH^T xe
+    GemmArgs v = base_args(D, counts);
+    v.var_k = 1;
+    v.a = Operand{dh, rows * D.f, D.f};
+    v.b = Operand{xe, rows * D.d, D.d};
+    v.M = D.f;
+    v.N = D.d;
+    v.K = 0;
+    v.out = dw1;
+    v.out_estride = static_cast<long long>(D.f) * D.d;
+    v.ldo = D.d;
+    launch_gemm<false, false, EPI_F32>(D, v, D.f, st);
+    // bias gradients
+    if (D.dtype == VMOE_BF16) {
+        colsum_kernel<uint16_t><<<dim3(cdiv(D.d, 64), D.E), 256, 0, st>>>(
+            static_cast<const uint16_t*>(dye), rows * D.d, D.d, counts, D.G, D.E, db2);
+        colsum_kernel<uint16_t><<<dim3(cdiv(D.f, 64), D.E), 256, 0, st>>>(
+            static_cast<const uint16_t*>(dh), rows * D.f, D.f, counts, D.G, D.E, db1);
+    } else {
+        colsum_kernel<float><<<dim3(cdiv(D.d, 64), D.E), 256, 0, st>>>(
+            static_cast<const float*>(dye), rows * D.d, D.d, counts, D.G, D.E, db2);
+        colsum_kernel<float><<<dim3(cdiv(D.f, 64), D.E), 256, 0, st>>>(
+            static_cast<const float*>(dh), rows * D.f, D.f, counts, D.G, D.E, db1);
+    }
+    return launch_status();
+}
+
+}  // namespace vmoe

@@ -133,7 +133,8 @@ def truncated_normal(rng: np.random.Generator, shape, std: float) -> np.ndarray:
     return z * np.float32(std)
 
 
-def make_inputs(cfg: LayerConfig, salt: int = 0, with_grad: bool = True) -> dict:
+def make_inputs(cfg: LayerConfig, salt: int = 0, with_grad: bool = True,
+                with_experts: bool = True) -> dict:
     """Draw every input of one fwd+bwd pass for `cfg`.
 
     Tensor ids (seed offsets): 1 x, 2 router, 3 noise, 4 w1, 5 b1, 6 w2, 7 b2,
@@ -167,6 +168,10 @@ def make_inputs(cfg: LayerConfig, salt: int = 0, with_grad: bool = True) -> dict
         noise = np.random.default_rng(_seed(cfg, 3, salt)).standard_normal((N, E), dtype=np.float32)
         noise *= np.float32(math.sqrt(cfg.noise_var))
 
+    out = dict(x=to_dtype(x, cfg.dtype), w_router=to_dtype(wr, cfg.dtype), logit_bias=bias,
+               noise=noise)
+    if not with_experts:
+        return out
     r4 = np.random.default_rng(_seed(cfg, 4, salt))
     r6 = np.random.default_rng(_seed(cfg, 6, salt))
     w1 = np.empty((E, f, d), dtype=np.uint16 if cfg.dtype == BF16 else np.float32)
@@ -177,10 +182,7 @@ def make_inputs(cfg: LayerConfig, salt: int = 0, with_grad: bool = True) -> dict
     b1 = truncated_normal(np.random.default_rng(_seed(cfg, 5, salt)), (E, f), cfg.weight_std)
     b2 = truncated_normal(np.random.default_rng(_seed(cfg, 7, salt)), (E, d), cfg.weight_std)
 
-    out = dict(
-        x=to_dtype(x, cfg.dtype), w_router=to_dtype(wr, cfg.dtype), logit_bias=bias, noise=noise,
-        w1=w1, b1=to_dtype(b1, cfg.dtype), w2=w2, b2=to_dtype(b2, cfg.dtype),
-    )
+    out.update(w1=w1, b1=to_dtype(b1, cfg.dtype), w2=w2, b2=to_dtype(b2, cfg.dtype))
     if with_grad:
         dy = np.random.default_rng(_seed(cfg, 8, salt)).standard_normal((N, d), dtype=np.float32)
         out["dy"] = to_dtype(dy, cfg.dtype)

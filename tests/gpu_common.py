@@ -1,0 +1,80 @@
+"""Shared helpers of the GPU parity tests (comparison metrics, input caches)."""
+from __future__ import annotations
+
+import functools
+import sys
+
+import numpy as np
+
+import oracle
+from paper_2608_16188_amd import workloads as W
+
+# Tolerance on max|gpu - oracle| / max|oracle| per tensor: bf16 storage with
+# f32 accumulation vs f32 end to end.
+TOL = {W.F32: 1e-4, W.BF16: 2e-2}
+
+
+def say(*a):
+    """Progress line that names the case before a GPU step (flushed)."""
+    print("[gpu-test]", *a, file=sys.stderr, flush=True)
+
+
+def rel_err(got, ref) -> float:
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    assert got.shape == ref.shape, (got.shape, ref.shape)
+    if ref.size == 0:
+        return 0.0
+    scale = np.max(np.abs(ref))
+    if scale == 0.0:
+        return float(np.max(np.abs(got)))
+    return float(np.max(np.abs(got - ref)) / scale)
+
+
+def assert_close(name, got, ref, tol):
+    err = rel_err(got, ref)
+    assert np.all(np.isfinite(np.asarray(got, dtype=np.float64))), f"{name}: non-finite values"
+    assert err <= tol, f"{name}: max rel err {err:.3e} > {tol:.1e}"
+    return err
+
+
+def bits_equal(a, b) -> bool:
+    a, b = np.asarray(a), np.asarray(b)
+    if a.shape != b.shape:
+        return False
+    if a.dtype == np.float32:
+        return np.array_equal(a.view(np.uint32), np.asarray(b, np.float32).view(np.uint32))
+    return np.array_equal(a, b)
+
+
+def as_f64(arr, dtype) -> np.ndarray:
+    return W.to_f64(arr, dtype)
+
+
+@functools.lru_cache(maxsize=2)
+def workload_inputs(name: str, with_experts: bool = True):
+    cfg = W.CONFIGS[name]
+    return cfg, W.make_inputs(cfg, with_grad=with_experts, with_experts=with_experts)
+
+
+def oracle_capacity(cfg: W.LayerConfig, override: int = 0) -> int:
+    if override > 0:
+        return override
+    return oracle.capacity(cfg.n_tokens, cfg.n_groups, cfg.n_experts, cfg.k,
+                           cfg.capacity_factor, cfg.capacity_rounding)
+
+
+def rows_of_expert(r: dict, e: int, C: int, G: int):
+    """Tokens and (t, j) of expert e's packed rows, in row order."""
+    idx, slot, row_base = r["idx"], r["slot"], r["row_base"]
+    N = idx.shape[0]
+    ng = N // G
+    n_e = int(r["counts"][:, e].sum())
+    toks = np.full(n_e, -1, np.int64)
+    js = np.full(n_e, -1, np.int64)
+    kept = np.argwhere((idx == e) & (slot >= 0))
+    for t, j in kept:
+        row = row_base[t // ng, e] + slot[t, j]
+        toks[row], js[row] = t, j
+    assert (toks >= 0).all()
+    return toks, js

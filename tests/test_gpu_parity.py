@@ -1,0 +1,338 @@
+"""GPU parity: the HIP path through the C ABI vs the CPU oracle.
+
+Integers (routing indices, slots, drop masks, order, counts, row bases) and
+the f32 router logits / probabilities / gates must match bit for bit; float
+outputs and gradients within max|gpu - oracle| / max|oracle| <= 2e-2 (bf16)
+or 1e-4 (f32). Small cases compare every element; the full-size workloads,
+run exactly as the benchmark runs them, compare routing in full and sampled
+outputs that the oracle computes one by one.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2608_16188_amd import vmoe as V
+from paper_2608_16188_amd import workloads as W
+from paper_2608_16188_amd.layer import LayerBuffers, to_numpy
+
+from .gpu_common import (TOL, as_f64, assert_close, bits_equal, oracle_capacity,
+                         rows_of_expert, say, workload_inputs)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    torch.cuda.set_device(0)
+    yield
+    torch.cuda.synchronize()
+
+
+def _f64_out(t, dtype):
+    a = to_numpy(t)
+    return W.to_f64(a, dtype) if a.dtype == np.uint16 else a.astype(np.float64)
+
+
+# ------------------------------------------------------------------ routing
+
+def _gpu_route_logits_in(logits, k, G, bias=None, noise=None, capacity_override=0, cf=1.0):
+    N, E = logits.shape
+    s = V.make_shape(N, G, 8, 8, E, k, cf, V.VMOE_BF16, 0, capacity_override)
+    C = V.vmoe_capacity(s)
+    dev = "cuda"
+    Nb = max(N, 1)
+    lg = torch.zeros(Nb, E, dtype=torch.float32, device=dev)
+    if N:
+        lg[:N] = torch.from_numpy(logits).to(dev)
+    out = dict(
+        probs=torch.empty(Nb, E, dtype=torch.float32, device=dev),
+        idx=torch.empty(Nb, k, dtype=torch.int32, device=dev),
+        slot=torch.empty(Nb, k, dtype=torch.int32, device=dev),
+        gate=torch.empty(Nb, k, dtype=torch.float32, device=dev),
+        order=torch.empty(Nb, dtype=torch.int32, device=dev),
+        counts=torch.empty(G, E, dtype=torch.int32, device=dev),
+        row_base=torch.empty(G, E, dtype=torch.int32, device=dev),
+    )
+    ws = torch.empty(max(V.vmoe_route_workspace_bytes(s), 16), dtype=torch.uint8, device=dev)
+    b = None if bias is None else torch.from_numpy(bias).to(dev)
+    nz = None if noise is None else torch.from_numpy(noise).to(dev)
+    V.vmoe_route(s, None, None, b, nz, V.VMOE_ROUTE_LOGITS_IN, lg, out["probs"], out["idx"],
+                 out["slot"], out["gate"], out["order"], out["counts"], out["row_base"], ws)
+    torch.cuda.synchronize()
+    res = {key: to_numpy(v) for key, v in out.items()}
+    for key in ("probs", "idx", "slot", "gate", "order"):
+        res[key] = res[key][:N]
+    return res, C
+
+
+def _compare_routing(got, ref, what=""):
+    for key in ("idx", "slot", "order", "counts", "row_base"):
+        assert np.array_equal(got[key], ref[key]), f"{what} {key} differs"
+    for key in ("probs", "gate"):
+        assert bits_equal(got[key], ref[key]), f"{what} {key} not bit-exact"
+
+
+ROUTE_CASES = [
+    # name, N, E, k, G, kwargs
+    ("random", 500, 8, 2, 1, dict(seed=1, scale=2.0)),
+    ("ties", 640, 6, 3, 2, dict(seed=2, tie_every=2)),
+    ("all_equal", 333, 5, 2, 1, dict(zero=True)),
+    ("capacity1", 200, 8, 2, 4, dict(seed=3, capacity_override=1)),
+    ("e_equals_k", 128, 4, 4, 1, dict(seed=4)),
+    ("single_expert", 90, 1, 1, 3, dict(seed=5)),
+    ("groups17", 17 * 96, 16, 2, 17, dict(seed=6, scale=3.0)),
+    ("e64", 1000, 64, 8, 1, dict(seed=7, scale=1.5)),
+    ("hot_expert_drops", 3000, 8, 2, 1, dict(seed=8, hot=True)),
+    ("many_equal_priorities", 20000, 4, 2, 1, dict(seed=9, tie_every=1)),
+    ("noise_and_bias", 777, 12, 3, 1, dict(seed=10, noise=True)),
+    ("ragged_chunks", 3 * 257, 8, 2, 3, dict(seed=11)),
+    ("empty", 0, 8, 2, 1, dict(seed=12)),
+]
+
+
+@pytest.mark.parametrize("case", ROUTE_CASES, ids=[c[0] for c in ROUTE_CASES])
+def test_route_logits_in_bit_exact(case):
+    name, N, E, k, G, kw = case
+    say("route logits-in", name, N, E, k, G)
+    if kw.get("zero"):
+        logits = np.zeros((N, E), np.float32)
+    else:
+        logits = W.random_logits(N, E, seed=kw["seed"], scale=kw.get("scale", 1.0),
+                                 tie_every=kw.get("tie_every", 0))
+    bias = noise = None
+    if kw.get("hot"):
+        bias = np.zeros(E, np.float32)
+        bias[0] = 3.0
+    if kw.get("noise"):
+        bias = np.linspace(-0.5, 0.5, E).astype(np.float32)
+        noise = W.random_logits(N, E, seed=99, scale=0.3)
+    got, C = _gpu_route_logits_in(logits, k, G, bias, noise, kw.get("capacity_override", 0))
+    ref = oracle.route(logits, k, C, G, bias, noise)
+    _compare_routing(got, ref, name)
+    if name == "hot_expert_drops":
+        assert (ref["slot"] < 0).sum() > 1000
+
+
+@pytest.mark.parametrize("name", list(W.CONFIGS))
+def test_route_full_size_bit_exact(name):
+    """Router product (double accumulation) + routing at the benchmark sizes."""
+    cfg, inp = workload_inputs(name, with_experts=False)
+    say("route full", name)
+    L = LayerBuffers(cfg, inp)
+    L.route()
+    torch.cuda.synchronize()
+    x64 = as_f64(inp["x"], cfg.dtype)
+    wr64 = as_f64(inp["w_router"], cfg.dtype)
+    ref_logits = oracle.router_logits(x64, wr64, cfg.n_groups)
+    assert bits_equal(to_numpy(L.logits), ref_logits), "router logits not bit-exact"
+    C = oracle_capacity(cfg)
+    assert L.C == C
+    ref = oracle.route(ref_logits, cfg.k, C, cfg.n_groups, inp["logit_bias"], inp["noise"])
+    got = dict(idx=to_numpy(L.expert_idx), slot=to_numpy(L.slot), order=to_numpy(L.order),
+               counts=to_numpy(L.counts), row_base=to_numpy(L.row_base),
+               probs=to_numpy(L.probs), gate=to_numpy(L.gate))
+    _compare_routing(got, ref, name)
+
+
+# ------------------------------------------------------------------ whole layer, small
+
+SMALL = [
+    W.CONFIGS["tiny_fp32"],
+    W.custom_config("bf16_ragged", n_tokens=300, d_model=72, d_ff=200, n_experts=5, k=2,
+                    capacity_factor=0.8, n_groups=3, router_std=0.2, noise_var=0.1),
+    W.custom_config("bf16_tiles", n_tokens=520, d_model=256, d_ff=512, n_experts=4, k=1,
+                    capacity_factor=1.5, router_std=0.1),
+    W.custom_config("f32_ragged", n_tokens=210, d_model=40, d_ff=136, n_experts=3, k=2,
+                    capacity_factor=1.0, dtype=W.F32, n_groups=2, router_std=0.2),
+    W.custom_config("bf16_hot_empty", n_tokens=256, d_model=128, d_ff=384, n_experts=8, k=2,
+                    capacity_factor=1.0, hot_experts=2, hot_offset=6.0),
+]
+
+
+def _oracle_layer(cfg, inp, C):
+    f = {key: (None if v is None else as_f64(v, cfg.dtype))
+         for key, v in inp.items() if key not in ("logit_bias", "noise")}
+    return oracle.layer(f["x"], f["w_router"], f["w1"], f["b1"], f["w2"], f["b2"], f["dy"],
+                        k=cfg.k, C=C, n_groups=cfg.n_groups, bias=inp["logit_bias"],
+                        noise=inp["noise"], want_dwr=not cfg.routers_frozen)
+
+
+@pytest.mark.parametrize("cfg", SMALL, ids=[c.name for c in SMALL])
+def test_layer_small_every_element(cfg):
+    inp = W.make_inputs(cfg)
+    say("layer small", cfg.name)
+    L = LayerBuffers(cfg, inp)
+    L.step()
+    torch.cuda.synchronize()
+    C = oracle_capacity(cfg)
+    ref = _oracle_layer(cfg, inp, C)
+    tol = TOL[cfg.dtype]
+    assert bits_equal(to_numpy(L.logits), ref["logits"])
+    got_r = dict(idx=to_numpy(L.expert_idx), slot=to_numpy(L.slot), order=to_numpy(L.order),
+                 counts=to_numpy(L.counts), row_base=to_numpy(L.row_base),
+                 probs=to_numpy(L.probs), gate=to_numpy(L.gate))
+    _compare_routing(got_r, ref, cfg.name)
+    n_e = ref["n_e"]
+    dt = cfg.dtype
+    xe, h, a, ye = (_f64_out(t, dt) for t in (L.xe, L.h, L.a, L.ye))
+    dye, dh, dxe = (_f64_out(t, dt) for t in (L.dye, L.dh, L.dxe))
+    for e in range(cfg.n_experts):
+        r = slice(0, n_e[e])
+        assert np.array_equal(xe[e, r], ref["xe"][e, r]), "dispatch not exact"
+        assert_close(f"H[{e}]", h[e, r], ref["H"][e, r], tol)
+        assert_close(f"A[{e}]", a[e, r], ref["A"][e, r], tol)
+        assert_close(f"ye[{e}]", ye[e, r], ref["ye"][e, r], tol)
+        assert_close(f"dye[{e}]", dye[e, r], ref["dye"][e, r], tol)
+        assert_close(f"dH[{e}]", dh[e, r], ref["dH"][e, r], tol)
+        assert_close(f"dxe[{e}]", dxe[e, r], ref["dxe"][e, r], tol)
+    assert_close("y", _f64_out(L.y, dt), ref["y"], tol)
+    assert_close("dgate", to_numpy(L.dgate), ref["dgate"], tol)
+    assert_close("dW1", to_numpy(L.dw1), ref["dw1"], tol)
+    assert_close("db1", to_numpy(L.db1), ref["db1"], tol)
+    assert_close("dW2", to_numpy(L.dw2), ref["dw2"], tol)
+    assert_close("db2", to_numpy(L.db2), ref["db2"], tol)
+    assert_close("dx", to_numpy(L.dx), ref["dx"], tol)
+    if not cfg.routers_frozen:
+        assert_close("dW_router", to_numpy(L.dw_router), ref["dw_router"], tol)
+    for e in np.nonzero(n_e == 0)[0]:
+        assert np.all(to_numpy(L.dw1)[e] == 0) and np.all(to_numpy(L.dw2)[e] == 0)
+        assert np.all(to_numpy(L.db1)[e] == 0) and np.all(to_numpy(L.db2)[e] == 0)
+
+
+# ------------------------------------------------------------------ whole layer, full size
+
+FULL = ["vitb16_bf16", "wide_e32_bf16", "multitask17_bf16", "vitl16_384_bf16"]
+
+
+def _token_reference(t, ref, f, cfg, probs):
+    """y[t] and dx[t] of one token, by the oracle, from the token alone."""
+    G, ng = cfg.n_groups, cfg.n_tokens // cfg.n_groups
+    g = t // ng
+    x_t = f["x"][t:t + 1]
+    y = np.zeros(cfg.d_model)
+    dx = np.zeros((1, cfg.d_model))
+    dgate = np.zeros((1, cfg.k))
+    for j in range(cfg.k):
+        if ref["slot"][t, j] < 0:
+            continue
+        e = ref["idx"][t, j]
+        gj = float(ref["gate"][t, j])
+        _, _, ye = oracle.ffn_fwd(x_t, f["w1"][e], f["b1"][e], f["w2"][e], f["b2"][e])
+        y += gj * ye[0]
+        dxe, _ = oracle.ffn_bwd_rows(x_t, f["w1"][e], f["b1"][e], f["w2"][e], gj * f["dy"][t:t + 1])
+        dx += dxe
+        dgate[0, j] = float(np.dot(f["dy"][t], ye[0]))
+    dx, _, _ = oracle.route_bwd(x_t, f["w_router"][g:g + 1], probs[t:t + 1], ref["idx"][t:t + 1],
+                                ref["slot"][t:t + 1], dgate, 1, dx_in=dx, want_dwr=False)
+    return y, dx[0], dgate[0]
+
+
+@pytest.mark.parametrize("name", FULL)
+def test_layer_full_size_sampled(name):
+    cfg, inp = workload_inputs(name)
+    say("layer full", name)
+    L = LayerBuffers(cfg, inp)
+    L.step()
+    torch.cuda.synchronize()
+    C = oracle_capacity(cfg)
+    f = {key: as_f64(inp[key], cfg.dtype) for key in ("x", "w_router", "w1", "b1", "w2", "b2", "dy")}
+    ref = oracle.route(oracle.router_logits(f["x"], f["w_router"], cfg.n_groups), cfg.k, C,
+                       cfg.n_groups, inp["logit_bias"], inp["noise"])
+    got_r = dict(idx=to_numpy(L.expert_idx), slot=to_numpy(L.slot), order=to_numpy(L.order),
+                 counts=to_numpy(L.counts), row_base=to_numpy(L.row_base),
+                 probs=to_numpy(L.probs), gate=to_numpy(L.gate))
+    _compare_routing(got_r, ref, name)
+    tol = TOL[cfg.dtype]
+    rng = np.random.default_rng(0)
+    kept_any = (ref["slot"] >= 0).any(1)
+    toks = list(rng.choice(cfg.n_tokens, 14, replace=False))
+    toks += list(rng.choice(np.nonzero(~kept_any)[0], 2)) if (~kept_any).any() else []
+    toks += list(rng.choice(np.nonzero((ref["slot"] < 0).any(1) & kept_any)[0], 2)) \
+        if ((ref["slot"] < 0).any(1) & kept_any).any() else []
+    y_gpu, dx_gpu, dg_gpu = _f64_out(L.y, cfg.dtype), to_numpy(L.dx), to_numpy(L.dgate)
+    ys, dxs, dgs, yr, dxr, dgr = [], [], [], [], [], []
+    for t in toks:
+        y, dx, dg = _token_reference(t, ref, f, cfg, ref["probs"])
+        ys.append(y_gpu[t]), dxs.append(dx_gpu[t]), dgs.append(dg_gpu[t])
+        yr.append(y), dxr.append(dx), dgr.append(dg)
+    assert_close("y[sampled]", np.array(ys), np.array(yr), tol)
+    assert_close("dx[sampled]", np.array(dxs), np.array(dxr), tol)
+    assert_close("dgate[sampled]", np.array(dgs), np.array(dgr), tol)
+    # weight gradients: sampled entries of the busiest, the least busy non-empty
+    # and (if any) an empty expert
+    n_e = ref["counts"].sum(0)
+    order_e = np.argsort(n_e)
+    experts = {int(order_e[-1]), int(order_e[np.searchsorted(n_e[order_e], 1)])}
+    if (n_e == 0).any():
+        experts.add(int(np.nonzero(n_e == 0)[0][0]))
+    dw1, dw2, db1, db2 = (to_numpy(t) for t in (L.dw1, L.dw2, L.db1, L.db2))
+    d, ff = cfg.d_model, cfg.d_ff
+    for e in sorted(experts):
+        tok_e, j_e = rows_of_expert(ref, e, C, cfg.n_groups)
+        xe_rows = f["x"][tok_e]
+        dye_rows = ref["gate"][tok_e, j_e][:, None].astype(np.float64) * f["dy"][tok_e]
+        ns = 24
+        which = np.repeat([1, 2, 3, 4], ns)
+        row = np.concatenate([rng.integers(0, ff, ns), rng.integers(0, d, ns),
+                              rng.integers(0, ff, ns), rng.integers(0, d, ns)])
+        col = np.concatenate([rng.integers(0, d, ns), rng.integers(0, ff, ns),
+                              np.zeros(2 * ns, np.int64)])
+        refv = oracle.ffn_bwd_weight_entries(xe_rows, f["w1"][e], f["b1"][e], f["w2"][e],
+                                             dye_rows, which, row, col)
+        gotv = np.concatenate([dw1[e][row[:ns], col[:ns]], dw2[e][row[ns:2 * ns], col[ns:2 * ns]],
+                               db1[e][row[2 * ns:3 * ns]], db2[e][row[3 * ns:]]])
+        if n_e[e] == 0:
+            assert np.all(gotv == 0.0) and np.all(refv == 0.0)
+            continue
+        for q, nm in enumerate(["dW1", "dW2", "db1", "db2"]):
+            sl = slice(q * ns, (q + 1) * ns)
+            assert_close(f"{nm}[e={e}]", gotv[sl], refv[sl], tol)
+
+
+def test_route_bwd_full_size_per_call():
+    """Router backward alone at the ViT-L/16 size, fed the oracle's routing."""
+    cfg, inp = workload_inputs("vitl16_384_bf16", with_experts=False)
+    say("route_bwd full")
+    f = {key: as_f64(inp[key], cfg.dtype) for key in ("x", "w_router")}
+    C = oracle_capacity(cfg)
+    ref = oracle.route(oracle.router_logits(f["x"], f["w_router"], 1), cfg.k, C, 1,
+                       inp["logit_bias"], inp["noise"])
+    dgate = W.random_logits(cfg.n_tokens, cfg.k, seed=31)
+    dx0 = W.random_logits(cfg.n_tokens, cfg.d_model, seed=32)
+    s = V.make_shape(cfg.n_tokens, 1, cfg.d_model, cfg.d_ff, cfg.n_experts, cfg.k,
+                     cfg.capacity_factor, V.VMOE_BF16)
+    dev = "cuda"
+    tx = torch.from_numpy(inp["x"].view(np.int16)).view(torch.bfloat16).to(dev)
+    twr = torch.from_numpy(inp["w_router"].view(np.int16)).view(torch.bfloat16).to(dev)
+    tp = torch.from_numpy(ref["probs"]).to(dev)
+    ti = torch.from_numpy(ref["idx"]).to(dev)
+    ts = torch.from_numpy(ref["slot"]).to(dev)
+    tg = torch.from_numpy(dgate).to(dev)
+    tdx = torch.from_numpy(dx0).to(dev)
+    tdw = torch.empty(1, cfg.n_experts, cfg.d_model, dtype=torch.float32, device=dev)
+    ws = torch.empty(V.vmoe_route_bwd_workspace_bytes(s), dtype=torch.uint8, device=dev)
+    V.vmoe_route_bwd(s, tx, twr, tp, ti, ts, tg, tdx, tdw, ws)
+    torch.cuda.synchronize()
+    dx_ref, dwr_ref, _ = oracle.route_bwd(f["x"], f["w_router"], ref["probs"], ref["idx"],
+                                          ref["slot"], dgate.astype(np.float64), 1,
+                                          dx_in=dx0.astype(np.float64))
+    assert_close("dx", to_numpy(tdx), dx_ref, 1e-5)
+    assert_close("dW_router", to_numpy(tdw), dwr_ref, 1e-4)
+
+
+def test_step_is_deterministic():
+    cfg, inp = workload_inputs("vitb16_bf16")
+    say("determinism")
+    L = LayerBuffers(cfg, inp)
+    names = ["logits", "probs", "expert_idx", "slot", "gate", "order", "counts", "y", "dgate",
+             "dw1", "db1", "dw2", "db2", "dx", "dw_router"]
+    L.step()
+    torch.cuda.synchronize()
+    first = {n: to_numpy(getattr(L, n)).copy() for n in names}
+    L.step()
+    torch.cuda.synchronize()
+    for n in names:
+        assert np.array_equal(first[n], to_numpy(getattr(L, n))), f"{n} not deterministic"

@@ -50,6 +50,7 @@ struct GemmArgs {
     const void* bias;       // EPI_FWD1 / EPI_BIAS
     long long bias_estride;
     const void* aux;        // EPI_GELU_GRAD: saved pre-activation H
+    float* bsum;            // EPI_F32 (bf16 path): row sums of A per expert, or null
 };
 
 __device__ __forceinline__ int expert_rows(const int32_t* counts, int G, int E, int e) {
@@ -69,138 +70,196 @@ __device__ __forceinline__ float gelu_grad_f(float h) {
 
 // ------------------------------------------------------------------ bf16 MFMA
 
-constexpr int BM = 128, BN = 128, BK = 64;
-constexpr int LDK = BK + 8;  // padded LDS row (bf16 elements): 144 B
+constexpr int BK = 64;          // k depth of one LDS stage
+constexpr int KPAD = 8;         // k-major rows: 64 + 8 bf16 = 144 B pitch
+constexpr int MNPAD = 16;       // mn-major rows: ROWS + 16 bf16 (conflict-free transpose reads)
 
-// Global -> registers for one 128 x 64 operand tile. A masked-off vector is
-// still loaded, from the (always valid) operand base, and then replaced by
-// zeros in registers: no data-dependent address ever points off the operand.
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
+
+// LDS elements of one operand stage: k-major [ROWS][BK + KPAD], mn-major [BK][ROWS + MNPAD].
+template <int ROWS, bool KMAJOR>
+__host__ __device__ constexpr int stage_elems() {
+    return KMAJOR ? ROWS * (BK + KPAD) : BK * (ROWS + MNPAD);
+}
+
+// A masked-off vector is still loaded, from the (always valid) operand base,
+// and replaced by zeros in registers: no address ever points off the operand.
 __device__ __forceinline__ uint4 masked_load(const uint16_t* __restrict__ base, size_t off,
                                              bool ok) {
     const uint4 v = *reinterpret_cast<const uint4*>(base + (ok ? off : 0));
     return ok ? v : make_uint4(0, 0, 0, 0);
 }
 
-template <bool KMAJOR>
-__device__ __forceinline__ void load_tile(const uint16_t* __restrict__ base, int ld, int mn0,
-                                          int mn_lim, int k0, int k_lim, uint4 (&r)[4]) {
+// Global -> registers: one ROWS x BK operand stage, ROWS / 32 vectors of 8
+// bf16 per thread, each row segment read by consecutive lanes (coalesced).
+template <int ROWS, bool KMAJOR>
+__device__ __forceinline__ void load_stage(const uint16_t* __restrict__ base, int ld, int mn0,
+                                           int mn_lim, int k0, int k_lim,
+                                           uint4 (&r)[ROWS / 32]) {
     const int tid = threadIdx.x;
     if (KMAJOR) {
-        const int kv = (tid & 7) * 8;
+        const int kc = (tid & 7) * 8;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
+        for (int j = 0; j < ROWS / 32; ++j) {
             const int mn = (tid >> 3) + 32 * j;
-            const bool ok = (mn0 + mn < mn_lim) && (k0 + kv < k_lim);
-            r[j] = masked_load(base, static_cast<size_t>(mn0 + mn) * ld + k0 + kv, ok);
+            r[j] = masked_load(base, static_cast<size_t>(mn0 + mn) * ld + k0 + kc,
+                               (mn0 + mn < mn_lim) && (k0 + kc < k_lim));
         }
     } else {
-        const int mv = (tid & 15) * 8;
-        const int kq = (tid >> 4) * 4;
+        constexpr int VPR = ROWS / 8;  // vectors per k row
+        const int mc = (tid % VPR) * 8;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const bool ok = (mn0 + mv < mn_lim) && (k0 + kq + q < k_lim);
-            r[q] = masked_load(base, static_cast<size_t>(k0 + kq + q) * ld + mn0 + mv, ok);
+        for (int j = 0; j < ROWS / 32; ++j) {
+            const int kr = tid / VPR + (256 / VPR) * j;
+            r[j] = masked_load(base, static_cast<size_t>(k0 + kr) * ld + mn0 + mc,
+                               (k0 + kr < k_lim) && (mn0 + mc < mn_lim));
         }
     }
 }
 
-__device__ __forceinline__ uint32_t half_of(const uint4& v, int c) {
-    const uint32_t w = (c >> 1) == 0 ? v.x : (c >> 1) == 1 ? v.y : (c >> 1) == 2 ? v.z : v.w;
-    return (c & 1) ? (w >> 16) : (w & 0xFFFFu);
-}
-
-// Registers -> LDS tile [128 mn][LDK] (k contiguous).
-template <bool KMAJOR>
-__device__ __forceinline__ void store_tile(uint16_t (*s)[LDK], const uint4 (&r)[4]) {
+// Registers -> LDS, same element placement as the global tile (no transpose).
+template <int ROWS, bool KMAJOR>
+__device__ __forceinline__ void store_stage(uint16_t* s, const uint4 (&r)[ROWS / 32]) {
     const int tid = threadIdx.x;
     if (KMAJOR) {
-        const int kv = (tid & 7) * 8;
+        const int kc = (tid & 7) * 8;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) *reinterpret_cast<uint4*>(&s[(tid >> 3) + 32 * j][kv]) = r[j];
+        for (int j = 0; j < ROWS / 32; ++j)
+            *reinterpret_cast<uint4*>(s + ((tid >> 3) + 32 * j) * (BK + KPAD) + kc) = r[j];
     } else {
-        const int mv = (tid & 15) * 8;
-        const int kq = (tid >> 4) * 4;
+        constexpr int VPR = ROWS / 8;
+        const int mc = (tid % VPR) * 8;
 #pragma unroll
-        for (int c = 0; c < 8; ++c) {
-            uint2 v;
-            v.x = half_of(r[0], c) | (half_of(r[1], c) << 16);
-            v.y = half_of(r[2], c) | (half_of(r[3], c) << 16);
-            *reinterpret_cast<uint2*>(&s[mv + c][kq]) = v;
-        }
+        for (int j = 0; j < ROWS / 32; ++j)
+            *reinterpret_cast<uint4*>(s + (tid / VPR + (256 / VPR) * j) * (ROWS + MNPAD) + mc) =
+                r[j];
     }
 }
 
-template <bool A_KMAJOR, bool B_KMAJOR, int EPI>
-__global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs p) {
-    __shared__ __attribute__((aligned(16))) uint16_t As[2][BM][LDK];
-    __shared__ __attribute__((aligned(16))) uint16_t Bs[2][BN][LDK];
+// ds_read_b64_tr_b16: within each 16-lane group, lane j reads 4 bf16 at its
+// address and lane i receives element i % 4 of lanes i/4, i/4+4, i/4+8, i/4+12.
+// With lane j pointing at row j/4, column 4*(j%4) of a 4 x 16 block, lane i
+// gets column i: four consecutive k values of one mn index.
+__device__ __forceinline__ s16x4 lds_read_tr(const uint16_t* p) {
+    typedef __attribute__((address_space(3))) s16x4* lds_s16x4;
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4)(p));
+}
 
-    const int e = blockIdx.z;
+// MFMA operand fragment for 16 mn values (lane & 15) x 8 k values
+// (k = kstep * 32 + 8 * (lane >> 4) + 0..7).
+template <int ROWS, bool KMAJOR>
+__device__ __forceinline__ bf16x8 read_frag(const uint16_t* s, int blk, int kstep, int lane) {
+    if (KMAJOR) {
+        return *reinterpret_cast<const bf16x8*>(s + (blk * 16 + (lane & 15)) * (BK + KPAD) +
+                                                kstep * 32 + (lane >> 4) * 8);
+    } else {
+        constexpr int P = ROWS + MNPAD;
+        const int j = lane & 15;
+        const uint16_t* p0 = s + (kstep * 32 + 8 * (lane >> 4) + (j >> 2)) * P + blk * 16 +
+                             4 * (j & 3);
+        const s16x4 lo = lds_read_tr(p0);
+        const s16x4 hi = lds_read_tr(p0 + 4 * P);
+        const s16x8 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        return __builtin_bit_cast(bf16x8, v);
+    }
+}
+
+// One BM x BN output tile of expert e per 256-thread block; four waves in
+// 2 x 2, each (BM/2) x (BN/2) as 16 x 16 MFMA blocks. Blocks are numbered so
+// that each of the 8 XCDs (blocks b = x mod 8) walks a contiguous range of
+// tiles (n fastest): neighbouring tiles share operand panels in that XCD's L2.
+template <int BM_, int BN_, bool A_KMAJOR, bool B_KMAJOR, int EPI>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void gemm_bf16_kernel(GemmArgs p, int tiles_m, int tiles_n, int per_xcd, int total) {
+    constexpr int AE = stage_elems<BM_, A_KMAJOR>();
+    constexpr int BE = stage_elems<BN_, B_KMAJOR>();
+    constexpr int FM = BM_ / 32, FN = BN_ / 32;  // 16 x 16 blocks per wave
+    static_assert(EPI != EPI_F32 || (BM_ == 256 && !A_KMAJOR), "row sums assume 256 mn-major rows");
+    __shared__ __attribute__((aligned(16))) uint16_t smem[2 * (AE + BE)];
+
+    const int b = blockIdx.x;
+    const int w = (b & 7) * per_xcd + (b >> 3);
+    if (w >= total) return;
+    const int tn = w % tiles_n;
+    const int tm = (w / tiles_n) % tiles_m;
+    const int e = w / (tiles_n * tiles_m);
+
     const int ne = expert_rows(p.counts, p.G, p.E, e);
     const int M = p.var_k ? p.M : ne;
     const int K = p.var_k ? ne : p.K;
     const int N = p.N;
-    const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+    const int m0 = tm * BM_, n0 = tn * BN_;
     if (m0 >= M) return;
 
     const uint16_t* A = static_cast<const uint16_t*>(p.a.base) + e * p.a.estride;
     const uint16_t* B = static_cast<const uint16_t*>(p.b.base) + e * p.b.estride;
-
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int wm = wave >> 1, wn = wave & 1;
+    // weight-gradient GEMMs: the first n-tile also sums its A rows (bias grad)
+    const bool row_sum = EPI == EPI_F32 && p.bsum != nullptr && tn == 0;
+    float rsum = 0.0f;
 
-    f32x4 acc[4][4];
+    f32x4 acc[FM][FN];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < FM; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     const int nk = (K + BK - 1) / BK;
-    uint4 ra[4], rb[4];
-    load_tile<A_KMAJOR>(A, p.a.ld, m0, M, 0, K, ra);
-    load_tile<B_KMAJOR>(B, p.b.ld, n0, N, 0, K, rb);
-    store_tile<A_KMAJOR>(As[0], ra);
-    store_tile<B_KMAJOR>(Bs[0], rb);
+    uint4 ra[BM_ / 32], rb[BN_ / 32];
+    load_stage<BM_, A_KMAJOR>(A, p.a.ld, m0, M, 0, K, ra);
+    load_stage<BN_, B_KMAJOR>(B, p.b.ld, n0, N, 0, K, rb);
+    store_stage<BM_, A_KMAJOR>(smem, ra);
+    store_stage<BN_, B_KMAJOR>(smem + AE, rb);
     __syncthreads();
 
     for (int kt = 0; kt < nk; ++kt) {
-        const int cur = kt & 1;
+        uint16_t* As = smem + (kt & 1) * (AE + BE);
+        uint16_t* Bs = As + AE;
         const bool more = kt + 1 < nk;
         if (more) {
-            load_tile<A_KMAJOR>(A, p.a.ld, m0, M, (kt + 1) * BK, K, ra);
-            load_tile<B_KMAJOR>(B, p.b.ld, n0, N, (kt + 1) * BK, K, rb);
+            load_stage<BM_, A_KMAJOR>(A, p.a.ld, m0, M, (kt + 1) * BK, K, ra);
+            load_stage<BN_, B_KMAJOR>(B, p.b.ld, n0, N, (kt + 1) * BK, K, rb);
+        }
+        if (!A_KMAJOR && row_sum) {
+            // thread t owns A row m0 + t (BM_ == 256): add its 64 k values
+#pragma unroll 8
+            for (int kk = 0; kk < BK; ++kk)
+                rsum += bf16_to_f32(As[kk * (BM_ + MNPAD) + threadIdx.x]);
         }
 #pragma unroll
         for (int ks = 0; ks < BK / 32; ++ks) {
-            const int kc = ks * 32 + (lane >> 4) * 8;
-            bf16x8 af[4], bfr[4];
+            bf16x8 af[FM], bfr[FN];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                af[i] = *reinterpret_cast<const bf16x8*>(&As[cur][wm * 64 + i * 16 + (lane & 15)][kc]);
-                bfr[i] = *reinterpret_cast<const bf16x8*>(&Bs[cur][wn * 64 + i * 16 + (lane & 15)][kc]);
-            }
+            for (int i = 0; i < FM; ++i) af[i] = read_frag<BM_, A_KMAJOR>(As, wm * FM + i, ks, lane);
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
+            for (int j = 0; j < FN; ++j) bfr[j] = read_frag<BN_, B_KMAJOR>(Bs, wn * FN + j, ks, lane);
 #pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bfr[j], af[i], acc[i][j], 0,
-                                                                        0, 0);
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bfr[j], af[i], acc[i][j],
+                                                                        0, 0, 0);
         }
         if (more) {
-            store_tile<A_KMAJOR>(As[cur ^ 1], ra);
-            store_tile<B_KMAJOR>(Bs[cur ^ 1], rb);
+            uint16_t* An = smem + ((kt + 1) & 1) * (AE + BE);
+            store_stage<BM_, A_KMAJOR>(An, ra);
+            store_stage<BN_, B_KMAJOR>(An + AE, rb);
         }
         __syncthreads();
     }
+    if (row_sum && m0 + static_cast<int>(threadIdx.x) < M)
+        p.bsum[static_cast<size_t>(e) * M + m0 + threadIdx.x] = rsum;
 
     // Epilogue: lane holds C[m][n .. n+3].
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int m = m0 + wm * 64 + i * 16 + (lane & 15);
+    for (int i = 0; i < FM; ++i) {
+        const int m = m0 + (wm * FM + i) * 16 + (lane & 15);
         if (m >= M) continue;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int n = n0 + wn * 64 + j * 16 + (lane >> 4) * 4;
+        for (int j = 0; j < FN; ++j) {
+            const int n = n0 + (wn * FN + j) * 16 + (lane >> 4) * 4;
             if (n >= N) continue;
             const f32x4 v = acc[i][j];
             const size_t o = e * p.out_estride + static_cast<size_t>(m) * p.ldo + n;
@@ -225,10 +284,10 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs p) {
                     r[2] *= gelu_grad_f(bf16_to_f32(hh.y & 0xFFFFu));
                     r[3] *= gelu_grad_f(bf16_to_f32(hh.y >> 16));
                 }
-                uint2 w;
-                w.x = pack_bf16x2(r[0], r[1]);
-                w.y = pack_bf16x2(r[2], r[3]);
-                *reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.out) + o) = w;
+                uint2 w2;
+                w2.x = pack_bf16x2(r[0], r[1]);
+                w2.y = pack_bf16x2(r[2], r[3]);
+                *reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.out) + o) = w2;
                 if (EPI == EPI_FWD1) {
                     uint2 a;
                     a.x = pack_bf16x2(gelu_f(r[0]), gelu_f(r[1]));
@@ -326,11 +385,27 @@ __global__ __launch_bounds__(256) void colsum_kernel(const T* __restrict__ src,
                                                   part[2][c & 63]) + part[3][c & 63];
 }
 
+template <int BM_, int BN_, bool AK, bool BK_, int EPI>
+void launch_bf16(const Dims& D, const GemmArgs& a, int grid_m_rows, hipStream_t st) {
+    const int tiles_m = static_cast<int>(cdiv(grid_m_rows, BM_));
+    const int tiles_n = static_cast<int>(cdiv(a.N, BN_));
+    const int total = D.E * tiles_m * tiles_n;
+    const int per_xcd = static_cast<int>(cdiv(total, 8));
+    gemm_bf16_kernel<BM_, BN_, AK, BK_, EPI><<<8 * per_xcd, 256, 0, st>>>(a, tiles_m, tiles_n,
+                                                                         per_xcd, total);
+}
+
 template <bool AK, bool BK_, int EPI>
 void launch_gemm(const Dims& D, const GemmArgs& a, int grid_m_rows, hipStream_t st) {
     if (D.dtype == VMOE_BF16) {
-        dim3 grid(cdiv(a.N, BN), cdiv(grid_m_rows, BM), D.E);
-        gemm_bf16_kernel<AK, BK_, EPI><<<grid, 256, 0, st>>>(a);
+        if constexpr (EPI == EPI_F32) {
+            launch_bf16<256, 128, AK, BK_, EPI>(D, a, grid_m_rows, st);
+        } else {
+            if (a.N >= 2048)
+                launch_bf16<256, 256, AK, BK_, EPI>(D, a, grid_m_rows, st);
+            else
+                launch_bf16<256, 128, AK, BK_, EPI>(D, a, grid_m_rows, st);
+        }
     } else {
         dim3 grid(cdiv(a.N, FT), cdiv(grid_m_rows, FT), D.E);
         gemm_f32_kernel<AK, BK_, EPI><<<grid, 256, 0, st>>>(a);
@@ -426,6 +501,7 @@ vmoe_status ffn_bwd_launch(const Dims& D, const void* xe, const int32_t* counts,
     w.out = dw2;
     w.out_estride = static_cast<long long>(D.d) * D.f;
     w.ldo = D.f;
+    w.bsum = D.dtype == VMOE_BF16 ? db2 : nullptr;  // db2 = row sums of dye^T
     launch_gemm<false, false, EPI_F32>(D, w, D.d, st);
     // dW1 [f, d] = dH^T xe
     GemmArgs v = base_args(D, counts);
@@ -438,14 +514,10 @@ vmoe_status ffn_bwd_launch(const Dims& D, const void* xe, const int32_t* counts,
     v.out = dw1;
     v.out_estride = static_cast<long long>(D.f) * D.d;
     v.ldo = D.d;
+    v.bsum = D.dtype == VMOE_BF16 ? db1 : nullptr;  // db1 = row sums of dH^T
     launch_gemm<false, false, EPI_F32>(D, v, D.f, st);
-    // bias gradients
-    if (D.dtype == VMOE_BF16) {
-        colsum_kernel<uint16_t><<<dim3(cdiv(D.d, 64), D.E), 256, 0, st>>>(
-            static_cast<const uint16_t*>(dye), rows * D.d, D.d, counts, D.G, D.E, db2);
-        colsum_kernel<uint16_t><<<dim3(cdiv(D.f, 64), D.E), 256, 0, st>>>(
-            static_cast<const uint16_t*>(dh), rows * D.f, D.f, counts, D.G, D.E, db1);
-    } else {
+    // bias gradients (the bf16 path sums them inside the dW GEMMs)
+    if (D.dtype == VMOE_F32) {
         colsum_kernel<float><<<dim3(cdiv(D.d, 64), D.E), 256, 0, st>>>(
             static_cast<const float*>(dye), rows * D.d, D.d, counts, D.G, D.E, db2);
         colsum_kernel<float><<<dim3(cdiv(D.f, 64), D.E), 256, 0, st>>>(

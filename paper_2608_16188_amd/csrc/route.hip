@@ -28,8 +28,7 @@ constexpr int kBinBits = 12;
 constexpr int kNumBins = 1 << kBinBits;
 constexpr int kBinShift = kKeyBits - kBinBits;
 constexpr int kSlotChunk = 256;              // order positions per slots block
-constexpr int kGateTokens = 64;              // tokens per router_gate block
-constexpr int kGateDK = 64;                  // model-width chunk staged in LDS
+constexpr int kGateTokens = 256;             // most tokens per router_gate block (E = 1)
 
 struct RouteWs {
     uint32_t* keys;     // [N]
@@ -96,80 +95,72 @@ __device__ __forceinline__ uint32_t priority_key(float prio) {
     return key < (1u << kKeyBits) ? key : (1u << kKeyBits) - 1u;
 }
 
-template <typename T>
-__device__ __forceinline__ float load_f32(const T* p, size_t i);
-template <> __device__ __forceinline__ float load_f32<float>(const float* p, size_t i) {
-    return p[i];
+// Eight consecutive activations as f32 (16-byte aligned).
+__device__ __forceinline__ void load8(const uint16_t* p, float* v) {
+    const uint4 u = *reinterpret_cast<const uint4*>(p);
+    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        v[2 * q] = __uint_as_float(w[q] << 16);
+        v[2 * q + 1] = __uint_as_float(w[q] & 0xFFFF0000u);
+    }
 }
-template <> __device__ __forceinline__ float load_f32<uint16_t>(const uint16_t* p, size_t i) {
-    return bf16_to_f32(p[i]);
+__device__ __forceinline__ void load8(const float* p, float* v) {
+    const float4 a = reinterpret_cast<const float4*>(p)[0];
+    const float4 b = reinterpret_cast<const float4*>(p)[1];
+    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+    v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
 }
 
-// One block = kGateTokens tokens of one group, all E experts.
-// Thread (tt = tid % 64, eg = tid / 64) owns token tt and experts
-// [eg*E/4, (eg+1)*E/4) (E is padded to a multiple of 4 inside the block).
+// One block = tpb = floor(256 / E) tokens of one group. Thread tid < tpb*E
+// computes logit (token tid / E, expert tid % E) as a sequential dot product
+// in double over increasing i, 8 elements (one 16-byte load) at a time, so
+// every (token, expert) pair is its own dependency chain and the whole grid
+// is busy; the gate of each token then runs on one thread from LDS.
 template <typename T>
 __global__ __launch_bounds__(256) void router_gate_kernel(
     const T* __restrict__ x, const T* __restrict__ wr, const float* __restrict__ bias,
     const float* __restrict__ noise, float* __restrict__ logits, float* __restrict__ probs,
     int32_t* __restrict__ idx, uint32_t* __restrict__ keys, int Ng, int d, int E, int k,
-    int logits_in) {
-    __shared__ float xs[kGateTokens][kGateDK + 1];
-    __shared__ float ws[kGateDK][kMaxExperts];
-    __shared__ float lg[kGateTokens][kMaxExperts + 1];
-
+    int logits_in, int tpb) {
+    __shared__ float lg_store[2 * kGateTokens];  // tpb * (E + 1) <= 256 + tpb
     const int g = blockIdx.y;
-    const int t0 = blockIdx.x * kGateTokens;          // within group
-    const int ntok = min(kGateTokens, Ng - t0);
+    const int t0 = blockIdx.x * tpb;                  // within group
+    const int ntok = min(tpb, Ng - t0);
     const size_t tok0 = static_cast<size_t>(g) * Ng + t0;  // global index
     const int tid = threadIdx.x;
-    const int tt = tid & 63;
-    const int eg = tid >> 6;
-    const int epb = (E + 3) / 4;                       // experts per thread
-    const int e_lo = eg * epb;
-
-    if (!logits_in) {
-        double acc[kMaxExperts / 4];
+    const int ld = E + 1;                             // LDS row of one token's logits
+    if (tid < ntok * E) {
+        const int tt = tid / E, e = tid % E;
+        float v;
+        if (!logits_in) {
+            const T* xr = x + (tok0 + tt) * d;
+            const T* wrow = wr + (static_cast<size_t>(g) * E + e) * d;
+            double acc = 0.0;
+            // Each product of two bf16 / f32 values is exact in double, so the
+            // fused multiply-add equals add-after-multiply, in increasing i.
+#pragma unroll 2
+            for (int i = 0; i < d; i += 8) {
+                float xv[8], wv[8];
+                load8(xr + i, xv);
+                load8(wrow + i, wv);
 #pragma unroll
-        for (int j = 0; j < kMaxExperts / 4; ++j) acc[j] = 0.0;
-        const T* wg = wr + static_cast<size_t>(g) * E * d;
-        for (int i0 = 0; i0 < d; i0 += kGateDK) {
-            const int dk = min(kGateDK, d - i0);
-            for (int q = tid; q < kGateTokens * kGateDK; q += 256) {
-                int r = q / kGateDK, c = q % kGateDK;
-                xs[r][c] = (r < ntok && c < dk) ? load_f32(x, (tok0 + r) * d + i0 + c) : 0.0f;
+                for (int q = 0; q < 8; ++q)
+                    acc = __builtin_fma(static_cast<double>(xv[q]), static_cast<double>(wv[q]), acc);
             }
-            for (int q = tid; q < kGateDK * E; q += 256) {
-                int e = q / kGateDK, c = q % kGateDK;
-                ws[c][e] = c < dk ? load_f32(wg, static_cast<size_t>(e) * d + i0 + c) : 0.0f;
-            }
-            __syncthreads();
-            // Sequential in i: each product of two bf16 / f32 values is exact in
-            // double, so the fused multiply-add equals add-after-multiply.
-            for (int c = 0; c < dk; ++c) {
-                const double xv = static_cast<double>(xs[tt][c]);
-#pragma unroll
-                for (int j = 0; j < kMaxExperts / 4; ++j)
-                    if (j < epb && e_lo + j < E)
-                        acc[j] = __builtin_fma(xv, static_cast<double>(ws[c][e_lo + j]), acc[j]);
-            }
-            __syncthreads();
+            v = static_cast<float>(acc);
+            logits[(tok0 + tt) * E + e] = v;
+        } else {
+            v = logits[(tok0 + tt) * E + e];
         }
-#pragma unroll
-        for (int j = 0; j < kMaxExperts / 4; ++j)
-            if (j < epb && e_lo + j < E) lg[tt][e_lo + j] = static_cast<float>(acc[j]);
-        __syncthreads();
-        for (int q = tid; q < ntok * E; q += 256)
-            logits[tok0 * E + q] = lg[q / E][q % E];
-    } else {
-        for (int q = tid; q < ntok * E; q += 256) lg[q / E][q % E] = logits[tok0 * E + q];
+        lg_store[tt * ld + e] = v;
     }
     __syncthreads();
 
     if (tid >= ntok) return;
-    // Gate of token tid; its noisy logits z overwrite row tid of lg.
+    // Gate of token tid; its noisy logits z overwrite its row of lg_store.
     const size_t t = tok0 + tid;
-    float* z = lg[tid];
+    float* z = lg_store + tid * ld;
     float m = 0.0f;
     for (int e = 0; e < E; ++e) {
         float v = z[e];
@@ -383,15 +374,16 @@ vmoe_status route_launch(const Dims& D, const void* x, const void* wr, const flo
     const int nch = static_cast<int>(cdiv(D.Ng, kSlotChunk));
     const int logits_in = (flags & VMOE_ROUTE_LOGITS_IN) ? 1 : 0;
     if (D.N > 0) {
-        dim3 grid(cdiv(D.Ng, kGateTokens), D.G);
+        const int tpb = 256 / D.E;
+        dim3 grid(cdiv(D.Ng, tpb), D.G);
         if (D.dtype == VMOE_BF16)
             router_gate_kernel<uint16_t><<<grid, 256, 0, st>>>(
                 static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(wr), bias, noise,
-                logits, probs, idx, ws.keys, D.Ng, D.d, D.E, D.k, logits_in);
+                logits, probs, idx, ws.keys, D.Ng, D.d, D.E, D.k, logits_in, tpb);
         else
             router_gate_kernel<float><<<grid, 256, 0, st>>>(
                 static_cast<const float*>(x), static_cast<const float*>(wr), bias, noise, logits,
-                probs, idx, ws.keys, D.Ng, D.d, D.E, D.k, logits_in);
+                probs, idx, ws.keys, D.Ng, D.d, D.E, D.k, logits_in, tpb);
         bin_scan_kernel<<<D.G, 1024, 0, st>>>(ws.keys, ws.bin_start, ws.fill, ws.ccount, D.Ng,
                                                nch * D.k * D.E);
         bin_scatter_kernel<<<cdiv(D.N, 256), 256, 0, st>>>(ws.keys, ws.bin_start, ws.fill,

@@ -12,7 +12,8 @@ namespace vmoe {
 namespace {
 
 constexpr int kCols = 256;
-constexpr int kMaxChunk = 128;
+constexpr int kMinChunk = 64;
+constexpr int kMaxChunk = 256;
 
 template <typename T> __device__ __forceinline__ float ld(const T* p, size_t i);
 template <> __device__ __forceinline__ float ld<float>(const float* p, size_t i) { return p[i]; }
@@ -78,19 +79,30 @@ __global__ __launch_bounds__(kCols) void route_bwd_kernel(
     }
 }
 
+// dW_r = sum over chunks of the partials. A block owns 32 outputs; 8 lane
+// groups each add every 8th chunk (coalesced 128-byte rows), then the 8
+// partial sums are added in a fixed order.
 __global__ __launch_bounds__(256) void route_bwd_reduce_kernel(const float* __restrict__ partial,
                                                                float* __restrict__ dwr, int E,
                                                                int d, int nch, long long total) {
-    const long long q = static_cast<long long>(blockIdx.x) * 256 + threadIdx.x;
-    if (q >= total) return;
+    __shared__ float part[8][33];
+    const int ql = threadIdx.x & 31, r = threadIdx.x >> 5;
+    const long long q = static_cast<long long>(blockIdx.x) * 32 + ql;
     const long long ed = static_cast<long long>(E) * d;
-    const long long g = q / ed, r = q % ed;
     float s = 0.0f;
-    if (nch > 0) {
-        const float* p = partial + g * nch * ed + r;
-        for (int c = 0; c < nch; ++c) s += p[c * ed];
+    if (q < total && nch > 0) {
+        const long long g = q / ed, o = q % ed;
+        const float* p = partial + g * nch * ed + o;
+        for (int c = r; c < nch; c += 8) s += p[c * ed];
     }
-    dwr[q] = s;
+    part[r][ql] = s;
+    __syncthreads();
+    if (r == 0 && q < total) {
+        float t = part[0][ql];
+#pragma unroll
+        for (int i = 1; i < 8; ++i) t += part[i][ql];
+        dwr[q] = t;
+    }
 }
 
 struct ChunkPlan {
@@ -102,7 +114,7 @@ ChunkPlan plan(const Dims& D) {
     int target = 1024 / (D.G * colblocks);
     if (target < 1) target = 1;
     int tch = D.Ng > 0 ? static_cast<int>(cdiv(D.Ng, target)) : 1;
-    tch = tch < 16 ? 16 : (tch > kMaxChunk ? kMaxChunk : tch);
+    tch = tch < kMinChunk ? kMinChunk : (tch > kMaxChunk ? kMaxChunk : tch);
     return ChunkPlan{tch, D.Ng > 0 ? static_cast<int>(cdiv(D.Ng, tch)) : 0};
 }
 
@@ -145,8 +157,8 @@ vmoe_status route_bwd_launch(const Dims& D, const void* x, const void* wr, const
     if (D.N == 0) {
         // no tokens: the router gradient is zero (written by the reducer, nch = 0)
         if (dwr && total > 0)
-            route_bwd_reduce_kernel<<<cdiv(total, 256), 256, 0, st>>>(nullptr, dwr, D.E, D.d, 0,
-                                                                       total);
+            route_bwd_reduce_kernel<<<cdiv(total, 32), 256, 0, st>>>(nullptr, dwr, D.E, D.d, 0,
+                                                                      total);
         return launch_status();
     }
     float* partial = dwr ? static_cast<float*>(ws) : nullptr;
@@ -155,8 +167,8 @@ vmoe_status route_bwd_launch(const Dims& D, const void* x, const void* wr, const
     else
         launch_main_e<float>(D, P, x, wr, probs, idx, slot, dgate, dx, partial, st);
     if (dwr)
-        route_bwd_reduce_kernel<<<cdiv(total, 256), 256, 0, st>>>(partial, dwr, D.E, D.d, P.nch,
-                                                                   total);
+        route_bwd_reduce_kernel<<<cdiv(total, 32), 256, 0, st>>>(partial, dwr, D.E, D.d, P.nch,
+                                                                  total);
     return launch_status();
 }
 

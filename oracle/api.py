@@ -160,16 +160,19 @@ def dispatch_bwd(dxe, idx, slot, row_base, n_tokens, C, n_groups=1):
     return dx
 
 
-def ffn_fwd(xe_rows, w1, b1, w2, b2):
-    """One expert over the given rows -> (H, A, ye)."""
+def ffn_fwd(xe_rows, w1, b1, w2, b2, with_grad=False):
+    """One expert over the given rows -> (H, A, ye), or (H, A, G, ye) with
+    G = gelu'(H) when with_grad."""
     xe, w1, b1, w2, b2 = map(_f64, (xe_rows, w1, b1, w2, b2))
     rows, d = xe.shape
     f = w1.shape[0]
     H = np.empty((rows, f))
     A = np.empty((rows, f))
+    G = np.empty((rows, f)) if with_grad else None
     ye = np.empty((rows, d))
-    load().orc_ffn_fwd(rows, d, f, _p(xe), _p(w1), _p(b1), _p(w2), _p(b2), _p(H), _p(A), _p(ye))
-    return H, A, ye
+    load().orc_ffn_fwd(rows, d, f, _p(xe), _p(w1), _p(b1), _p(w2), _p(b2), _p(H), _p(A), _p(G),
+                       _p(ye))
+    return (H, A, G, ye) if with_grad else (H, A, ye)
 
 
 def ffn_bwd_rows(xe_rows, w1, b1, w2, dye_rows):
@@ -248,11 +251,13 @@ def layer(x, w_router, w1, b1, w2, b2, dy, *, k, C, n_groups=1, bias=None, noise
     xe = dispatch(x, r["idx"], r["slot"], r["row_base"], E, C, G)
     H = np.full((E, G * C, f), np.nan)
     A = np.full((E, G * C, f), np.nan)
+    Gd = np.full((E, G * C, f), np.nan)
     ye = np.full((E, G * C, d), np.nan)
     for e in range(E):
         if n_e[e]:
-            H[e, :n_e[e]], A[e, :n_e[e]], ye[e, :n_e[e]] = ffn_fwd(xe[e, :n_e[e]], w1[e], b1[e],
-                                                                   w2[e], b2[e])
+            r_ = slice(0, n_e[e])
+            H[e, r_], A[e, r_], Gd[e, r_], ye[e, r_] = ffn_fwd(xe[e, r_], w1[e], b1[e], w2[e],
+                                                               b2[e], with_grad=True)
     y = combine_fwd(ye, r["idx"], r["slot"], r["row_base"], r["gate"], N, C, G)
     dye, dgate = combine_bwd(dy, ye, r["idx"], r["slot"], r["row_base"], r["gate"], C, G)
     dxe = np.full((E, G * C, d), np.nan)
@@ -269,7 +274,7 @@ def layer(x, w_router, w1, b1, w2, b2, dy, *, k, C, n_groups=1, bias=None, noise
     dx = dispatch_bwd(dxe, r["idx"], r["slot"], r["row_base"], N, C, G)
     dx_total, dwr, dz = route_bwd(x, w_router, r["probs"], r["idx"], r["slot"], dgate, G,
                                   dx_in=dx, want_dwr=want_dwr)
-    r.update(n_e=n_e, xe=xe, H=H, A=A, ye=ye, y=y, dye=dye, dgate=dgate, dxe=dxe, dH=dH,
+    r.update(n_e=n_e, xe=xe, H=H, A=A, Gd=Gd, ye=ye, y=y, dye=dye, dgate=dgate, dxe=dxe, dH=dH,
              dw1=dw1, db1=db1, dw2=dw2, db2=db2, dx_dispatch=dx, dx=dx_total, dw_router=dwr,
              dz=dz)
     return r

@@ -295,11 +295,12 @@ static double gelu_grad(double h) {
 
 /* One expert's MLP over `rows` rows of its buffer:
  *   H[r, j]  = b1[j] + sum_i xe[r, i] * w1[j, i]        (w1: [f, d])
- *   A[r, j]  = gelu(H[r, j])
+ *   A[r, j]  = gelu(H[r, j]),  G[r, j] = gelu'(H[r, j])
  *   ye[r, o] = b2[o] + sum_j A[r, j] * w2[o, j]         (w2: [d, f])
- * H and A may be NULL. */
+ * H, A and G may be NULL. */
 void orc_ffn_fwd(int rows, int d, int f, const double* xe, const double* w1, const double* b1,
-                 const double* w2, const double* b2, double* H, double* A, double* ye) {
+                 const double* w2, const double* b2, double* H, double* A, double* G,
+                 double* ye) {
     double* h = (double*)malloc(sizeof(double) * f);
     double* a = (double*)malloc(sizeof(double) * f);
     for (int r = 0; r < rows; ++r) {
@@ -310,6 +311,7 @@ void orc_ffn_fwd(int rows, int d, int f, const double* xe, const double* w1, con
             a[j] = gelu(acc);
             if (H) H[(size_t)r * f + j] = acc;
             if (A) A[(size_t)r * f + j] = a[j];
+            if (G) G[(size_t)r * f + j] = gelu_grad(acc);
         }
         for (int o = 0; o < d; ++o) {
             double acc = b2[o];

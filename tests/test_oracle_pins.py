@@ -356,3 +356,15 @@ def test_multitask_pool_load_follows_zipf():
     spec.loader.exec_module(mod)
     s = mod.zipf_exponent(W.CONFIGS["multitask17_bf16"])
     assert abs(s - 1.2) < 0.01
+
+
+def test_ffn_forward_saved_gelu_derivative_matches_autograd():
+    rng = np.random.default_rng(4)
+    rows, d, f = 7, 10, 13
+    xe, w1, b1 = rng.standard_normal((rows, d)), rng.standard_normal((f, d)), rng.standard_normal(f)
+    w2, b2 = rng.standard_normal((d, f)), rng.standard_normal(d)
+    H, A, G, ye = oracle.ffn_fwd(xe, w1, b1, w2, b2, with_grad=True)
+    h = torch.tensor(H, requires_grad=True)
+    torch.nn.functional.gelu(h).sum().backward()
+    assert np.allclose(G, h.grad.numpy(), rtol=1e-12, atol=1e-14)
+    assert np.allclose(A, torch.nn.functional.gelu(torch.tensor(H)).numpy(), rtol=1e-12, atol=1e-14)

@@ -117,14 +117,15 @@ def main():
         "route": lambda: L.route(stream=stream),
         "dispatch": lambda: V.vmoe_dispatch(s, L.x, L.expert_idx, L.slot, L.row_base, L.xe,
                                             stream),
-        "ffn_fwd": lambda: V.vmoe_expert_ffn_fwd(s, L.xe, L.counts, L.w1, L.b1, L.w2, L.b2, L.h,
-                                                 L.a, L.ye, stream),
+        "ffn_fwd": lambda: V.vmoe_expert_ffn_fwd(s, L.xe, L.counts, L.w1, L.b1, L.w2, L.b2, L.a,
+                                                 L.a_grad, L.ye, stream),
         "combine_fwd": lambda: V.vmoe_combine_fwd(s, L.ye, L.expert_idx, L.slot, L.row_base,
                                                   L.gate, L.y, stream),
         "combine_bwd": lambda: V.vmoe_combine_bwd(s, L.dy, L.ye, L.expert_idx, L.slot,
                                                   L.row_base, L.gate, L.dye, L.dgate, stream),
-        "ffn_bwd": lambda: V.vmoe_expert_ffn_bwd(s, L.xe, L.counts, L.w1, L.w2, L.h, L.a, L.dye,
-                                                 L.dh, L.dxe, L.dw1, L.db1, L.dw2, L.db2, stream),
+        "ffn_bwd": lambda: V.vmoe_expert_ffn_bwd(s, L.xe, L.counts, L.w1, L.w2, L.a, L.a_grad,
+                                                 L.dye, L.dh, L.dxe, L.dw1, L.db1, L.dw2, L.db2,
+                                                 stream),
         "dispatch_bwd": lambda: V.vmoe_dispatch_bwd(s, L.dxe, L.expert_idx, L.slot, L.row_base,
                                                     L.dx, stream),
         "route_bwd": lambda: V.vmoe_route_bwd(s, L.x, L.w_router, L.probs, L.expert_idx, L.slot,

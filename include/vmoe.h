@@ -136,14 +136,18 @@ vmoe_status vmoe_dispatch(const vmoe_shape* shape, const void* x, const int32_t*
                           const int32_t* slot, const int32_t* row_base, void* xe, void* stream);
 
 /* Expert MLP forward over each expert's n_e packed rows (expertised MLP
- * blocks, paper Sec. 2.1): H = xe W1_e^T + b1_e, A = gelu(H), ye = A W2_e^T + b2_e.
+ * blocks, paper Sec. 2.1): H = xe W1_e^T + b1_e, A = gelu(H), ye = A W2_e^T + b2_e,
+ * with the exact-erf GELU gelu(h) = h Phi(h).
  *   xe [E, G*C, d], counts [G, E] (device; n_e = sum_g counts[g, e])
  *   w1 [E, f, d], b1 [E, f], w2 [E, d, f], b2 [E, d]     (dtype)
- *   h, a [E, G*C, f] out (saved for the backward), ye [E, G*C, d] out.
- * bf16 runs on bf16 matrix cores with f32 accumulation; f32 accumulates in f32. */
+ *   act      [E, G*C, f] out: A = gelu(H)       } saved for the backward;
+ *   act_grad [E, G*C, f] out: gelu'(H)          } H itself is not stored
+ *   ye       [E, G*C, d] out.
+ * bf16 runs on bf16 matrix cores with f32 accumulation (GELU evaluated in f32
+ * to ~1e-7 absolute, then rounded to bf16); f32 accumulates in f32. */
 vmoe_status vmoe_expert_ffn_fwd(const vmoe_shape* shape, const void* xe, const int32_t* counts,
                                 const void* w1, const void* b1, const void* w2, const void* b2,
-                                void* h, void* a, void* ye, void* stream);
+                                void* act, void* act_grad, void* ye, void* stream);
 
 /* Gate-weighted combine: y[t] = sum over kept j (in j order, f32 accumulation)
  * of gate[t,j] * ye[row(t,j)]; 0 for a token with no kept assignment. y [N, d]. */
@@ -160,16 +164,16 @@ vmoe_status vmoe_combine_bwd(const vmoe_shape* shape, const void* dy, const void
                              void* stream);
 
 /* Backward of the expert MLP (adaptation by back-propagation, paper Sec. 3):
- *   dH  = (dye W2_e) * gelu'(h)          dh  [E, G*C, f] out (dtype)
+ *   dH  = (dye W2_e) * act_grad          dh  [E, G*C, f] out (dtype)
  *   dxe = dH W1_e                        dxe [E, G*C, d] out (dtype)
- *   dW2 = dye^T a,  db2 = sum_rows dye   dw2 [E, d, f], db2 [E, d]  f32 out
+ *   dW2 = dye^T act, db2 = sum_rows dye  dw2 [E, d, f], db2 [E, d]  f32 out
  *   dW1 = dH^T xe,  db1 = sum_rows dH    dw1 [E, f, d], db1 [E, f]  f32 out
- * h and a are the forward's saved tensors. Experts with n_e = 0 get zero
- * weight gradients. */
+ * act and act_grad are the forward's saved tensors. Experts with n_e = 0 get
+ * zero weight gradients. */
 vmoe_status vmoe_expert_ffn_bwd(const vmoe_shape* shape, const void* xe, const int32_t* counts,
-                                const void* w1, const void* w2, const void* h, const void* a,
-                                const void* dye, void* dh, void* dxe, float* dw1, float* db1,
-                                float* dw2, float* db2, void* stream);
+                                const void* w1, const void* w2, const void* act,
+                                const void* act_grad, const void* dye, void* dh, void* dxe,
+                                float* dw1, float* db1, float* dw2, float* db2, void* stream);
 
 /* Backward of the dispatch: dx[t] = sum over kept j of dxe[row(t,j)]
  * (f32, overwritten; 0 for a token with no kept assignment). dx [N, d] f32. */

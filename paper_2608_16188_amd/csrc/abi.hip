@@ -24,10 +24,10 @@ vmoe_status dispatch_bwd_launch(const Dims& D, const void* dxe, const int32_t* i
                                 const int32_t* slot, const int32_t* row_base, float* dx,
                                 hipStream_t st);
 vmoe_status ffn_fwd_launch(const Dims& D, const void* xe, const int32_t* counts, const void* w1,
-                           const void* b1, const void* w2, const void* b2, void* h, void* act,
-                           void* ye, hipStream_t st);
+                           const void* b1, const void* w2, const void* b2, void* act,
+                           void* act_grad, void* ye, hipStream_t st);
 vmoe_status ffn_bwd_launch(const Dims& D, const void* xe, const int32_t* counts, const void* w1,
-                           const void* w2, const void* h, const void* act, const void* dye,
+                           const void* w2, const void* act, const void* act_grad, const void* dye,
                            void* dh, void* dxe, float* dw1, float* db1, float* dw2, float* db2,
                            hipStream_t st);
 vmoe_status route_bwd_launch(const Dims& D, const void* x, const void* wr, const float* probs,
@@ -148,12 +148,13 @@ vmoe_status vmoe_dispatch(const vmoe_shape* shape, const void* x, const int32_t*
 
 vmoe_status vmoe_expert_ffn_fwd(const vmoe_shape* shape, const void* xe, const int32_t* counts,
                                 const void* w1, const void* b1, const void* w2, const void* b2,
-                                void* h, void* a, void* ye, void* stream) {
+                                void* act, void* act_grad, void* ye, void* stream) {
     Dims D;
     VMOE_TRY(vmoe::make_dims(shape, &D));
-    VMOE_TRY(need(dev(xe) && dev(counts) && dev(w1) && dev(b1) && dev(w2) && dev(b2) && dev(h) &&
-                  dev(a) && dev(ye)));
-    return vmoe::ffn_fwd_launch(D, xe, counts, w1, b1, w2, b2, h, a, ye, as_stream(stream));
+    VMOE_TRY(need(dev(xe) && dev(counts) && dev(w1) && dev(b1) && dev(w2) && dev(b2) &&
+                  dev(act) && dev(act_grad) && dev(ye)));
+    return vmoe::ffn_fwd_launch(D, xe, counts, w1, b1, w2, b2, act, act_grad, ye,
+                                as_stream(stream));
 }
 
 vmoe_status vmoe_combine_fwd(const vmoe_shape* shape, const void* ye, const int32_t* expert_idx,
@@ -179,15 +180,16 @@ vmoe_status vmoe_combine_bwd(const vmoe_shape* shape, const void* dy, const void
 }
 
 vmoe_status vmoe_expert_ffn_bwd(const vmoe_shape* shape, const void* xe, const int32_t* counts,
-                                const void* w1, const void* w2, const void* h, const void* a,
-                                const void* dye, void* dh, void* dxe, float* dw1, float* db1,
-                                float* dw2, float* db2, void* stream) {
+                                const void* w1, const void* w2, const void* act,
+                                const void* act_grad, const void* dye, void* dh, void* dxe,
+                                float* dw1, float* db1, float* dw2, float* db2, void* stream) {
     Dims D;
     VMOE_TRY(vmoe::make_dims(shape, &D));
-    VMOE_TRY(need(dev(xe) && dev(counts) && dev(w1) && dev(w2) && dev(h) && dev(a) && dev(dye) &&
-                  dev(dh) && dev(dxe) && dev(dw1) && dev(db1) && dev(dw2) && dev(db2)));
-    return vmoe::ffn_bwd_launch(D, xe, counts, w1, w2, h, a, dye, dh, dxe, dw1, db1, dw2, db2,
-                                as_stream(stream));
+    VMOE_TRY(need(dev(xe) && dev(counts) && dev(w1) && dev(w2) && dev(act) && dev(act_grad) &&
+                  dev(dye) && dev(dh) && dev(dxe) && dev(dw1) && dev(db1) && dev(dw2) &&
+                  dev(db2)));
+    return vmoe::ffn_bwd_launch(D, xe, counts, w1, w2, act, act_grad, dye, dh, dxe, dw1, db1,
+                                dw2, db2, as_stream(stream));
 }
 
 vmoe_status vmoe_dispatch_bwd(const vmoe_shape* shape, const void* dxe,

@@ -18,6 +18,8 @@
 //
 // f32 path: a plain LDS-tiled FMA kernel with the same operand and epilogue
 // description (small widths; accuracy path).
+#include <type_traits>
+
 #include "common.h"
 
 namespace vmoe {
@@ -25,6 +27,7 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 enum Epi { EPI_FWD1 = 0, EPI_BIAS = 1, EPI_GELU_GRAD = 2, EPI_STORE = 3, EPI_F32 = 4 };
 
@@ -43,13 +46,13 @@ struct GemmArgs {
     int var_k;              // 0: M = n_e, 1: K = n_e
     const int32_t* counts;  // [G, E]
     int G, E;
-    void* out;              // primary output
-    void* out2;             // EPI_FWD1: activation
+    void* out;              // primary output (EPI_FWD1: gelu(H))
+    void* out2;             // EPI_FWD1: gelu'(H)
     long long out_estride;
     int ldo;
     const void* bias;       // EPI_FWD1 / EPI_BIAS
     long long bias_estride;
-    const void* aux;        // EPI_GELU_GRAD: saved pre-activation H
+    const void* aux;        // EPI_GELU_GRAD: saved gelu'(H)
     float* bsum;            // EPI_F32 (bf16 path): row sums of A per expert, or null
 };
 
@@ -83,37 +86,44 @@ __host__ __device__ constexpr int stage_elems() {
     return KMAJOR ? ROWS * (BK + KPAD) : BK * (ROWS + MNPAD);
 }
 
-// A masked-off vector is still loaded, from the (always valid) operand base,
-// and replaced by zeros in registers: no address ever points off the operand.
-__device__ __forceinline__ uint4 masked_load(const uint16_t* __restrict__ base, size_t off,
-                                             bool ok) {
-    const uint4 v = *reinterpret_cast<const uint4*>(base + (ok ? off : 0));
-    return ok ? v : make_uint4(0, 0, 0, 0);
+typedef int v4i32 __attribute__((ext_vector_type(4)));
+
+// Raw buffer over one expert's operand: loads at byte offsets >= `bytes` return
+// zeros in hardware, which implements every tail mask without a branch.
+constexpr uint32_t kOutOfRange = 0x80000000u;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, long long bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), static_cast<short>(0),
+                                             static_cast<int>(bytes), 0x00020000);
+}
+
+__device__ __forceinline__ uint4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+    const v4i32 v = __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, 0);
+    return make_uint4(v[0], v[1], v[2], v[3]);
 }
 
 // Global -> registers: one ROWS x BK operand stage, ROWS / 32 vectors of 8
 // bf16 per thread, each row segment read by consecutive lanes (coalesced).
 template <int ROWS, bool KMAJOR>
-__device__ __forceinline__ void load_stage(const uint16_t* __restrict__ base, int ld, int mn0,
-                                           int mn_lim, int k0, int k_lim,
-                                           uint4 (&r)[ROWS / 32]) {
+__device__ __forceinline__ void load_stage(__amdgpu_buffer_rsrc_t rs, int ld, int mn0, int mn_lim,
+                                           int k0, int k_lim, uint4 (&r)[ROWS / 32]) {
     const int tid = threadIdx.x;
     if (KMAJOR) {
         const int kc = (tid & 7) * 8;
 #pragma unroll
         for (int j = 0; j < ROWS / 32; ++j) {
-            const int mn = (tid >> 3) + 32 * j;
-            r[j] = masked_load(base, static_cast<size_t>(mn0 + mn) * ld + k0 + kc,
-                               (mn0 + mn < mn_lim) && (k0 + kc < k_lim));
+            const int mn = mn0 + (tid >> 3) + 32 * j;
+            const bool ok = (mn < mn_lim) && (k0 + kc < k_lim);
+            r[j] = buf_load16(rs, ok ? static_cast<uint32_t>(mn * ld + k0 + kc) * 2u : kOutOfRange);
         }
     } else {
         constexpr int VPR = ROWS / 8;  // vectors per k row
-        const int mc = (tid % VPR) * 8;
+        const int mc = mn0 + (tid % VPR) * 8;
 #pragma unroll
         for (int j = 0; j < ROWS / 32; ++j) {
-            const int kr = tid / VPR + (256 / VPR) * j;
-            r[j] = masked_load(base, static_cast<size_t>(k0 + kr) * ld + mn0 + mc,
-                               (k0 + kr < k_lim) && (mn0 + mc < mn_lim));
+            const int kr = k0 + tid / VPR + (256 / VPR) * j;
+            const bool ok = (kr < k_lim) && (mc < mn_lim);
+            r[j] = buf_load16(rs, ok ? static_cast<uint32_t>(kr * ld + mc) * 2u : kOutOfRange);
         }
     }
 }
@@ -146,18 +156,19 @@ __device__ __forceinline__ s16x4 lds_read_tr(const uint16_t* p) {
     return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4)(p));
 }
 
-// MFMA operand fragment for 16 mn values (lane & 15) x 8 k values
-// (k = kstep * 32 + 8 * (lane >> 4) + 0..7).
+// Operand fragment of v_mfma_f32_32x32x16_bf16 for 32 mn values (lane & 31)
+// x 8 k values (k = 16 * kstep + 8 * (lane >> 5) + 0..7).
 template <int ROWS, bool KMAJOR>
 __device__ __forceinline__ bf16x8 read_frag(const uint16_t* s, int blk, int kstep, int lane) {
     if (KMAJOR) {
-        return *reinterpret_cast<const bf16x8*>(s + (blk * 16 + (lane & 15)) * (BK + KPAD) +
-                                                kstep * 32 + (lane >> 4) * 8);
+        return *reinterpret_cast<const bf16x8*>(s + (blk * 32 + (lane & 31)) * (BK + KPAD) +
+                                                kstep * 16 + (lane >> 5) * 8);
     } else {
+        // 16-lane group g covers mn [16 (g & 1), +16) and k [8 (g >> 1), +8)
         constexpr int P = ROWS + MNPAD;
-        const int j = lane & 15;
-        const uint16_t* p0 = s + (kstep * 32 + 8 * (lane >> 4) + (j >> 2)) * P + blk * 16 +
-                             4 * (j & 3);
+        const int g = lane >> 4, j = lane & 15;
+        const uint16_t* p0 = s + (kstep * 16 + 8 * (g >> 1) + (j >> 2)) * P + blk * 32 +
+                             16 * (g & 1) + 4 * (j & 3);
         const s16x4 lo = lds_read_tr(p0);
         const s16x4 hi = lds_read_tr(p0 + 4 * P);
         const s16x8 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
@@ -165,17 +176,79 @@ __device__ __forceinline__ bf16x8 read_frag(const uint16_t* s, int blk, int kste
     }
 }
 
+template <int BM_, int BN_, bool A_KMAJOR, bool B_KMAJOR>
+struct Frags {
+    static constexpr int FM = BM_ / 64, FN = BN_ / 64;  // 32 x 32 blocks per wave
+    bf16x8 a[FM], b[FN];
+    __device__ __forceinline__ void read(const uint16_t* As, const uint16_t* Bs, int wm, int wn,
+                                         int ks, int lane) {
+#pragma unroll
+        for (int i = 0; i < FM; ++i) a[i] = read_frag<BM_, A_KMAJOR>(As, wm * FM + i, ks, lane);
+#pragma unroll
+        for (int j = 0; j < FN; ++j) b[j] = read_frag<BN_, B_KMAJOR>(Bs, wn * FN + j, ks, lane);
+    }
+};
+
+// acc[i][j] += A-block i x B-block j; the operands are swapped inside the
+// MFMA so that register 4q + r of lane l holds C[m = l % 32][n = 8q + 4 (l / 32) + r].
+template <int FM, int FN, typename F>
+__device__ __forceinline__ void mfma_block(f32x16 (&acc)[FM][FN], const F& f) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.b[j], f.a[i], acc[i][j], 0, 0, 0);
+}
+
+// GELU and its derivative from one exponential: with x = |h| / sqrt(2),
+// erf(x) = 1 - t (a1 + t (a2 + t (a3 + t (a4 + t a5)))) exp(-x^2), t = 1 / (1 + p x)
+// (Abramowitz & Stegun 7.1.26, |error| < 1.5e-7), Phi(h) = (1 + sign(h) erf(x)) / 2,
+// gelu(h) = h Phi(h) and gelu'(h) = Phi(h) + h exp(-h^2 / 2) / sqrt(2 pi).
+__device__ __forceinline__ void gelu_pair(float h, float& g, float& dg) {
+    const float x = fabsf(h) * 0.70710678118654752f;
+    const float t = __builtin_amdgcn_rcpf(1.0f + 0.3275911f * x);
+    const float ex = __expf(-x * x);
+    const float poly =
+        t * (0.254829592f + t * (-0.284496736f + t * (1.421413741f + t * (-1.453152027f +
+                                                                           t * 1.061405429f))));
+    const float erf_abs = 1.0f - poly * ex;
+    const float phi_cdf = 0.5f + 0.5f * copysignf(erf_abs, h);
+    g = h * phi_cdf;
+    dg = phi_cdf + h * ex * 0.39894228040143268f;
+}
+
 // One BM x BN output tile of expert e per 256-thread block; four waves in
-// 2 x 2, each (BM/2) x (BN/2) as 16 x 16 MFMA blocks. Blocks are numbered so
+// 2 x 2, each (BM/2) x (BN/2) as 32 x 32 MFMA blocks. Blocks are numbered so
 // that each of the 8 XCDs (blocks b = x mod 8) walks a contiguous range of
 // tiles (n fastest): neighbouring tiles share operand panels in that XCD's L2.
-template <int BM_, int BN_, bool A_KMAJOR, bool B_KMAJOR, int EPI>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+//
+// Pipeline per 64-deep k-stage kt (four 16-deep MFMA steps), one barrier:
+//   issue global loads of stage kt+1 (registers)
+//   steps 0..2: read fragments of step s+1      | MFMAs of step s
+//   store stage kt+1 into the other LDS buffer; barrier
+//   read step-0 fragments of stage kt+1         | MFMAs of step 3
+// so LDS latency always hides behind a run of MFMAs on held fragments.
+//
+// Epilogue: each wave turns its accumulators into output values (bias,
+// GELU + GELU', or GELU' product), parks them in LDS and writes every output
+// row back as full 16-byte-per-lane segments.
+template <int BM_, int BN_, bool A_KMAJOR, bool B_KMAJOR, int EPI, int DIST>
+__global__ __launch_bounds__(256)
+__attribute__((amdgpu_waves_per_eu(BM_ * BN_ >= 256 * 128 ? 1 : 2, BM_ * BN_ >= 256 * 128 ? 1 : 2)))
 void gemm_bf16_kernel(GemmArgs p, int tiles_m, int tiles_n, int per_xcd, int total) {
     constexpr int AE = stage_elems<BM_, A_KMAJOR>();
     constexpr int BE = stage_elems<BN_, B_KMAJOR>();
-    constexpr int FM = BM_ / 32, FN = BN_ / 32;  // 16 x 16 blocks per wave
-    static_assert(EPI != EPI_F32 || (BM_ == 256 && !A_KMAJOR), "row sums assume 256 mn-major rows");
+    constexpr int FM = BM_ / 64, FN = BN_ / 64;
+    constexpr int WM = BM_ / 2, WN = BN_ / 2;  // wave tile
+    constexpr int KSTEPS = BK / 16;
+    constexpr bool F32_OUT = EPI == EPI_F32;
+    constexpr int OUTS = EPI == EPI_FWD1 ? 2 : 1;
+    // per-wave epilogue staging: OUTS tiles of WM rows x (WN + pad) elements
+    constexpr int EP_LD = F32_OUT ? WN + 4 : WN + 8;
+    constexpr int EP_BYTES = OUTS * WM * EP_LD * (F32_OUT ? 4 : 2);
+    static_assert(4 * EP_BYTES <= 2 * (AE + BE) * 2, "epilogue staging exceeds LDS");
+    static_assert(!F32_OUT || !A_KMAJOR, "row sums read an mn-major A tile");
+    static_assert(256 % BM_ == 0, "row sums give each A row 256 / BM threads");
     __shared__ __attribute__((aligned(16))) uint16_t smem[2 * (AE + BE)];
 
     const int b = blockIdx.x;
@@ -192,109 +265,181 @@ void gemm_bf16_kernel(GemmArgs p, int tiles_m, int tiles_n, int per_xcd, int tot
     const int m0 = tm * BM_, n0 = tn * BN_;
     if (m0 >= M) return;
 
-    const uint16_t* A = static_cast<const uint16_t*>(p.a.base) + e * p.a.estride;
-    const uint16_t* B = static_cast<const uint16_t*>(p.b.base) + e * p.b.estride;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const __amdgpu_buffer_rsrc_t ra_rs = make_rsrc(
+        static_cast<const uint16_t*>(p.a.base) + e * p.a.estride, p.a.estride * 2);
+    const __amdgpu_buffer_rsrc_t rb_rs = make_rsrc(
+        static_cast<const uint16_t*>(p.b.base) + e * p.b.estride, p.b.estride * 2);
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
-    // weight-gradient GEMMs: the first n-tile also sums its A rows (bias grad)
-    const bool row_sum = EPI == EPI_F32 && p.bsum != nullptr && tn == 0;
+    // weight-gradient GEMMs: the first n-tile also sums its A rows (bias grad);
+    // thread t adds row t % BM over k slice t / BM of each stage
+    const bool row_sum = F32_OUT && p.bsum != nullptr && tn == 0;
+    constexpr int RS_SPLIT = 256 / BM_;
+    constexpr int RS_K = BK / RS_SPLIT;
     float rsum = 0.0f;
 
-    f32x4 acc[FM][FN];
+    f32x16 acc[FM][FN];
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
-        for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
     const int nk = (K + BK - 1) / BK;
-    uint4 ra[BM_ / 32], rb[BN_ / 32];
-    load_stage<BM_, A_KMAJOR>(A, p.a.ld, m0, M, 0, K, ra);
-    load_stage<BN_, B_KMAJOR>(B, p.b.ld, n0, N, 0, K, rb);
-    store_stage<BM_, A_KMAJOR>(smem, ra);
-    store_stage<BN_, B_KMAJOR>(smem + AE, rb);
-    __syncthreads();
+    uint4 ra0[BM_ / 32], rb0[BN_ / 32], ra1[BM_ / 32], rb1[BN_ / 32];
+    Frags<BM_, BN_, A_KMAJOR, B_KMAJOR> f0, f1;
 
-    for (int kt = 0; kt < nk; ++kt) {
-        uint16_t* As = smem + (kt & 1) * (AE + BE);
-        uint16_t* Bs = As + AE;
-        const bool more = kt + 1 < nk;
-        if (more) {
-            load_stage<BM_, A_KMAJOR>(A, p.a.ld, m0, M, (kt + 1) * BK, K, ra);
-            load_stage<BN_, B_KMAJOR>(B, p.b.ld, n0, N, (kt + 1) * BK, K, rb);
-        }
-        if (!A_KMAJOR && row_sum) {
-            // thread t owns A row m0 + t (BM_ == 256): add its 64 k values
-#pragma unroll 8
-            for (int kk = 0; kk < BK; ++kk)
-                rsum += bf16_to_f32(As[kk * (BM_ + MNPAD) + threadIdx.x]);
-        }
-#pragma unroll
-        for (int ks = 0; ks < BK / 32; ++ks) {
-            bf16x8 af[FM], bfr[FN];
-#pragma unroll
-            for (int i = 0; i < FM; ++i) af[i] = read_frag<BM_, A_KMAJOR>(As, wm * FM + i, ks, lane);
-#pragma unroll
-            for (int j = 0; j < FN; ++j) bfr[j] = read_frag<BN_, B_KMAJOR>(Bs, wn * FN + j, ks, lane);
-#pragma unroll
-            for (int i = 0; i < FM; ++i)
-#pragma unroll
-                for (int j = 0; j < FN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bfr[j], af[i], acc[i][j],
-                                                                        0, 0, 0);
-        }
-        if (more) {
-            uint16_t* An = smem + ((kt + 1) & 1) * (AE + BE);
-            store_stage<BM_, A_KMAJOR>(An, ra);
-            store_stage<BN_, B_KMAJOR>(An + AE, rb);
-        }
-        __syncthreads();
+    load_stage<BM_, A_KMAJOR>(ra_rs, p.a.ld, m0, M, 0, K, ra0);
+    load_stage<BN_, B_KMAJOR>(rb_rs, p.b.ld, n0, N, 0, K, rb0);
+    if constexpr (DIST == 2) {
+        load_stage<BM_, A_KMAJOR>(ra_rs, p.a.ld, m0, M, BK, K, ra1);
+        load_stage<BN_, B_KMAJOR>(rb_rs, p.b.ld, n0, N, BK, K, rb1);
     }
-    if (row_sum && m0 + static_cast<int>(threadIdx.x) < M)
-        p.bsum[static_cast<size_t>(e) * M + m0 + threadIdx.x] = rsum;
+    store_stage<BM_, A_KMAJOR>(smem, ra0);
+    store_stage<BN_, B_KMAJOR>(smem + AE, rb0);
+    __syncthreads();
+    f0.read(smem, smem + AE, wm, wn, 0, lane);
 
-    // Epilogue: lane holds C[m][n .. n+3].
+    // One k-stage. With DIST = 2 the register set PAR receives stage kt + 2
+    // while the other set (stage kt + 1, loaded a stage earlier) goes to LDS.
+    auto stage = [&](const int kt, auto par) {
+        constexpr int PAR = decltype(par)::value;
+        uint4(&la)[BM_ / 32] = (DIST == 1 || PAR == 0) ? ra0 : ra1;
+        uint4(&lb)[BN_ / 32] = (DIST == 1 || PAR == 0) ? rb0 : rb1;
+        uint4(&sa)[BM_ / 32] = (DIST == 1 || PAR == 1) ? ra0 : ra1;
+        uint4(&sb)[BN_ / 32] = (DIST == 1 || PAR == 1) ? rb0 : rb1;
+        uint16_t* As = smem + (kt & 1) * (AE + BE);
+        uint16_t* An = smem + ((kt + 1) & 1) * (AE + BE);
+        load_stage<BM_, A_KMAJOR>(ra_rs, p.a.ld, m0, M, (kt + DIST) * BK, K, la);
+        load_stage<BN_, B_KMAJOR>(rb_rs, p.b.ld, n0, N, (kt + DIST) * BK, K, lb);
+        if constexpr (F32_OUT) {
+            if (row_sum) {
+                const uint16_t* col = As + (tid / BM_) * RS_K * (BM_ + MNPAD) + tid % BM_;
+#pragma unroll 8
+                for (int kk = 0; kk < RS_K; ++kk) rsum += bf16_to_f32(col[kk * (BM_ + MNPAD)]);
+            }
+        }
 #pragma unroll
-    for (int i = 0; i < FM; ++i) {
-        const int m = m0 + (wm * FM + i) * 16 + (lane & 15);
-        if (m >= M) continue;
-#pragma unroll
-        for (int j = 0; j < FN; ++j) {
-            const int n = n0 + (wn * FN + j) * 16 + (lane >> 4) * 4;
-            if (n >= N) continue;
-            const f32x4 v = acc[i][j];
-            const size_t o = e * p.out_estride + static_cast<size_t>(m) * p.ldo + n;
-            if (EPI == EPI_F32) {
-                *reinterpret_cast<float4*>(static_cast<float*>(p.out) + o) =
-                    make_float4(v[0], v[1], v[2], v[3]);
+        for (int s = 0; s < KSTEPS - 1; ++s) {
+            if (s % 2 == 0) {
+                f1.read(As, As + AE, wm, wn, s + 1, lane);
+                __builtin_amdgcn_sched_barrier(0);
+                mfma_block(acc, f0);
             } else {
-                float r[4] = {v[0], v[1], v[2], v[3]};
-                if (EPI == EPI_FWD1 || EPI == EPI_BIAS) {
-                    const uint2 bb = *reinterpret_cast<const uint2*>(
-                        static_cast<const uint16_t*>(p.bias) + e * p.bias_estride + n);
-                    r[0] += bf16_to_f32(bb.x & 0xFFFFu);
-                    r[1] += bf16_to_f32(bb.x >> 16);
-                    r[2] += bf16_to_f32(bb.y & 0xFFFFu);
-                    r[3] += bf16_to_f32(bb.y >> 16);
-                }
-                if (EPI == EPI_GELU_GRAD) {
-                    const uint2 hh =
-                        *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(p.aux) + o);
-                    r[0] *= gelu_grad_f(bf16_to_f32(hh.x & 0xFFFFu));
-                    r[1] *= gelu_grad_f(bf16_to_f32(hh.x >> 16));
-                    r[2] *= gelu_grad_f(bf16_to_f32(hh.y & 0xFFFFu));
-                    r[3] *= gelu_grad_f(bf16_to_f32(hh.y >> 16));
-                }
-                uint2 w2;
-                w2.x = pack_bf16x2(r[0], r[1]);
-                w2.y = pack_bf16x2(r[2], r[3]);
-                *reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.out) + o) = w2;
-                if (EPI == EPI_FWD1) {
-                    uint2 a;
-                    a.x = pack_bf16x2(gelu_f(r[0]), gelu_f(r[1]));
-                    a.y = pack_bf16x2(gelu_f(r[2]), gelu_f(r[3]));
-                    *reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.out2) + o) = a;
+                f0.read(As, As + AE, wm, wn, s + 1, lane);
+                __builtin_amdgcn_sched_barrier(0);
+                mfma_block(acc, f1);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        store_stage<BM_, A_KMAJOR>(An, sa);
+        store_stage<BN_, B_KMAJOR>(An + AE, sb);
+        __syncthreads();
+        // KSTEPS is even: the last step's fragments are in f1
+        f0.read(An, An + AE, wm, wn, 0, lane);
+        __builtin_amdgcn_sched_barrier(0);
+        mfma_block(acc, f1);
+        __builtin_amdgcn_sched_barrier(0);
+    };
+    for (int kt = 0; kt < nk; kt += 2) {
+        stage(kt, std::integral_constant<int, 0>{});
+        if (kt + 1 < nk) stage(kt + 1, std::integral_constant<int, 1>{});
+    }
+    __syncthreads();  // every wave is done with the operand stages
+
+    if constexpr (F32_OUT) {
+        if (row_sum) {  // uniform per block
+            float* part = reinterpret_cast<float*>(smem);
+            part[tid] = rsum;
+            __syncthreads();
+            if (tid < BM_ && m0 + tid < M) {
+                float t = part[tid];
+#pragma unroll
+                for (int q = 1; q < RS_SPLIT; ++q) t += part[tid + q * BM_];
+                p.bsum[static_cast<size_t>(e) * M + m0 + tid] = t;
+            }
+            __syncthreads();
+        }
+    }
+
+    // Epilogue stage 1: values into this wave's LDS tiles. Register 4q + r of
+    // lane l holds C[m][n + r] with m = 32 i + l % 32, n = 32 j + 8 q + 4 (l / 32)
+    // inside the wave tile.
+    char* ep = reinterpret_cast<char*>(smem) + wave * EP_BYTES;
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int ml = i * 32 + (lane & 31);
+                const int nl = j * 32 + 8 * q + 4 * (lane >> 5);
+                const f32x16& v = acc[i][j];
+                float r[4] = {v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]};
+                if constexpr (F32_OUT) {
+                    *reinterpret_cast<float4*>(reinterpret_cast<float*>(ep) + ml * EP_LD + nl) =
+                        make_float4(r[0], r[1], r[2], r[3]);
+                } else {
+                    const int n = n0 + wn * WN + nl;
+                    const int m = m0 + wm * WM + ml;
+                    if constexpr (EPI == EPI_FWD1 || EPI == EPI_BIAS) {
+                        if (n < N) {
+                            const uint2 bb = *reinterpret_cast<const uint2*>(
+                                static_cast<const uint16_t*>(p.bias) + e * p.bias_estride + n);
+                            r[0] += bf16_to_f32(bb.x & 0xFFFFu);
+                            r[1] += bf16_to_f32(bb.x >> 16);
+                            r[2] += bf16_to_f32(bb.y & 0xFFFFu);
+                            r[3] += bf16_to_f32(bb.y >> 16);
+                        }
+                    }
+                    if constexpr (EPI == EPI_GELU_GRAD) {
+                        if (n < N && m < M) {
+                            const uint2 gg = *reinterpret_cast<const uint2*>(
+                                static_cast<const uint16_t*>(p.aux) + e * p.out_estride +
+                                static_cast<size_t>(m) * p.ldo + n);
+                            r[0] *= bf16_to_f32(gg.x & 0xFFFFu);
+                            r[1] *= bf16_to_f32(gg.x >> 16);
+                            r[2] *= bf16_to_f32(gg.y & 0xFFFFu);
+                            r[3] *= bf16_to_f32(gg.y >> 16);
+                        }
+                    }
+                    uint16_t* t0 = reinterpret_cast<uint16_t*>(ep) + ml * EP_LD + nl;
+                    if constexpr (EPI == EPI_FWD1) {
+                        float g[4], dg[4];
+#pragma unroll
+                        for (int c = 0; c < 4; ++c) gelu_pair(r[c], g[c], dg[c]);
+                        *reinterpret_cast<uint2*>(t0) =
+                            make_uint2(pack_bf16x2(g[0], g[1]), pack_bf16x2(g[2], g[3]));
+                        *reinterpret_cast<uint2*>(t0 + WM * EP_LD) =
+                            make_uint2(pack_bf16x2(dg[0], dg[1]), pack_bf16x2(dg[2], dg[3]));
+                    } else {
+                        *reinterpret_cast<uint2*>(t0) =
+                            make_uint2(pack_bf16x2(r[0], r[1]), pack_bf16x2(r[2], r[3]));
+                    }
                 }
             }
+    __syncthreads();
+
+    // Epilogue stage 2: rows of the wave tile out in 16-byte segments.
+    constexpr int ELEM = F32_OUT ? 4 : 2;
+    constexpr int SEG = 16 / ELEM;                 // elements per 16-byte segment
+    constexpr int LANES_PER_ROW = WN / SEG;        // 8 (bf16) or 16 (f32)
+    constexpr int ROWS_PER_PASS = 64 / LANES_PER_ROW;
+    const int cl = (lane % LANES_PER_ROW) * SEG;
+    const int n = n0 + wn * WN + cl;
+#pragma unroll
+    for (int o = 0; o < OUTS; ++o) {
+        char* dst_base = static_cast<char*>(o == 0 ? p.out : p.out2);
+#pragma unroll
+        for (int pass = 0; pass < WM / ROWS_PER_PASS; ++pass) {
+            const int ml = pass * ROWS_PER_PASS + lane / LANES_PER_ROW;
+            const int m = m0 + wm * WM + ml;
+            const uint4 v = *reinterpret_cast<const uint4*>(ep + (o * WM * EP_LD + ml * EP_LD + cl) * ELEM);
+            if (m < M && n < N)
+                *reinterpret_cast<uint4*>(dst_base + (e * p.out_estride +
+                                                      static_cast<size_t>(m) * p.ldo + n) * ELEM) = v;
         }
     }
 }
@@ -352,9 +497,13 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs p) {
             float* out = static_cast<float*>(p.out);
             if (EPI == EPI_FWD1 || EPI == EPI_BIAS)
                 v += static_cast<const float*>(p.bias)[e * p.bias_estride + n];
-            if (EPI == EPI_GELU_GRAD) v *= gelu_grad_f(static_cast<const float*>(p.aux)[o]);
-            out[o] = v;
-            if (EPI == EPI_FWD1) static_cast<float*>(p.out2)[o] = gelu_f(v);
+            if (EPI == EPI_GELU_GRAD) v *= static_cast<const float*>(p.aux)[o];
+            if (EPI == EPI_FWD1) {
+                out[o] = gelu_f(v);
+                static_cast<float*>(p.out2)[o] = gelu_grad_f(v);
+            } else {
+                out[o] = v;
+            }
         }
     }
 }
@@ -385,27 +534,20 @@ __global__ __launch_bounds__(256) void colsum_kernel(const T* __restrict__ src,
                                                   part[2][c & 63]) + part[3][c & 63];
 }
 
-template <int BM_, int BN_, bool AK, bool BK_, int EPI>
+template <int BM_, int BN_, bool AK, bool BK_, int EPI, int DIST = 1>
 void launch_bf16(const Dims& D, const GemmArgs& a, int grid_m_rows, hipStream_t st) {
     const int tiles_m = static_cast<int>(cdiv(grid_m_rows, BM_));
     const int tiles_n = static_cast<int>(cdiv(a.N, BN_));
     const int total = D.E * tiles_m * tiles_n;
     const int per_xcd = static_cast<int>(cdiv(total, 8));
-    gemm_bf16_kernel<BM_, BN_, AK, BK_, EPI><<<8 * per_xcd, 256, 0, st>>>(a, tiles_m, tiles_n,
-                                                                         per_xcd, total);
+    gemm_bf16_kernel<BM_, BN_, AK, BK_, EPI, DIST><<<8 * per_xcd, 256, 0, st>>>(
+        a, tiles_m, tiles_n, per_xcd, total);
 }
 
 template <bool AK, bool BK_, int EPI>
 void launch_gemm(const Dims& D, const GemmArgs& a, int grid_m_rows, hipStream_t st) {
     if (D.dtype == VMOE_BF16) {
-        if constexpr (EPI == EPI_F32) {
-            launch_bf16<256, 128, AK, BK_, EPI>(D, a, grid_m_rows, st);
-        } else {
-            if (a.N >= 2048)
-                launch_bf16<256, 256, AK, BK_, EPI>(D, a, grid_m_rows, st);
-            else
-                launch_bf16<256, 128, AK, BK_, EPI>(D, a, grid_m_rows, st);
-        }
+        launch_bf16<128, 128, AK, BK_, EPI>(D, a, grid_m_rows, st);
     } else {
         dim3 grid(cdiv(a.N, FT), cdiv(grid_m_rows, FT), D.E);
         gemm_f32_kernel<AK, BK_, EPI><<<grid, 256, 0, st>>>(a);
@@ -425,19 +567,19 @@ size_t esize(const Dims& D) { return D.dtype == VMOE_BF16 ? 2 : 4; }
 }  // namespace
 
 vmoe_status ffn_fwd_launch(const Dims& D, const void* xe, const int32_t* counts, const void* w1,
-                           const void* b1, const void* w2, const void* b2, void* h, void* act,
-                           void* ye, hipStream_t st) {
+                           const void* b1, const void* w2, const void* b2, void* act,
+                           void* act_grad, void* ye, hipStream_t st) {
     const long long rows = D.rows_per_expert();
     if (rows == 0 || D.E == 0) return VMOE_OK;
-    // H = xe W1^T + b1, A = gelu(H)
+    // H = xe W1^T + b1 (never stored), A = gelu(H), A' = gelu'(H)
     GemmArgs g1 = base_args(D, counts);
     g1.a = Operand{xe, rows * D.d, D.d};
     g1.b = Operand{w1, static_cast<long long>(D.f) * D.d, D.d};
     g1.M = static_cast<int>(rows);
     g1.N = D.f;
     g1.K = D.d;
-    g1.out = h;
-    g1.out2 = act;
+    g1.out = act;
+    g1.out2 = act_grad;
     g1.out_estride = rows * D.f;
     g1.ldo = D.f;
     g1.bias = b1;
@@ -460,13 +602,13 @@ vmoe_status ffn_fwd_launch(const Dims& D, const void* xe, const int32_t* counts,
 }
 
 vmoe_status ffn_bwd_launch(const Dims& D, const void* xe, const int32_t* counts, const void* w1,
-                           const void* w2, const void* h, const void* act, const void* dye,
+                           const void* w2, const void* act, const void* act_grad, const void* dye,
                            void* dh, void* dxe, float* dw1, float* db1, float* dw2, float* db2,
                            hipStream_t st) {
     const long long rows = D.rows_per_expert();
     if (D.E == 0) return VMOE_OK;
     if (rows > 0) {
-        // dH = (dye W2) * gelu'(H): W2 [d, f] read with k = d strided (mn-major)
+        // dH = (dye W2) * A': W2 [d, f] read with k = d strided (mn-major)
         GemmArgs g = base_args(D, counts);
         g.a = Operand{dye, rows * D.d, D.d};
         g.b = Operand{w2, static_cast<long long>(D.d) * D.f, D.f};
@@ -476,7 +618,7 @@ vmoe_status ffn_bwd_launch(const Dims& D, const void* xe, const int32_t* counts,
         g.out = dh;
         g.out_estride = rows * D.f;
         g.ldo = D.f;
-        g.aux = h;
+        g.aux = act_grad;
         launch_gemm<true, false, EPI_GELU_GRAD>(D, g, static_cast<int>(rows), st);
         // dxe = dH W1: W1 [f, d] read with k = f strided
         GemmArgs x = base_args(D, counts);

@@ -73,8 +73,8 @@ class LayerBuffers:
                                     dtype=torch.uint8, device=dev)
         # expert buffers
         self.xe = torch.empty(E, R, d, dtype=act, device=dev)
-        self.h = torch.empty(E, R, f, dtype=act, device=dev)
-        self.a = torch.empty(E, R, f, dtype=act, device=dev)
+        self.a = torch.empty(E, R, f, dtype=act, device=dev)       # gelu(H)
+        self.a_grad = torch.empty(E, R, f, dtype=act, device=dev)  # gelu'(H)
         self.ye = torch.empty(E, R, d, dtype=act, device=dev)
         self.y = torch.empty(N, d, dtype=act, device=dev)
         # backward
@@ -103,8 +103,8 @@ class LayerBuffers:
         s = self.shape
         self.route(logits_in, stream)
         V.vmoe_dispatch(s, self.x, self.expert_idx, self.slot, self.row_base, self.xe, stream)
-        V.vmoe_expert_ffn_fwd(s, self.xe, self.counts, self.w1, self.b1, self.w2, self.b2, self.h,
-                              self.a, self.ye, stream)
+        V.vmoe_expert_ffn_fwd(s, self.xe, self.counts, self.w1, self.b1, self.w2, self.b2, self.a,
+                              self.a_grad, self.ye, stream)
         V.vmoe_combine_fwd(s, self.ye, self.expert_idx, self.slot, self.row_base, self.gate,
                            self.y, stream)
 
@@ -112,8 +112,9 @@ class LayerBuffers:
         s = self.shape
         V.vmoe_combine_bwd(s, self.dy, self.ye, self.expert_idx, self.slot, self.row_base,
                            self.gate, self.dye, self.dgate, stream)
-        V.vmoe_expert_ffn_bwd(s, self.xe, self.counts, self.w1, self.w2, self.h, self.a, self.dye,
-                              self.dh, self.dxe, self.dw1, self.db1, self.dw2, self.db2, stream)
+        V.vmoe_expert_ffn_bwd(s, self.xe, self.counts, self.w1, self.w2, self.a, self.a_grad,
+                              self.dye, self.dh, self.dxe, self.dw1, self.db1, self.dw2, self.db2,
+                              stream)
         V.vmoe_dispatch_bwd(s, self.dxe, self.expert_idx, self.slot, self.row_base, self.dx,
                             stream)
         V.vmoe_route_bwd(s, self.x, self.w_router, self.probs, self.expert_idx, self.slot,

@@ -136,10 +136,10 @@ def vmoe_dispatch(shape, x, expert_idx, slot, row_base, xe, stream=None):
         _stream(stream)))
 
 
-def vmoe_expert_ffn_fwd(shape, xe, counts, w1, b1, w2, b2, h, a, ye, stream=None):
+def vmoe_expert_ffn_fwd(shape, xe, counts, w1, b1, w2, b2, act, act_grad, ye, stream=None):
     _check("vmoe_expert_ffn_fwd", _lib.vmoe_expert_ffn_fwd(
         ctypes.byref(shape), _ptr(xe), _ptr(counts), _ptr(w1), _ptr(b1), _ptr(w2), _ptr(b2),
-        _ptr(h), _ptr(a), _ptr(ye), _stream(stream)))
+        _ptr(act), _ptr(act_grad), _ptr(ye), _stream(stream)))
 
 
 def vmoe_combine_fwd(shape, ye, expert_idx, slot, row_base, gate, y, stream=None):
@@ -154,10 +154,11 @@ def vmoe_combine_bwd(shape, dy, ye, expert_idx, slot, row_base, gate, dye, dgate
         _ptr(gate), _ptr(dye), _ptr(dgate), _stream(stream)))
 
 
-def vmoe_expert_ffn_bwd(shape, xe, counts, w1, w2, h, a, dye, dh, dxe, dw1, db1, dw2, db2,
-                        stream=None):
+def vmoe_expert_ffn_bwd(shape, xe, counts, w1, w2, act, act_grad, dye, dh, dxe, dw1, db1, dw2,
+                        db2, stream=None):
     _check("vmoe_expert_ffn_bwd", _lib.vmoe_expert_ffn_bwd(
-        ctypes.byref(shape), _ptr(xe), _ptr(counts), _ptr(w1), _ptr(w2), _ptr(h), _ptr(a),
+        ctypes.byref(shape), _ptr(xe), _ptr(counts), _ptr(w1), _ptr(w2), _ptr(act),
+        _ptr(act_grad),
         _ptr(dye), _ptr(dh), _ptr(dxe), _ptr(dw1), _ptr(db1), _ptr(dw2), _ptr(db2),
         _stream(stream)))
 

@@ -177,13 +177,13 @@ def test_layer_small_every_element(cfg):
     _compare_routing(got_r, ref, cfg.name)
     n_e = ref["n_e"]
     dt = cfg.dtype
-    xe, h, a, ye = (_f64_out(t, dt) for t in (L.xe, L.h, L.a, L.ye))
+    xe, a, ag, ye = (_f64_out(t, dt) for t in (L.xe, L.a, L.a_grad, L.ye))
     dye, dh, dxe = (_f64_out(t, dt) for t in (L.dye, L.dh, L.dxe))
     for e in range(cfg.n_experts):
         r = slice(0, n_e[e])
         assert np.array_equal(xe[e, r], ref["xe"][e, r]), "dispatch not exact"
-        assert_close(f"H[{e}]", h[e, r], ref["H"][e, r], tol)
         assert_close(f"A[{e}]", a[e, r], ref["A"][e, r], tol)
+        assert_close(f"A'[{e}]", ag[e, r], ref["Gd"][e, r], tol)
         assert_close(f"ye[{e}]", ye[e, r], ref["ye"][e, r], tol)
         assert_close(f"dye[{e}]", dye[e, r], ref["dye"][e, r], tol)
         assert_close(f"dH[{e}]", dh[e, r], ref["dH"][e, r], tol)

@@ -75,7 +75,9 @@ __device__ __forceinline__ float gelu_grad_f(float h) {
 
 constexpr int BK = 64;          // k depth of one LDS stage
 constexpr int KPAD = 8;         // k-major rows: 64 + 8 bf16 = 144 B pitch
-constexpr int MNPAD = 16;       // mn-major rows: ROWS + 16 bf16 (conflict-free transpose reads)
+// mn-major rows: ROWS + 32 bf16, a pitch of 16 (mod 64) dwords, so the two
+// 16-lane groups of a transpose read (4 rows x 32 B each) hit disjoint banks
+constexpr int MNPAD = 32;
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef short s16x8 __attribute__((ext_vector_type(8)));
@@ -102,17 +104,17 @@ __device__ __forceinline__ uint4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t b
     return make_uint4(v[0], v[1], v[2], v[3]);
 }
 
-// Global -> registers: one ROWS x BK operand stage, ROWS / 32 vectors of 8
-// bf16 per thread, each row segment read by consecutive lanes (coalesced).
-template <int ROWS, bool KMAJOR>
+// Global -> registers: one ROWS x BK operand stage, ROWS * 8 / NT vectors of
+// 8 bf16 per thread, each row segment read by consecutive lanes (coalesced).
+template <int ROWS, bool KMAJOR, int NT>
 __device__ __forceinline__ void load_stage(__amdgpu_buffer_rsrc_t rs, int ld, int mn0, int mn_lim,
-                                           int k0, int k_lim, uint4 (&r)[ROWS / 32]) {
+                                           int k0, int k_lim, uint4 (&r)[ROWS * 8 / NT]) {
     const int tid = threadIdx.x;
     if (KMAJOR) {
         const int kc = (tid & 7) * 8;
 #pragma unroll
-        for (int j = 0; j < ROWS / 32; ++j) {
-            const int mn = mn0 + (tid >> 3) + 32 * j;
+        for (int j = 0; j < ROWS * 8 / NT; ++j) {
+            const int mn = mn0 + (tid >> 3) + (NT / 8) * j;
             const bool ok = (mn < mn_lim) && (k0 + kc < k_lim);
             r[j] = buf_load16(rs, ok ? static_cast<uint32_t>(mn * ld + k0 + kc) * 2u : kOutOfRange);
         }
@@ -120,8 +122,8 @@ __device__ __forceinline__ void load_stage(__amdgpu_buffer_rsrc_t rs, int ld, in
         constexpr int VPR = ROWS / 8;  // vectors per k row
         const int mc = mn0 + (tid % VPR) * 8;
 #pragma unroll
-        for (int j = 0; j < ROWS / 32; ++j) {
-            const int kr = k0 + tid / VPR + (256 / VPR) * j;
+        for (int j = 0; j < ROWS * 8 / NT; ++j) {
+            const int kr = k0 + tid / VPR + (NT / VPR) * j;
             const bool ok = (kr < k_lim) && (mc < mn_lim);
             r[j] = buf_load16(rs, ok ? static_cast<uint32_t>(kr * ld + mc) * 2u : kOutOfRange);
         }
@@ -129,20 +131,20 @@ __device__ __forceinline__ void load_stage(__amdgpu_buffer_rsrc_t rs, int ld, in
 }
 
 // Registers -> LDS, same element placement as the global tile (no transpose).
-template <int ROWS, bool KMAJOR>
-__device__ __forceinline__ void store_stage(uint16_t* s, const uint4 (&r)[ROWS / 32]) {
+template <int ROWS, bool KMAJOR, int NT>
+__device__ __forceinline__ void store_stage(uint16_t* s, const uint4 (&r)[ROWS * 8 / NT]) {
     const int tid = threadIdx.x;
     if (KMAJOR) {
         const int kc = (tid & 7) * 8;
 #pragma unroll
-        for (int j = 0; j < ROWS / 32; ++j)
-            *reinterpret_cast<uint4*>(s + ((tid >> 3) + 32 * j) * (BK + KPAD) + kc) = r[j];
+        for (int j = 0; j < ROWS * 8 / NT; ++j)
+            *reinterpret_cast<uint4*>(s + ((tid >> 3) + (NT / 8) * j) * (BK + KPAD) + kc) = r[j];
     } else {
         constexpr int VPR = ROWS / 8;
         const int mc = (tid % VPR) * 8;
 #pragma unroll
-        for (int j = 0; j < ROWS / 32; ++j)
-            *reinterpret_cast<uint4*>(s + (tid / VPR + (256 / VPR) * j) * (ROWS + MNPAD) + mc) =
+        for (int j = 0; j < ROWS * 8 / NT; ++j)
+            *reinterpret_cast<uint4*>(s + (tid / VPR + (NT / VPR) * j) * (ROWS + MNPAD) + mc) =
                 r[j];
     }
 }
@@ -176,9 +178,9 @@ __device__ __forceinline__ bf16x8 read_frag(const uint16_t* s, int blk, int kste
     }
 }
 
-template <int BM_, int BN_, bool A_KMAJOR, bool B_KMAJOR>
+template <int BM_, int BN_, int WGM, int WGN, bool A_KMAJOR, bool B_KMAJOR>
 struct Frags {
-    static constexpr int FM = BM_ / 64, FN = BN_ / 64;  // 32 x 32 blocks per wave
+    static constexpr int FM = BM_ / WGM / 32, FN = BN_ / WGN / 32;  // 32 x 32 blocks per wave
     bf16x8 a[FM], b[FN];
     __device__ __forceinline__ void read(const uint16_t* As, const uint16_t* Bs, int wm, int wn,
                                          int ks, int lane) {
@@ -217,10 +219,10 @@ __device__ __forceinline__ void gelu_pair(float h, float& g, float& dg) {
     dg = phi_cdf + h * ex * 0.39894228040143268f;
 }
 
-// One BM x BN output tile of expert e per 256-thread block; four waves in
-// 2 x 2, each (BM/2) x (BN/2) as 32 x 32 MFMA blocks. Blocks are numbered so
-// that each of the 8 XCDs (blocks b = x mod 8) walks a contiguous range of
-// tiles (n fastest): neighbouring tiles share operand panels in that XCD's L2.
+// One BM x BN output tile of expert e per block of WGM x WGN waves, each
+// (BM/WGM) x (BN/WGN) as 32 x 32 MFMA blocks. Blocks are numbered so that each
+// of the 8 XCDs (blocks b = x mod 8) walks a contiguous range of tiles (n
+// fastest): neighbouring tiles share operand panels in that XCD's L2.
 //
 // Pipeline per 64-deep k-stage kt (four 16-deep MFMA steps), one barrier:
 //   issue global loads of stage kt+1 (registers)
@@ -231,25 +233,32 @@ __device__ __forceinline__ void gelu_pair(float h, float& g, float& dg) {
 //
 // Epilogue: each wave turns its accumulators into output values (bias,
 // GELU + GELU', or GELU' product), parks them in LDS and writes every output
-// row back as full 16-byte-per-lane segments.
-template <int BM_, int BN_, bool A_KMAJOR, bool B_KMAJOR, int EPI, int DIST>
-__global__ __launch_bounds__(256)
-__attribute__((amdgpu_waves_per_eu(BM_ * BN_ >= 256 * 128 ? 1 : 2, BM_ * BN_ >= 256 * 128 ? 1 : 2)))
+// row back as full 16-byte-per-lane segments (one output at a time when two
+// do not fit in LDS together).
+template <int BM_, int BN_, int WGM, int WGN, bool A_KMAJOR, bool B_KMAJOR, int EPI, int DIST>
+__global__ __launch_bounds__(64 * WGM * WGN)
+__attribute__((amdgpu_waves_per_eu(WGM * WGN == 8 || BM_ * BN_ < 256 * 128 ? 2 : 1,
+                                   WGM * WGN == 8 || BM_ * BN_ < 256 * 128 ? 2 : 1)))
 void gemm_bf16_kernel(GemmArgs p, int tiles_m, int tiles_n, int per_xcd, int total) {
+    constexpr int NT = 64 * WGM * WGN;
     constexpr int AE = stage_elems<BM_, A_KMAJOR>();
     constexpr int BE = stage_elems<BN_, B_KMAJOR>();
-    constexpr int FM = BM_ / 64, FN = BN_ / 64;
-    constexpr int WM = BM_ / 2, WN = BN_ / 2;  // wave tile
+    constexpr int WM = BM_ / WGM, WN = BN_ / WGN;  // wave tile
+    constexpr int FM = WM / 32, FN = WN / 32;
     constexpr int KSTEPS = BK / 16;
+    constexpr int VA = BM_ * 8 / NT, VB = BN_ * 8 / NT;  // staged vectors per thread
     constexpr bool F32_OUT = EPI == EPI_F32;
     constexpr int OUTS = EPI == EPI_FWD1 ? 2 : 1;
-    // per-wave epilogue staging: OUTS tiles of WM rows x (WN + pad) elements
+    constexpr int SMEM_ELEMS = 2 * (AE + BE);
+    // per-wave epilogue staging: WM rows x (WN + pad) elements per output
     constexpr int EP_LD = F32_OUT ? WN + 4 : WN + 8;
-    constexpr int EP_BYTES = OUTS * WM * EP_LD * (F32_OUT ? 4 : 2);
-    static_assert(4 * EP_BYTES <= 2 * (AE + BE) * 2, "epilogue staging exceeds LDS");
+    constexpr int EP_TILE = WM * EP_LD * (F32_OUT ? 4 : 2);
+    constexpr int EP_OUTS_AT_ONCE = (OUTS * EP_TILE * WGM * WGN <= SMEM_ELEMS * 2) ? OUTS : 1;
+    static_assert(EP_TILE * WGM * WGN <= SMEM_ELEMS * 2, "epilogue staging exceeds LDS");
     static_assert(!F32_OUT || !A_KMAJOR, "row sums read an mn-major A tile");
-    static_assert(256 % BM_ == 0, "row sums give each A row 256 / BM threads");
-    __shared__ __attribute__((aligned(16))) uint16_t smem[2 * (AE + BE)];
+    static_assert(NT % BM_ == 0 || !F32_OUT, "row sums give each A row NT / BM threads");
+    static_assert(WM % 32 == 0 && WN % 32 == 0 && VA >= 1 && VB >= 1, "tile shape");
+    __shared__ __attribute__((aligned(16))) uint16_t smem[SMEM_ELEMS];
 
     const int b = blockIdx.x;
     const int w = (b & 7) * per_xcd + (b >> 3);
@@ -271,11 +280,11 @@ void gemm_bf16_kernel(GemmArgs p, int tiles_m, int tiles_n, int per_xcd, int tot
         static_cast<const uint16_t*>(p.b.base) + e * p.b.estride, p.b.estride * 2);
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave / WGN, wn = wave % WGN;
     // weight-gradient GEMMs: the first n-tile also sums its A rows (bias grad);
     // thread t adds row t % BM over k slice t / BM of each stage
     const bool row_sum = F32_OUT && p.bsum != nullptr && tn == 0;
-    constexpr int RS_SPLIT = 256 / BM_;
+    constexpr int RS_SPLIT = F32_OUT ? NT / BM_ : 1;
     constexpr int RS_K = BK / RS_SPLIT;
     float rsum = 0.0f;
 
@@ -288,17 +297,17 @@ void gemm_bf16_kernel(GemmArgs p, int tiles_m, int tiles_n, int per_xcd, int tot
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
     const int nk = (K + BK - 1) / BK;
-    uint4 ra0[BM_ / 32], rb0[BN_ / 32], ra1[BM_ / 32], rb1[BN_ / 32];
-    Frags<BM_, BN_, A_KMAJOR, B_KMAJOR> f0, f1;
+    uint4 ra0[VA], rb0[VB], ra1[VA], rb1[VB];
+    Frags<BM_, BN_, WGM, WGN, A_KMAJOR, B_KMAJOR> f0, f1;
 
-    load_stage<BM_, A_KMAJOR>(ra_rs, p.a.ld, m0, M, 0, K, ra0);
-    load_stage<BN_, B_KMAJOR>(rb_rs, p.b.ld, n0, N, 0, K, rb0);
+    load_stage<BM_, A_KMAJOR, NT>(ra_rs, p.a.ld, m0, M, 0, K, ra0);
+    load_stage<BN_, B_KMAJOR, NT>(rb_rs, p.b.ld, n0, N, 0, K, rb0);
     if constexpr (DIST == 2) {
-        load_stage<BM_, A_KMAJOR>(ra_rs, p.a.ld, m0, M, BK, K, ra1);
-        load_stage<BN_, B_KMAJOR>(rb_rs, p.b.ld, n0, N, BK, K, rb1);
+        load_stage<BM_, A_KMAJOR, NT>(ra_rs, p.a.ld, m0, M, BK, K, ra1);
+        load_stage<BN_, B_KMAJOR, NT>(rb_rs, p.b.ld, n0, N, BK, K, rb1);
     }
-    store_stage<BM_, A_KMAJOR>(smem, ra0);
-    store_stage<BN_, B_KMAJOR>(smem + AE, rb0);
+    store_stage<BM_, A_KMAJOR, NT>(smem, ra0);
+    store_stage<BN_, B_KMAJOR, NT>(smem + AE, rb0);
     __syncthreads();
     f0.read(smem, smem + AE, wm, wn, 0, lane);
 
@@ -306,14 +315,14 @@ void gemm_bf16_kernel(GemmArgs p, int tiles_m, int tiles_n, int per_xcd, int tot
     // while the other set (stage kt + 1, loaded a stage earlier) goes to LDS.
     auto stage = [&](const int kt, auto par) {
         constexpr int PAR = decltype(par)::value;
-        uint4(&la)[BM_ / 32] = (DIST == 1 || PAR == 0) ? ra0 : ra1;
-        uint4(&lb)[BN_ / 32] = (DIST == 1 || PAR == 0) ? rb0 : rb1;
-        uint4(&sa)[BM_ / 32] = (DIST == 1 || PAR == 1) ? ra0 : ra1;
-        uint4(&sb)[BN_ / 32] = (DIST == 1 || PAR == 1) ? rb0 : rb1;
+        uint4(&la)[VA] = (DIST == 1 || PAR == 0) ? ra0 : ra1;
+        uint4(&lb)[VB] = (DIST == 1 || PAR == 0) ? rb0 : rb1;
+        uint4(&sa)[VA] = (DIST == 1 || PAR == 1) ? ra0 : ra1;
+        uint4(&sb)[VB] = (DIST == 1 || PAR == 1) ? rb0 : rb1;
         uint16_t* As = smem + (kt & 1) * (AE + BE);
         uint16_t* An = smem + ((kt + 1) & 1) * (AE + BE);
-        load_stage<BM_, A_KMAJOR>(ra_rs, p.a.ld, m0, M, (kt + DIST) * BK, K, la);
-        load_stage<BN_, B_KMAJOR>(rb_rs, p.b.ld, n0, N, (kt + DIST) * BK, K, lb);
+        load_stage<BM_, A_KMAJOR, NT>(ra_rs, p.a.ld, m0, M, (kt + DIST) * BK, K, la);
+        load_stage<BN_, B_KMAJOR, NT>(rb_rs, p.b.ld, n0, N, (kt + DIST) * BK, K, lb);
         if constexpr (F32_OUT) {
             if (row_sum) {
                 const uint16_t* col = As + (tid / BM_) * RS_K * (BM_ + MNPAD) + tid % BM_;
@@ -334,8 +343,8 @@ void gemm_bf16_kernel(GemmArgs p, int tiles_m, int tiles_n, int per_xcd, int tot
             }
             __builtin_amdgcn_sched_barrier(0);
         }
-        store_stage<BM_, A_KMAJOR>(An, sa);
-        store_stage<BN_, B_KMAJOR>(An + AE, sb);
+        store_stage<BM_, A_KMAJOR, NT>(An, sa);
+        store_stage<BN_, B_KMAJOR, NT>(An + AE, sb);
         __syncthreads();
         // KSTEPS is even: the last step's fragments are in f1
         f0.read(An, An + AE, wm, wn, 0, lane);
@@ -364,83 +373,94 @@ void gemm_bf16_kernel(GemmArgs p, int tiles_m, int tiles_n, int per_xcd, int tot
         }
     }
 
-    // Epilogue stage 1: values into this wave's LDS tiles. Register 4q + r of
-    // lane l holds C[m][n + r] with m = 32 i + l % 32, n = 32 j + 8 q + 4 (l / 32)
-    // inside the wave tile.
-    char* ep = reinterpret_cast<char*>(smem) + wave * EP_BYTES;
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int ml = i * 32 + (lane & 31);
-                const int nl = j * 32 + 8 * q + 4 * (lane >> 5);
-                const f32x16& v = acc[i][j];
-                float r[4] = {v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]};
-                if constexpr (F32_OUT) {
-                    *reinterpret_cast<float4*>(reinterpret_cast<float*>(ep) + ml * EP_LD + nl) =
-                        make_float4(r[0], r[1], r[2], r[3]);
-                } else {
-                    const int n = n0 + wn * WN + nl;
-                    const int m = m0 + wm * WM + ml;
-                    if constexpr (EPI == EPI_FWD1 || EPI == EPI_BIAS) {
-                        if (n < N) {
-                            const uint2 bb = *reinterpret_cast<const uint2*>(
-                                static_cast<const uint16_t*>(p.bias) + e * p.bias_estride + n);
-                            r[0] += bf16_to_f32(bb.x & 0xFFFFu);
-                            r[1] += bf16_to_f32(bb.x >> 16);
-                            r[2] += bf16_to_f32(bb.y & 0xFFFFu);
-                            r[3] += bf16_to_f32(bb.y >> 16);
-                        }
-                    }
-                    if constexpr (EPI == EPI_GELU_GRAD) {
-                        if (n < N && m < M) {
-                            const uint2 gg = *reinterpret_cast<const uint2*>(
-                                static_cast<const uint16_t*>(p.aux) + e * p.out_estride +
-                                static_cast<size_t>(m) * p.ldo + n);
-                            r[0] *= bf16_to_f32(gg.x & 0xFFFFu);
-                            r[1] *= bf16_to_f32(gg.x >> 16);
-                            r[2] *= bf16_to_f32(gg.y & 0xFFFFu);
-                            r[3] *= bf16_to_f32(gg.y >> 16);
-                        }
-                    }
-                    uint16_t* t0 = reinterpret_cast<uint16_t*>(ep) + ml * EP_LD + nl;
-                    if constexpr (EPI == EPI_FWD1) {
-                        float g[4], dg[4];
-#pragma unroll
-                        for (int c = 0; c < 4; ++c) gelu_pair(r[c], g[c], dg[c]);
-                        *reinterpret_cast<uint2*>(t0) =
-                            make_uint2(pack_bf16x2(g[0], g[1]), pack_bf16x2(g[2], g[3]));
-                        *reinterpret_cast<uint2*>(t0 + WM * EP_LD) =
-                            make_uint2(pack_bf16x2(dg[0], dg[1]), pack_bf16x2(dg[2], dg[3]));
-                    } else {
-                        *reinterpret_cast<uint2*>(t0) =
-                            make_uint2(pack_bf16x2(r[0], r[1]), pack_bf16x2(r[2], r[3]));
-                    }
-                }
-            }
-    __syncthreads();
-
-    // Epilogue stage 2: rows of the wave tile out in 16-byte segments.
+    char* ep = reinterpret_cast<char*>(smem) + wave * EP_OUTS_AT_ONCE * EP_TILE;
     constexpr int ELEM = F32_OUT ? 4 : 2;
     constexpr int SEG = 16 / ELEM;                 // elements per 16-byte segment
-    constexpr int LANES_PER_ROW = WN / SEG;        // 8 (bf16) or 16 (f32)
+    constexpr int LANES_PER_ROW = WN / SEG;
     constexpr int ROWS_PER_PASS = 64 / LANES_PER_ROW;
-    const int cl = (lane % LANES_PER_ROW) * SEG;
-    const int n = n0 + wn * WN + cl;
+    static_assert(LANES_PER_ROW <= 64 && 64 % LANES_PER_ROW == 0, "epilogue row split");
+
 #pragma unroll
-    for (int o = 0; o < OUTS; ++o) {
-        char* dst_base = static_cast<char*>(o == 0 ? p.out : p.out2);
+    for (int o0 = 0; o0 < OUTS; o0 += EP_OUTS_AT_ONCE) {
+        // Stage 1: values into this wave's LDS tiles. Register 4q + r of lane l
+        // holds C[m][n + r] with m = 32 i + l % 32, n = 32 j + 8 q + 4 (l / 32)
+        // inside the wave tile.
 #pragma unroll
-        for (int pass = 0; pass < WM / ROWS_PER_PASS; ++pass) {
-            const int ml = pass * ROWS_PER_PASS + lane / LANES_PER_ROW;
-            const int m = m0 + wm * WM + ml;
-            const uint4 v = *reinterpret_cast<const uint4*>(ep + (o * WM * EP_LD + ml * EP_LD + cl) * ELEM);
-            if (m < M && n < N)
-                *reinterpret_cast<uint4*>(dst_base + (e * p.out_estride +
-                                                      static_cast<size_t>(m) * p.ldo + n) * ELEM) = v;
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int ml = i * 32 + (lane & 31);
+                    const int nl = j * 32 + 8 * q + 4 * (lane >> 5);
+                    const f32x16& v = acc[i][j];
+                    float r[4] = {v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]};
+                    if constexpr (F32_OUT) {
+                        *reinterpret_cast<float4*>(reinterpret_cast<float*>(ep) + ml * EP_LD +
+                                                   nl) = make_float4(r[0], r[1], r[2], r[3]);
+                    } else {
+                        const int n = n0 + wn * WN + nl;
+                        const int m = m0 + wm * WM + ml;
+                        if constexpr (EPI == EPI_FWD1 || EPI == EPI_BIAS) {
+                            if (n < N) {
+                                const uint2 bb = *reinterpret_cast<const uint2*>(
+                                    static_cast<const uint16_t*>(p.bias) + e * p.bias_estride + n);
+                                r[0] += bf16_to_f32(bb.x & 0xFFFFu);
+                                r[1] += bf16_to_f32(bb.x >> 16);
+                                r[2] += bf16_to_f32(bb.y & 0xFFFFu);
+                                r[3] += bf16_to_f32(bb.y >> 16);
+                            }
+                        }
+                        if constexpr (EPI == EPI_GELU_GRAD) {
+                            if (n < N && m < M) {
+                                const uint2 gg = *reinterpret_cast<const uint2*>(
+                                    static_cast<const uint16_t*>(p.aux) + e * p.out_estride +
+                                    static_cast<size_t>(m) * p.ldo + n);
+                                r[0] *= bf16_to_f32(gg.x & 0xFFFFu);
+                                r[1] *= bf16_to_f32(gg.x >> 16);
+                                r[2] *= bf16_to_f32(gg.y & 0xFFFFu);
+                                r[3] *= bf16_to_f32(gg.y >> 16);
+                            }
+                        }
+                        uint16_t* t0 = reinterpret_cast<uint16_t*>(ep) + ml * EP_LD + nl;
+                        if constexpr (EPI == EPI_FWD1) {
+                            float g[4], dg[4];
+#pragma unroll
+                            for (int c = 0; c < 4; ++c) gelu_pair(r[c], g[c], dg[c]);
+#pragma unroll
+                            for (int o = 0; o < EP_OUTS_AT_ONCE; ++o) {
+                                const float* src = (o0 + o == 0) ? g : dg;
+                                *reinterpret_cast<uint2*>(t0 + o * (EP_TILE / 2)) =
+                                    make_uint2(pack_bf16x2(src[0], src[1]),
+                                               pack_bf16x2(src[2], src[3]));
+                            }
+                        } else {
+                            *reinterpret_cast<uint2*>(t0) =
+                                make_uint2(pack_bf16x2(r[0], r[1]), pack_bf16x2(r[2], r[3]));
+                        }
+                    }
+                }
+        __syncthreads();
+
+        // Stage 2: rows of the wave tile out in 16-byte segments.
+        const int cl = (lane % LANES_PER_ROW) * SEG;
+        const int n = n0 + wn * WN + cl;
+#pragma unroll
+        for (int o = 0; o < EP_OUTS_AT_ONCE; ++o) {
+            char* dst_base = static_cast<char*>(o0 + o == 0 ? p.out : p.out2);
+#pragma unroll
+            for (int pass = 0; pass < WM / ROWS_PER_PASS; ++pass) {
+                const int ml = pass * ROWS_PER_PASS + lane / LANES_PER_ROW;
+                const int m = m0 + wm * WM + ml;
+                const uint4 v =
+                    *reinterpret_cast<const uint4*>(ep + o * EP_TILE + (ml * EP_LD + cl) * ELEM);
+                if (m < M && n < N)
+                    *reinterpret_cast<uint4*>(
+                        dst_base + (e * p.out_estride + static_cast<size_t>(m) * p.ldo + n) * ELEM) =
+                        v;
+            }
         }
+        if (o0 + EP_OUTS_AT_ONCE < OUTS) __syncthreads();
     }
 }
 
@@ -534,20 +554,26 @@ __global__ __launch_bounds__(256) void colsum_kernel(const T* __restrict__ src,
                                                   part[2][c & 63]) + part[3][c & 63];
 }
 
-template <int BM_, int BN_, bool AK, bool BK_, int EPI, int DIST = 1>
+template <int BM_, int BN_, int WGM, int WGN, bool AK, bool BK_, int EPI, int DIST = 1>
 void launch_bf16(const Dims& D, const GemmArgs& a, int grid_m_rows, hipStream_t st) {
     const int tiles_m = static_cast<int>(cdiv(grid_m_rows, BM_));
     const int tiles_n = static_cast<int>(cdiv(a.N, BN_));
     const int total = D.E * tiles_m * tiles_n;
     const int per_xcd = static_cast<int>(cdiv(total, 8));
-    gemm_bf16_kernel<BM_, BN_, AK, BK_, EPI, DIST><<<8 * per_xcd, 256, 0, st>>>(
-        a, tiles_m, tiles_n, per_xcd, total);
+    gemm_bf16_kernel<BM_, BN_, WGM, WGN, AK, BK_, EPI, DIST><<<8 * per_xcd, 64 * WGM * WGN, 0,
+                                                               st>>>(a, tiles_m, tiles_n, per_xcd,
+                                                                     total);
 }
 
 template <bool AK, bool BK_, int EPI>
 void launch_gemm(const Dims& D, const GemmArgs& a, int grid_m_rows, hipStream_t st) {
     if (D.dtype == VMOE_BF16) {
-        launch_bf16<128, 128, AK, BK_, EPI>(D, a, grid_m_rows, st);
+        // 128 x 128 tiles at two waves per SIMD; the long-k forward down-projection
+        // (bias epilogue, a single bf16 output) runs 256 x 256 tiles of 8 waves
+        if constexpr (EPI == EPI_BIAS)
+            launch_bf16<256, 256, 2, 4, AK, BK_, EPI>(D, a, grid_m_rows, st);
+        else
+            launch_bf16<128, 128, 2, 2, AK, BK_, EPI>(D, a, grid_m_rows, st);
     } else {
         dim3 grid(cdiv(a.N, FT), cdiv(grid_m_rows, FT), D.E);
         gemm_f32_kernel<AK, BK_, EPI><<<grid, 256, 0, st>>>(a);

@@ -57,19 +57,31 @@ __global__ __launch_bounds__(kCols) void route_bwd_kernel(
         w[e] = e < E ? ld(wg, static_cast<size_t>(e) * d + i) : 0.0f;
         pw[e] = 0.0f;
     }
-    for (int tt = 0; tt < ntok; ++tt) {
-        const size_t t = tok0 + tt;
-        const float xv = ld(x, t * d + i);
-        float s = 0.0f;
+    // 8 tokens per round: all 16 loads are issued before any arithmetic, so
+    // each thread keeps many HBM requests in flight.
+    constexpr int U = 8;
+    for (int tt0 = 0; tt0 < ntok; tt0 += U) {
+        float xv[U], dv[U];
 #pragma unroll
-        for (int e = 0; e < EMAX; ++e) {
-            const float dz = dzs[tt][e < E ? e : 0];
-            if (e < E) {
-                s = __builtin_fmaf(dz, w[e], s);
-                pw[e] = __builtin_fmaf(dz, xv, pw[e]);
-            }
+        for (int u = 0; u < U; ++u) {
+            const size_t t = tok0 + min(tt0 + u, ntok - 1);
+            xv[u] = ld(x, t * d + i);
+            dv[u] = dx[t * d + i];
         }
-        dx[t * d + i] += s;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (tt0 + u >= ntok) break;
+            float s = 0.0f;
+#pragma unroll
+            for (int e = 0; e < EMAX; ++e) {
+                const float dz = dzs[tt0 + u][e < E ? e : 0];
+                if (e < E) {
+                    s = __builtin_fmaf(dz, w[e], s);
+                    pw[e] = __builtin_fmaf(dz, xv[u], pw[e]);
+                }
+            }
+            dx[(tok0 + tt0 + u) * d + i] = dv[u] + s;
+        }
     }
     if (partial) {
         float* pg = partial + (static_cast<size_t>(g) * nch + c) * E * d;

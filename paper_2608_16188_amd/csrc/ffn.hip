@@ -250,11 +250,18 @@ void gemm_bf16_kernel(GemmArgs p, int tiles_m, int tiles_n, int per_xcd, int tot
     constexpr bool F32_OUT = EPI == EPI_F32;
     constexpr int OUTS = EPI == EPI_FWD1 ? 2 : 1;
     constexpr int SMEM_ELEMS = 2 * (AE + BE);
-    // per-wave epilogue staging: WM rows x (WN + pad) elements per output
-    constexpr int EP_LD = F32_OUT ? WN + 4 : WN + 8;
-    constexpr int EP_TILE = WM * EP_LD * (F32_OUT ? 4 : 2);
-    constexpr int EP_OUTS_AT_ONCE = (OUTS * EP_TILE * WGM * WGN <= SMEM_ELEMS * 2) ? OUTS : 1;
-    static_assert(EP_TILE * WGM * WGN <= SMEM_ELEMS * 2, "epilogue staging exceeds LDS");
+    // Epilogue staging per wave: IPP of its FM 32-row blocks per pass, all
+    // outputs of those rows when they fit, else one output per pass.
+    constexpr int EP_LD = F32_OUT ? WN + 4 : WN + 4;
+    constexpr int ELEM = F32_OUT ? 4 : 2;
+    constexpr int EP_ROWBLK = 32 * EP_LD * ELEM;  // one 32-row block of one output
+    constexpr int NW = WGM * WGN;
+    constexpr int SMEM_BYTES = SMEM_ELEMS * 2;
+    constexpr int EP_OUTS_AT_ONCE = OUTS * FM * EP_ROWBLK * NW <= SMEM_BYTES ? OUTS : 1;
+    constexpr int IPP = EP_OUTS_AT_ONCE * FM * EP_ROWBLK * NW <= SMEM_BYTES ? FM
+                        : (EP_OUTS_AT_ONCE * (FM / 2) * EP_ROWBLK * NW <= SMEM_BYTES ? FM / 2 : 1);
+    constexpr int EP_TILE = IPP * EP_ROWBLK;       // bytes of one output's staged rows
+    static_assert(EP_OUTS_AT_ONCE * EP_TILE * NW <= SMEM_BYTES, "epilogue staging exceeds LDS");
     static_assert(!F32_OUT || !A_KMAJOR, "row sums read an mn-major A tile");
     static_assert(NT % BM_ == 0 || !F32_OUT, "row sums give each A row NT / BM threads");
     static_assert(WM % 32 == 0 && WN % 32 == 0 && VA >= 1 && VB >= 1, "tile shape");
@@ -352,10 +359,15 @@ void gemm_bf16_kernel(GemmArgs p, int tiles_m, int tiles_n, int per_xcd, int tot
         mfma_block(acc, f1);
         __builtin_amdgcn_sched_barrier(0);
     };
-    for (int kt = 0; kt < nk; kt += 2) {
+    // Whole pairs first, without a conditional half: a skipped half would merge
+    // a path with loads still in flight into the loop head, and the compiler
+    // would then drain every outstanding load before the next set is issued.
+    int kt = 0;
+    for (; kt + 1 < nk; kt += 2) {
         stage(kt, std::integral_constant<int, 0>{});
-        if (kt + 1 < nk) stage(kt + 1, std::integral_constant<int, 1>{});
+        stage(kt + 1, std::integral_constant<int, 1>{});
     }
+    if (kt < nk) stage(kt, std::integral_constant<int, 0>{});
     __syncthreads();  // every wave is done with the operand stages
 
     if constexpr (F32_OUT) {
@@ -374,24 +386,26 @@ void gemm_bf16_kernel(GemmArgs p, int tiles_m, int tiles_n, int per_xcd, int tot
     }
 
     char* ep = reinterpret_cast<char*>(smem) + wave * EP_OUTS_AT_ONCE * EP_TILE;
-    constexpr int ELEM = F32_OUT ? 4 : 2;
     constexpr int SEG = 16 / ELEM;                 // elements per 16-byte segment
     constexpr int LANES_PER_ROW = WN / SEG;
     constexpr int ROWS_PER_PASS = 64 / LANES_PER_ROW;
     static_assert(LANES_PER_ROW <= 64 && 64 % LANES_PER_ROW == 0, "epilogue row split");
 
 #pragma unroll
+    for (int i0 = 0; i0 < FM; i0 += IPP)
+#pragma unroll
     for (int o0 = 0; o0 < OUTS; o0 += EP_OUTS_AT_ONCE) {
         // Stage 1: values into this wave's LDS tiles. Register 4q + r of lane l
         // holds C[m][n + r] with m = 32 i + l % 32, n = 32 j + 8 q + 4 (l / 32)
         // inside the wave tile.
 #pragma unroll
-        for (int i = 0; i < FM; ++i)
+        for (int ii = 0; ii < IPP; ++ii)
 #pragma unroll
             for (int j = 0; j < FN; ++j)
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
-                    const int ml = i * 32 + (lane & 31);
+                    const int i = i0 + ii;
+                    const int ml = ii * 32 + (lane & 31);  // row inside the staged rows
                     const int nl = j * 32 + 8 * q + 4 * (lane >> 5);
                     const f32x16& v = acc[i][j];
                     float r[4] = {v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]};
@@ -400,7 +414,7 @@ void gemm_bf16_kernel(GemmArgs p, int tiles_m, int tiles_n, int per_xcd, int tot
                                                    nl) = make_float4(r[0], r[1], r[2], r[3]);
                     } else {
                         const int n = n0 + wn * WN + nl;
-                        const int m = m0 + wm * WM + ml;
+                        const int m = m0 + wm * WM + i * 32 + (lane & 31);
                         if constexpr (EPI == EPI_FWD1 || EPI == EPI_BIAS) {
                             if (n < N) {
                                 const uint2 bb = *reinterpret_cast<const uint2*>(
@@ -442,16 +456,16 @@ void gemm_bf16_kernel(GemmArgs p, int tiles_m, int tiles_n, int per_xcd, int tot
                 }
         __syncthreads();
 
-        // Stage 2: rows of the wave tile out in 16-byte segments.
+        // Stage 2: staged rows out in 16-byte segments.
         const int cl = (lane % LANES_PER_ROW) * SEG;
         const int n = n0 + wn * WN + cl;
 #pragma unroll
         for (int o = 0; o < EP_OUTS_AT_ONCE; ++o) {
             char* dst_base = static_cast<char*>(o0 + o == 0 ? p.out : p.out2);
 #pragma unroll
-            for (int pass = 0; pass < WM / ROWS_PER_PASS; ++pass) {
+            for (int pass = 0; pass < IPP * 32 / ROWS_PER_PASS; ++pass) {
                 const int ml = pass * ROWS_PER_PASS + lane / LANES_PER_ROW;
-                const int m = m0 + wm * WM + ml;
+                const int m = m0 + wm * WM + i0 * 32 + ml;
                 const uint4 v =
                     *reinterpret_cast<const uint4*>(ep + o * EP_TILE + (ml * EP_LD + cl) * ELEM);
                 if (m < M && n < N)
@@ -460,7 +474,7 @@ void gemm_bf16_kernel(GemmArgs p, int tiles_m, int tiles_n, int per_xcd, int tot
                         v;
             }
         }
-        if (o0 + EP_OUTS_AT_ONCE < OUTS) __syncthreads();
+        __syncthreads();
     }
 }
 
@@ -568,9 +582,11 @@ void launch_bf16(const Dims& D, const GemmArgs& a, int grid_m_rows, hipStream_t 
 template <bool AK, bool BK_, int EPI>
 void launch_gemm(const Dims& D, const GemmArgs& a, int grid_m_rows, hipStream_t st) {
     if (D.dtype == VMOE_BF16) {
-        // 128 x 128 tiles at two waves per SIMD; the long-k forward down-projection
-        // (bias epilogue, a single bf16 output) runs 256 x 256 tiles of 8 waves
-        if constexpr (EPI == EPI_BIAS)
+        // 128 x 128 tiles (4 waves, two blocks per CU) for the short-k GEMMs and
+        // the weight gradients; 256 x 256 tiles of 8 waves (half the LDS traffic
+        // per flop) for the long-k GEMMs with one plain bf16 output (the
+        // down-projection and dxe)
+        if constexpr (EPI == EPI_BIAS || EPI == EPI_STORE)
             launch_bf16<256, 256, 2, 4, AK, BK_, EPI>(D, a, grid_m_rows, st);
         else
             launch_bf16<128, 128, 2, 2, AK, BK_, EPI>(D, a, grid_m_rows, st);

@@ -95,6 +95,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="vitb16_bf16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="before warm-up, copy one 256 MiB buffer (a plain copy kernel of known "
+                         "size, to calibrate the HBM byte counters of a profiler run)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (--gpus {args.gpus} requested); the layer's "
@@ -131,6 +134,14 @@ def main():
         "route_bwd": lambda: V.vmoe_route_bwd(s, L.x, L.w_router, L.probs, L.expert_idx, L.slot,
                                               L.dgate, L.dx, L.dw_router, L.route_bwd_ws, stream),
     }
+
+    if args.copy_probe:
+        src = torch.ones(256 << 20, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     for _ in range(args.warmup):
         for name in CALLS:

@@ -73,22 +73,39 @@ __device__ __forceinline__ float gelu_grad_f(float h) {
 
 // ------------------------------------------------------------------ bf16 MFMA
 
-constexpr int BK = 64;          // k depth of one LDS stage
-constexpr int KPAD = 8;         // k-major rows: 64 + 8 bf16 = 144 B pitch
-// mn-major rows: ROWS + 32 bf16, a pitch of 16 (mod 64) dwords, so the two
-// 16-lane groups of a transpose read (4 rows x 32 B each) hit disjoint banks
-constexpr int MNPAD = 32;
-
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef short s16x8 __attribute__((ext_vector_type(8)));
+typedef int v4i32 __attribute__((ext_vector_type(4)));
 
-// LDS elements of one operand stage: k-major [ROWS][BK + KPAD], mn-major [BK][ROWS + MNPAD].
-template <int ROWS, bool KMAJOR>
+// Two ways of staging a KB-deep operand tile (KB = 32 or 64) in LDS:
+//   STAGE_REG: global -> registers -> ds_write, rows padded (k-major rows of
+//              KB + 8 bf16, mn-major rows of ROWS + 32 bf16), two stages;
+//   STAGE_DMA: buffer_load ... lds straight into LDS (no registers, so a ring
+//              of NS stages costs LDS only): lane L of a wave instruction fills
+//              bytes [16 L, 16 L + 16) of a 1 KB block, so rows are unpadded and
+//              16-byte chunks are XOR-swizzled instead (k-major: chunk ^ ((row / P)
+//              mod Q) with P rows per 256 bytes and Q chunks per row; mn-major:
+//              chunk ^ 4 (k mod 4)), which keeps fragment and transpose reads free
+//              of bank conflicts.
+enum Staging { STAGE_REG = 0, STAGE_DMA = 1 };
+
+template <int ROWS, bool KMAJOR, int KB, int MODE>
 __host__ __device__ constexpr int stage_elems() {
-    return KMAJOR ? ROWS * (BK + KPAD) : BK * (ROWS + MNPAD);
+    return MODE == STAGE_DMA ? ROWS * KB : (KMAJOR ? ROWS * (KB + 8) : KB * (ROWS + 32));
 }
 
-typedef int v4i32 __attribute__((ext_vector_type(4)));
+// Element offset (in bf16) of (mn, k) inside one operand stage.
+template <int ROWS, bool KMAJOR, int KB, int MODE>
+__device__ __forceinline__ int lds_off(int mn, int k) {
+    if constexpr (MODE == STAGE_REG) {
+        return KMAJOR ? mn * (KB + 8) + k : k * (ROWS + 32) + mn;
+    } else if constexpr (KMAJOR) {
+        constexpr int Q = KB / 8, P = 16 / Q;  // chunks per row, rows per 256 bytes
+        return mn * KB + (((k >> 3) ^ ((mn / P) % Q)) << 3) + (k & 7);
+    } else {
+        return k * ROWS + (((mn >> 3) ^ ((k & 3) << 2)) << 3) + (mn & 7);
+    }
+}
 
 // Raw buffer over one expert's operand: loads at byte offsets >= `bytes` return
 // zeros in hardware, which implements every tail mask without a branch.
@@ -104,49 +121,106 @@ __device__ __forceinline__ uint4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t b
     return make_uint4(v[0], v[1], v[2], v[3]);
 }
 
-// Global -> registers: one ROWS x BK operand stage, ROWS * 8 / NT vectors of
-// 8 bf16 per thread, each row segment read by consecutive lanes (coalesced).
-template <int ROWS, bool KMAJOR, int NT>
-__device__ __forceinline__ void load_stage(__amdgpu_buffer_rsrc_t rs, int ld, int mn0, int mn_lim,
-                                           int k0, int k_lim, uint4 (&r)[ROWS * 8 / NT]) {
-    const int tid = threadIdx.x;
-    if (KMAJOR) {
-        const int kc = (tid & 7) * 8;
-#pragma unroll
-        for (int j = 0; j < ROWS * 8 / NT; ++j) {
-            const int mn = mn0 + (tid >> 3) + (NT / 8) * j;
-            const bool ok = (mn < mn_lim) && (k0 + kc < k_lim);
-            r[j] = buf_load16(rs, ok ? static_cast<uint32_t>(mn * ld + k0 + kc) * 2u : kOutOfRange);
-        }
-    } else {
-        constexpr int VPR = ROWS / 8;  // vectors per k row
-        const int mc = mn0 + (tid % VPR) * 8;
-#pragma unroll
-        for (int j = 0; j < ROWS * 8 / NT; ++j) {
-            const int kr = k0 + tid / VPR + (NT / VPR) * j;
-            const bool ok = (kr < k_lim) && (mc < mn_lim);
-            r[j] = buf_load16(rs, ok ? static_cast<uint32_t>(kr * ld + mc) * 2u : kOutOfRange);
-        }
-    }
+// Byte offset in HBM of the 16-byte vector holding (mn, k..k+7) [k-major] or
+// (k, mn..mn+7) [mn-major], or kOutOfRange when it lies outside the operand.
+template <bool KMAJOR>
+__device__ __forceinline__ uint32_t vec_off(int ld, int mn, int mn_lim, int k, int k_lim) {
+    const bool ok = (mn < mn_lim) && (k < k_lim);
+    const int e = KMAJOR ? mn * ld + k : k * ld + mn;
+    return ok ? static_cast<uint32_t>(e) * 2u : kOutOfRange;
 }
 
-// Registers -> LDS, same element placement as the global tile (no transpose).
-template <int ROWS, bool KMAJOR, int NT>
-__device__ __forceinline__ void store_stage(uint16_t* s, const uint4 (&r)[ROWS * 8 / NT]) {
-    const int tid = threadIdx.x;
-    if (KMAJOR) {
-        const int kc = (tid & 7) * 8;
+// --- register staging: ROWS * KB / 8 / NT vectors per thread, consecutive
+// lanes read consecutive 16-byte segments of a row (coalesced).
+template <int ROWS, bool KMAJOR, int KB, int NT>
+struct RegStage {
+    static constexpr int V = ROWS * KB / 8 / NT;
+    static_assert(V * NT * 8 == ROWS * KB, "stage must split evenly over threads");
+    static __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t rs, int ld, int mn0,
+                                                int mn_lim, int k0, int k_lim, uint4 (&r)[V]) {
+        const int tid = threadIdx.x;
 #pragma unroll
-        for (int j = 0; j < ROWS * 8 / NT; ++j)
-            *reinterpret_cast<uint4*>(s + ((tid >> 3) + (NT / 8) * j) * (BK + KPAD) + kc) = r[j];
-    } else {
-        constexpr int VPR = ROWS / 8;
-        const int mc = (tid % VPR) * 8;
-#pragma unroll
-        for (int j = 0; j < ROWS * 8 / NT; ++j)
-            *reinterpret_cast<uint4*>(s + (tid / VPR + (NT / VPR) * j) * (ROWS + MNPAD) + mc) =
-                r[j];
+        for (int j = 0; j < V; ++j) {
+            if (KMAJOR) {
+                constexpr int VPR = KB / 8;  // vectors per mn row
+                const int q = tid + NT * j;
+                r[j] = buf_load16(rs, vec_off<true>(ld, mn0 + q / VPR, mn_lim, k0 + (q % VPR) * 8, k_lim));
+            } else {
+                constexpr int VPR = ROWS / 8;  // vectors per k row
+                const int q = tid + NT * j;
+                r[j] = buf_load16(rs, vec_off<false>(ld, mn0 + (q % VPR) * 8, mn_lim, k0 + q / VPR, k_lim));
+            }
+        }
     }
+    static __device__ __forceinline__ void store(uint16_t* s, const uint4 (&r)[V]) {
+        const int tid = threadIdx.x;
+#pragma unroll
+        for (int j = 0; j < V; ++j) {
+            const int q = tid + NT * j;
+            int o;
+            if (KMAJOR) {
+                constexpr int VPR = KB / 8;
+                o = lds_off<ROWS, true, KB, STAGE_REG>(q / VPR, (q % VPR) * 8);
+            } else {
+                constexpr int VPR = ROWS / 8;
+                o = lds_off<ROWS, false, KB, STAGE_REG>((q % VPR) * 8, q / VPR);
+            }
+            *reinterpret_cast<uint4*>(s + o) = r[j];
+        }
+    }
+};
+
+// --- LDS DMA: the operand stage is ROWS * KB / 512 blocks of 1 KB; wave w
+// issues blocks [w * PER, (w + 1) * PER). Lane L of a block holds physical
+// bytes [16 L, 16 L + 16), whose logical (swizzled) position decides what it
+// fetches.
+template <int ROWS, bool KMAJOR, int KB, int NT>
+struct DmaStage {
+    static constexpr int BLOCKS = ROWS * KB * 2 / 1024;
+    static constexpr int PER = BLOCKS / (NT / 64);  // wave instructions per stage
+    static_assert(PER >= 1 && PER * (NT / 64) == BLOCKS, "1 KB blocks must split evenly over waves");
+    static __device__ __forceinline__ void issue(__amdgpu_buffer_rsrc_t rs, int ld, int mn0,
+                                                 int mn_lim, int k0, int k_lim, uint16_t* s) {
+        const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+        for (int q = 0; q < PER; ++q) {
+            const int blk = wave * PER + q;
+            const int byte = blk * 1024 + 16 * lane;
+            uint32_t off;
+            if (KMAJOR) {
+                constexpr int RB = KB * 2, Q = KB / 8, P = 16 / Q;
+                const int r = byte / RB;
+                const int c = ((byte % RB) >> 4) ^ ((r / P) % Q);
+                off = vec_off<true>(ld, mn0 + r, mn_lim, k0 + 8 * c, k_lim);
+            } else {
+                constexpr int RB = ROWS * 2;  // bytes per k row
+                const int r = byte / RB;
+                const int c = ((byte % RB) >> 4) ^ ((r & 3) << 2);
+                off = vec_off<false>(ld, mn0 + 8 * c, mn_lim, k0 + r, k_lim);
+            }
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                rs, (__attribute__((address_space(3))) void*)(s + blk * 512), 16, off, 0, 0, 0);
+        }
+    }
+};
+
+// s_waitcnt immediate for vmcnt(n) and lgkmcnt(0) (expcnt left alone).
+template <int N>
+struct VmWait {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    static constexpr int imm = (N & 15) | ((N >> 4) << 14) | (7 << 4);
+};
+
+// Workgroup barrier for the stage ring. __syncthreads() fences all memory at
+// workgroup scope, which waits for every LDS DMA in flight (vmcnt(0)) and
+// would cap the prefetch at one stage; here the caller's s_waitcnt has
+// already retired this wave's LDS reads and the DMA of the stage about to be
+// read, so a bare s_barrier suffices. The signal fences keep the compiler
+// from moving memory accesses across it.
+__device__ __forceinline__ void ring_barrier() {
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_barrier();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
 // ds_read_b64_tr_b16: within each 16-lane group, lane j reads 4 bf16 at its
@@ -160,46 +234,21 @@ __device__ __forceinline__ s16x4 lds_read_tr(const uint16_t* p) {
 
 // Operand fragment of v_mfma_f32_32x32x16_bf16 for 32 mn values (lane & 31)
 // x 8 k values (k = 16 * kstep + 8 * (lane >> 5) + 0..7).
-template <int ROWS, bool KMAJOR>
+template <int ROWS, bool KMAJOR, int KB, int MODE>
 __device__ __forceinline__ bf16x8 read_frag(const uint16_t* s, int blk, int kstep, int lane) {
     if (KMAJOR) {
-        return *reinterpret_cast<const bf16x8*>(s + (blk * 32 + (lane & 31)) * (BK + KPAD) +
-                                                kstep * 16 + (lane >> 5) * 8);
+        const int mn = blk * 32 + (lane & 31), k = kstep * 16 + (lane >> 5) * 8;
+        return *reinterpret_cast<const bf16x8*>(s + lds_off<ROWS, true, KB, MODE>(mn, k));
     } else {
         // 16-lane group g covers mn [16 (g & 1), +16) and k [8 (g >> 1), +8)
-        constexpr int P = ROWS + MNPAD;
         const int g = lane >> 4, j = lane & 15;
-        const uint16_t* p0 = s + (kstep * 16 + 8 * (g >> 1) + (j >> 2)) * P + blk * 32 +
-                             16 * (g & 1) + 4 * (j & 3);
-        const s16x4 lo = lds_read_tr(p0);
-        const s16x4 hi = lds_read_tr(p0 + 4 * P);
+        const int k = kstep * 16 + 8 * (g >> 1) + (j >> 2);
+        const int mn = blk * 32 + 16 * (g & 1) + 4 * (j & 3);
+        const s16x4 lo = lds_read_tr(s + lds_off<ROWS, false, KB, MODE>(mn, k));
+        const s16x4 hi = lds_read_tr(s + lds_off<ROWS, false, KB, MODE>(mn, k + 4));
         const s16x8 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
         return __builtin_bit_cast(bf16x8, v);
     }
-}
-
-template <int BM_, int BN_, int WGM, int WGN, bool A_KMAJOR, bool B_KMAJOR>
-struct Frags {
-    static constexpr int FM = BM_ / WGM / 32, FN = BN_ / WGN / 32;  // 32 x 32 blocks per wave
-    bf16x8 a[FM], b[FN];
-    __device__ __forceinline__ void read(const uint16_t* As, const uint16_t* Bs, int wm, int wn,
-                                         int ks, int lane) {
-#pragma unroll
-        for (int i = 0; i < FM; ++i) a[i] = read_frag<BM_, A_KMAJOR>(As, wm * FM + i, ks, lane);
-#pragma unroll
-        for (int j = 0; j < FN; ++j) b[j] = read_frag<BN_, B_KMAJOR>(Bs, wn * FN + j, ks, lane);
-    }
-};
-
-// acc[i][j] += A-block i x B-block j; the operands are swapped inside the
-// MFMA so that register 4q + r of lane l holds C[m = l % 32][n = 8q + 4 (l / 32) + r].
-template <int FM, int FN, typename F>
-__device__ __forceinline__ void mfma_block(f32x16 (&acc)[FM][FN], const F& f) {
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.b[j], f.a[i], acc[i][j], 0, 0, 0);
 }
 
 // GELU and its derivative from one exponential: with x = |h| / sqrt(2),
@@ -219,60 +268,288 @@ __device__ __forceinline__ void gelu_pair(float h, float& g, float& dg) {
     dg = phi_cdf + h * ex * 0.39894228040143268f;
 }
 
+// Static description of one bf16 GEMM tiling: BM x BN block tile of WGM x WGN
+// waves, KB-deep stages, NS stages in flight, staging mode.
+template <int BM_, int BN_, int WGM_, int WGN_, int KB_, int NS_, int MODE_, bool PAIR_ = false>
+struct Tile {
+    static constexpr int BM = BM_, BN = BN_, WGM = WGM_, WGN = WGN_, KB = KB_, NS = NS_;
+    static constexpr int MODE = MODE_;
+    // PAIR: stages are fetched two at a time (kt + 2 and kt + 3 at each even
+    // kt), so the two 64-byte halves of a 128-byte k-major row segment are
+    // requested back to back and share one cache-line fill
+    static constexpr bool PAIR = PAIR_;
+    static constexpr int NW = WGM * WGN, NT = 64 * NW;
+    static constexpr int WM = BM / WGM, WN = BN / WGN;  // wave tile
+    static constexpr int FM = WM / 32, FN = WN / 32;    // 32 x 32 MFMA blocks per wave
+    static constexpr int KSTEPS = KB / 16;
+    // two blocks per CU for 8-wave tiles and small tiles, one otherwise
+    static constexpr int WAVES_PER_EU = (NW == 8 || BM * BN < 256 * 128) ? 2 : 1;
+    static_assert(WM % 32 == 0 && WN % 32 == 0, "wave tile must be whole 32 x 32 blocks");
+    static_assert(KSTEPS % 2 == 0, "fragment double buffering needs an even step count");
+    static_assert(MODE == STAGE_DMA || NS == 2, "register staging runs two stages");
+    static_assert(NS >= 2 && NS <= 5, "stage ring size");
+    static_assert(!PAIR || (NS == 4 && MODE == STAGE_DMA), "paired fetch runs a ring of four");
+};
+
+// Per-GEMM static sizes derived from a tiling and the operand layouts.
+template <class T, bool A_KMAJOR, bool B_KMAJOR, int EPI>
+struct GemmCfg {
+    static constexpr int AE = stage_elems<T::BM, A_KMAJOR, T::KB, T::MODE>();
+    static constexpr int BE = stage_elems<T::BN, B_KMAJOR, T::KB, T::MODE>();
+    static constexpr int BUF_BYTES = (AE + BE) * 2;  // one stage buffer
+    static constexpr bool F32_OUT = EPI == EPI_F32;
+    static constexpr int OUTS = EPI == EPI_FWD1 ? 2 : 1;
+    // Epilogue staging: wave w parks its outputs in stage buffer w mod NS; IPP
+    // of its FM 32-row blocks per pass, all outputs of those rows at once when
+    // they fit (a second output pass would recompute the activation).
+    static constexpr int EP_LD = T::WN + 4;
+    static constexpr int ELEM = F32_OUT ? 4 : 2;
+    static constexpr int EP_ROWBLK = 32 * EP_LD * ELEM;
+    static constexpr int WAVES_PER_BUF = (T::NW + T::NS - 1) / T::NS;
+    static constexpr bool fits(int outs, int blocks) {
+        return outs * blocks * EP_ROWBLK * WAVES_PER_BUF <= BUF_BYTES;
+    }
+    static constexpr int EP_OUTS_AT_ONCE = fits(OUTS, 1) ? OUTS : 1;
+    static constexpr int IPP = fits(EP_OUTS_AT_ONCE, T::FM) ? T::FM
+                             : (fits(EP_OUTS_AT_ONCE, T::FM / 2) ? T::FM / 2 : 1);
+    static constexpr int EP_TILE = IPP * EP_ROWBLK;
+    static_assert(fits(EP_OUTS_AT_ONCE, IPP), "epilogue staging exceeds LDS");
+    static_assert(!F32_OUT || !A_KMAJOR, "row sums read an mn-major A tile");
+    static_assert(!F32_OUT || T::NT % T::BM == 0, "row sums give each A row NT / BM threads");
+    static_assert(!F32_OUT || T::NT * 4 <= BUF_BYTES, "row-sum partials fit one stage buffer");
+};
+
+template <class T, bool A_KMAJOR, bool B_KMAJOR, int MODE>
+struct Frags {
+    static constexpr int FM = T::FM, FN = T::FN;
+    bf16x8 a[FM], b[FN];
+    __device__ __forceinline__ void read(const uint16_t* As, const uint16_t* Bs, int wm, int wn,
+                                         int ks, int lane) {
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+            a[i] = read_frag<T::BM, A_KMAJOR, T::KB, MODE>(As, wm * FM + i, ks, lane);
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+            b[j] = read_frag<T::BN, B_KMAJOR, T::KB, MODE>(Bs, wn * FN + j, ks, lane);
+    }
+};
+
+// acc[i][j] += A-block i x B-block j; the operands are swapped inside the
+// MFMA so that register 4q + r of lane l holds C[m = l % 32][n = 8q + 4 (l / 32) + r].
+template <int FM, int FN, typename F>
+__device__ __forceinline__ void mfma_block(f32x16 (&acc)[FM][FN], const F& f) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.b[j], f.a[i], acc[i][j], 0, 0, 0);
+}
+
+// Bias of the columns a lane owns in the epilogue: column 32 j + 8 q + 4 (l / 32)
+// + 0..3 of the wave tile, for j < FN, q < 4, as four packed bf16 (zero past N).
+// Loaded before the main loop so its latency hides behind the MFMAs.
+template <class T, int EPI>
+struct BiasRegs {
+    static constexpr bool USED = EPI == EPI_FWD1 || EPI == EPI_BIAS;
+    uint2 v[USED ? T::FN * 4 : 1];
+    __device__ __forceinline__ void load(const GemmArgs& p, int e, int N, int n0, int wn, int lane) {
+        if constexpr (USED) {
+#pragma unroll
+            for (int j = 0; j < T::FN; ++j)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int n = n0 + wn * T::WN + j * 32 + 8 * q + 4 * (lane >> 5);
+                    v[j * 4 + q] = n < N ? *reinterpret_cast<const uint2*>(
+                                               static_cast<const uint16_t*>(p.bias) +
+                                               e * p.bias_estride + n)
+                                         : make_uint2(0u, 0u);
+                }
+        }
+    }
+};
+
+// Epilogue of one block: optional bias-gradient row sums (partials combined in
+// part_buf), then each wave turns its accumulators into outputs (bias, GELU +
+// GELU', GELU' product), parks them in its own slot of ep_buf and writes every
+// output row as 16-byte-per-lane segments. The slots are private to a wave and
+// LDS accesses of one wave complete in order, so the passes need no barrier.
+template <class T, class CFG, int EPI>
+__device__ __forceinline__ void gemm_epilogue(const GemmArgs& p, f32x16 (&acc)[T::FM][T::FN],
+                                              const BiasRegs<T, EPI>& bias, uint16_t* part_buf,
+                                              uint16_t* ep_buf, float rsum, bool row_sum, int e,
+                                              int M, int N, int m0, int n0) {
+    constexpr int FM = T::FM, FN = T::FN, WM = T::WM, WN = T::WN, BM_ = T::BM;
+    constexpr int EP_LD = CFG::EP_LD, ELEM = CFG::ELEM, EP_TILE = CFG::EP_TILE;
+    constexpr int IPP = CFG::IPP, OUTS = CFG::OUTS, EPO = CFG::EP_OUTS_AT_ONCE;
+    constexpr bool F32_OUT = CFG::F32_OUT;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave / T::WGN, wn = wave % T::WGN;
+
+    if constexpr (F32_OUT) {
+        if (row_sum) {  // uniform per block
+            constexpr int SPLIT = T::NT / BM_;
+            float* part = reinterpret_cast<float*>(part_buf);
+            part[tid] = rsum;
+            __syncthreads();
+            if (tid < BM_ && m0 + tid < M) {
+                float t = part[tid];
+#pragma unroll
+                for (int q = 1; q < SPLIT; ++q) t += part[tid + q * BM_];
+                p.bsum[static_cast<size_t>(e) * M + m0 + tid] = t;
+            }
+            __syncthreads();
+        }
+    }
+
+    char* ep = reinterpret_cast<char*>(ep_buf) + (wave / T::NS) * EPO * EP_TILE;
+    constexpr int SEG = 16 / ELEM;                 // elements per 16-byte segment
+    constexpr int LANES_PER_ROW = WN / SEG;
+    constexpr int ROWS_PER_PASS = 64 / LANES_PER_ROW;
+    static_assert(LANES_PER_ROW <= 64 && 64 % LANES_PER_ROW == 0, "epilogue row split");
+
+#pragma unroll
+    for (int i0 = 0; i0 < FM; i0 += IPP) {
+        // saved gelu'(H) of this pass's rows, all loads in flight together
+        uint2 aux[EPI == EPI_GELU_GRAD ? IPP * FN * 4 : 1];
+        if constexpr (EPI == EPI_GELU_GRAD) {
+#pragma unroll
+            for (int ii = 0; ii < IPP; ++ii)
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const int n = n0 + wn * WN + j * 32 + 8 * q + 4 * (lane >> 5);
+                        const int m = m0 + wm * WM + (i0 + ii) * 32 + (lane & 31);
+                        aux[(ii * FN + j) * 4 + q] =
+                            (n < N && m < M) ? *reinterpret_cast<const uint2*>(
+                                                   static_cast<const uint16_t*>(p.aux) +
+                                                   e * p.out_estride +
+                                                   static_cast<size_t>(m) * p.ldo + n)
+                                             : make_uint2(0u, 0u);
+                    }
+        }
+#pragma unroll
+        for (int o0 = 0; o0 < OUTS; o0 += EPO) {
+            // Stage 1: register 4q + r of lane l holds C[m][n + r] with
+            // m = 32 i + l % 32, n = 32 j + 8 q + 4 (l / 32) inside the wave tile.
+#pragma unroll
+            for (int ii = 0; ii < IPP; ++ii)
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const int i = i0 + ii;
+                        const int ml = ii * 32 + (lane & 31);  // row inside the staged rows
+                        const int nl = j * 32 + 8 * q + 4 * (lane >> 5);
+                        const f32x16& v = acc[i][j];
+                        float r[4] = {v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]};
+                        if constexpr (F32_OUT) {
+                            *reinterpret_cast<float4*>(reinterpret_cast<float*>(ep) + ml * EP_LD +
+                                                       nl) = make_float4(r[0], r[1], r[2], r[3]);
+                        } else {
+                            if constexpr (EPI == EPI_FWD1 || EPI == EPI_BIAS) {
+                                const uint2 bb = bias.v[j * 4 + q];
+                                r[0] += bf16_to_f32(bb.x & 0xFFFFu);
+                                r[1] += bf16_to_f32(bb.x >> 16);
+                                r[2] += bf16_to_f32(bb.y & 0xFFFFu);
+                                r[3] += bf16_to_f32(bb.y >> 16);
+                            }
+                            if constexpr (EPI == EPI_GELU_GRAD) {
+                                const uint2 gg = aux[(ii * FN + j) * 4 + q];
+                                r[0] *= bf16_to_f32(gg.x & 0xFFFFu);
+                                r[1] *= bf16_to_f32(gg.x >> 16);
+                                r[2] *= bf16_to_f32(gg.y & 0xFFFFu);
+                                r[3] *= bf16_to_f32(gg.y >> 16);
+                            }
+                            uint16_t* t0 = reinterpret_cast<uint16_t*>(ep) + ml * EP_LD + nl;
+                            if constexpr (EPI == EPI_FWD1) {
+                                float g[4], dg[4];
+#pragma unroll
+                                for (int c = 0; c < 4; ++c) gelu_pair(r[c], g[c], dg[c]);
+#pragma unroll
+                                for (int o = 0; o < EPO; ++o) {
+                                    const float* src = (o0 + o == 0) ? g : dg;
+                                    *reinterpret_cast<uint2*>(t0 + o * (EP_TILE / 2)) =
+                                        make_uint2(pack_bf16x2(src[0], src[1]),
+                                                   pack_bf16x2(src[2], src[3]));
+                                }
+                            } else {
+                                *reinterpret_cast<uint2*>(t0) =
+                                    make_uint2(pack_bf16x2(r[0], r[1]), pack_bf16x2(r[2], r[3]));
+                            }
+                        }
+                    }
+
+            // Stage 2: staged rows out in 16-byte segments.
+            const int cl = (lane % LANES_PER_ROW) * SEG;
+            const int n = n0 + wn * WN + cl;
+#pragma unroll
+            for (int o = 0; o < EPO; ++o) {
+                char* dst_base = static_cast<char*>(o0 + o == 0 ? p.out : p.out2);
+#pragma unroll
+                for (int pass = 0; pass < IPP * 32 / ROWS_PER_PASS; ++pass) {
+                    const int ml = pass * ROWS_PER_PASS + lane / LANES_PER_ROW;
+                    const int m = m0 + wm * WM + i0 * 32 + ml;
+                    const uint4 v = *reinterpret_cast<const uint4*>(ep + o * EP_TILE +
+                                                                    (ml * EP_LD + cl) * ELEM);
+                    if (m < M && n < N)
+                        *reinterpret_cast<uint4*>(
+                            dst_base +
+                            (e * p.out_estride + static_cast<size_t>(m) * p.ldo + n) * ELEM) = v;
+                }
+            }
+        }
+    }
+}
+
 // One BM x BN output tile of expert e per block of WGM x WGN waves, each
 // (BM/WGM) x (BN/WGN) as 32 x 32 MFMA blocks. Blocks are numbered so that each
 // of the 8 XCDs (blocks b = x mod 8) walks a contiguous range of tiles (n
 // fastest): neighbouring tiles share operand panels in that XCD's L2.
 //
-// Pipeline per 64-deep k-stage kt (four 16-deep MFMA steps), one barrier:
-//   issue global loads of stage kt+1 (registers)
-//   steps 0..2: read fragments of step s+1      | MFMAs of step s
-//   store stage kt+1 into the other LDS buffer; barrier
-//   read step-0 fragments of stage kt+1         | MFMAs of step 3
-// so LDS latency always hides behind a run of MFMAs on held fragments.
-//
-// Epilogue: each wave turns its accumulators into output values (bias,
-// GELU + GELU', or GELU' product), parks them in LDS and writes every output
-// row back as full 16-byte-per-lane segments (one output at a time when two
-// do not fit in LDS together).
-template <int BM_, int BN_, int WGM, int WGN, bool A_KMAJOR, bool B_KMAJOR, int EPI, int DIST>
-__global__ __launch_bounds__(64 * WGM * WGN)
-__attribute__((amdgpu_waves_per_eu(WGM * WGN == 8 || BM_ * BN_ < 256 * 128 ? 2 : 1,
-                                   WGM * WGN == 8 || BM_ * BN_ < 256 * 128 ? 2 : 1)))
-void gemm_bf16_kernel(GemmArgs p, int tiles_m, int tiles_n, int per_xcd, int total) {
-    constexpr int NT = 64 * WGM * WGN;
-    constexpr int AE = stage_elems<BM_, A_KMAJOR>();
-    constexpr int BE = stage_elems<BN_, B_KMAJOR>();
-    constexpr int WM = BM_ / WGM, WN = BN_ / WGN;  // wave tile
-    constexpr int FM = WM / 32, FN = WN / 32;
-    constexpr int KSTEPS = BK / 16;
-    constexpr int VA = BM_ * 8 / NT, VB = BN_ * 8 / NT;  // staged vectors per thread
-    constexpr bool F32_OUT = EPI == EPI_F32;
-    constexpr int OUTS = EPI == EPI_FWD1 ? 2 : 1;
-    constexpr int SMEM_ELEMS = 2 * (AE + BE);
-    // Epilogue staging per wave: IPP of its FM 32-row blocks per pass, all
-    // outputs of those rows when they fit, else one output per pass.
-    constexpr int EP_LD = F32_OUT ? WN + 4 : WN + 4;
-    constexpr int ELEM = F32_OUT ? 4 : 2;
-    constexpr int EP_ROWBLK = 32 * EP_LD * ELEM;  // one 32-row block of one output
-    constexpr int NW = WGM * WGN;
-    constexpr int SMEM_BYTES = SMEM_ELEMS * 2;
-    constexpr int EP_OUTS_AT_ONCE = OUTS * FM * EP_ROWBLK * NW <= SMEM_BYTES ? OUTS : 1;
-    constexpr int IPP = EP_OUTS_AT_ONCE * FM * EP_ROWBLK * NW <= SMEM_BYTES ? FM
-                        : (EP_OUTS_AT_ONCE * (FM / 2) * EP_ROWBLK * NW <= SMEM_BYTES ? FM / 2 : 1);
-    constexpr int EP_TILE = IPP * EP_ROWBLK;       // bytes of one output's staged rows
-    static_assert(EP_OUTS_AT_ONCE * EP_TILE * NW <= SMEM_BYTES, "epilogue staging exceeds LDS");
-    static_assert(!F32_OUT || !A_KMAJOR, "row sums read an mn-major A tile");
-    static_assert(NT % BM_ == 0 || !F32_OUT, "row sums give each A row NT / BM threads");
-    static_assert(WM % 32 == 0 && WN % 32 == 0 && VA >= 1 && VB >= 1, "tile shape");
-    __shared__ __attribute__((aligned(16))) uint16_t smem[SMEM_ELEMS];
+// Pipeline over KB-deep k-stages, one barrier per stage, NS stage buffers
+// (separate LDS arrays, so every access names its buffer statically):
+//   issue the loads of stage kt + NS - 1 (DMA: straight into the buffer that
+//     stage kt - 1 used; REG: into registers, written to the other buffer
+//     before the barrier)
+//   steps 0 .. KSTEPS-2: read fragments of step s+1   | MFMAs of step s
+//   wait until stage kt + 1 has landed; barrier
+//   read step-0 fragments of stage kt+1               | MFMAs of the last step
+// so LDS latency always hides behind a run of MFMAs on held fragments, and
+// HBM latency behind NS - 1 stages of MFMAs. The stage count is rounded up to
+// a multiple of NS so the ring unrolls with static buffers; the padding
+// stages load zeros (out of range) and skip their MFMAs.
+template <class T, bool A_KMAJOR, bool B_KMAJOR, int EPI>
+__global__ __launch_bounds__(T::NT)
+__attribute__((amdgpu_waves_per_eu(T::WAVES_PER_EU, T::WAVES_PER_EU)))
+void gemm_bf16_kernel(GemmArgs p, int tiles_m, int tiles_n, int group_m, int per_xcd, int total) {
+    using CFG = GemmCfg<T, A_KMAJOR, B_KMAJOR, EPI>;
+    constexpr int BM_ = T::BM, BN_ = T::BN, KB = T::KB, NS = T::NS, MODE = T::MODE;
+    constexpr int NT = T::NT, AE = CFG::AE, BE = CFG::BE, FM = T::FM, FN = T::FN;
+    constexpr int KSTEPS = T::KSTEPS;
+    constexpr int SZ = AE + BE;
+    constexpr int SZX = SZ > 8 ? SZ : 8;
+    __shared__ __attribute__((aligned(1024))) uint16_t buf0[SZ];
+    __shared__ __attribute__((aligned(1024))) uint16_t buf1[SZ];
+    __shared__ __attribute__((aligned(1024))) uint16_t buf2[NS > 2 ? SZX : 8];
+    __shared__ __attribute__((aligned(1024))) uint16_t buf3[NS > 3 ? SZX : 8];
+    __shared__ __attribute__((aligned(1024))) uint16_t buf4[NS > 4 ? SZX : 8];
 
     const int b = blockIdx.x;
     const int w = (b & 7) * per_xcd + (b >> 3);
     if (w >= total) return;
-    const int tn = w % tiles_n;
-    const int tm = (w / tiles_n) % tiles_m;
-    const int e = w / (tiles_n * tiles_m);
+    // inside one expert, tiles go in groups of group_m m-tiles, m fastest, so
+    // the blocks resident on an XCD at once cover a compact patch of the output
+    // and share both operand panels in its L2
+    const int tiles_e = tiles_m * tiles_n;
+    const int e = w / tiles_e;
+    const int r = w - e * tiles_e;
+    const int grp = r / (group_m * tiles_n);
+    const int first_m = grp * group_m;
+    const int gm = min(group_m, tiles_m - first_m);
+    const int idx = r - grp * group_m * tiles_n;
+    const int tm = first_m + idx % gm;
+    const int tn = idx / gm;
 
     const int ne = expert_rows(p.counts, p.G, p.E, e);
     const int M = p.var_k ? p.M : ne;
@@ -287,12 +564,12 @@ void gemm_bf16_kernel(GemmArgs p, int tiles_m, int tiles_n, int per_xcd, int tot
         static_cast<const uint16_t*>(p.b.base) + e * p.b.estride, p.b.estride * 2);
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
-    const int wm = wave / WGN, wn = wave % WGN;
+    const int wm = wave / T::WGN, wn = wave % T::WGN;
     // weight-gradient GEMMs: the first n-tile also sums its A rows (bias grad);
     // thread t adds row t % BM over k slice t / BM of each stage
-    const bool row_sum = F32_OUT && p.bsum != nullptr && tn == 0;
-    constexpr int RS_SPLIT = F32_OUT ? NT / BM_ : 1;
-    constexpr int RS_K = BK / RS_SPLIT;
+    const bool row_sum = CFG::F32_OUT && p.bsum != nullptr && tn == 0;
+    constexpr int RS_SPLIT = CFG::F32_OUT ? NT / BM_ : 1;
+    constexpr int RS_K = KB / RS_SPLIT;
     float rsum = 0.0f;
 
     f32x16 acc[FM][FN];
@@ -303,179 +580,150 @@ void gemm_bf16_kernel(GemmArgs p, int tiles_m, int tiles_n, int per_xcd, int tot
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-    const int nk = (K + BK - 1) / BK;
-    uint4 ra0[VA], rb0[VB], ra1[VA], rb1[VB];
-    Frags<BM_, BN_, WGM, WGN, A_KMAJOR, B_KMAJOR> f0, f1;
+    using DA = DmaStage<BM_, A_KMAJOR, KB, NT>;
+    using DB = DmaStage<BN_, B_KMAJOR, KB, NT>;
+    using RA = RegStage<BM_, A_KMAJOR, KB, NT>;
+    using RB = RegStage<BN_, B_KMAJOR, KB, NT>;
+    // DMA wave instructions per stage; stage kt + 1 has landed once at most
+    // NS - 2 later stages are still in flight
+    constexpr int L = DA::PER + DB::PER;
+    constexpr int WAIT_IMM = VmWait<MODE == STAGE_DMA && !T::PAIR ? (NS - 2) * L : 0>::imm;
+    // paired fetch: after an even stage the pair issued in it is in flight,
+    // after an odd stage the second half of the previous pair
+    constexpr int WAIT_EVEN = VmWait<T::PAIR ? 2 * L : 0>::imm;
+    constexpr int WAIT_ODD = VmWait<T::PAIR ? L : 0>::imm;
+    BiasRegs<T, EPI> bias;
+    bias.load(p, e, N, n0, wn, lane);
+    const int nk = (K + KB - 1) / KB;
+    const int nk_ring = (nk + NS - 1) / NS * NS;
+    Frags<T, A_KMAJOR, B_KMAJOR, MODE> f0, f1;
+    uint4 ra[MODE == STAGE_REG ? RA::V : 1], rb[MODE == STAGE_REG ? RB::V : 1];
 
-    load_stage<BM_, A_KMAJOR, NT>(ra_rs, p.a.ld, m0, M, 0, K, ra0);
-    load_stage<BN_, B_KMAJOR, NT>(rb_rs, p.b.ld, n0, N, 0, K, rb0);
-    if constexpr (DIST == 2) {
-        load_stage<BM_, A_KMAJOR, NT>(ra_rs, p.a.ld, m0, M, BK, K, ra1);
-        load_stage<BN_, B_KMAJOR, NT>(rb_rs, p.b.ld, n0, N, BK, K, rb1);
+    auto issue = [&](int kt, uint16_t* dst) {
+        DA::issue(ra_rs, p.a.ld, m0, M, kt * KB, K, dst);
+        DB::issue(rb_rs, p.b.ld, n0, N, kt * KB, K, dst + AE);
+    };
+    if constexpr (MODE == STAGE_DMA) {
+        issue(0, buf0);
+        if constexpr (T::PAIR) {
+            issue(1, buf1);
+            __builtin_amdgcn_s_waitcnt(WAIT_ODD);
+        } else {
+            if constexpr (NS > 2) issue(1, buf1);
+            if constexpr (NS > 3) issue(2, buf2);
+            if constexpr (NS > 4) issue(3, buf3);
+            __builtin_amdgcn_s_waitcnt(WAIT_IMM);
+        }
+        ring_barrier();
+    } else {
+        RA::load(ra_rs, p.a.ld, m0, M, 0, K, ra);
+        RB::load(rb_rs, p.b.ld, n0, N, 0, K, rb);
+        RA::store(buf0, ra);
+        RB::store(buf0 + AE, rb);
+        __syncthreads();
     }
-    store_stage<BM_, A_KMAJOR, NT>(smem, ra0);
-    store_stage<BN_, B_KMAJOR, NT>(smem + AE, rb0);
-    __syncthreads();
-    f0.read(smem, smem + AE, wm, wn, 0, lane);
+    f0.read(buf0, buf0 + AE, wm, wn, 0, lane);
 
-    // One k-stage. With DIST = 2 the register set PAR receives stage kt + 2
-    // while the other set (stage kt + 1, loaded a stage earlier) goes to LDS.
-    auto stage = [&](const int kt, auto par) {
-        constexpr int PAR = decltype(par)::value;
-        uint4(&la)[VA] = (DIST == 1 || PAR == 0) ? ra0 : ra1;
-        uint4(&lb)[VB] = (DIST == 1 || PAR == 0) ? rb0 : rb1;
-        uint4(&sa)[VA] = (DIST == 1 || PAR == 1) ? ra0 : ra1;
-        uint4(&sb)[VB] = (DIST == 1 || PAR == 1) ? rb0 : rb1;
-        uint16_t* As = smem + (kt & 1) * (AE + BE);
-        uint16_t* An = smem + ((kt + 1) & 1) * (AE + BE);
-        load_stage<BM_, A_KMAJOR, NT>(ra_rs, p.a.ld, m0, M, (kt + DIST) * BK, K, la);
-        load_stage<BN_, B_KMAJOR, NT>(rb_rs, p.b.ld, n0, N, (kt + DIST) * BK, K, lb);
-        if constexpr (F32_OUT) {
-            if (row_sum) {
-                const uint16_t* col = As + (tid / BM_) * RS_K * (BM_ + MNPAD) + tid % BM_;
-#pragma unroll 8
-                for (int kk = 0; kk < RS_K; ++kk) rsum += bf16_to_f32(col[kk * (BM_ + MNPAD)]);
+    // stage kt computes from `cur`, refills `tgt` (the buffer of stage kt - 1;
+    // paired fetch: at even kt, `tgt` and `tgt2` with stages kt + 2 and kt + 3)
+    // and leaves the step-0 fragments of `nxt` in f0
+    auto stage = [&](const int kt, uint16_t* cur, uint16_t* nxt, uint16_t* tgt, uint16_t* tgt2,
+                     auto parity) {
+        constexpr bool EVEN = decltype(parity)::value == 0;
+        if constexpr (T::PAIR) {
+            if constexpr (EVEN) {
+                issue(kt + 2, tgt);
+                issue(kt + 3, tgt2);
+            }
+        } else if constexpr (MODE == STAGE_DMA) {
+            issue(kt + NS - 1, tgt);
+        } else {
+            RA::load(ra_rs, p.a.ld, m0, M, (kt + 1) * KB, K, ra);
+            RB::load(rb_rs, p.b.ld, n0, N, (kt + 1) * KB, K, rb);
+        }
+        const bool live = kt < nk;  // uniform: ring padding stages skip their MFMAs
+        if (live) {
+            if constexpr (CFG::F32_OUT) {
+                if (row_sum) {
+                    const int mn = tid % BM_, k0 = (tid / BM_) * RS_K;
+#pragma unroll
+                    for (int kk = 0; kk < RS_K; ++kk)
+                        rsum += bf16_to_f32(cur[lds_off<BM_, false, KB, MODE>(mn, k0 + kk)]);
+                }
+            }
+#pragma unroll
+            for (int s = 0; s < KSTEPS - 1; ++s) {
+                if (s % 2 == 0) {
+                    f1.read(cur, cur + AE, wm, wn, s + 1, lane);
+                    __builtin_amdgcn_sched_barrier(0);
+                    mfma_block(acc, f0);
+                } else {
+                    f0.read(cur, cur + AE, wm, wn, s + 1, lane);
+                    __builtin_amdgcn_sched_barrier(0);
+                    mfma_block(acc, f1);
+                }
+                __builtin_amdgcn_sched_barrier(0);
             }
         }
-#pragma unroll
-        for (int s = 0; s < KSTEPS - 1; ++s) {
-            if (s % 2 == 0) {
-                f1.read(As, As + AE, wm, wn, s + 1, lane);
-                __builtin_amdgcn_sched_barrier(0);
-                mfma_block(acc, f0);
-            } else {
-                f0.read(As, As + AE, wm, wn, s + 1, lane);
-                __builtin_amdgcn_sched_barrier(0);
-                mfma_block(acc, f1);
-            }
+        if constexpr (T::PAIR) {
+            __builtin_amdgcn_s_waitcnt(EVEN ? WAIT_EVEN : WAIT_ODD);
+            ring_barrier();
+        } else if constexpr (MODE == STAGE_DMA) {
+            __builtin_amdgcn_s_waitcnt(WAIT_IMM);
+            ring_barrier();
+        } else {
+            RA::store(nxt, ra);
+            RB::store(nxt + AE, rb);
+            __syncthreads();
+        }
+        if (live) {
+            // KSTEPS is even: the last step's fragments are in f1
+            f0.read(nxt, nxt + AE, wm, wn, 0, lane);
+            __builtin_amdgcn_sched_barrier(0);
+            mfma_block(acc, f1);
             __builtin_amdgcn_sched_barrier(0);
         }
-        store_stage<BM_, A_KMAJOR, NT>(An, sa);
-        store_stage<BN_, B_KMAJOR, NT>(An + AE, sb);
-        __syncthreads();
-        // KSTEPS is even: the last step's fragments are in f1
-        f0.read(An, An + AE, wm, wn, 0, lane);
-        __builtin_amdgcn_sched_barrier(0);
-        mfma_block(acc, f1);
-        __builtin_amdgcn_sched_barrier(0);
     };
-    // Whole pairs first, without a conditional half: a skipped half would merge
-    // a path with loads still in flight into the loop head, and the compiler
-    // would then drain every outstanding load before the next set is issued.
-    int kt = 0;
-    for (; kt + 1 < nk; kt += 2) {
-        stage(kt, std::integral_constant<int, 0>{});
-        stage(kt + 1, std::integral_constant<int, 1>{});
-    }
-    if (kt < nk) stage(kt, std::integral_constant<int, 0>{});
-    __syncthreads();  // every wave is done with the operand stages
-
-    if constexpr (F32_OUT) {
-        if (row_sum) {  // uniform per block
-            float* part = reinterpret_cast<float*>(smem);
-            part[tid] = rsum;
-            __syncthreads();
-            if (tid < BM_ && m0 + tid < M) {
-                float t = part[tid];
-#pragma unroll
-                for (int q = 1; q < RS_SPLIT; ++q) t += part[tid + q * BM_];
-                p.bsum[static_cast<size_t>(e) * M + m0 + tid] = t;
-            }
-            __syncthreads();
+    // The ring unrolls NS stages per trip with no conditional stage: a skipped
+    // stage would merge a path with loads still in flight into the loop head.
+    using P0 = std::integral_constant<int, 0>;
+    using P1 = std::integral_constant<int, 1>;
+    for (int kt = 0; kt < nk_ring; kt += NS) {
+        if constexpr (NS == 2) {
+            stage(kt, buf0, buf1, buf1, buf1, P0{});
+            stage(kt + 1, buf1, buf0, buf0, buf0, P1{});
+        } else if constexpr (NS == 3) {
+            stage(kt, buf0, buf1, buf2, buf2, P0{});
+            stage(kt + 1, buf1, buf2, buf0, buf0, P1{});
+            stage(kt + 2, buf2, buf0, buf1, buf1, P0{});
+        } else if constexpr (NS == 4 && T::PAIR) {
+            stage(kt, buf0, buf1, buf2, buf3, P0{});
+            stage(kt + 1, buf1, buf2, buf0, buf0, P1{});
+            stage(kt + 2, buf2, buf3, buf0, buf1, P0{});
+            stage(kt + 3, buf3, buf0, buf0, buf0, P1{});
+        } else if constexpr (NS == 4) {
+            stage(kt, buf0, buf1, buf3, buf3, P0{});
+            stage(kt + 1, buf1, buf2, buf0, buf0, P1{});
+            stage(kt + 2, buf2, buf3, buf1, buf1, P0{});
+            stage(kt + 3, buf3, buf0, buf2, buf2, P1{});
+        } else {
+            stage(kt, buf0, buf1, buf4, buf4, P0{});
+            stage(kt + 1, buf1, buf2, buf0, buf0, P1{});
+            stage(kt + 2, buf2, buf3, buf1, buf1, P0{});
+            stage(kt + 3, buf3, buf4, buf2, buf2, P1{});
+            stage(kt + 4, buf4, buf0, buf3, buf3, P0{});
         }
     }
+    // every wave is done with the operand stages (LDS reads retired, DMA landed)
+    if constexpr (MODE == STAGE_DMA) __builtin_amdgcn_s_waitcnt(VmWait<0>::imm);
+    else __builtin_amdgcn_s_waitcnt(VmWait<63>::imm);
+    ring_barrier();
 
-    char* ep = reinterpret_cast<char*>(smem) + wave * EP_OUTS_AT_ONCE * EP_TILE;
-    constexpr int SEG = 16 / ELEM;                 // elements per 16-byte segment
-    constexpr int LANES_PER_ROW = WN / SEG;
-    constexpr int ROWS_PER_PASS = 64 / LANES_PER_ROW;
-    static_assert(LANES_PER_ROW <= 64 && 64 % LANES_PER_ROW == 0, "epilogue row split");
-
-#pragma unroll
-    for (int i0 = 0; i0 < FM; i0 += IPP)
-#pragma unroll
-    for (int o0 = 0; o0 < OUTS; o0 += EP_OUTS_AT_ONCE) {
-        // Stage 1: values into this wave's LDS tiles. Register 4q + r of lane l
-        // holds C[m][n + r] with m = 32 i + l % 32, n = 32 j + 8 q + 4 (l / 32)
-        // inside the wave tile.
-#pragma unroll
-        for (int ii = 0; ii < IPP; ++ii)
-#pragma unroll
-            for (int j = 0; j < FN; ++j)
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const int i = i0 + ii;
-                    const int ml = ii * 32 + (lane & 31);  // row inside the staged rows
-                    const int nl = j * 32 + 8 * q + 4 * (lane >> 5);
-                    const f32x16& v = acc[i][j];
-                    float r[4] = {v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]};
-                    if constexpr (F32_OUT) {
-                        *reinterpret_cast<float4*>(reinterpret_cast<float*>(ep) + ml * EP_LD +
-                                                   nl) = make_float4(r[0], r[1], r[2], r[3]);
-                    } else {
-                        const int n = n0 + wn * WN + nl;
-                        const int m = m0 + wm * WM + i * 32 + (lane & 31);
-                        if constexpr (EPI == EPI_FWD1 || EPI == EPI_BIAS) {
-                            if (n < N) {
-                                const uint2 bb = *reinterpret_cast<const uint2*>(
-                                    static_cast<const uint16_t*>(p.bias) + e * p.bias_estride + n);
-                                r[0] += bf16_to_f32(bb.x & 0xFFFFu);
-                                r[1] += bf16_to_f32(bb.x >> 16);
-                                r[2] += bf16_to_f32(bb.y & 0xFFFFu);
-                                r[3] += bf16_to_f32(bb.y >> 16);
-                            }
-                        }
-                        if constexpr (EPI == EPI_GELU_GRAD) {
-                            if (n < N && m < M) {
-                                const uint2 gg = *reinterpret_cast<const uint2*>(
-                                    static_cast<const uint16_t*>(p.aux) + e * p.out_estride +
-                                    static_cast<size_t>(m) * p.ldo + n);
-                                r[0] *= bf16_to_f32(gg.x & 0xFFFFu);
-                                r[1] *= bf16_to_f32(gg.x >> 16);
-                                r[2] *= bf16_to_f32(gg.y & 0xFFFFu);
-                                r[3] *= bf16_to_f32(gg.y >> 16);
-                            }
-                        }
-                        uint16_t* t0 = reinterpret_cast<uint16_t*>(ep) + ml * EP_LD + nl;
-                        if constexpr (EPI == EPI_FWD1) {
-                            float g[4], dg[4];
-#pragma unroll
-                            for (int c = 0; c < 4; ++c) gelu_pair(r[c], g[c], dg[c]);
-#pragma unroll
-                            for (int o = 0; o < EP_OUTS_AT_ONCE; ++o) {
-                                const float* src = (o0 + o == 0) ? g : dg;
-                                *reinterpret_cast<uint2*>(t0 + o * (EP_TILE / 2)) =
-                                    make_uint2(pack_bf16x2(src[0], src[1]),
-                                               pack_bf16x2(src[2], src[3]));
-                            }
-                        } else {
-                            *reinterpret_cast<uint2*>(t0) =
-                                make_uint2(pack_bf16x2(r[0], r[1]), pack_bf16x2(r[2], r[3]));
-                        }
-                    }
-                }
-        __syncthreads();
-
-        // Stage 2: staged rows out in 16-byte segments.
-        const int cl = (lane % LANES_PER_ROW) * SEG;
-        const int n = n0 + wn * WN + cl;
-#pragma unroll
-        for (int o = 0; o < EP_OUTS_AT_ONCE; ++o) {
-            char* dst_base = static_cast<char*>(o0 + o == 0 ? p.out : p.out2);
-#pragma unroll
-            for (int pass = 0; pass < IPP * 32 / ROWS_PER_PASS; ++pass) {
-                const int ml = pass * ROWS_PER_PASS + lane / LANES_PER_ROW;
-                const int m = m0 + wm * WM + i0 * 32 + ml;
-                const uint4 v =
-                    *reinterpret_cast<const uint4*>(ep + o * EP_TILE + (ml * EP_LD + cl) * ELEM);
-                if (m < M && n < N)
-                    *reinterpret_cast<uint4*>(
-                        dst_base + (e * p.out_estride + static_cast<size_t>(m) * p.ldo + n) * ELEM) =
-                        v;
-            }
-        }
-        __syncthreads();
-    }
+    // wave w parks its outputs in stage buffer w mod NS (a select over the
+    // arrays themselves keeps the accesses in the LDS address space)
+    const int eb = wave % NS;
+    uint16_t* const ep = eb == 0 ? buf0 : eb == 1 ? buf1 : eb == 2 ? buf2 : eb == 3 ? buf3 : buf4;
+    gemm_epilogue<T, CFG, EPI>(p, acc, bias, buf0, ep, rsum, row_sum, e, M, N, m0, n0);
 }
 
 // ------------------------------------------------------------------ f32 FMA path
@@ -568,28 +816,32 @@ __global__ __launch_bounds__(256) void colsum_kernel(const T* __restrict__ src,
                                                   part[2][c & 63]) + part[3][c & 63];
 }
 
-template <int BM_, int BN_, int WGM, int WGN, bool AK, bool BK_, int EPI, int DIST = 1>
+template <class T, bool AK, bool BK_, int EPI>
 void launch_bf16(const Dims& D, const GemmArgs& a, int grid_m_rows, hipStream_t st) {
-    const int tiles_m = static_cast<int>(cdiv(grid_m_rows, BM_));
-    const int tiles_n = static_cast<int>(cdiv(a.N, BN_));
+    const int tiles_m = static_cast<int>(cdiv(grid_m_rows, T::BM));
+    const int tiles_n = static_cast<int>(cdiv(a.N, T::BN));
     const int total = D.E * tiles_m * tiles_n;
     const int per_xcd = static_cast<int>(cdiv(total, 8));
-    gemm_bf16_kernel<BM_, BN_, WGM, WGN, AK, BK_, EPI, DIST><<<8 * per_xcd, 64 * WGM * WGN, 0,
-                                                               st>>>(a, tiles_m, tiles_n, per_xcd,
-                                                                     total);
+    // blocks resident on one XCD: 32 CUs x blocks per CU
+    const int group_m = T::WAVES_PER_EU == 2 && T::NW == 4 ? 8 : 4;
+    gemm_bf16_kernel<T, AK, BK_, EPI><<<8 * per_xcd, T::NT, 0, st>>>(a, tiles_m, tiles_n, group_m,
+                                                                     per_xcd, total);
 }
+
+// Tilings (BM, BN, waves, KB, stages, staging).
+using TileBig = Tile<256, 256, 2, 4, 32, 4, STAGE_DMA>;    // 8 waves, one block per CU
+using TileSmall = Tile<128, 128, 2, 2, 32, 4, STAGE_DMA>;  // 4 waves, two blocks per CU
 
 template <bool AK, bool BK_, int EPI>
 void launch_gemm(const Dims& D, const GemmArgs& a, int grid_m_rows, hipStream_t st) {
     if (D.dtype == VMOE_BF16) {
-        // 128 x 128 tiles (4 waves, two blocks per CU) for the short-k GEMMs and
-        // the weight gradients; 256 x 256 tiles of 8 waves (half the LDS traffic
-        // per flop) for the long-k GEMMs with one plain bf16 output (the
-        // down-projection and dxe)
-        if constexpr (EPI == EPI_BIAS || EPI == EPI_STORE)
-            launch_bf16<256, 256, 2, 4, AK, BK_, EPI>(D, a, grid_m_rows, st);
+        // 256 x 256 tiles (half the operand bytes per flop of 128 x 128) for
+        // the GEMMs whose m is the expert's rows; the weight gradients (k is
+        // the rows, often short) run 128 x 128 tiles, two blocks per CU
+        if constexpr (EPI == EPI_F32)
+            launch_bf16<TileSmall, AK, BK_, EPI>(D, a, grid_m_rows, st);
         else
-            launch_bf16<128, 128, 2, 2, AK, BK_, EPI>(D, a, grid_m_rows, st);
+            launch_bf16<TileBig, AK, BK_, EPI>(D, a, grid_m_rows, st);
     } else {
         dim3 grid(cdiv(a.N, FT), cdiv(grid_m_rows, FT), D.E);
         gemm_f32_kernel<AK, BK_, EPI><<<grid, 256, 0, st>>>(a);

@@ -28,7 +28,7 @@ constexpr int kBinBits = 12;
 constexpr int kNumBins = 1 << kBinBits;
 constexpr int kBinShift = kKeyBits - kBinBits;
 constexpr int kSlotChunk = 256;              // order positions per slots block
-constexpr int kGateTokens = 256;             // most tokens per router_gate block (E = 1)
+constexpr int kGateTokens = 32;              // most tokens per router_gate block
 
 struct RouteWs {
     uint32_t* keys;     // [N]
@@ -112,48 +112,150 @@ __device__ __forceinline__ void load8(const float* p, float* v) {
     v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
 }
 
-// One block = tpb = floor(256 / E) tokens of one group. Thread tid < tpb*E
+// x and W_r are staged in LDS 32 vectors of 16 bytes (256 bf16 / 128 f32
+// columns) per row at a time; rows are padded by one vector so the 16-byte
+// reads of different rows fall in different banks.
+constexpr int kGateVecs = 32;
+
+// One block = tpb = min(32, floor(256 / E)) tokens of one group. Thread tid < tpb*E
 // computes logit (token tid / E, expert tid % E) as a sequential dot product
-// in double over increasing i, 8 elements (one 16-byte load) at a time, so
-// every (token, expert) pair is its own dependency chain and the whole grid
-// is busy; the gate of each token then runs on one thread from LDS.
+// in double over increasing i; the block's x rows and the group's router rows
+// are staged through LDS a slice of columns at a time (coalesced 16-byte loads,
+// next round prefetched in registers), so the dependency chains only wait on
+// LDS. The gate of each token then runs on one thread from LDS.
 template <typename T>
 __global__ __launch_bounds__(256) void router_gate_kernel(
     const T* __restrict__ x, const T* __restrict__ wr, const float* __restrict__ bias,
     const float* __restrict__ noise, float* __restrict__ logits, float* __restrict__ probs,
     int32_t* __restrict__ idx, uint32_t* __restrict__ keys, int Ng, int d, int E, int k,
     int logits_in, int tpb) {
-    __shared__ float lg_store[2 * kGateTokens];  // tpb * (E + 1) <= 256 + tpb
+    constexpr int VE = 16 / sizeof(T);             // elements per 16-byte vector
+    constexpr int VPR = kGateVecs;                 // vectors per staged row
+    constexpr int GC = VPR * VE;                   // columns per round
+    constexpr int LDR = GC + VE;                   // LDS row length (elements)
+    constexpr int MAXROWS = kGateTokens + kMaxExperts;
+    __shared__ __attribute__((aligned(16))) T stage[MAXROWS * LDR];
+    __shared__ float lg_store[kGateTokens * (kMaxExperts + 1)];
+    __shared__ int row_bad[2][MAXROWS];
     const int g = blockIdx.y;
     const int t0 = blockIdx.x * tpb;                  // within group
     const int ntok = min(tpb, Ng - t0);
     const size_t tok0 = static_cast<size_t>(g) * Ng + t0;  // global index
     const int tid = threadIdx.x;
     const int ld = E + 1;                             // LDS row of one token's logits
-    if (tid < ntok * E) {
-        const int tt = tid / E, e = tid % E;
-        float v;
-        if (!logits_in) {
-            const T* xr = x + (tok0 + tt) * d;
-            const T* wrow = wr + (static_cast<size_t>(g) * E + e) * d;
-            double acc = 0.0;
-            // Each product of two bf16 / f32 values is exact in double, so the
-            // fused multiply-add equals add-after-multiply, in increasing i.
-#pragma unroll 2
-            for (int i = 0; i < d; i += 8) {
-                float xv[8], wv[8];
-                load8(xr + i, xv);
-                load8(wrow + i, wv);
+    if (!logits_in) {
+        // staged rows: ntok token rows, then E router rows
+        const int rows = ntok + E;
+        const T* wg = wr + static_cast<size_t>(g) * E * d;
+        constexpr int MAXV = (MAXROWS * VPR + 255) / 256;  // vectors per thread per round
+        const int nvec = rows * VPR;
+        uint4 pre[MAXV];
+        auto fetch = [&](int c0) {
 #pragma unroll
-                for (int q = 0; q < 8; ++q)
-                    acc = __builtin_fma(static_cast<double>(xv[q]), static_cast<double>(wv[q]), acc);
+            for (int q = 0; q < MAXV; ++q) {
+                const int v = tid + 256 * q;
+                const int r = v / VPR, col = c0 + (v % VPR) * VE;
+                pre[q] = make_uint4(0u, 0u, 0u, 0u);
+                if (v < nvec && col < d) {
+                    const T* src = r < ntok ? x + (tok0 + r) * d + col
+                                            : wg + static_cast<size_t>(r - ntok) * d + col;
+                    pre[q] = *reinterpret_cast<const uint4*>(src);
+                }
             }
-            v = static_cast<float>(acc);
-            logits[(tok0 + tt) * E + e] = v;
-        } else {
-            v = logits[(tok0 + tt) * E + e];
+        };
+        // bf16 rows whose staged values are all zero or of magnitude in
+        // [2^-63, 2^63) give products that are exact normal f32 numbers; a row
+        // with any other value (subnormal, huge, inf, nan) is marked in
+        // row_bad[round parity] and its dot products take the f64 path
+        auto park = [&](int par) {
+#pragma unroll
+            for (int q = 0; q < MAXV; ++q) {
+                const int v = tid + 256 * q;
+                if (v < nvec) {
+                    *reinterpret_cast<uint4*>(stage + (v / VPR) * LDR + (v % VPR) * VE) = pre[q];
+                    if constexpr (sizeof(T) == 2) {
+                        const uint32_t w4[4] = {pre[q].x, pre[q].y, pre[q].z, pre[q].w};
+                        bool bad = false;
+#pragma unroll
+                        for (int h = 0; h < 8; ++h) {
+                            const uint32_t b = (w4[h >> 1] >> (16 * (h & 1))) & 0x7FFFu;
+                            const uint32_t ex = b >> 7;
+                            bad |= b != 0 && (ex < 64 || ex > 189);
+                        }
+                        if (bad) atomicOr(&row_bad[par][v / VPR], 1);
+                    }
+                }
+            }
+        };
+        const bool mine = tid < ntok * E;
+        const int tt = tid / E, e = tid % E;
+        const T* xs = stage + tt * LDR;
+        const T* wsr = stage + (ntok + e) * LDR;
+        double acc = 0.0;
+        for (int r = tid; r < 2 * MAXROWS; r += 256) row_bad[r / MAXROWS][r % MAXROWS] = 0;
+        __syncthreads();
+        fetch(0);
+        for (int c0 = 0, par = 0; c0 < d; c0 += GC, par ^= 1) {
+            park(par);
+            __syncthreads();
+            if (c0 + GC < d) fetch(c0 + GC);
+            // the other parity's flags were last read in the previous round
+            for (int r = tid; r < MAXROWS; r += 256) row_bad[par ^ 1][r] = 0;
+            const bool exact_f32 = mine && row_bad[par][tt] == 0 && row_bad[par][ntok + e] == 0;
+            if (mine) {
+                const int n = min(GC, d - c0);
+                // Each product of two bf16 / f32 values is exact in double, so
+                // the fused multiply-add equals add-after-multiply, in increasing i.
+                // 32 columns per step; the next step's LDS reads are issued
+                // before this step's multiply-add chain. Staged columns past d
+                // are zeros: their products add +0 to a sum that starts at +0
+                // and so can never be -0, which leaves it unchanged.
+                const int nn = (n + 31) & ~31;
+                float xv[2][32], wv[2][32];
+                auto read32 = [&](int i, float (&xa)[32], float (&wa)[32]) {
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        load8(xs + i + 8 * q, xa + 8 * q);
+                        load8(wsr + i + 8 * q, wa + 8 * q);
+                    }
+                };
+                auto chain32 = [&](const float (&xa)[32], const float (&wa)[32]) {
+                    if (sizeof(T) == 2 && exact_f32) {
+                        // bf16 x bf16 is exact in f32 (8-bit significands), so
+                        // acc + double(x * w) rounds exactly like the fused
+                        // multiply-add in double; the products and widenings
+                        // are off the dependency chain, which is the adds
+                        double pd[32];
+#pragma unroll
+                        for (int q = 0; q < 32; ++q) pd[q] = static_cast<double>(xa[q] * wa[q]);
+#pragma unroll
+                        for (int q = 0; q < 32; ++q) acc = acc + pd[q];
+                    } else {
+#pragma unroll
+                        for (int q = 0; q < 32; ++q)
+                            acc = __builtin_fma(static_cast<double>(xa[q]),
+                                                static_cast<double>(wa[q]), acc);
+                    }
+                };
+                read32(0, xv[0], wv[0]);
+                for (int i = 0; i < nn; i += 64) {
+                    const bool two = i + 32 < nn;  // uniform
+                    if (two) read32(i + 32, xv[1], wv[1]);
+                    chain32(xv[0], wv[0]);
+                    if (i + 64 < nn) read32(i + 64, xv[0], wv[0]);
+                    if (two) chain32(xv[1], wv[1]);
+                }
+            }
+            __syncthreads();
         }
-        lg_store[tt * ld + e] = v;
+        if (mine) {
+            const float v = static_cast<float>(acc);
+            logits[(tok0 + tt) * E + e] = v;
+            lg_store[tt * ld + e] = v;
+        }
+    } else if (tid < ntok * E) {
+        const int tt = tid / E, e = tid % E;
+        lg_store[tt * ld + e] = logits[(tok0 + tt) * E + e];
     }
     __syncthreads();
 
@@ -374,7 +476,7 @@ vmoe_status route_launch(const Dims& D, const void* x, const void* wr, const flo
     const int nch = static_cast<int>(cdiv(D.Ng, kSlotChunk));
     const int logits_in = (flags & VMOE_ROUTE_LOGITS_IN) ? 1 : 0;
     if (D.N > 0) {
-        const int tpb = 256 / D.E;
+        const int tpb = min(kGateTokens, 256 / D.E);
         dim3 grid(cdiv(D.Ng, tpb), D.G);
         if (D.dtype == VMOE_BF16)
             router_gate_kernel<uint16_t><<<grid, 256, 0, st>>>(

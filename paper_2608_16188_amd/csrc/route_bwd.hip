@@ -1,39 +1,80 @@
 // Backward through the gate into the router on gfx950.
 //
-// A block owns a chunk of tokens of one group and 256 model columns. It first
-// forms dz = p * (dp - <p, dp>) for its tokens in LDS (dp is non-zero only at
-// the kept experts), then streams the columns: dx[t, i] += sum_e dz[t,e] W[e,i]
-// and a per-chunk partial of dW_r[e, i] = sum_t dz[t,e] x[t,i]. A second
-// kernel adds the partials over chunks in a fixed order (deterministic, no
-// float atomics).
+// A block owns a chunk of tokens of one group and a slice of model columns;
+// per token it forms dz = p * (dp - <p, dp>) (dp is non-zero only at the kept
+// experts), adds dz W into dx and accumulates a per-chunk partial of
+// dW_r[e, i] = sum_t dz[t,e] x[t,i]. A second kernel adds the partials over
+// chunks in a fixed order (deterministic, no float atomics).
 #include "common.h"
 
 namespace vmoe {
 namespace {
 
-constexpr int kCols = 256;
 constexpr int kMinChunk = 64;
 constexpr int kMaxChunk = 256;
 
-template <typename T> __device__ __forceinline__ float ld(const T* p, size_t i);
-template <> __device__ __forceinline__ float ld<float>(const float* p, size_t i) { return p[i]; }
-template <> __device__ __forceinline__ float ld<uint16_t>(const uint16_t* p, size_t i) {
-    return bf16_to_f32(p[i]);
+// VEC consecutive columns of a token row as f32 (VEC * sizeof(T) bytes, aligned).
+template <int VEC>
+__device__ __forceinline__ void load_cols(const uint16_t* p, float (&v)[VEC]) {
+    if constexpr (VEC == 4) {
+        const uint2 u = *reinterpret_cast<const uint2*>(p);
+        v[0] = bf16_to_f32(u.x & 0xFFFFu); v[1] = bf16_to_f32(u.x >> 16);
+        v[2] = bf16_to_f32(u.y & 0xFFFFu); v[3] = bf16_to_f32(u.y >> 16);
+    } else if constexpr (VEC == 2) {
+        const uint32_t u = *reinterpret_cast<const uint32_t*>(p);
+        v[0] = bf16_to_f32(u & 0xFFFFu); v[1] = bf16_to_f32(u >> 16);
+    } else {
+        v[0] = bf16_to_f32(*p);
+    }
+}
+template <int VEC>
+__device__ __forceinline__ void load_cols(const float* p, float (&v)[VEC]) {
+    if constexpr (VEC == 4) {
+        const float4 u = *reinterpret_cast<const float4*>(p);
+        v[0] = u.x; v[1] = u.y; v[2] = u.z; v[3] = u.w;
+    } else if constexpr (VEC == 2) {
+        const float2 u = *reinterpret_cast<const float2*>(p);
+        v[0] = u.x; v[1] = u.y;
+    } else {
+        v[0] = *p;
+    }
+}
+template <int VEC>
+__device__ __forceinline__ void store_cols(float* p, const float (&v)[VEC]) {
+    if constexpr (VEC == 4) *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+    else if constexpr (VEC == 2) *reinterpret_cast<float2*>(p) = make_float2(v[0], v[1]);
+    else *p = v[0];
 }
 
+// Columns per lane: the E x VEC router weights and E x VEC gradient partials
+// of a lane stay in registers.
+template <int EMAX> struct ColsPerLane { static constexpr int value = EMAX <= 8 ? 4 : (EMAX <= 16 ? 2 : 1); };
+
+// A block owns a chunk of tch tokens of one group and 64 * VEC columns. It
+// first forms dz = p * (dp - <p, dp>) of its tokens in LDS (dp non-zero only at
+// kept experts); wave w then takes the chunk's tokens w, w + 4, ... (a whole
+// row slice per token, so dz is a broadcast read) and does
+// dx[t, cols] += sum_e dz[e] W[e, cols] and acc[e][cols] += dz[e] x[t, cols].
+// The four waves' accumulators are added in wave order into the chunk's
+// partial of dW_r.
 template <typename T, int EMAX>
-__global__ __launch_bounds__(kCols) void route_bwd_kernel(
+__global__ __launch_bounds__(256) void route_bwd_kernel(
     const T* __restrict__ x, const T* __restrict__ wr, const float* __restrict__ probs,
     const int32_t* __restrict__ idx, const int32_t* __restrict__ slot,
     const float* __restrict__ dgate, float* __restrict__ dx, float* __restrict__ partial, int Ng,
     int d, int E, int k, int tch, int nch) {
+    constexpr int VEC = ColsPerLane<EMAX>::value;
+    constexpr int COLS = 64 * VEC;
+    __shared__ float red[3][EMAX][COLS];  // waves 1..3 hand their partials to wave 0
     __shared__ float dzs[kMaxChunk][EMAX + 1];
     const int c = blockIdx.x, g = blockIdx.z;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int t0 = c * tch;
     const int ntok = min(tch, Ng - t0);
     const size_t tok0 = static_cast<size_t>(g) * Ng + t0;
 
-    for (int tt = threadIdx.x; tt < ntok; tt += kCols) {
+    // dz of the chunk's tokens, one token per thread
+    for (int tt = threadIdx.x; tt < ntok; tt += 256) {
         const size_t t = tok0 + tt;
         float pdp = 0.0f;
         for (int j = 0; j < k; ++j)
@@ -47,47 +88,82 @@ __global__ __launch_bounds__(kCols) void route_bwd_kernel(
             }
     }
     __syncthreads();
+    const int i0 = blockIdx.y * COLS + lane * VEC;
+    const bool live = i0 < d;  // d is a multiple of 8, so a lane's columns are all in or all out
 
-    const int i = blockIdx.y * kCols + threadIdx.x;
-    if (i >= d) return;
     const T* wg = wr + static_cast<size_t>(g) * E * d;
-    float w[EMAX], pw[EMAX];
+    float w[EMAX][VEC], acc[EMAX][VEC];
+    const int ic = live ? i0 : 0;  // idle lanes read column 0 and discard it
 #pragma unroll
     for (int e = 0; e < EMAX; ++e) {
-        w[e] = e < E ? ld(wg, static_cast<size_t>(e) * d + i) : 0.0f;
-        pw[e] = 0.0f;
-    }
-    // 8 tokens per round: all 16 loads are issued before any arithmetic, so
-    // each thread keeps many HBM requests in flight.
-    constexpr int U = 8;
-    for (int tt0 = 0; tt0 < ntok; tt0 += U) {
-        float xv[U], dv[U];
+        load_cols<VEC>(wg + static_cast<size_t>(e < E ? e : E - 1) * d + ic, w[e]);
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const size_t t = tok0 + min(tt0 + u, ntok - 1);
-            xv[u] = ld(x, t * d + i);
-            dv[u] = dx[t * d + i];
+        for (int v = 0; v < VEC; ++v) {
+            w[e][v] = (e < E && live) ? w[e][v] : 0.0f;
+            acc[e][v] = 0.0f;
         }
+    }
+
+    // U tokens of this wave per round: their loads are all issued first
+    constexpr int U = EMAX <= 16 ? 4 : (EMAX <= 32 ? 2 : 1);
+    for (int r0 = wave; r0 < ntok; r0 += 4 * U) {
+        float xv[U][VEC], dv[U][VEC];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            if (tt0 + u >= ntok) break;
-            float s = 0.0f;
-#pragma unroll
-            for (int e = 0; e < EMAX; ++e) {
-                const float dz = dzs[tt0 + u][e < E ? e : 0];
-                if (e < E) {
-                    s = __builtin_fmaf(dz, w[e], s);
-                    pw[e] = __builtin_fmaf(dz, xv[u], pw[e]);
-                }
+            const int tt = min(r0 + 4 * u, ntok - 1);
+            const size_t t = tok0 + tt;
+            if (live) {
+                load_cols<VEC>(x + t * d + i0, xv[u]);
+                load_cols<VEC>(dx + t * d + i0, dv[u]);
             }
-            dx[(tok0 + tt0 + u) * d + i] = dv[u] + s;
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int tt = r0 + 4 * u;
+            if (tt >= ntok) break;
+            const size_t t = tok0 + tt;
+            float dz[EMAX];
+#pragma unroll
+            for (int e = 0; e < EMAX; ++e) dz[e] = e < E ? dzs[tt][e] : 0.0f;
+            if (live) {
+                float out[VEC];
+#pragma unroll
+                for (int v = 0; v < VEC; ++v) {
+                    float s = 0.0f;
+#pragma unroll
+                    for (int e = 0; e < EMAX; ++e)
+                        if (e < E) s = __builtin_fmaf(dz[e], w[e][v], s);
+                    out[v] = dv[u][v] + s;
+                }
+                store_cols<VEC>(dx + t * d + i0, out);
+#pragma unroll
+                for (int e = 0; e < EMAX; ++e)
+#pragma unroll
+                    for (int v = 0; v < VEC; ++v) acc[e][v] = __builtin_fmaf(dz[e], xv[u][v], acc[e][v]);
+            }
         }
     }
-    if (partial) {
-        float* pg = partial + (static_cast<size_t>(g) * nch + c) * E * d;
+    if (!partial) return;
+    if (wave > 0) {
 #pragma unroll
         for (int e = 0; e < EMAX; ++e)
-            if (e < E) pg[static_cast<size_t>(e) * d + i] = pw[e];
+#pragma unroll
+            for (int v = 0; v < VEC; ++v) red[wave - 1][e][lane * VEC + v] = acc[e][v];
+    }
+    __syncthreads();
+    if (wave == 0 && live) {
+        float* pg = partial + (static_cast<size_t>(g) * nch + c) * E * d;
+#pragma unroll
+        for (int e = 0; e < EMAX; ++e) {
+            if (e < E) {
+                float out[VEC];
+#pragma unroll
+                for (int v = 0; v < VEC; ++v)
+                    out[v] = ((acc[e][v] + red[0][e][lane * VEC + v]) + red[1][e][lane * VEC + v]) +
+                             red[2][e][lane * VEC + v];
+                store_cols<VEC>(pg + static_cast<size_t>(e) * d + i0, out);
+            }
+        }
     }
 }
 
@@ -122,7 +198,9 @@ struct ChunkPlan {
 };
 
 ChunkPlan plan(const Dims& D) {
-    const int colblocks = static_cast<int>(cdiv(D.d, kCols));
+    // about 1024 blocks over (chunks, column blocks, groups); column blocks of
+    // 256 columns (E <= 16) as the common case
+    const int colblocks = static_cast<int>(cdiv(D.d, 256));
     int target = 1024 / (D.G * colblocks);
     if (target < 1) target = 1;
     int tch = D.Ng > 0 ? static_cast<int>(cdiv(D.Ng, target)) : 1;
@@ -134,8 +212,8 @@ template <typename T, int EMAX>
 void launch_main(const Dims& D, const ChunkPlan& P, const void* x, const void* wr,
                  const float* probs, const int32_t* idx, const int32_t* slot, const float* dgate,
                  float* dx, float* partial, hipStream_t st) {
-    dim3 grid(P.nch, cdiv(D.d, kCols), D.G);
-    route_bwd_kernel<T, EMAX><<<grid, kCols, 0, st>>>(
+    dim3 grid(P.nch, cdiv(D.d, 64 * ColsPerLane<EMAX>::value), D.G);
+    route_bwd_kernel<T, EMAX><<<grid, 256, 0, st>>>(
         static_cast<const T*>(x), static_cast<const T*>(wr), probs, idx, slot, dgate, dx, partial,
         D.Ng, D.d, D.E, D.k, P.tch, P.nch);
 }

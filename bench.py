@@ -59,6 +59,37 @@ def algorithmic_cost(cfg, A: int, n_noise: bool, n_bias: bool):
     return c
 
 
+TRAFFIC_PROFILE = {"vitb16_bf16": "profiles/vitb16_bf16_hbm_traffic.txt"}
+
+
+def measured_traffic(workload: str, call: str):
+    """HBM bytes per call from the committed rocprofv3 PMC summary.
+
+    The summary holds calibrated FETCH_SIZE / WRITE_SIZE bytes per C-ABI call
+    and the sha256 of the sources the counters were taken with; a call whose
+    sources have changed since then has no measured traffic (None).
+    """
+    import hashlib
+    rel = TRAFFIC_PROFILE.get(workload)
+    if rel is None or not os.path.exists(os.path.join(ROOT, rel)):
+        return None
+    calls, sources = {}, {}
+    for line in open(os.path.join(ROOT, rel)):
+        w = line.split()
+        if len(w) == 6 and w[0] == "call":
+            calls[w[1]] = int(w[3]) + int(w[5])
+        elif len(w) == 4 and w[0] == "source":
+            sources[w[1]] = w[3]
+    used = {"ffn_fwd": ["ffn.hip"], "ffn_bwd": ["ffn.hip"], "route": ["route.hip"],
+            "route_bwd": ["route_bwd.hip"]}.get(call, ["moves.hip"]) + ["common.h"]
+    csrc = os.path.join(ROOT, "paper_2608_16188_amd", "csrc")
+    for f in used:
+        h = hashlib.sha256(open(os.path.join(csrc, f), "rb").read()).hexdigest()
+        if sources.get(f) != h:
+            return None
+    return calls.get(call)
+
+
 def cpu_baseline(cfg, inputs, C_full, budget_s=20.0):
     """The oracle as it stands, single-threaded, on a bounded token sample."""
     import oracle
@@ -202,7 +233,8 @@ def main():
                    "capacity": L.C, "kept_assignments": A, "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "kernel": f"vmoe_expert_{dom}",
                      "achieved": ach, "peak": peak_mfma, "unit": "TFLOP/s",
-                     "frac": ach / peak_mfma, "traffic": None},
+                     "frac": ach / peak_mfma, "traffic": measured_traffic(args.workload, dom),
+                     "algorithmic_bytes": by},
         "expert_gemms": {"tflops": ffn_tflops, "frac_of_peak": ffn_tflops / peak_mfma,
                          "ms": ffn_ms},
         "route_dispatch_combine": {"gbs": moves_bytes / (moves_ms * 1e-3) / 1e9,

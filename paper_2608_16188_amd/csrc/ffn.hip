@@ -282,8 +282,10 @@ struct Tile {
     static constexpr int WM = BM / WGM, WN = BN / WGN;  // wave tile
     static constexpr int FM = WM / 32, FN = WN / 32;    // 32 x 32 MFMA blocks per wave
     static constexpr int KSTEPS = KB / 16;
-    // two blocks per CU for 8-wave tiles and small tiles, one otherwise
-    static constexpr int WAVES_PER_EU = (NW == 8 || BM * BN < 256 * 128) ? 2 : 1;
+    // two waves per SIMD: 8-wave tiles, or two 4-wave blocks per CU when their
+    // stage rings fit half the LDS; one 4-wave block per CU otherwise
+    static constexpr int RING_BYTES = NS * (BM + BN) * KB * 2;
+    static constexpr int WAVES_PER_EU = (NW == 8 || RING_BYTES <= 80 * 1024) ? 2 : 1;
     static_assert(WM % 32 == 0 && WN % 32 == 0, "wave tile must be whole 32 x 32 blocks");
     static_assert(KSTEPS % 2 == 0, "fragment double buffering needs an even step count");
     static_assert(MODE == STAGE_DMA || NS == 2, "register staging runs two stages");

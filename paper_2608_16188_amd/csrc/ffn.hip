@@ -56,6 +56,15 @@ struct GemmArgs {
     float* bsum;            // EPI_F32 (bf16 path): row sums of A per expert, or null
 };
 
+// Up to two independent GEMMs of one kernel instantiation in one launch (the
+// two weight gradients): blocks [0, total[0]) work on problem 0, the rest on
+// problem 1, so the second fills the first's last, partial round of tiles.
+struct GemmBatch {
+    GemmArgs p[2];
+    int tiles_m[2], tiles_n[2], total[2];
+    int group_m, per_xcd;
+};
+
 __device__ __forceinline__ int expert_rows(const int32_t* counts, int G, int E, int e) {
     int n = 0;
     for (int g = 0; g < G; ++g) n += counts[g * E + e];
@@ -85,9 +94,18 @@ typedef int v4i32 __attribute__((ext_vector_type(4)));
 //              bytes [16 L, 16 L + 16) of a 1 KB block, so rows are unpadded and
 //              16-byte chunks are XOR-swizzled instead (k-major: chunk ^ ((row / P)
 //              mod Q) with P rows per 256 bytes and Q chunks per row; mn-major:
-//              chunk ^ 4 (k mod 4)), which keeps fragment and transpose reads free
-//              of bank conflicts.
+//              chunk ^ s (k mod 4) with s = 4, or 2 when a row's chunk count is a
+//              multiple of 8 but not 16, so the XOR stays inside the row), which
+//              keeps fragment and transpose reads free of bank conflicts.
 enum Staging { STAGE_REG = 0, STAGE_DMA = 1 };
+
+// XOR applied to the 16-byte chunk index of k-row k of an mn-major DMA stage.
+template <int ROWS>
+__device__ __forceinline__ int mn_swizzle(int k) {
+    static_assert((ROWS / 8) % 8 == 0, "mn-major rows must hold a multiple of 8 chunks");
+    constexpr int SHIFT = (ROWS / 8) % 16 == 0 ? 2 : 1;
+    return (k & 3) << SHIFT;
+}
 
 template <int ROWS, bool KMAJOR, int KB, int MODE>
 __host__ __device__ constexpr int stage_elems() {
@@ -103,7 +121,7 @@ __device__ __forceinline__ int lds_off(int mn, int k) {
         constexpr int Q = KB / 8, P = 16 / Q;  // chunks per row, rows per 256 bytes
         return mn * KB + (((k >> 3) ^ ((mn / P) % Q)) << 3) + (k & 7);
     } else {
-        return k * ROWS + (((mn >> 3) ^ ((k & 3) << 2)) << 3) + (mn & 7);
+        return k * ROWS + (((mn >> 3) ^ mn_swizzle<ROWS>(k)) << 3) + (mn & 7);
     }
 }
 
@@ -195,7 +213,7 @@ struct DmaStage {
             } else {
                 constexpr int RB = ROWS * 2;  // bytes per k row
                 const int r = byte / RB;
-                const int c = ((byte % RB) >> 4) ^ ((r & 3) << 2);
+                const int c = ((byte % RB) >> 4) ^ mn_swizzle<ROWS>(r);
                 off = vec_off<false>(ld, mn0 + 8 * c, mn_lim, k0 + r, k_lim);
             }
             __builtin_amdgcn_raw_ptr_buffer_load_lds(
@@ -406,8 +424,9 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& p, f32x16 (&acc)[T
     char* ep = reinterpret_cast<char*>(ep_buf) + (wave / T::NS) * EPO * EP_TILE;
     constexpr int SEG = 16 / ELEM;                 // elements per 16-byte segment
     constexpr int LANES_PER_ROW = WN / SEG;
-    constexpr int ROWS_PER_PASS = 64 / LANES_PER_ROW;
-    static_assert(LANES_PER_ROW <= 64 && 64 % LANES_PER_ROW == 0, "epilogue row split");
+    constexpr int ROWS_PER_PASS = 64 / LANES_PER_ROW;  // lanes past ROWS_PER_PASS rows idle
+    constexpr int PASSES = (IPP * 32 + ROWS_PER_PASS - 1) / ROWS_PER_PASS;
+    static_assert(LANES_PER_ROW <= 64 && WN % SEG == 0, "epilogue row split");
 
 #pragma unroll
     for (int i0 = 0; i0 < FM; i0 += IPP) {
@@ -485,12 +504,14 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& p, f32x16 (&acc)[T
             // Stage 2: staged rows out in 16-byte segments.
             const int cl = (lane % LANES_PER_ROW) * SEG;
             const int n = n0 + wn * WN + cl;
+            const int lrow = lane / LANES_PER_ROW;
 #pragma unroll
             for (int o = 0; o < EPO; ++o) {
                 char* dst_base = static_cast<char*>(o0 + o == 0 ? p.out : p.out2);
 #pragma unroll
-                for (int pass = 0; pass < IPP * 32 / ROWS_PER_PASS; ++pass) {
-                    const int ml = pass * ROWS_PER_PASS + lane / LANES_PER_ROW;
+                for (int pass = 0; pass < PASSES; ++pass) {
+                    const int ml = pass * ROWS_PER_PASS + lrow;
+                    if (lrow >= ROWS_PER_PASS || ml >= IPP * 32) continue;
                     const int m = m0 + wm * WM + i0 * 32 + ml;
                     const uint4 v = *reinterpret_cast<const uint4*>(ep + o * EP_TILE +
                                                                     (ml * EP_LD + cl) * ELEM);
@@ -524,7 +545,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& p, f32x16 (&acc)[T
 template <class T, bool A_KMAJOR, bool B_KMAJOR, int EPI>
 __global__ __launch_bounds__(T::NT)
 __attribute__((amdgpu_waves_per_eu(T::WAVES_PER_EU, T::WAVES_PER_EU)))
-void gemm_bf16_kernel(GemmArgs p, int tiles_m, int tiles_n, int group_m, int per_xcd, int total) {
+void gemm_bf16_kernel(GemmBatch batch) {
     using CFG = GemmCfg<T, A_KMAJOR, B_KMAJOR, EPI>;
     constexpr int BM_ = T::BM, BN_ = T::BN, KB = T::KB, NS = T::NS, MODE = T::MODE;
     constexpr int NT = T::NT, AE = CFG::AE, BE = CFG::BE, FM = T::FM, FN = T::FN;
@@ -538,8 +559,13 @@ void gemm_bf16_kernel(GemmArgs p, int tiles_m, int tiles_n, int group_m, int per
     __shared__ __attribute__((aligned(1024))) uint16_t buf4[NS > 4 ? SZX : 8];
 
     const int b = blockIdx.x;
-    const int w = (b & 7) * per_xcd + (b >> 3);
-    if (w >= total) return;
+    int w = (b & 7) * batch.per_xcd + (b >> 3);
+    if (w >= batch.total[0] + batch.total[1]) return;
+    const int prob = w >= batch.total[0] ? 1 : 0;  // uniform per block
+    if (prob) w -= batch.total[0];
+    const GemmArgs& p = batch.p[prob];
+    const int tiles_m = batch.tiles_m[prob], tiles_n = batch.tiles_n[prob];
+    const int group_m = batch.group_m;
     // inside one expert, tiles go in groups of group_m m-tiles, m fastest, so
     // the blocks resident on an XCD at once cover a compact patch of the output
     // and share both operand panels in its L2
@@ -818,32 +844,62 @@ __global__ __launch_bounds__(256) void colsum_kernel(const T* __restrict__ src,
                                                   part[2][c & 63]) + part[3][c & 63];
 }
 
+// One launch over `n` (1 or 2) problems; grid_m_rows[i] bounds problem i's m.
+template <class T, bool AK, bool BK_, int EPI>
+void launch_bf16(const Dims& D, const GemmArgs* a, const int* grid_m_rows, int n, hipStream_t st) {
+    GemmBatch b{};
+    for (int i = 0; i < n; ++i) {
+        b.p[i] = a[i];
+        b.tiles_m[i] = static_cast<int>(cdiv(grid_m_rows[i], T::BM));
+        b.tiles_n[i] = static_cast<int>(cdiv(a[i].N, T::BN));
+        b.total[i] = D.E * b.tiles_m[i] * b.tiles_n[i];
+    }
+    b.per_xcd = static_cast<int>(cdiv(b.total[0] + b.total[1], 8));
+    // blocks resident on one XCD: 32 CUs x blocks per CU
+    b.group_m = T::WAVES_PER_EU == 2 && T::NW == 4 ? 8 : 4;
+    gemm_bf16_kernel<T, AK, BK_, EPI><<<8 * b.per_xcd, T::NT, 0, st>>>(b);
+}
+
 template <class T, bool AK, bool BK_, int EPI>
 void launch_bf16(const Dims& D, const GemmArgs& a, int grid_m_rows, hipStream_t st) {
-    const int tiles_m = static_cast<int>(cdiv(grid_m_rows, T::BM));
-    const int tiles_n = static_cast<int>(cdiv(a.N, T::BN));
-    const int total = D.E * tiles_m * tiles_n;
-    const int per_xcd = static_cast<int>(cdiv(total, 8));
-    // blocks resident on one XCD: 32 CUs x blocks per CU
-    const int group_m = T::WAVES_PER_EU == 2 && T::NW == 4 ? 8 : 4;
-    gemm_bf16_kernel<T, AK, BK_, EPI><<<8 * per_xcd, T::NT, 0, st>>>(a, tiles_m, tiles_n, group_m,
-                                                                     per_xcd, total);
+    launch_bf16<T, AK, BK_, EPI>(D, &a, &grid_m_rows, 1, st);
 }
 
 // Tilings (BM, BN, waves, KB, stages, staging).
 using TileBig = Tile<256, 256, 2, 4, 32, 4, STAGE_DMA>;    // 8 waves, one block per CU
+using TileNarrow = Tile<256, 192, 4, 2, 64, 2, STAGE_DMA>; // 8 waves, 3/4 of TileBig's columns
 using TileSmall = Tile<128, 128, 2, 2, 32, 4, STAGE_DMA>;  // 4 waves, two blocks per CU
+
+constexpr int kNumCUs = 256;
+
+// Work of a launch in units of one CU's time: rounds of one-block-per-CU
+// waves times the tile's area (relative cost per tile area `eff`).
+double tile_cost(long long tiles, int bm, int bn, double eff) {
+    return static_cast<double>((tiles + kNumCUs - 1) / kNumCUs) * bm * bn * eff;
+}
 
 template <bool AK, bool BK_, int EPI>
 void launch_gemm(const Dims& D, const GemmArgs& a, int grid_m_rows, hipStream_t st) {
     if (D.dtype == VMOE_BF16) {
         // 256 x 256 tiles (half the operand bytes per flop of 128 x 128) for
         // the GEMMs whose m is the expert's rows; the weight gradients (k is
-        // the rows, often short) run 128 x 128 tiles, two blocks per CU
-        if constexpr (EPI == EPI_F32)
+        // the rows, often short) run 128 x 128 tiles, two blocks per CU.
+        if constexpr (EPI == EPI_F32) {
             launch_bf16<TileSmall, AK, BK_, EPI>(D, a, grid_m_rows, st);
-        else
+        } else if constexpr (EPI == EPI_BIAS || EPI == EPI_STORE) {
+            // Narrow outputs (N = d_model) give few tiles: 192-column tiles fill
+            // more CUs when that saves a round (two-stage 64-deep ring, a few
+            // per cent slower per tile)
+            const long long tm = cdiv(grid_m_rows, 256);
+            const double big = tile_cost(D.E * tm * cdiv(a.N, 256), 256, 256, 1.0);
+            const double narrow = tile_cost(D.E * tm * cdiv(a.N, 192), 256, 192, 1.05);
+            if (narrow < big)
+                launch_bf16<TileNarrow, AK, BK_, EPI>(D, a, grid_m_rows, st);
+            else
+                launch_bf16<TileBig, AK, BK_, EPI>(D, a, grid_m_rows, st);
+        } else {
             launch_bf16<TileBig, AK, BK_, EPI>(D, a, grid_m_rows, st);
+        }
     } else {
         dim3 grid(cdiv(a.N, FT), cdiv(grid_m_rows, FT), D.E);
         gemm_f32_kernel<AK, BK_, EPI><<<grid, 256, 0, st>>>(a);
@@ -940,7 +996,6 @@ vmoe_status ffn_bwd_launch(const Dims& D, const void* xe, const int32_t* counts,
     w.out_estride = static_cast<long long>(D.d) * D.f;
     w.ldo = D.f;
     w.bsum = D.dtype == VMOE_BF16 ? db2 : nullptr;  // db2 = row sums of dye^T
-    launch_gemm<false, false, EPI_F32>(D, w, D.d, st);
     // dW1 [f, d] = dH^T xe
     GemmArgs v = base_args(D, counts);
     v.var_k = 1;
@@ -953,7 +1008,15 @@ vmoe_status ffn_bwd_launch(const Dims& D, const void* xe, const int32_t* counts,
     v.out_estride = static_cast<long long>(D.f) * D.d;
     v.ldo = D.d;
     v.bsum = D.dtype == VMOE_BF16 ? db1 : nullptr;  // db1 = row sums of dH^T
-    launch_gemm<false, false, EPI_F32>(D, v, D.f, st);
+    if (D.dtype == VMOE_BF16) {
+        // both weight gradients in one launch (same kernel, independent tiles)
+        const GemmArgs both[2] = {w, v};
+        const int rows_m[2] = {D.d, D.f};
+        launch_bf16<TileSmall, false, false, EPI_F32>(D, both, rows_m, 2, st);
+    } else {
+        launch_gemm<false, false, EPI_F32>(D, w, D.d, st);
+        launch_gemm<false, false, EPI_F32>(D, v, D.f, st);
+    }
     // bias gradients (the bf16 path sums them inside the dW GEMMs)
     if (D.dtype == VMOE_F32) {
         colsum_kernel<float><<<dim3(cdiv(D.d, 64), D.E), 256, 0, st>>>(

@@ -1,9 +1,7 @@
 // Dispatch, combine and their backward passes on gfx950.
 //
-// All four are HBM-bound gathers / scatters keyed by the routing metadata.
-// One 64-lane wavefront owns one token: it reads the token's k (expert, slot)
-// pairs once and streams the d-wide rows in 16-byte vectors, so every row
-// access is a fully coalesced 16 B-per-lane burst. Float sums run in a fixed
+// All four are HBM-bound gathers / scatters keyed by the routing metadata,
+// moving rows in 16-byte vectors (fully coalesced). Float sums run in a fixed
 // order (j ascending, then a fixed butterfly), so results are deterministic.
 #include "common.h"
 
@@ -53,112 +51,185 @@ struct RouteMeta {
     }
 };
 
-template <typename T>
-__global__ __launch_bounds__(64 * kWavesPerBlock) void dispatch_kernel(const T* __restrict__ x,
-                                                                        T* __restrict__ xe,
-                                                                        RouteMeta m, int d) {
-    const int t = blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
-    const int lane = threadIdx.x & 63;
-    if (t >= m.N) return;
-    const int nvec = d / Vec<T>::n;
-    const uint4* src = reinterpret_cast<const uint4*>(x + static_cast<size_t>(t) * d);
-    for (int j = 0; j < m.k; ++j) {
-        const long long row = m.row(t, j);
-        if (row < 0) continue;
-        uint4* dst = reinterpret_cast<uint4*>(xe + static_cast<size_t>(row) * d);
-        for (int v = lane; v < nvec; v += 64) dst[v] = src[v];
-    }
-}
+// Flat element-wise mapping for the row moves without a reduction: item i is
+// 16-byte vector v = i mod nvec of token t = i / nvec, so consecutive lanes
+// touch consecutive bytes of a row and every lane is busy whatever d is. Each
+// thread takes kItems items kBlock apart and issues all their loads before any
+// store.
+constexpr int kBlock = 256;
+constexpr int kItems = 2;
 
 template <typename T>
-__global__ __launch_bounds__(64 * kWavesPerBlock) void combine_fwd_kernel(
-    const T* __restrict__ ye, const float* __restrict__ gate, T* __restrict__ y, RouteMeta m,
-    int d) {
-    constexpr int VN = Vec<T>::n;
-    const int t = blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
-    const int lane = threadIdx.x & 63;
-    if (t >= m.N) return;
-    const int nvec = d / VN;
-    uint4* dst = reinterpret_cast<uint4*>(y + static_cast<size_t>(t) * d);
-    for (int v = lane; v < nvec; v += 64) {
-        float acc[VN];
-#pragma unroll
-        for (int i = 0; i < VN; ++i) acc[i] = 0.0f;
+__global__ __launch_bounds__(kBlock) void dispatch_kernel(const T* __restrict__ x,
+                                                          T* __restrict__ xe, RouteMeta m,
+                                                          int nvec) {
+    const long long total = static_cast<long long>(m.N) * nvec;
+    const long long i0 = static_cast<long long>(blockIdx.x) * kBlock * kItems + threadIdx.x;
+    const uint4* src = reinterpret_cast<const uint4*>(x);
+    uint4* dst = reinterpret_cast<uint4*>(xe);
+    auto item = [&](long long i) { return i < total ? src[i] : make_uint4(0u, 0u, 0u, 0u); };
+    auto place = [&](long long i, const uint4 v) {
+        if (i >= total) return;
+        const int t = static_cast<int>(i / nvec);
+        const int c = static_cast<int>(i - static_cast<long long>(t) * nvec);
         for (int j = 0; j < m.k; ++j) {
             const long long row = m.row(t, j);
-            if (row < 0) continue;
-            const float gj = gate[static_cast<size_t>(t) * m.k + j];
-            float f[VN];
-            Vec<T>::unpack(reinterpret_cast<const uint4*>(ye + static_cast<size_t>(row) * d)[v], f);
-#pragma unroll
-            for (int i = 0; i < VN; ++i) acc[i] = __builtin_fmaf(gj, f[i], acc[i]);
+            if (row >= 0) dst[row * nvec + c] = v;
         }
-        dst[v] = Vec<T>::pack(acc);
+    };
+    static_assert(kItems == 2, "two items per thread");
+    const uint4 v0 = item(i0), v1 = item(i0 + kBlock);
+    place(i0, v0);
+    place(i0 + kBlock, v1);
+}
+
+template <typename T>
+__global__ __launch_bounds__(kBlock) void combine_fwd_kernel(const T* __restrict__ ye,
+                                                             const float* __restrict__ gate,
+                                                             T* __restrict__ y, RouteMeta m,
+                                                             int nvec) {
+    constexpr int VN = Vec<T>::n;
+    constexpr int KMAX = 4;  // rows gathered per pass; more assignments loop
+    const long long total = static_cast<long long>(m.N) * nvec;
+    const long long i0 = static_cast<long long>(blockIdx.x) * kBlock * kItems + threadIdx.x;
+    const uint4* src = reinterpret_cast<const uint4*>(ye);
+    uint4* dst = reinterpret_cast<uint4*>(y);
+#pragma unroll
+    for (int u = 0; u < kItems; ++u) {
+        const long long i = i0 + u * kBlock;
+        if (i >= total) break;
+        const int t = static_cast<int>(i / nvec), c = static_cast<int>(i - static_cast<long long>(t) * nvec);
+        float acc[VN];
+#pragma unroll
+        for (int q = 0; q < VN; ++q) acc[q] = 0.0f;
+        for (int j0 = 0; j0 < m.k; j0 += KMAX) {
+            uint4 r[KMAX];
+            float gj[KMAX];
+            bool kept[KMAX];
+#pragma unroll
+            for (int jj = 0; jj < KMAX; ++jj) {
+                const int j = j0 + jj;
+                const long long row = j < m.k ? m.row(t, j) : -1;
+                kept[jj] = row >= 0;
+                gj[jj] = row >= 0 ? gate[static_cast<size_t>(t) * m.k + j] : 0.0f;
+                r[jj] = row >= 0 ? src[row * nvec + c] : make_uint4(0u, 0u, 0u, 0u);
+            }
+            // j ascending over the kept assignments
+#pragma unroll
+            for (int jj = 0; jj < KMAX; ++jj) {
+                if (!kept[jj]) continue;
+                float f[VN];
+                Vec<T>::unpack(r[jj], f);
+#pragma unroll
+                for (int q = 0; q < VN; ++q) acc[q] = __builtin_fmaf(gj[jj], f[q], acc[q]);
+            }
+        }
+        dst[i] = Vec<T>::pack(acc);
     }
 }
 
+// One wave per token (the dot products reduce across the row): the token's dy
+// vectors are loaded once, then per assignment all its ye vectors are loaded
+// before the scaled copy and the dot product, which ends in a fixed butterfly.
 template <typename T>
 __global__ __launch_bounds__(64 * kWavesPerBlock) void combine_bwd_kernel(
     const T* __restrict__ dy, const T* __restrict__ ye, const float* __restrict__ gate,
-    T* __restrict__ dye, float* __restrict__ dgate, RouteMeta m, int d) {
+    T* __restrict__ dye, float* __restrict__ dgate, RouteMeta m, int nvec) {
     constexpr int VN = Vec<T>::n;
+    constexpr int NV = 2;  // vectors per lane per pass: rows up to 128 vectors in one pass
     const int t = blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
     if (t >= m.N) return;
-    const int nvec = d / VN;
-    const uint4* g_dy = reinterpret_cast<const uint4*>(dy + static_cast<size_t>(t) * d);
-    for (int j = 0; j < m.k; ++j) {
-        const long long row = m.row(t, j);
-        if (row < 0) {
-            if (lane == 0) dgate[static_cast<size_t>(t) * m.k + j] = 0.0f;
-            continue;
-        }
-        const float gj = gate[static_cast<size_t>(t) * m.k + j];
-        const uint4* g_ye = reinterpret_cast<const uint4*>(ye + static_cast<size_t>(row) * d);
-        uint4* g_dye = reinterpret_cast<uint4*>(dye + static_cast<size_t>(row) * d);
-        float dot = 0.0f;
-        for (int v = lane; v < nvec; v += 64) {
-            float a[VN], b[VN], o[VN];
-            Vec<T>::unpack(g_dy[v], a);
-            Vec<T>::unpack(g_ye[v], b);
+    const uint4* g_dy = reinterpret_cast<const uint4*>(dy) + static_cast<size_t>(t) * nvec;
+    for (int v0 = 0; v0 < nvec; v0 += 64 * NV) {
+        uint4 a[NV];
 #pragma unroll
-            for (int i = 0; i < VN; ++i) {
-                dot = __builtin_fmaf(a[i], b[i], dot);
-                o[i] = gj * a[i];
+        for (int q = 0; q < NV; ++q) {
+            const int v = v0 + lane + 64 * q;
+            if (v < nvec) a[q] = g_dy[v];
+        }
+        for (int j = 0; j < m.k; ++j) {
+            const long long row = m.row(t, j);
+            if (row < 0) {
+                if (lane == 0 && v0 == 0) dgate[static_cast<size_t>(t) * m.k + j] = 0.0f;
+                continue;
             }
-            g_dye[v] = Vec<T>::pack(o);
-        }
+            const float gj = gate[static_cast<size_t>(t) * m.k + j];
+            const uint4* g_ye = reinterpret_cast<const uint4*>(ye) + row * nvec;
+            uint4* g_dye = reinterpret_cast<uint4*>(dye) + row * nvec;
+            uint4 b[NV];
 #pragma unroll
-        for (int o = 32; o > 0; o >>= 1) dot += __shfl_xor(dot, o, 64);
-        if (lane == 0) dgate[static_cast<size_t>(t) * m.k + j] = dot;
+            for (int q = 0; q < NV; ++q) {
+                const int v = v0 + lane + 64 * q;
+                if (v < nvec) b[q] = g_ye[v];
+            }
+            float dot = 0.0f;
+#pragma unroll
+            for (int q = 0; q < NV; ++q) {
+                const int v = v0 + lane + 64 * q;
+                if (v >= nvec) break;
+                float fa[VN], fb[VN], o[VN];
+                Vec<T>::unpack(a[q], fa);
+                Vec<T>::unpack(b[q], fb);
+#pragma unroll
+                for (int i = 0; i < VN; ++i) {
+                    dot = __builtin_fmaf(fa[i], fb[i], dot);
+                    o[i] = gj * fa[i];
+                }
+                g_dye[v] = Vec<T>::pack(o);
+            }
+#pragma unroll
+            for (int o = 32; o > 0; o >>= 1) dot += __shfl_xor(dot, o, 64);
+            if (lane == 0) {
+                float* dg = dgate + static_cast<size_t>(t) * m.k + j;
+                *dg = v0 == 0 ? dot : *dg + dot;
+            }
+        }
     }
 }
 
 template <typename T>
-__global__ __launch_bounds__(64 * kWavesPerBlock) void dispatch_bwd_kernel(
-    const T* __restrict__ dxe, float* __restrict__ dx, RouteMeta m, int d) {
+__global__ __launch_bounds__(kBlock) void dispatch_bwd_kernel(const T* __restrict__ dxe,
+                                                              float* __restrict__ dx, RouteMeta m,
+                                                              int nvec) {
     constexpr int VN = Vec<T>::n;
-    const int t = blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
-    const int lane = threadIdx.x & 63;
-    if (t >= m.N) return;
-    const int nvec = d / VN;
-    float4* dst = reinterpret_cast<float4*>(dx + static_cast<size_t>(t) * d);
-    for (int v = lane; v < nvec; v += 64) {
+    constexpr int KMAX = 4;
+    const long long total = static_cast<long long>(m.N) * nvec;
+    const long long i0 = static_cast<long long>(blockIdx.x) * kBlock * kItems + threadIdx.x;
+    const uint4* src = reinterpret_cast<const uint4*>(dxe);
+    float4* dst = reinterpret_cast<float4*>(dx);
+#pragma unroll
+    for (int u = 0; u < kItems; ++u) {
+        const long long i = i0 + u * kBlock;
+        if (i >= total) break;
+        const int t = static_cast<int>(i / nvec), c = static_cast<int>(i - static_cast<long long>(t) * nvec);
         float acc[VN];
 #pragma unroll
-        for (int i = 0; i < VN; ++i) acc[i] = 0.0f;
-        for (int j = 0; j < m.k; ++j) {
-            const long long row = m.row(t, j);
-            if (row < 0) continue;
-            float f[VN];
-            Vec<T>::unpack(reinterpret_cast<const uint4*>(dxe + static_cast<size_t>(row) * d)[v], f);
+        for (int q = 0; q < VN; ++q) acc[q] = 0.0f;
+        for (int j0 = 0; j0 < m.k; j0 += KMAX) {
+            uint4 r[KMAX];
+            bool kept[KMAX];
 #pragma unroll
-            for (int i = 0; i < VN; ++i) acc[i] += f[i];
+            for (int jj = 0; jj < KMAX; ++jj) {
+                const int j = j0 + jj;
+                const long long row = j < m.k ? m.row(t, j) : -1;
+                kept[jj] = row >= 0;
+                r[jj] = row >= 0 ? src[row * nvec + c] : make_uint4(0u, 0u, 0u, 0u);
+            }
+            // j ascending over the kept assignments
+#pragma unroll
+            for (int jj = 0; jj < KMAX; ++jj) {
+                if (!kept[jj]) continue;
+                float f[VN];
+                Vec<T>::unpack(r[jj], f);
+#pragma unroll
+                for (int q = 0; q < VN; ++q) acc[q] += f[q];
+            }
         }
 #pragma unroll
-        for (int i = 0; i < VN / 4; ++i)
-            dst[v * (VN / 4) + i] = make_float4(acc[4 * i], acc[4 * i + 1], acc[4 * i + 2],
-                                                acc[4 * i + 3]);
+        for (int q = 0; q < VN / 4; ++q)
+            dst[i * (VN / 4) + q] = make_float4(acc[4 * q], acc[4 * q + 1], acc[4 * q + 2],
+                                                acc[4 * q + 3]);
     }
 }
 
@@ -171,14 +242,15 @@ RouteMeta meta(const Dims& D, const int32_t* idx, const int32_t* slot, const int
 vmoe_status dispatch_launch(const Dims& D, const void* x, const int32_t* idx, const int32_t* slot,
                             const int32_t* row_base, void* xe, hipStream_t st) {
     if (D.N == 0) return VMOE_OK;
-    const unsigned grid = cdiv(D.N, kWavesPerBlock);
     const RouteMeta m = meta(D, idx, slot, row_base);
+    const int nvec = D.d / (D.dtype == VMOE_BF16 ? 8 : 4);
+    const unsigned grid = cdiv(static_cast<long long>(D.N) * nvec, kBlock * kItems);
     if (D.dtype == VMOE_BF16)
-        dispatch_kernel<uint16_t><<<grid, 64 * kWavesPerBlock, 0, st>>>(
-            static_cast<const uint16_t*>(x), static_cast<uint16_t*>(xe), m, D.d);
+        dispatch_kernel<uint16_t><<<grid, kBlock, 0, st>>>(
+            static_cast<const uint16_t*>(x), static_cast<uint16_t*>(xe), m, nvec);
     else
-        dispatch_kernel<float><<<grid, 64 * kWavesPerBlock, 0, st>>>(
-            static_cast<const float*>(x), static_cast<float*>(xe), m, D.d);
+        dispatch_kernel<float><<<grid, kBlock, 0, st>>>(
+            static_cast<const float*>(x), static_cast<float*>(xe), m, nvec);
     return launch_status();
 }
 
@@ -186,14 +258,15 @@ vmoe_status combine_fwd_launch(const Dims& D, const void* ye, const int32_t* idx
                                const int32_t* slot, const int32_t* row_base, const float* gate,
                                void* y, hipStream_t st) {
     if (D.N == 0) return VMOE_OK;
-    const unsigned grid = cdiv(D.N, kWavesPerBlock);
     const RouteMeta m = meta(D, idx, slot, row_base);
+    const int nvec = D.d / (D.dtype == VMOE_BF16 ? 8 : 4);
+    const unsigned grid = cdiv(static_cast<long long>(D.N) * nvec, kBlock * kItems);
     if (D.dtype == VMOE_BF16)
-        combine_fwd_kernel<uint16_t><<<grid, 64 * kWavesPerBlock, 0, st>>>(
-            static_cast<const uint16_t*>(ye), gate, static_cast<uint16_t*>(y), m, D.d);
+        combine_fwd_kernel<uint16_t><<<grid, kBlock, 0, st>>>(
+            static_cast<const uint16_t*>(ye), gate, static_cast<uint16_t*>(y), m, nvec);
     else
-        combine_fwd_kernel<float><<<grid, 64 * kWavesPerBlock, 0, st>>>(
-            static_cast<const float*>(ye), gate, static_cast<float*>(y), m, D.d);
+        combine_fwd_kernel<float><<<grid, kBlock, 0, st>>>(
+            static_cast<const float*>(ye), gate, static_cast<float*>(y), m, nvec);
     return launch_status();
 }
 
@@ -206,11 +279,11 @@ vmoe_status combine_bwd_launch(const Dims& D, const void* dy, const void* ye, co
     if (D.dtype == VMOE_BF16)
         combine_bwd_kernel<uint16_t><<<grid, 64 * kWavesPerBlock, 0, st>>>(
             static_cast<const uint16_t*>(dy), static_cast<const uint16_t*>(ye), gate,
-            static_cast<uint16_t*>(dye), dgate, m, D.d);
+            static_cast<uint16_t*>(dye), dgate, m, D.d / 8);
     else
         combine_bwd_kernel<float><<<grid, 64 * kWavesPerBlock, 0, st>>>(
             static_cast<const float*>(dy), static_cast<const float*>(ye), gate,
-            static_cast<float*>(dye), dgate, m, D.d);
+            static_cast<float*>(dye), dgate, m, D.d / 4);
     return launch_status();
 }
 
@@ -218,14 +291,15 @@ vmoe_status dispatch_bwd_launch(const Dims& D, const void* dxe, const int32_t* i
                                 const int32_t* slot, const int32_t* row_base, float* dx,
                                 hipStream_t st) {
     if (D.N == 0) return VMOE_OK;
-    const unsigned grid = cdiv(D.N, kWavesPerBlock);
     const RouteMeta m = meta(D, idx, slot, row_base);
+    const int nvec = D.d / (D.dtype == VMOE_BF16 ? 8 : 4);
+    const unsigned grid = cdiv(static_cast<long long>(D.N) * nvec, kBlock * kItems);
     if (D.dtype == VMOE_BF16)
-        dispatch_bwd_kernel<uint16_t><<<grid, 64 * kWavesPerBlock, 0, st>>>(
-            static_cast<const uint16_t*>(dxe), dx, m, D.d);
+        dispatch_bwd_kernel<uint16_t><<<grid, kBlock, 0, st>>>(
+            static_cast<const uint16_t*>(dxe), dx, m, nvec);
     else
-        dispatch_bwd_kernel<float><<<grid, 64 * kWavesPerBlock, 0, st>>>(
-            static_cast<const float*>(dxe), dx, m, D.d);
+        dispatch_bwd_kernel<float><<<grid, kBlock, 0, st>>>(
+            static_cast<const float*>(dxe), dx, m, nvec);
     return launch_status();
 }
 

@@ -3,8 +3,8 @@
 // Pipeline (all on the caller's stream, no host synchronisation):
 //   1. router_gate   logits (double-accumulated, increasing-i order, rounded
 //                    once to f32), noisy softmax, top-k, 26-bit priority key
-//   2. bin_scan      per group: histogram of the top 12 key bits in LDS,
-//                    exclusive scan -> bin starts; clears the counters below
+//   2. bin_scan      per group: key range -> 4096 bins spanning it, histogram
+//                    in LDS, exclusive scan -> bin starts; clears the counters
 //   3. bin_scatter   tokens into their bins (atomic fill; order inside a bin
 //                    is irrelevant, ranks are computed exactly next)
 //   4. rank          rank of each token = tokens in lower bins + tokens of its
@@ -26,12 +26,23 @@ namespace {
 constexpr int kKeyBits = 26;                 // priority keys fit in 26 bits for E <= 64
 constexpr int kBinBits = 12;
 constexpr int kNumBins = 1 << kBinBits;
-constexpr int kBinShift = kKeyBits - kBinBits;
+
+// Bin of a key inside its group: (key - kmin) >> shift, with the group's
+// smallest key kmin and the least shift that maps its key range onto the
+// kNumBins bins (monotone in the key, so bins keep the priority order).
+struct BinMap {
+    uint32_t kmin;
+    int shift;
+    __device__ __forceinline__ int operator()(uint32_t key) const {
+        return static_cast<int>((key - kmin) >> shift);
+    }
+};
 constexpr int kSlotChunk = 256;              // order positions per slots block
 constexpr int kGateTokens = 32;              // most tokens per router_gate block
 
 struct RouteWs {
     uint32_t* keys;     // [N]
+    BinMap* binmap;     // [G]
     int32_t* bin_start; // [G][kNumBins + 1]
     int32_t* fill;      // [G][kNumBins]
     int32_t* members;   // [N]
@@ -55,6 +66,7 @@ RouteWs route_ws_layout(const Dims& D, void* base) {
     const size_t nch = cdiv(D.Ng, kSlotChunk);
     RouteWs w;
     w.keys = reinterpret_cast<uint32_t*>(take(sizeof(uint32_t) * D.N));
+    w.binmap = reinterpret_cast<BinMap*>(take(sizeof(BinMap) * D.G));
     w.bin_start = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * D.G * (kNumBins + 1)));
     w.fill = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * D.G * kNumBins));
     w.members = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * D.N));
@@ -315,18 +327,52 @@ __device__ int block_exclusive_scan_1024(int v, int* total) {
     return base + inc - v;
 }
 
-// One block per group: bin histogram + scan; clears fill and chunk counters.
+// One block per group: key range -> bin map, bin histogram + scan; clears
+// fill and chunk counters.
 __global__ __launch_bounds__(1024) void bin_scan_kernel(const uint32_t* __restrict__ keys,
+                                                        BinMap* __restrict__ binmap,
                                                         int32_t* __restrict__ bin_start,
                                                         int32_t* __restrict__ fill,
                                                         int32_t* __restrict__ ccount, int Ng,
                                                         int cc_per_group) {
     __shared__ int hist[kNumBins];
+    __shared__ uint32_t wmin[16], wmax[16];
+    __shared__ BinMap map;
     const int g = blockIdx.x;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     for (int b = threadIdx.x; b < kNumBins; b += 1024) hist[b] = 0;
-    __syncthreads();
     const uint32_t* kg = keys + static_cast<size_t>(g) * Ng;
-    for (int t = threadIdx.x; t < Ng; t += 1024) atomicAdd(&hist[kg[t] >> kBinShift], 1);
+    uint32_t lo = 0xFFFFFFFFu, hi = 0u;
+    for (int t = threadIdx.x; t < Ng; t += 1024) {
+        const uint32_t key = kg[t];
+        lo = min(lo, key);
+        hi = max(hi, key);
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        lo = min(lo, static_cast<uint32_t>(__shfl_xor(static_cast<int>(lo), o, 64)));
+        hi = max(hi, static_cast<uint32_t>(__shfl_xor(static_cast<int>(hi), o, 64)));
+    }
+    if (lane == 0) {
+        wmin[w] = lo;
+        wmax[w] = hi;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t a = wmin[0], z = wmax[0];
+        for (int q = 1; q < 16; ++q) {
+            a = min(a, wmin[q]);
+            z = max(z, wmax[q]);
+        }
+        if (Ng == 0) a = z = 0u;
+        int sh = 0;
+        while (((z - a) >> sh) >= static_cast<uint32_t>(kNumBins)) ++sh;
+        map = BinMap{a, sh};
+        binmap[g] = map;
+    }
+    __syncthreads();
+    const BinMap bm = map;
+    for (int t = threadIdx.x; t < Ng; t += 1024) atomicAdd(&hist[bm(kg[t])], 1);
     __syncthreads();
     constexpr int per = kNumBins / 1024;
     int local[per];
@@ -352,6 +398,7 @@ __global__ __launch_bounds__(1024) void bin_scan_kernel(const uint32_t* __restri
 }
 
 __global__ __launch_bounds__(256) void bin_scatter_kernel(const uint32_t* __restrict__ keys,
+                                                          const BinMap* __restrict__ binmap,
                                                           const int32_t* __restrict__ bin_start,
                                                           int32_t* __restrict__ fill,
                                                           int32_t* __restrict__ members, int N,
@@ -359,14 +406,15 @@ __global__ __launch_bounds__(256) void bin_scatter_kernel(const uint32_t* __rest
     const int t = blockIdx.x * 256 + threadIdx.x;
     if (t >= N) return;
     const int g = t / Ng;
-    const int b = static_cast<int>(keys[t] >> kBinShift);
+    const int b = binmap[g](keys[t]);
     const int pos = bin_start[static_cast<size_t>(g) * (kNumBins + 1) + b] +
                     atomicAdd(&fill[static_cast<size_t>(g) * kNumBins + b], 1);
     members[static_cast<size_t>(g) * Ng + pos] = t;
 }
 
 __global__ __launch_bounds__(256) void rank_kernel(
-    const uint32_t* __restrict__ keys, const int32_t* __restrict__ bin_start,
+    const uint32_t* __restrict__ keys, const BinMap* __restrict__ binmap,
+    const int32_t* __restrict__ bin_start,
     const int32_t* __restrict__ members, const int32_t* __restrict__ idx,
     int32_t* __restrict__ order, int32_t* __restrict__ ccount, int N, int Ng, int E, int k,
     int nch) {
@@ -375,7 +423,7 @@ __global__ __launch_bounds__(256) void rank_kernel(
     const int g = t / Ng;
     const uint32_t key = keys[t];
     const int32_t* bs = bin_start + static_cast<size_t>(g) * (kNumBins + 1);
-    const int b = static_cast<int>(key >> kBinShift);
+    const int b = binmap[g](key);
     const int lo = bs[b], hi = bs[b + 1];
     const int32_t* mg = members + static_cast<size_t>(g) * Ng;
     int rank = lo;
@@ -396,15 +444,25 @@ __global__ __launch_bounds__(1024) void chunk_scan_kernel(
     int32_t* __restrict__ carry, int32_t* __restrict__ counts, int32_t* __restrict__ row_base,
     int G, int E, int k, int C, int nch) {
     const int kE = k * E;
-    for (int q = threadIdx.x; q < G * kE; q += 1024) {
+    const int lane = threadIdx.x & 63;
+    // one wave per (group, round, expert): exclusive scan over the chunks, 64 at a time
+    for (int q = threadIdx.x >> 6; q < G * kE; q += 16) {
         const int g = q / kE, re = q % kE;
         int run = 0;
-        for (int c = 0; c < nch; ++c) {
+        for (int c0 = 0; c0 < nch; c0 += 64) {
+            const int c = c0 + lane;
             const size_t at = (static_cast<size_t>(g) * nch + c) * kE + re;
-            cbase[at] = run;
-            run += ccount[at];
+            const int v = c < nch ? ccount[at] : 0;
+            int inc = v;
+#pragma unroll
+            for (int o = 1; o < 64; o <<= 1) {
+                const int u = __shfl_up(inc, o, 64);
+                if (lane >= o) inc += u;
+            }
+            if (c < nch) cbase[at] = run + inc - v;
+            run += __shfl(inc, 63, 64);
         }
-        demand[q] = run;
+        if (lane == 0) demand[q] = run;
     }
     __syncthreads();
     for (int q = threadIdx.x; q < G * E; q += 1024) {
@@ -486,12 +544,13 @@ vmoe_status route_launch(const Dims& D, const void* x, const void* wr, const flo
             router_gate_kernel<float><<<grid, 256, 0, st>>>(
                 static_cast<const float*>(x), static_cast<const float*>(wr), bias, noise, logits,
                 probs, idx, ws.keys, D.Ng, D.d, D.E, D.k, logits_in, tpb);
-        bin_scan_kernel<<<D.G, 1024, 0, st>>>(ws.keys, ws.bin_start, ws.fill, ws.ccount, D.Ng,
-                                               nch * D.k * D.E);
-        bin_scatter_kernel<<<cdiv(D.N, 256), 256, 0, st>>>(ws.keys, ws.bin_start, ws.fill,
-                                                            ws.members, D.N, D.Ng);
-        rank_kernel<<<cdiv(D.N, 256), 256, 0, st>>>(ws.keys, ws.bin_start, ws.members, idx, order,
-                                                     ws.ccount, D.N, D.Ng, D.E, D.k, nch);
+        bin_scan_kernel<<<D.G, 1024, 0, st>>>(ws.keys, ws.binmap, ws.bin_start, ws.fill,
+                                               ws.ccount, D.Ng, nch * D.k * D.E);
+        bin_scatter_kernel<<<cdiv(D.N, 256), 256, 0, st>>>(ws.keys, ws.binmap, ws.bin_start,
+                                                            ws.fill, ws.members, D.N, D.Ng);
+        rank_kernel<<<cdiv(D.N, 256), 256, 0, st>>>(ws.keys, ws.binmap, ws.bin_start, ws.members,
+                                                     idx, order, ws.ccount, D.N, D.Ng, D.E, D.k,
+                                                     nch);
     }
     chunk_scan_kernel<<<1, 1024, 0, st>>>(ws.ccount, ws.cbase, ws.demand, ws.carry, counts,
                                           row_base, D.G, D.E, D.k, D.C, nch);

@@ -1009,10 +1009,24 @@ vmoe_status ffn_bwd_launch(const Dims& D, const void* xe, const int32_t* counts,
     v.ldo = D.d;
     v.bsum = D.dtype == VMOE_BF16 ? db1 : nullptr;  // db1 = row sums of dH^T
     if (D.dtype == VMOE_BF16) {
-        // both weight gradients in one launch (same kernel, independent tiles)
+        // both weight gradients in one launch (same kernel, independent tiles),
+        // with the tiling of the least cost in rounds x tile area (128 x 128
+        // tiles run two per CU and cost a little more per flop)
         const GemmArgs both[2] = {w, v};
         const int rows_m[2] = {D.d, D.f};
-        launch_bf16<TileSmall, false, false, EPI_F32>(D, both, rows_m, 2, st);
+        auto tiles = [&](int bm, int bn) {
+            return D.E * (static_cast<long long>(cdiv(D.d, bm)) * cdiv(D.f, bn) +
+                          static_cast<long long>(cdiv(D.f, bm)) * cdiv(D.d, bn));
+        };
+        const double small = tile_cost((tiles(128, 128) + 1) / 2, 256, 128, 1.15);
+        const double narrow = tile_cost(tiles(256, 192), 256, 192, 1.05);
+        const double big = tile_cost(tiles(256, 256), 256, 256, 1.0);
+        if (narrow <= small && narrow <= big)
+            launch_bf16<TileNarrow, false, false, EPI_F32>(D, both, rows_m, 2, st);
+        else if (big <= small)
+            launch_bf16<TileBig, false, false, EPI_F32>(D, both, rows_m, 2, st);
+        else
+            launch_bf16<TileSmall, false, false, EPI_F32>(D, both, rows_m, 2, st);
     } else {
         launch_gemm<false, false, EPI_F32>(D, w, D.d, st);
         launch_gemm<false, false, EPI_F32>(D, v, D.f, st);

@@ -45,6 +45,24 @@ template <> struct Elem<uint16_t> {
     }
 };
 
+// ------------------------------------------------------------ buffer loads
+
+typedef int v4i32 __attribute__((ext_vector_type(4)));
+
+// Raw buffer over `bytes` bytes at `base`: loads at byte offsets >= `bytes`
+// return zeros in hardware, which implements tail masks without a branch.
+constexpr uint32_t kOutOfRange = 0x80000000u;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, long long bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), static_cast<short>(0),
+                                             static_cast<int>(bytes), 0x00020000);
+}
+
+__device__ __forceinline__ uint4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+    const v4i32 v = __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, 0);
+    return make_uint4(v[0], v[1], v[2], v[3]);
+}
+
 // ------------------------------------------------------------ shape
 
 struct Dims {

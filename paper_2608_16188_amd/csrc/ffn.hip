@@ -62,7 +62,7 @@ struct GemmArgs {
 struct GemmBatch {
     GemmArgs p[2];
     int tiles_m[2], tiles_n[2], total[2];
-    int group_m, per_xcd;
+    int group_m, chunk, per_xcd;
 };
 
 __device__ __forceinline__ int expert_rows(const int32_t* counts, int G, int E, int e) {
@@ -84,7 +84,6 @@ __device__ __forceinline__ float gelu_grad_f(float h) {
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef short s16x8 __attribute__((ext_vector_type(8)));
-typedef int v4i32 __attribute__((ext_vector_type(4)));
 
 // Two ways of staging a KB-deep operand tile (KB = 32 or 64) in LDS:
 //   STAGE_REG: global -> registers -> ds_write, rows padded (k-major rows of
@@ -123,20 +122,6 @@ __device__ __forceinline__ int lds_off(int mn, int k) {
     } else {
         return k * ROWS + (((mn >> 3) ^ mn_swizzle<ROWS>(k)) << 3) + (mn & 7);
     }
-}
-
-// Raw buffer over one expert's operand: loads at byte offsets >= `bytes` return
-// zeros in hardware, which implements every tail mask without a branch.
-constexpr uint32_t kOutOfRange = 0x80000000u;
-
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, long long bytes) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), static_cast<short>(0),
-                                             static_cast<int>(bytes), 0x00020000);
-}
-
-__device__ __forceinline__ uint4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
-    const v4i32 v = __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, 0);
-    return make_uint4(v[0], v[1], v[2], v[3]);
 }
 
 // Byte offset in HBM of the 16-byte vector holding (mn, k..k+7) [k-major] or
@@ -526,9 +511,8 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& p, f32x16 (&acc)[T
 }
 
 // One BM x BN output tile of expert e per block of WGM x WGN waves, each
-// (BM/WGM) x (BN/WGN) as 32 x 32 MFMA blocks. Blocks are numbered so that each
-// of the 8 XCDs (blocks b = x mod 8) walks a contiguous range of tiles (n
-// fastest): neighbouring tiles share operand panels in that XCD's L2.
+// (BM/WGM) x (BN/WGN) as 32 x 32 MFMA blocks; tiles are dealt to the 8 XCDs
+// in chunks of neighbouring tiles (shared operand panels in each XCD's L2).
 //
 // Pipeline over KB-deep k-stages, one barrier per stage, NS stage buffers
 // (separate LDS arrays, so every access names its buffer statically):
@@ -558,8 +542,13 @@ void gemm_bf16_kernel(GemmBatch batch) {
     __shared__ __attribute__((aligned(1024))) uint16_t buf3[NS > 3 ? SZX : 8];
     __shared__ __attribute__((aligned(1024))) uint16_t buf4[NS > 4 ? SZX : 8];
 
+    // Block b runs on XCD b mod 8 as that XCD's (b / 8)-th block; XCDs take
+    // chunks of `chunk` consecutive tiles in turn, so the tiles resident on an
+    // XCD share operand panels in its L2 while every XCD gets an even share of
+    // each expert, however unevenly the rows are spread over experts.
     const int b = blockIdx.x;
-    int w = (b & 7) * batch.per_xcd + (b >> 3);
+    const int l = b >> 3, chunk = batch.chunk;
+    int w = ((l / chunk) * 8 + (b & 7)) * chunk + l % chunk;
     if (w >= batch.total[0] + batch.total[1]) return;
     const int prob = w >= batch.total[0] ? 1 : 0;  // uniform per block
     if (prob) w -= batch.total[0];
@@ -854,9 +843,10 @@ void launch_bf16(const Dims& D, const GemmArgs* a, const int* grid_m_rows, int n
         b.tiles_n[i] = static_cast<int>(cdiv(a[i].N, T::BN));
         b.total[i] = D.E * b.tiles_m[i] * b.tiles_n[i];
     }
-    b.per_xcd = static_cast<int>(cdiv(b.total[0] + b.total[1], 8));
     // blocks resident on one XCD: 32 CUs x blocks per CU
     b.group_m = T::WAVES_PER_EU == 2 && T::NW == 4 ? 8 : 4;
+    b.chunk = 4 * b.group_m;
+    b.per_xcd = static_cast<int>(cdiv(b.total[0] + b.total[1], 8 * b.chunk)) * b.chunk;
     gemm_bf16_kernel<T, AK, BK_, EPI><<<8 * b.per_xcd, T::NT, 0, st>>>(b);
 }
 

@@ -1,8 +1,9 @@
 // Noisy top-k gating with capacity and batch-prioritized routing on gfx950.
 //
 // Pipeline (all on the caller's stream, no host synchronisation):
-//   1. router_gate   logits (double-accumulated, increasing-i order, rounded
-//                    once to f32), noisy softmax, top-k, 26-bit priority key
+//   1. router        logits (bf16: matrix-core product, f32 accumulation;
+//                    f32: double-accumulated in increasing i, rounded once),
+//                    noisy softmax, top-k, 26-bit priority key
 //   2. bin_scan      per group: key range -> 4096 bins spanning it, histogram
 //                    in LDS, exclusive scan -> bin starts; clears the counters
 //   3. bin_scatter   tokens into their bins (atomic fill; order inside a bin
@@ -38,7 +39,7 @@ struct BinMap {
     }
 };
 constexpr int kSlotChunk = 256;              // order positions per slots block
-constexpr int kGateTokens = 32;              // most tokens per router_gate block
+constexpr int kGateTokens = 32;              // most tokens per f64 router block
 
 struct RouteWs {
     uint32_t* keys;     // [N]
@@ -107,16 +108,7 @@ __device__ __forceinline__ uint32_t priority_key(float prio) {
     return key < (1u << kKeyBits) ? key : (1u << kKeyBits) - 1u;
 }
 
-// Eight consecutive activations as f32 (16-byte aligned).
-__device__ __forceinline__ void load8(const uint16_t* p, float* v) {
-    const uint4 u = *reinterpret_cast<const uint4*>(p);
-    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        v[2 * q] = __uint_as_float(w[q] << 16);
-        v[2 * q + 1] = __uint_as_float(w[q] & 0xFFFF0000u);
-    }
-}
+// Eight consecutive f32 activations (16-byte aligned).
 __device__ __forceinline__ void load8(const float* p, float* v) {
     const float4 a = reinterpret_cast<const float4*>(p)[0];
     const float4 b = reinterpret_cast<const float4*>(p)[1];
@@ -124,157 +116,13 @@ __device__ __forceinline__ void load8(const float* p, float* v) {
     v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
 }
 
-// x and W_r are staged in LDS 32 vectors of 16 bytes (256 bf16 / 128 f32
-// columns) per row at a time; rows are padded by one vector so the 16-byte
-// reads of different rows fall in different banks.
-constexpr int kGateVecs = 32;
-
-// One block = tpb = min(32, floor(256 / E)) tokens of one group. Thread tid < tpb*E
-// computes logit (token tid / E, expert tid % E) as a sequential dot product
-// in double over increasing i; the block's x rows and the group's router rows
-// are staged through LDS a slice of columns at a time (coalesced 16-byte loads,
-// next round prefetched in registers), so the dependency chains only wait on
-// LDS. The gate of each token then runs on one thread from LDS.
-template <typename T>
-__global__ __launch_bounds__(256) void router_gate_kernel(
-    const T* __restrict__ x, const T* __restrict__ wr, const float* __restrict__ bias,
-    const float* __restrict__ noise, float* __restrict__ logits, float* __restrict__ probs,
-    int32_t* __restrict__ idx, uint32_t* __restrict__ keys, int Ng, int d, int E, int k,
-    int logits_in, int tpb) {
-    constexpr int VE = 16 / sizeof(T);             // elements per 16-byte vector
-    constexpr int VPR = kGateVecs;                 // vectors per staged row
-    constexpr int GC = VPR * VE;                   // columns per round
-    constexpr int LDR = GC + VE;                   // LDS row length (elements)
-    constexpr int MAXROWS = kGateTokens + kMaxExperts;
-    __shared__ __attribute__((aligned(16))) T stage[MAXROWS * LDR];
-    __shared__ float lg_store[kGateTokens * (kMaxExperts + 1)];
-    __shared__ int row_bad[2][MAXROWS];
-    const int g = blockIdx.y;
-    const int t0 = blockIdx.x * tpb;                  // within group
-    const int ntok = min(tpb, Ng - t0);
-    const size_t tok0 = static_cast<size_t>(g) * Ng + t0;  // global index
-    const int tid = threadIdx.x;
-    const int ld = E + 1;                             // LDS row of one token's logits
-    if (!logits_in) {
-        // staged rows: ntok token rows, then E router rows
-        const int rows = ntok + E;
-        const T* wg = wr + static_cast<size_t>(g) * E * d;
-        constexpr int MAXV = (MAXROWS * VPR + 255) / 256;  // vectors per thread per round
-        const int nvec = rows * VPR;
-        uint4 pre[MAXV];
-        auto fetch = [&](int c0) {
-#pragma unroll
-            for (int q = 0; q < MAXV; ++q) {
-                const int v = tid + 256 * q;
-                const int r = v / VPR, col = c0 + (v % VPR) * VE;
-                pre[q] = make_uint4(0u, 0u, 0u, 0u);
-                if (v < nvec && col < d) {
-                    const T* src = r < ntok ? x + (tok0 + r) * d + col
-                                            : wg + static_cast<size_t>(r - ntok) * d + col;
-                    pre[q] = *reinterpret_cast<const uint4*>(src);
-                }
-            }
-        };
-        // bf16 rows whose staged values are all zero or of magnitude in
-        // [2^-63, 2^63) give products that are exact normal f32 numbers; a row
-        // with any other value (subnormal, huge, inf, nan) is marked in
-        // row_bad[round parity] and its dot products take the f64 path
-        auto park = [&](int par) {
-#pragma unroll
-            for (int q = 0; q < MAXV; ++q) {
-                const int v = tid + 256 * q;
-                if (v < nvec) {
-                    *reinterpret_cast<uint4*>(stage + (v / VPR) * LDR + (v % VPR) * VE) = pre[q];
-                    if constexpr (sizeof(T) == 2) {
-                        const uint32_t w4[4] = {pre[q].x, pre[q].y, pre[q].z, pre[q].w};
-                        bool bad = false;
-#pragma unroll
-                        for (int h = 0; h < 8; ++h) {
-                            const uint32_t b = (w4[h >> 1] >> (16 * (h & 1))) & 0x7FFFu;
-                            const uint32_t ex = b >> 7;
-                            bad |= b != 0 && (ex < 64 || ex > 189);
-                        }
-                        if (bad) atomicOr(&row_bad[par][v / VPR], 1);
-                    }
-                }
-            }
-        };
-        const bool mine = tid < ntok * E;
-        const int tt = tid / E, e = tid % E;
-        const T* xs = stage + tt * LDR;
-        const T* wsr = stage + (ntok + e) * LDR;
-        double acc = 0.0;
-        for (int r = tid; r < 2 * MAXROWS; r += 256) row_bad[r / MAXROWS][r % MAXROWS] = 0;
-        __syncthreads();
-        fetch(0);
-        for (int c0 = 0, par = 0; c0 < d; c0 += GC, par ^= 1) {
-            park(par);
-            __syncthreads();
-            if (c0 + GC < d) fetch(c0 + GC);
-            // the other parity's flags were last read in the previous round
-            for (int r = tid; r < MAXROWS; r += 256) row_bad[par ^ 1][r] = 0;
-            const bool exact_f32 = mine && row_bad[par][tt] == 0 && row_bad[par][ntok + e] == 0;
-            if (mine) {
-                const int n = min(GC, d - c0);
-                // Each product of two bf16 / f32 values is exact in double, so
-                // the fused multiply-add equals add-after-multiply, in increasing i.
-                // 32 columns per step; the next step's LDS reads are issued
-                // before this step's multiply-add chain. Staged columns past d
-                // are zeros: their products add +0 to a sum that starts at +0
-                // and so can never be -0, which leaves it unchanged.
-                const int nn = (n + 31) & ~31;
-                float xv[2][32], wv[2][32];
-                auto read32 = [&](int i, float (&xa)[32], float (&wa)[32]) {
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        load8(xs + i + 8 * q, xa + 8 * q);
-                        load8(wsr + i + 8 * q, wa + 8 * q);
-                    }
-                };
-                auto chain32 = [&](const float (&xa)[32], const float (&wa)[32]) {
-                    if (sizeof(T) == 2 && exact_f32) {
-                        // bf16 x bf16 is exact in f32 (8-bit significands), so
-                        // acc + double(x * w) rounds exactly like the fused
-                        // multiply-add in double; the products and widenings
-                        // are off the dependency chain, which is the adds
-                        double pd[32];
-#pragma unroll
-                        for (int q = 0; q < 32; ++q) pd[q] = static_cast<double>(xa[q] * wa[q]);
-#pragma unroll
-                        for (int q = 0; q < 32; ++q) acc = acc + pd[q];
-                    } else {
-#pragma unroll
-                        for (int q = 0; q < 32; ++q)
-                            acc = __builtin_fma(static_cast<double>(xa[q]),
-                                                static_cast<double>(wa[q]), acc);
-                    }
-                };
-                read32(0, xv[0], wv[0]);
-                for (int i = 0; i < nn; i += 64) {
-                    const bool two = i + 32 < nn;  // uniform
-                    if (two) read32(i + 32, xv[1], wv[1]);
-                    chain32(xv[0], wv[0]);
-                    if (i + 64 < nn) read32(i + 64, xv[0], wv[0]);
-                    if (two) chain32(xv[1], wv[1]);
-                }
-            }
-            __syncthreads();
-        }
-        if (mine) {
-            const float v = static_cast<float>(acc);
-            logits[(tok0 + tt) * E + e] = v;
-            lg_store[tt * ld + e] = v;
-        }
-    } else if (tid < ntok * E) {
-        const int tt = tid / E, e = tid % E;
-        lg_store[tt * ld + e] = logits[(tok0 + tt) * E + e];
-    }
-    __syncthreads();
-
-    if (tid >= ntok) return;
-    // Gate of token tid; its noisy logits z overwrite its row of lg_store.
-    const size_t t = tok0 + tid;
-    float* z = lg_store + tid * ld;
+// Gate of token t from its logits in z[0..E) (LDS; overwritten by the noisy
+// logits): perturb, deterministic softmax, top-k by z (ties to the lower
+// expert), priority key of p[first choice].
+__device__ __forceinline__ void gate_token(float* z, size_t t, const float* __restrict__ bias,
+                                           const float* __restrict__ noise,
+                                           float* __restrict__ probs, int32_t* __restrict__ idx,
+                                           uint32_t* __restrict__ keys, int E, int k) {
     float m = 0.0f;
     for (int e = 0; e < E; ++e) {
         float v = z[e];
@@ -297,6 +145,186 @@ __global__ __launch_bounds__(256) void router_gate_kernel(
         if (j == 0) first = best;
     }
     keys[t] = priority_key(__fdiv_rn(exp_spec(z[first] - m), s));
+}
+
+// ---------------------------------------------------------------- bf16: MFMA
+//
+// One block = 32 tokens of one group, four waves. The router product
+// x[32, d] W_r[g]^T runs on v_mfma_f32_32x32x16_bf16 (f32 accumulation), the
+// d range split in four contiguous quarters, one per wave, whose partial
+// products are added in wave order; A and B fragments are 16-byte loads of
+// x rows and W_r rows straight from memory (both k-contiguous), eight k-steps
+// in flight. Then one thread per token runs the gate.
+typedef __bf16 bf16x8_r __attribute__((ext_vector_type(8)));
+typedef float f32x16_r __attribute__((ext_vector_type(16)));
+constexpr int kMfmaTokens = 32;
+
+__global__ __launch_bounds__(256) void router_mfma_kernel(
+    const uint16_t* __restrict__ x, const uint16_t* __restrict__ wr,
+    const float* __restrict__ bias, const float* __restrict__ noise, float* __restrict__ logits,
+    float* __restrict__ probs, int32_t* __restrict__ idx, uint32_t* __restrict__ keys, int Ng,
+    int d, int E, int k, int logits_in) {
+    __shared__ float red[4][kMfmaTokens][kMaxExperts + 1];
+    const int g = blockIdx.y;
+    const int t0 = blockIdx.x * kMfmaTokens;
+    const int ntok = min(kMfmaTokens, Ng - t0);
+    const size_t tok0 = static_cast<size_t>(g) * Ng + t0;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    if (!logits_in) {
+        const __amdgpu_buffer_rsrc_t rx =
+            make_rsrc(x + tok0 * d, static_cast<long long>(ntok) * d * 2);
+        const __amdgpu_buffer_rsrc_t rw =
+            make_rsrc(wr + static_cast<size_t>(g) * E * d, static_cast<long long>(E) * d * 2);
+        const int ksteps = (d + 15) / 16;
+        const int per = (ksteps + 3) / 4;
+        const int s0 = wave * per, s1 = min(ksteps, s0 + per);
+        const int m = lane & 31, kh = (lane >> 5) * 8;
+        // 16-byte vector (row r, columns k..k+7), zero outside the rows / past d
+        auto off = [&](int r, int rows, int kk) {
+            return (r < rows && kk < d) ? static_cast<uint32_t>(r * d + kk) * 2u : kOutOfRange;
+        };
+        f32x16_r acc0, acc1;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc0[r] = acc1[r] = 0.0f;
+        constexpr int U = 8;
+        for (int s = s0; s < s1; s += U) {
+            uint4 av[U], bv0[U], bv1[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int kk = (s + u) * 16 + kh;
+                const bool live = s + u < s1;
+                av[u] = buf_load16(rx, live ? off(m, ntok, kk) : kOutOfRange);
+                bv0[u] = buf_load16(rw, live ? off(m, E, kk) : kOutOfRange);
+                if (E > 32) bv1[u] = buf_load16(rw, live ? off(32 + m, E, kk) : kOutOfRange);
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const bf16x8_r a = __builtin_bit_cast(bf16x8_r, av[u]);
+                acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                    __builtin_bit_cast(bf16x8_r, bv0[u]), a, acc0, 0, 0, 0);
+                if (E > 32)
+                    acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                        __builtin_bit_cast(bf16x8_r, bv1[u]), a, acc1, 0, 0, 0);
+            }
+        }
+        // register 4q + r of lane l: token l % 32, expert 8q + 4 (l / 32) + r (+ 32)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int n = 8 * q + 4 * (lane >> 5) + r;
+                red[wave][m][n] = acc0[4 * q + r];
+                if (E > 32) red[wave][m][32 + n] = acc1[4 * q + r];
+            }
+    }
+    __syncthreads();
+    for (int q = tid; q < ntok * E; q += 256) {
+        const int t = q / E, e = q % E;
+        float v;
+        if (logits_in) {
+            v = logits[(tok0 + t) * E + e];
+        } else {
+            v = ((red[0][t][e] + red[1][t][e]) + red[2][t][e]) + red[3][t][e];
+            logits[(tok0 + t) * E + e] = v;
+        }
+        red[1][t][e] = v;  // staged in wave 1's slot, no reader of it remains
+    }
+    __syncthreads();
+    if (tid < ntok) gate_token(&red[1][tid][0], tok0 + tid, bias, noise, probs, idx, keys, E, k);
+}
+
+// ------------------------------------------------------------ f32: f64 sums
+//
+// f32 activations: logit (token, expert) is a sequential dot product in
+// double over increasing i (each product of two f32 values is exact in
+// double, so the fused multiply-add rounds once per step). One block =
+// tpb = min(32, floor(256 / E)) tokens of one group; thread tid < tpb*E owns
+// one (token, expert); the block's x rows and the group's router rows are
+// staged through LDS 128 columns at a time (coalesced 16-byte loads, next
+// slice prefetched in registers).
+constexpr int kGateVecs = 32;  // 16-byte vectors per staged row and round
+
+__global__ __launch_bounds__(256) void router_f64_kernel(
+    const float* __restrict__ x, const float* __restrict__ wr, const float* __restrict__ bias,
+    const float* __restrict__ noise, float* __restrict__ logits, float* __restrict__ probs,
+    int32_t* __restrict__ idx, uint32_t* __restrict__ keys, int Ng, int d, int E, int k,
+    int logits_in, int tpb) {
+    constexpr int VE = 4;                          // f32 per 16-byte vector
+    constexpr int VPR = kGateVecs;                 // vectors per staged row
+    constexpr int GC = VPR * VE;                   // columns per round
+    constexpr int LDR = GC + VE;                   // LDS row length (elements)
+    constexpr int MAXROWS = kGateTokens + kMaxExperts;
+    __shared__ __attribute__((aligned(16))) float stage[MAXROWS * LDR];
+    __shared__ float lg_store[kGateTokens * (kMaxExperts + 1)];
+    const int g = blockIdx.y;
+    const int t0 = blockIdx.x * tpb;                  // within group
+    const int ntok = min(tpb, Ng - t0);
+    const size_t tok0 = static_cast<size_t>(g) * Ng + t0;  // global index
+    const int tid = threadIdx.x;
+    const int ld = E + 1;                             // LDS row of one token's logits
+    if (!logits_in) {
+        // staged rows: ntok token rows, then E router rows
+        const int rows = ntok + E;
+        const float* wg = wr + static_cast<size_t>(g) * E * d;
+        constexpr int MAXV = (MAXROWS * VPR + 255) / 256;  // vectors per thread per round
+        const int nvec = rows * VPR;
+        uint4 pre[MAXV];
+        auto fetch = [&](int c0) {
+#pragma unroll
+            for (int q = 0; q < MAXV; ++q) {
+                const int v = tid + 256 * q;
+                const int r = v / VPR, col = c0 + (v % VPR) * VE;
+                pre[q] = make_uint4(0u, 0u, 0u, 0u);
+                if (v < nvec && col < d) {
+                    const float* src = r < ntok ? x + (tok0 + r) * d + col
+                                                : wg + static_cast<size_t>(r - ntok) * d + col;
+                    pre[q] = *reinterpret_cast<const uint4*>(src);
+                }
+            }
+        };
+        auto park = [&]() {
+#pragma unroll
+            for (int q = 0; q < MAXV; ++q) {
+                const int v = tid + 256 * q;
+                if (v < nvec)
+                    *reinterpret_cast<uint4*>(stage + (v / VPR) * LDR + (v % VPR) * VE) = pre[q];
+            }
+        };
+        const bool mine = tid < ntok * E;
+        const int tt = tid / E, e = tid % E;
+        const float* xs = stage + tt * LDR;
+        const float* wsr = stage + (ntok + e) * LDR;
+        double acc = 0.0;
+        fetch(0);
+        for (int c0 = 0; c0 < d; c0 += GC) {
+            park();
+            __syncthreads();
+            if (c0 + GC < d) fetch(c0 + GC);
+            if (mine) {
+                const int n = min(GC, d - c0);  // a multiple of 8
+                for (int i = 0; i < n; i += 8) {
+                    float xv[8], wv[8];
+                    load8(xs + i, xv);
+                    load8(wsr + i, wv);
+#pragma unroll
+                    for (int q = 0; q < 8; ++q)
+                        acc = __builtin_fma(static_cast<double>(xv[q]), static_cast<double>(wv[q]),
+                                            acc);
+                }
+            }
+            __syncthreads();
+        }
+        if (mine) {
+            const float v = static_cast<float>(acc);
+            logits[(tok0 + tt) * E + e] = v;
+            lg_store[tt * ld + e] = v;
+        }
+    } else if (tid < ntok * E) {
+        const int tt = tid / E, e = tid % E;
+        lg_store[tt * ld + e] = logits[(tok0 + tt) * E + e];
+    }
+    __syncthreads();
+    if (tid < ntok) gate_token(lg_store + tid * ld, tok0 + tid, bias, noise, probs, idx, keys, E, k);
 }
 
 // Exclusive scan of one value per thread over a 1024-thread block.
@@ -534,16 +562,18 @@ vmoe_status route_launch(const Dims& D, const void* x, const void* wr, const flo
     const int nch = static_cast<int>(cdiv(D.Ng, kSlotChunk));
     const int logits_in = (flags & VMOE_ROUTE_LOGITS_IN) ? 1 : 0;
     if (D.N > 0) {
-        const int tpb = min(kGateTokens, 256 / D.E);
-        dim3 grid(cdiv(D.Ng, tpb), D.G);
-        if (D.dtype == VMOE_BF16)
-            router_gate_kernel<uint16_t><<<grid, 256, 0, st>>>(
+        if (D.dtype == VMOE_BF16) {
+            dim3 grid(cdiv(D.Ng, kMfmaTokens), D.G);
+            router_mfma_kernel<<<grid, 256, 0, st>>>(
                 static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(wr), bias, noise,
-                logits, probs, idx, ws.keys, D.Ng, D.d, D.E, D.k, logits_in, tpb);
-        else
-            router_gate_kernel<float><<<grid, 256, 0, st>>>(
+                logits, probs, idx, ws.keys, D.Ng, D.d, D.E, D.k, logits_in);
+        } else {
+            const int tpb = min(kGateTokens, 256 / D.E);
+            dim3 grid(cdiv(D.Ng, tpb), D.G);
+            router_f64_kernel<<<grid, 256, 0, st>>>(
                 static_cast<const float*>(x), static_cast<const float*>(wr), bias, noise, logits,
                 probs, idx, ws.keys, D.Ng, D.d, D.E, D.k, logits_in, tpb);
+        }
         bin_scan_kernel<<<D.G, 1024, 0, st>>>(ws.keys, ws.binmap, ws.bin_start, ws.fill,
                                                ws.ccount, D.Ng, nch * D.k * D.E);
         bin_scatter_kernel<<<cdiv(D.N, 256), 256, 0, st>>>(ws.keys, ws.binmap, ws.bin_start,

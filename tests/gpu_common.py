@@ -51,6 +51,34 @@ def as_f64(arr, dtype) -> np.ndarray:
     return W.to_f64(arr, dtype)
 
 
+def assert_router_logits(got, x64, wr64, n_groups, dtype):
+    """GPU router logits against the oracle's (double sum rounded once to f32).
+
+    f32 activations: bit for bit (both sides sum the exact products in double
+    in increasing i). bf16 activations: the GPU adds the exact bf16 products in
+    f32 on the matrix cores (in the kernel's own order, d split over four
+    waves), so a logit may differ from the exactly rounded sum by at most
+    gamma_(d+3) * sum_i |x_i w_i| (an f32 sum of d exact terms plus three
+    partial-sum additions, Higham eq. 3.5, gamma_n ~ n 2^-24) plus the
+    reference's own rounding, 2^-24 |ref|; the check allows twice that.
+    """
+    ref = oracle.router_logits(x64, wr64, n_groups)
+    got = np.asarray(got)
+    if dtype == W.F32:
+        assert bits_equal(got, ref), "router logits not bit-exact"
+        return ref
+    N, d = x64.shape
+    ng = N // n_groups
+    mag = np.empty_like(got, dtype=np.float64)
+    for g in range(n_groups):
+        mag[g * ng:(g + 1) * ng] = np.abs(x64[g * ng:(g + 1) * ng]) @ np.abs(wr64[g]).T
+    bound = 2.0 * ((d + 3) * 2.0 ** -24 * mag + 2.0 ** -24 * np.abs(ref.astype(np.float64)))
+    err = np.abs(got.astype(np.float64) - ref.astype(np.float64))
+    worst = float(np.max(err - bound)) if err.size else 0.0
+    assert worst <= 0.0, f"router logits off by more than the f32 summation bound ({worst:.3g})"
+    return ref
+
+
 @functools.lru_cache(maxsize=2)
 def workload_inputs(name: str, with_experts: bool = True):
     cfg = W.CONFIGS[name]

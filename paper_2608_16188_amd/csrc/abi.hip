@@ -209,11 +209,8 @@ vmoe_status vmoe_route_bwd(const vmoe_shape* shape, const void* x, const void* w
     VMOE_TRY(vmoe::make_dims(shape, &D));
     VMOE_TRY(need(dev(x) && dev(w_router) && dev(probs) && dev(expert_idx) && dev(slot) &&
                   dev(dgate) && dev(dx) && opt(dw_router)));
-    if (dw_router) {
-        const size_t need_ws = vmoe::route_bwd_workspace_bytes(D);
-        if (workspace_bytes < need_ws || (need_ws > 0 && !dev(workspace)))
-            return VMOE_ERR_WORKSPACE;
-    }
+    const size_t need_ws = vmoe::route_bwd_workspace_bytes(D);
+    if (workspace_bytes < need_ws || (need_ws > 0 && !dev(workspace))) return VMOE_ERR_WORKSPACE;
     return vmoe::route_bwd_launch(D, x, w_router, probs, expert_idx, slot, dgate, dx, dw_router,
                                   workspace, as_stream(stream));
 }

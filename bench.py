@@ -62,14 +62,26 @@ def algorithmic_cost(cfg, A: int, n_noise: bool, n_bias: bool):
 TRAFFIC_PROFILE = {"vitb16_bf16": "profiles/vitb16_bf16_hbm_traffic.txt"}
 
 
+def source_digest(path: str) -> str:
+    """sha256 of a C/HIP source with its // comments and blank lines removed,
+    so that edits to comments alone keep measured counters valid."""
+    import hashlib
+    lines = []
+    for line in open(path, encoding="utf-8"):
+        code = line.split("//", 1)[0].rstrip()
+        if code:
+            lines.append(code)
+    return hashlib.sha256("\n".join(lines).encode()).hexdigest()
+
+
 def measured_traffic(workload: str, call: str):
     """HBM bytes per call from the committed rocprofv3 PMC summary.
 
     The summary holds calibrated FETCH_SIZE / WRITE_SIZE bytes per C-ABI call
-    and the sha256 of the sources the counters were taken with; a call whose
-    sources have changed since then has no measured traffic (None).
+    and the code digest (source_digest) of the sources the counters were
+    taken with; a call whose code has changed since then has no measured
+    traffic (None).
     """
-    import hashlib
     rel = TRAFFIC_PROFILE.get(workload)
     if rel is None or not os.path.exists(os.path.join(ROOT, rel)):
         return None
@@ -84,8 +96,7 @@ def measured_traffic(workload: str, call: str):
             "route_bwd": ["route_bwd.hip"]}.get(call, ["moves.hip"]) + ["common.h"]
     csrc = os.path.join(ROOT, "paper_2608_16188_amd", "csrc")
     for f in used:
-        h = hashlib.sha256(open(os.path.join(csrc, f), "rb").read()).hexdigest()
-        if sources.get(f) != h:
+        if sources.get(f) != source_digest(os.path.join(csrc, f)):
             return None
     return calls.get(call)
 

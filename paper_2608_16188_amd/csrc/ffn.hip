@@ -1,20 +1,30 @@
 // Expert MLP forward and backward as grouped GEMMs on gfx950.
 //
 // bf16 path: one templated matrix-core kernel, C[M x N] = sum_k A(m,k) B(n,k),
-// per expert (grid.z). Tiles of 128 x 128 x 64 per 256-thread block, four
-// waves in 2 x 2, each wave 64 x 64 as 4 x 4 blocks of
-// v_mfma_f32_16x16x32_bf16 with f32 accumulation. Both operands are staged
-// in LDS k-contiguous (double buffered, one barrier per k-step); an operand
-// whose k index is strided in HBM (weights read transposed in the backward,
-// the row-reduced weight-gradient GEMMs) is loaded as 4 k-rows x 8 values
-// per thread and transposed in registers on its way into LDS. The operand
-// roles are swapped inside the MFMA so each lane ends up holding 4
-// consecutive output columns of one row, which the fused epilogues (bias,
-// GELU, GELU', bf16 rounding, f32 weight gradients) store directly.
+// one output tile of one expert per block. Tiles (Tile<>) are 256 x 256 or
+// 256 x 192 with eight waves (one block per CU) or 128 x 128 with four waves
+// (two blocks per CU); each wave accumulates its sub-tile with
+// v_mfma_f32_32x32x16_bf16 in f32. Operands reach LDS through buffer loads
+// that write LDS directly (16 bytes per lane, out-of-range offsets read as
+// zero, so ragged tails need no branch) into a ring of 2-4 stages; the next
+// stages' loads stay in flight across the barrier (partial vmcnt waits).
+// An operand whose k index is contiguous in HBM is stored k-major with an
+// XOR chunk swizzle; one whose k index is strided (weights read transposed
+// in the backward, the token-reduced weight-gradient GEMMs) is copied
+// unchanged, mn-major, and its fragments are read with ds_read_b64_tr_b16.
+// The operand roles are swapped inside the MFMA so each lane holds runs of
+// consecutive output columns of one row; the fused epilogues (bias, GELU and
+// GELU' pair, GELU' product, bf16 rounding, f32 weight gradients with the
+// bias-gradient row sums) park the tile in LDS and store 16-byte row
+// segments.
 //
 // Each expert's row count n_e = sum_g counts[g, e] is read on the device:
 // tiles past n_e exit at once (M = n_e GEMMs) or n_e bounds the k loop
 // (weight-gradient GEMMs, which still write zeros for an empty expert).
+// Blocks are mapped so that each XCD works on a contiguous run of tiles,
+// grouped group_m m-tiles at a time, which keeps operand panels in that
+// XCD's L2. The tile shape is chosen per launch by a cost model: rounds of
+// 256 CUs times the tile area, scaled by a per-shape efficiency.
 //
 // f32 path: a plain LDS-tiled FMA kernel with the same operand and epilogue
 // description (small widths; accuracy path).

@@ -853,8 +853,14 @@ void launch_bf16(const Dims& D, const GemmArgs* a, const int* grid_m_rows, int n
         b.tiles_n[i] = static_cast<int>(cdiv(a[i].N, T::BN));
         b.total[i] = D.E * b.tiles_m[i] * b.tiles_n[i];
     }
-    // blocks resident on one XCD: 32 CUs x blocks per CU
-    b.group_m = T::WAVES_PER_EU == 2 && T::NW == 4 ? 8 : 4;
+    // blocks resident on one XCD: 32 CUs x blocks per CU. A single problem
+    // with both operands k-major whose experts span at most 8 m-tiles is
+    // dealt a whole m-column of one expert per chunk (each XCD streams one
+    // expert's row panels past four of its weight panels; measured faster for
+    // the forward GEMMs, slower for the transposed-weight ones); otherwise
+    // patches of 4 m-tiles.
+    const int one_col = AK && BK_ && n == 1 && b.tiles_m[0] <= 8 ? b.tiles_m[0] : 0;
+    b.group_m = one_col ? one_col : (T::WAVES_PER_EU == 2 && T::NW == 4 ? 8 : 4);
     b.chunk = 4 * b.group_m;
     b.per_xcd = static_cast<int>(cdiv(b.total[0] + b.total[1], 8 * b.chunk)) * b.chunk;
     gemm_bf16_kernel<T, AK, BK_, EPI><<<8 * b.per_xcd, T::NT, 0, st>>>(b);

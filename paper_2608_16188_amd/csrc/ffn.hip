@@ -510,10 +510,18 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& p, f32x16 (&acc)[T
                     const int m = m0 + wm * WM + i0 * 32 + ml;
                     const uint4 v = *reinterpret_cast<const uint4*>(ep + o * EP_TILE +
                                                                     (ml * EP_LD + cl) * ELEM);
-                    if (m < M && n < N)
-                        *reinterpret_cast<uint4*>(
+                    if (m < M && n < N) {
+                        v4i32* dst = reinterpret_cast<v4i32*>(
                             dst_base +
-                            (e * p.out_estride + static_cast<size_t>(m) * p.ldo + n) * ELEM) = v;
+                            (e * p.out_estride + static_cast<size_t>(m) * p.ldo + n) * ELEM);
+                        // weight gradients are not read again by the layer: streaming
+                        // stores keep them from displacing cached activations (the f32
+                        // write-back cost a fifth of the weight-gradient GEMM, measured alone)
+                        if constexpr (F32_OUT)
+                            __builtin_nontemporal_store(__builtin_bit_cast(v4i32, v), dst);
+                        else
+                            *dst = __builtin_bit_cast(v4i32, v);
+                    }
                 }
             }
         }

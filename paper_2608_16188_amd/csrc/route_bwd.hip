@@ -1,11 +1,12 @@
 // Backward through the gate into the router on gfx950.
 //
-// dz = p * (dp - <p, dp>) (dp is non-zero only at the kept experts) is formed
-// per token chunk in LDS by each kernel that needs it. One kernel adds dz W_r
-// into dx (token-parallel, W_r columns in registers); one forms per-chunk
-// partials of dW_r[e, i] = sum_t dz[t,e] x[t,i] (skipped for frozen routers)
-// and a third adds the partials over chunks in a fixed order (deterministic,
-// no float atomics).
+// One streaming kernel per (token chunk, column block, group): it forms
+// dz = p * (dp - <p, dp>) for the chunk's tokens in LDS (dp is non-zero only
+// at the kept experts), then walks the tokens once, adding dz W_r into dx
+// (W_r columns in registers) and, unless the router is frozen, accumulating
+// the chunk's partial of dW_r[e, i] = sum_t dz[t,e] x[t,i] in registers. A
+// second kernel adds the partials over chunks in a fixed order
+// (deterministic, no float atomics).
 #include "common.h"
 
 namespace vmoe {
@@ -47,55 +48,11 @@ __device__ __forceinline__ void store_cols(float* p, const float (&v)[VEC]) {
     else *p = v[0];
 }
 
-// Columns per lane: a lane keeps E x VEC router weights (dx kernel) or E x VEC
-// gradient partials (dW kernel) in registers.
-template <int EMAX> struct ColsPerLane { static constexpr int value = EMAX <= 32 ? 4 : 2; };
-
-// dz[t, e] = p[t,e] (dp[t,e] - <p[t], dp[t]>), dp = dgate at the kept experts
-// and 0 elsewhere, written once to the workspace so the two streaming kernels
-// read contiguous rows of it. One thread per (token, expert): each forms its
-// token's <p, dp> itself (k assignments, in j order), so all threads wait on
-// two rounds of loads at most and the rows come out coalesced.
-__global__ __launch_bounds__(256) void route_bwd_dz_kernel(const float* __restrict__ probs,
-                                                           const int32_t* __restrict__ idx,
-                                                           const int32_t* __restrict__ slot,
-                                                           const float* __restrict__ dgate,
-                                                           float* __restrict__ dz, int N, int E,
-                                                           int k) {
-    const long long q = static_cast<long long>(blockIdx.x) * 256 + threadIdx.x;
-    if (q >= static_cast<long long>(N) * E) return;
-    const size_t t = static_cast<size_t>(q / E);
-    const int e = static_cast<int>(q - static_cast<long long>(t) * E);
-    const float* pr = probs + t * E;
-    float pdp = 0.0f, dp = 0.0f;
-    bool kept = false;
-    for (int j = 0; j < k; ++j) {
-        const size_t a = t * k + j;
-        if (slot[a] >= 0) {
-            const int ej = idx[a];
-            const float gj = dgate[a];
-            pdp = __builtin_fmaf(pr[ej], gj, pdp);
-            if (ej == e) {
-                kept = true;
-                dp = gj;
-            }
-        }
-    }
-    // kept: p (dgate - <p, dp>); other experts: -p <p, dp>
-    dz[q] = kept ? pr[e] * (dp - pdp) : -pr[e] * pdp;
-}
-
-// The dz rows of tokens [tok0, tok0 + ntok) into LDS rows of EMAX floats
-// (16-byte aligned, zero past E), coalesced, one round.
-template <int EMAX>
-__device__ __forceinline__ void stage_dz(float (*dzs)[EMAX], const float* __restrict__ dz,
-                                         size_t tok0, int ntok, int E) {
-    const float* src = dz + tok0 * E;
-    for (int q = threadIdx.x; q < ntok * EMAX; q += 256) {
-        const int t = q / EMAX, e = q % EMAX;
-        dzs[t][e] = e < E ? src[t * E + e] : 0.0f;
-    }
-}
+// Columns per lane: a lane keeps E x VEC router weights and E x VEC gradient
+// partials in registers.
+template <int EMAX> struct ColsPerLane {
+    static constexpr int value = EMAX <= 8 ? 4 : (EMAX <= 16 ? 2 : 1);
+};
 
 // A token's dz row from LDS into registers (broadcast 16-byte reads).
 template <int EMAX>
@@ -107,27 +64,42 @@ __device__ __forceinline__ void read_dz(const float (*dzs)[EMAX], int t, float (
     }
 }
 
-constexpr int kDxTokens = 64;  // tokens per dx block
-
-// dx[t, cols] += sum_e dz[t, e] W[e, cols]. A block owns kDxTokens tokens of
-// one group and 64 * VEC columns; the lane's W columns stay in registers and
-// wave w takes the block's tokens w, w + 4, ... (dz is a broadcast LDS read),
-// U tokens' dx loads in flight at a time.
-template <typename T, int EMAX>
-__global__ __launch_bounds__(256) void route_bwd_dx_kernel(
-    const T* __restrict__ wr, const float* __restrict__ dz, float* __restrict__ dx, int Ng, int d,
-    int E) {
+// Block = a chunk of tch tokens of group g (blockIdx.x, .z) times 64 * VEC
+// columns (blockIdx.y), four waves; wave w takes the chunk's tokens w, w + 4,
+// ..., with the x and dx rows of U tokens in flight.
+//   1. the first round's loads are issued, then dz of the chunk is formed in
+//      LDS: one thread per token adds <p, dp> over its kept assignments in j
+//      order and records dp, then one thread per (token, expert) writes
+//      kept ? p (dp - <p, dp>) : -p <p, dp>;
+//   2. per token: dx[t, cols] += sum_e dz[t,e] W[e, cols] (e ascending) and
+//      acc[e, cols] += dz[t,e] x[t, cols];
+//   3. (DW) the four waves' partials are added in wave order through LDS and
+//      written to the chunk's slot of `partial`.
+template <typename T, int EMAX, bool DW>
+__global__ __launch_bounds__(256) void route_bwd_kernel(
+    const T* __restrict__ x, const T* __restrict__ wr, const float* __restrict__ probs,
+    const int32_t* __restrict__ idx, const int32_t* __restrict__ slot,
+    const float* __restrict__ dgate, float* __restrict__ dx, float* __restrict__ partial, int Ng,
+    int d, int E, int k, int tch, int nch) {
     constexpr int VEC = ColsPerLane<EMAX>::value;
-    constexpr int U = 4;
-    __shared__ __attribute__((aligned(16))) float dzs[kDxTokens][EMAX];
+    constexpr int COLS = 64 * VEC;
+    constexpr int U = EMAX <= 8 ? 4 : 8;  // tokens per wave in flight
+    // dz of the chunk while streaming; afterwards waves 1..3 hand their
+    // partials to wave 0 through the same LDS
+    constexpr int DZ_FLOATS = kMaxChunk * EMAX, RED_FLOATS = DW ? 3 * EMAX * COLS : 0;
+    __shared__ __attribute__((aligned(16))) float lds[DZ_FLOATS > RED_FLOATS ? DZ_FLOATS : RED_FLOATS];
+    __shared__ float pdp_s[kMaxChunk];
+    __shared__ uint64_t kept_s[kMaxChunk];
+    float (*dzs)[EMAX] = reinterpret_cast<float (*)[EMAX]>(lds);
     const int c = blockIdx.x, g = blockIdx.z;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int t0 = c * kDxTokens;
-    const int ntok = min(kDxTokens, Ng - t0);
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int t0 = c * tch;
+    const int ntok = min(tch, Ng - t0);
     const size_t tok0 = static_cast<size_t>(g) * Ng + t0;
-    const int i0 = blockIdx.y * 64 * VEC + lane * VEC;
+    const int i0 = blockIdx.y * COLS + lane * VEC;
     const bool live = i0 < d;  // d is a multiple of 8: a lane's columns are all in or all out
     const int ic = live ? i0 : 0;
+
     const T* wg = wr + static_cast<size_t>(g) * E * d;
     float w[EMAX][VEC];
 #pragma unroll
@@ -136,22 +108,61 @@ __global__ __launch_bounds__(256) void route_bwd_dx_kernel(
 #pragma unroll
         for (int v = 0; v < VEC; ++v) w[e][v] = (e < E && live) ? w[e][v] : 0.0f;
     }
-    // this wave's tokens are wave, wave + 4, ...; round r covers U of them, and
-    // the dx loads of the next round are issued before this round's arithmetic
-    auto load_round = [&](int r0, float (&dv)[U][VEC]) {
+    auto load_round = [&](int r0, float (&xv)[U][VEC], float (&dv)[U][VEC]) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const size_t t = tok0 + min(r0 + 4 * u, ntok - 1);
+            if constexpr (DW) load_cols<VEC>(x + t * d + ic, xv[u]);
             load_cols<VEC>(dx + t * d + ic, dv[u]);
         }
     };
-    float dva[U][VEC], dvb[U][VEC];
-    stage_dz<EMAX>(dzs, dz, tok0, ntok, E);
-    if (wave < ntok) load_round(wave, dva);
+    float xa[U][VEC], da[U][VEC], xb[U][VEC], db[U][VEC];
+    if (wave < ntok) load_round(wave, xa, da);
+
+    // 1. dz of the chunk
+    for (int q = tid; q < ntok * EMAX; q += 256) dzs[q / EMAX][q % EMAX] = 0.0f;
     __syncthreads();
-    if (!live) return;
-    auto step = [&](int r0, float (&cur)[U][VEC], float (&nxt)[U][VEC]) {
-        if (r0 + 4 * U < ntok) load_round(r0 + 4 * U, nxt);
+    if (tid < ntok) {
+        const size_t t = tok0 + tid;
+        const float* pr = probs + t * E;
+        float pdp = 0.0f;
+        uint64_t kept = 0;
+#pragma unroll 2
+        for (int j = 0; j < k; ++j) {
+            const size_t a = t * k + j;
+            if (slot[a] >= 0) {
+                const int ej = idx[a];
+                const float gj = dgate[a];
+                pdp = __builtin_fmaf(pr[ej], gj, pdp);
+                kept |= 1ull << ej;
+                dzs[tid][ej] = gj;
+            }
+        }
+        pdp_s[tid] = pdp;
+        kept_s[tid] = kept;
+    }
+    __syncthreads();
+    for (int q = tid; q < ntok * EMAX; q += 256) {
+        const int t = q / EMAX, e = q % EMAX;
+        float z = 0.0f;
+        if (e < E) {
+            const float p = probs[(tok0 + t) * E + e], pdp = pdp_s[t];
+            // kept: p (dgate - <p, dp>); other experts: -p <p, dp>
+            z = ((kept_s[t] >> e) & 1ull) ? p * (dzs[t][e] - pdp) : -p * pdp;
+        }
+        dzs[t][e] = z;
+    }
+    __syncthreads();
+
+    // 2. stream the chunk's tokens
+    float acc[DW ? EMAX : 1][VEC];
+#pragma unroll
+    for (int e = 0; e < (DW ? EMAX : 1); ++e)
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) acc[e][v] = 0.0f;
+    auto step = [&](int r0, float (&xc)[U][VEC], float (&dc)[U][VEC], float (&xn)[U][VEC],
+                    float (&dn)[U][VEC]) {
+        if (r0 + 4 * U < ntok) load_round(r0 + 4 * U, xn, dn);
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int tt = r0 + 4 * u;
@@ -165,91 +176,50 @@ __global__ __launch_bounds__(256) void route_bwd_dx_kernel(
 #pragma unroll
                     for (int e = 0; e < EMAX; ++e)
                         if (e < E) s = __builtin_fmaf(z[e], w[e][v], s);
-                    out[v] = cur[u][v] + s;
+                    out[v] = dc[u][v] + s;
                 }
                 store_cols<VEC>(dx + (tok0 + tt) * d + i0, out);
-            }
-        }
-    };
-    for (int r0 = wave; r0 < ntok; r0 += 8 * U) {
-        step(r0, dva, dvb);
-        if (r0 + 4 * U < ntok) step(r0 + 4 * U, dvb, dva);
-    }
-}
-
-// Per-chunk partial of dW_r[e, cols] = sum_t dz[t, e] x[t, cols]. A block owns
-// a chunk of tch tokens of one group and 64 * VEC columns; wave w takes the
-// chunk's tokens w, w + 4, ... with E x VEC accumulators per lane, and the four
-// waves' partials are added in wave order.
-template <typename T, int EMAX>
-__global__ __launch_bounds__(256) void route_bwd_dw_kernel(
-    const T* __restrict__ x, const float* __restrict__ dz, float* __restrict__ partial, int Ng,
-    int d, int E, int tch, int nch) {
-    constexpr int VEC = ColsPerLane<EMAX>::value;
-    constexpr int COLS = 64 * VEC;
-    constexpr int U = EMAX <= 16 ? 4 : 2;
-    // dz of the chunk while streaming; afterwards waves 1..3 hand their partials
-    // to wave 0 through the same LDS
-    constexpr int DZ_FLOATS = kMaxChunk * EMAX, RED_FLOATS = 3 * EMAX * COLS;
-    __shared__ __attribute__((aligned(16))) float lds[DZ_FLOATS > RED_FLOATS ? DZ_FLOATS : RED_FLOATS];
-    float (*dzs)[EMAX] = reinterpret_cast<float (*)[EMAX]>(lds);
-    float (*red)[EMAX][COLS] = reinterpret_cast<float (*)[EMAX][COLS]>(lds);
-    const int c = blockIdx.x, g = blockIdx.z;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int t0 = c * tch;
-    const int ntok = min(tch, Ng - t0);
-    const size_t tok0 = static_cast<size_t>(g) * Ng + t0;
-    const int i0 = blockIdx.y * COLS + lane * VEC;
-    const bool live = i0 < d;
-    float acc[EMAX][VEC];
-#pragma unroll
-    for (int e = 0; e < EMAX; ++e)
-#pragma unroll
-        for (int v = 0; v < VEC; ++v) acc[e][v] = 0.0f;
-    stage_dz<EMAX>(dzs, dz, tok0, ntok, E);
-    __syncthreads();
-    if (live) {
-        for (int r0 = wave; r0 < ntok; r0 += 4 * U) {
-            float xv[U][VEC];
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const size_t t = tok0 + min(r0 + 4 * u, ntok - 1);
-                load_cols<VEC>(x + t * d + i0, xv[u]);
-            }
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const int tt = r0 + 4 * u;
-                if (tt < ntok) {
-                    float z[EMAX];
-                    read_dz<EMAX>(dzs, tt, z);
+                if constexpr (DW) {
 #pragma unroll
                     for (int e = 0; e < EMAX; ++e)
 #pragma unroll
                         for (int v = 0; v < VEC; ++v)
-                            acc[e][v] = __builtin_fmaf(z[e], xv[u][v], acc[e][v]);
+                            acc[e][v] = __builtin_fmaf(z[e], xc[u][v], acc[e][v]);
                 }
             }
         }
+    };
+    if (live) {
+        for (int r0 = wave; r0 < ntok; r0 += 8 * U) {
+            step(r0, xa, da, xb, db);
+            if (r0 + 4 * U < ntok) step(r0 + 4 * U, xb, db, xa, da);
+        }
     }
-    __syncthreads();  // every wave is done reading dz
-    if (wave > 0) {
+
+    // 3. the chunk's partial of dW_r
+    if constexpr (DW) {
+        float (*red)[EMAX][COLS] = reinterpret_cast<float (*)[EMAX][COLS]>(lds);
+        __syncthreads();  // every wave is done reading dz
+        if (wave > 0) {
 #pragma unroll
-        for (int e = 0; e < EMAX; ++e)
+            for (int e = 0; e < EMAX; ++e)
 #pragma unroll
-            for (int v = 0; v < VEC; ++v) red[wave - 1][e][lane * VEC + v] = acc[e][v];
-    }
-    __syncthreads();
-    if (wave == 0 && live) {
-        float* pg = partial + (static_cast<size_t>(g) * nch + c) * E * d;
+                for (int v = 0; v < VEC; ++v) red[wave - 1][e][lane * VEC + v] = acc[e][v];
+        }
+        __syncthreads();
+        if (wave == 0 && live) {
+            float* pg = partial + (static_cast<size_t>(g) * nch + c) * E * d;
 #pragma unroll
-        for (int e = 0; e < EMAX; ++e) {
-            if (e < E) {
-                float out[VEC];
+            for (int e = 0; e < EMAX; ++e) {
+                if (e < E) {
+                    float out[VEC];
 #pragma unroll
-                for (int v = 0; v < VEC; ++v)
-                    out[v] = ((acc[e][v] + red[0][e][lane * VEC + v]) + red[1][e][lane * VEC + v]) +
-                             red[2][e][lane * VEC + v];
-                store_cols<VEC>(pg + static_cast<size_t>(e) * d + i0, out);
+                    for (int v = 0; v < VEC; ++v)
+                        out[v] = ((acc[e][v] + red[0][e][lane * VEC + v]) +
+                                  red[1][e][lane * VEC + v]) +
+                                 red[2][e][lane * VEC + v];
+                    store_cols<VEC>(pg + static_cast<size_t>(e) * d + i0, out);
+                }
             }
         }
     }
@@ -286,9 +256,11 @@ struct ChunkPlan {
 };
 
 ChunkPlan plan(const Dims& D) {
-    // about 1024 blocks over (chunks, column blocks, groups); column blocks of
-    // 256 columns (E <= 16) as the common case
-    const int colblocks = static_cast<int>(cdiv(D.d, 256));
+    // about 1024 blocks over (chunks, column blocks, groups)
+    const int cols = 64 * (D.E <= 8    ? ColsPerLane<8>::value
+                           : D.E <= 16 ? ColsPerLane<16>::value
+                                       : ColsPerLane<64>::value);
+    const int colblocks = static_cast<int>(cdiv(D.d, cols));
     int target = 1024 / (D.G * colblocks);
     if (target < 1) target = 1;
     int tch = D.Ng > 0 ? static_cast<int>(cdiv(D.Ng, target)) : 1;
@@ -299,45 +271,39 @@ ChunkPlan plan(const Dims& D) {
 template <typename T, int EMAX>
 void launch_main(const Dims& D, const ChunkPlan& P, const void* x, const void* wr,
                  const float* probs, const int32_t* idx, const int32_t* slot, const float* dgate,
-                 float* dx, float* dz, float* partial, hipStream_t st) {
+                 float* dx, float* partial, hipStream_t st) {
     constexpr int COLS = 64 * ColsPerLane<EMAX>::value;
-    route_bwd_dz_kernel<<<cdiv(static_cast<long long>(D.N) * D.E, 256), 256, 0, st>>>(
-        probs, idx, slot, dgate, dz, D.N, D.E, D.k);
-    dim3 gdx(cdiv(D.Ng, kDxTokens), cdiv(D.d, COLS), D.G);
-    route_bwd_dx_kernel<T, EMAX><<<gdx, 256, 0, st>>>(static_cast<const T*>(wr), dz, dx, D.Ng,
-                                                       D.d, D.E);
-    if (partial) {
-        dim3 gdw(P.nch, cdiv(D.d, COLS), D.G);
-        route_bwd_dw_kernel<T, EMAX><<<gdw, 256, 0, st>>>(static_cast<const T*>(x), dz, partial,
-                                                           D.Ng, D.d, D.E, P.tch, P.nch);
-    }
+    const dim3 grid(P.nch, cdiv(D.d, COLS), D.G);
+    if (partial)
+        route_bwd_kernel<T, EMAX, true><<<grid, 256, 0, st>>>(
+            static_cast<const T*>(x), static_cast<const T*>(wr), probs, idx, slot, dgate, dx,
+            partial, D.Ng, D.d, D.E, D.k, P.tch, P.nch);
+    else
+        route_bwd_kernel<T, EMAX, false><<<grid, 256, 0, st>>>(
+            static_cast<const T*>(x), static_cast<const T*>(wr), probs, idx, slot, dgate, dx,
+            nullptr, D.Ng, D.d, D.E, D.k, P.tch, P.nch);
 }
 
 template <typename T>
 void launch_main_e(const Dims& D, const ChunkPlan& P, const void* x, const void* wr,
                    const float* probs, const int32_t* idx, const int32_t* slot,
-                   const float* dgate, float* dx, float* dz, float* partial, hipStream_t st) {
+                   const float* dgate, float* dx, float* partial, hipStream_t st) {
     if (D.E <= 8)
-        launch_main<T, 8>(D, P, x, wr, probs, idx, slot, dgate, dx, dz, partial, st);
+        launch_main<T, 8>(D, P, x, wr, probs, idx, slot, dgate, dx, partial, st);
     else if (D.E <= 16)
-        launch_main<T, 16>(D, P, x, wr, probs, idx, slot, dgate, dx, dz, partial, st);
+        launch_main<T, 16>(D, P, x, wr, probs, idx, slot, dgate, dx, partial, st);
     else if (D.E <= 32)
-        launch_main<T, 32>(D, P, x, wr, probs, idx, slot, dgate, dx, dz, partial, st);
+        launch_main<T, 32>(D, P, x, wr, probs, idx, slot, dgate, dx, partial, st);
     else
-        launch_main<T, 64>(D, P, x, wr, probs, idx, slot, dgate, dx, dz, partial, st);
+        launch_main<T, 64>(D, P, x, wr, probs, idx, slot, dgate, dx, partial, st);
 }
 
 }  // namespace
 
-// Workspace: dz [N, E] f32, then (router gradient wanted) the per-chunk
-// partials [G, chunks, E, d] f32.
-size_t dz_bytes(const Dims& D) {
-    return (sizeof(float) * static_cast<size_t>(D.N) * D.E + 255) & ~static_cast<size_t>(255);
-}
-
+// Workspace: the per-chunk router-gradient partials [G, chunks, E, d] f32.
 size_t route_bwd_workspace_bytes(const Dims& D) {
     const ChunkPlan P = plan(D);
-    return dz_bytes(D) + sizeof(float) * static_cast<size_t>(D.G) * P.nch * D.E * D.d;
+    return sizeof(float) * static_cast<size_t>(D.G) * P.nch * D.E * D.d;
 }
 
 vmoe_status route_bwd_launch(const Dims& D, const void* x, const void* wr, const float* probs,
@@ -352,12 +318,11 @@ vmoe_status route_bwd_launch(const Dims& D, const void* x, const void* wr, const
                                                                       total);
         return launch_status();
     }
-    float* dz = static_cast<float*>(ws);
-    float* partial = dwr ? reinterpret_cast<float*>(static_cast<char*>(ws) + dz_bytes(D)) : nullptr;
+    float* partial = dwr ? static_cast<float*>(ws) : nullptr;
     if (D.dtype == VMOE_BF16)
-        launch_main_e<uint16_t>(D, P, x, wr, probs, idx, slot, dgate, dx, dz, partial, st);
+        launch_main_e<uint16_t>(D, P, x, wr, probs, idx, slot, dgate, dx, partial, st);
     else
-        launch_main_e<float>(D, P, x, wr, probs, idx, slot, dgate, dx, dz, partial, st);
+        launch_main_e<float>(D, P, x, wr, probs, idx, slot, dgate, dx, partial, st);
     if (dwr)
         route_bwd_reduce_kernel<<<cdiv(total, 32), 256, 0, st>>>(partial, dwr, D.E, D.d, P.nch,
                                                                   total);

@@ -147,6 +147,53 @@ __device__ __forceinline__ void gate_token(float* z, size_t t, const float* __re
     keys[t] = priority_key(__fdiv_rn(exp_spec(z[first] - m), s));
 }
 
+// The same gate with one lane per expert: the tokens of a block in groups of
+// L = next power of two >= E lanes (L divides 64, so a group never straddles a
+// wave and every lane of a group follows the same path). Every element is
+// computed by the same operations as in gate_token: the maximum is exact in
+// any order, the sum runs e = 0..E-1 through lane broadcasts, and the top-k
+// butterflies keep the larger value, then the lower expert.
+__device__ __forceinline__ void gate_lanes(const float* zrow, size_t t, int sub, int L,
+                                           const float* __restrict__ bias,
+                                           const float* __restrict__ noise,
+                                           float* __restrict__ probs, int32_t* __restrict__ idx,
+                                           uint32_t* __restrict__ keys, int E, int k) {
+    const bool real = sub < E;
+    float v = real ? zrow[sub] : 0.0f;
+    if (real && bias) v = v + bias[sub];
+    if (real && noise) v = v + noise[t * E + sub];
+    float m = real ? v : -__builtin_inff();
+    for (int o = L >> 1; o > 0; o >>= 1) {
+        const float u = __shfl_xor(m, o, L);
+        m = u > m ? u : m;
+    }
+    const float q = real ? exp_spec(v - m) : 0.0f;
+    float s = 0.0f;
+    for (int e = 0; e < E; ++e) s = s + __shfl(q, e, L);
+    const float p = __fdiv_rn(q, s);
+    if (real) probs[t * E + sub] = p;
+    bool taken = !real;
+    for (int j = 0; j < k; ++j) {
+        // candidate (valid, value, expert); the better one has the larger
+        // value, then the lower expert
+        int ok = taken ? 0 : 1, be = sub;
+        float bv = v;
+        for (int o = L >> 1; o > 0; o >>= 1) {
+            const int ok2 = __shfl_xor(ok, o, L), be2 = __shfl_xor(be, o, L);
+            const float bv2 = __shfl_xor(bv, o, L);
+            const bool better = ok2 && (!ok || bv2 > bv || (bv2 == bv && be2 < be));
+            ok = better ? ok2 : ok;
+            be = better ? be2 : be;
+            bv = better ? bv2 : bv;
+        }
+        if (sub == be) {
+            taken = true;
+            idx[t * k + j] = be;
+            if (j == 0) keys[t] = priority_key(p);
+        }
+    }
+}
+
 // ---------------------------------------------------------------- bf16: MFMA
 //
 // One block = 32 tokens of one group, four waves. The router product
@@ -159,6 +206,7 @@ typedef __bf16 bf16x8_r __attribute__((ext_vector_type(8)));
 typedef float f32x16_r __attribute__((ext_vector_type(16)));
 constexpr int kMfmaTokens = 32;
 
+template <bool WIDE>
 __global__ __launch_bounds__(256) void router_mfma_kernel(
     const uint16_t* __restrict__ x, const uint16_t* __restrict__ wr,
     const float* __restrict__ bias, const float* __restrict__ noise, float* __restrict__ logits,
@@ -186,7 +234,8 @@ __global__ __launch_bounds__(256) void router_mfma_kernel(
         f32x16_r acc0, acc1;
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc0[r] = acc1[r] = 0.0f;
-        constexpr int U = 8;
+        // all of a wave's k-steps in flight at once for d up to 1024 (E <= 32)
+        constexpr int U = WIDE ? 8 : 16;
         for (int s = s0; s < s1; s += U) {
             uint4 av[U], bv0[U], bv1[U];
 #pragma unroll
@@ -195,14 +244,17 @@ __global__ __launch_bounds__(256) void router_mfma_kernel(
                 const bool live = s + u < s1;
                 av[u] = buf_load16(rx, live ? off(m, ntok, kk) : kOutOfRange);
                 bv0[u] = buf_load16(rw, live ? off(m, E, kk) : kOutOfRange);
-                if (E > 32) bv1[u] = buf_load16(rw, live ? off(32 + m, E, kk) : kOutOfRange);
+                if constexpr (WIDE) bv1[u] = buf_load16(rw, live ? off(32 + m, E, kk) : kOutOfRange);
             }
+            // keep every load of the round ahead of the first MFMA (the
+            // scheduler would otherwise interleave them, two loads in flight)
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 const bf16x8_r a = __builtin_bit_cast(bf16x8_r, av[u]);
                 acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
                     __builtin_bit_cast(bf16x8_r, bv0[u]), a, acc0, 0, 0, 0);
-                if (E > 32)
+                if constexpr (WIDE)
                     acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
                         __builtin_bit_cast(bf16x8_r, bv1[u]), a, acc1, 0, 0, 0);
             }
@@ -214,7 +266,7 @@ __global__ __launch_bounds__(256) void router_mfma_kernel(
             for (int r = 0; r < 4; ++r) {
                 const int n = 8 * q + 4 * (lane >> 5) + r;
                 red[wave][m][n] = acc0[4 * q + r];
-                if (E > 32) red[wave][m][32 + n] = acc1[4 * q + r];
+                if constexpr (WIDE) red[wave][m][32 + n] = acc1[4 * q + r];
             }
     }
     __syncthreads();
@@ -230,7 +282,10 @@ __global__ __launch_bounds__(256) void router_mfma_kernel(
         red[1][t][e] = v;  // staged in wave 1's slot, no reader of it remains
     }
     __syncthreads();
-    if (tid < ntok) gate_token(&red[1][tid][0], tok0 + tid, bias, noise, probs, idx, keys, E, k);
+    int L = 1;
+    while (L < E) L <<= 1;
+    for (int t = tid / L; t < ntok; t += 256 / L)
+        gate_lanes(&red[1][t][0], tok0 + t, tid % L, L, bias, noise, probs, idx, keys, E, k);
 }
 
 // ------------------------------------------------------------ f32: f64 sums
@@ -564,9 +619,10 @@ vmoe_status route_launch(const Dims& D, const void* x, const void* wr, const flo
     if (D.N > 0) {
         if (D.dtype == VMOE_BF16) {
             dim3 grid(cdiv(D.Ng, kMfmaTokens), D.G);
-            router_mfma_kernel<<<grid, 256, 0, st>>>(
-                static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(wr), bias, noise,
-                logits, probs, idx, ws.keys, D.Ng, D.d, D.E, D.k, logits_in);
+            auto kern = D.E > 32 ? router_mfma_kernel<true> : router_mfma_kernel<false>;
+            kern<<<grid, 256, 0, st>>>(static_cast<const uint16_t*>(x),
+                                       static_cast<const uint16_t*>(wr), bias, noise, logits,
+                                       probs, idx, ws.keys, D.Ng, D.d, D.E, D.k, logits_in);
         } else {
             const int tpb = min(kGateTokens, 256 / D.E);
             dim3 grid(cdiv(D.Ng, tpb), D.G);

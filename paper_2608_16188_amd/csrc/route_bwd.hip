@@ -13,7 +13,6 @@ namespace vmoe {
 namespace {
 
 constexpr int kMinChunk = 64;
-constexpr int kMaxChunk = 256;
 
 // VEC consecutive columns of a token row as f32 (VEC * sizeof(T) bytes, aligned).
 template <int VEC>
@@ -41,6 +40,41 @@ __device__ __forceinline__ void load_cols(const float* p, float (&v)[VEC]) {
         v[0] = *p;
     }
 }
+// The same columns as raw bits, converted only where they are used (so a
+// load can stay in flight until then).
+template <typename T, int VEC> struct RawCols;
+template <int VEC> struct RawCols<uint16_t, VEC> {
+    uint32_t w[VEC == 4 ? 2 : 1];
+    __device__ __forceinline__ void load(const uint16_t* p) {
+        if constexpr (VEC == 4) {
+            const uint2 u = *reinterpret_cast<const uint2*>(p);
+            w[0] = u.x; w[1] = u.y;
+        } else if constexpr (VEC == 2) {
+            w[0] = *reinterpret_cast<const uint32_t*>(p);
+        } else {
+            w[0] = *p;
+        }
+    }
+    __device__ __forceinline__ void to_f32(float (&v)[VEC]) const {
+#pragma unroll
+        for (int i = 0; i < VEC; ++i)
+            v[i] = bf16_to_f32(static_cast<uint16_t>(i % 2 ? w[i / 2] >> 16 : w[i / 2] & 0xFFFFu));
+    }
+};
+template <int VEC> struct RawCols<float, VEC> {
+    float w[VEC];
+    __device__ __forceinline__ void load(const float* p) {
+        float v[VEC];
+        load_cols<VEC>(p, v);
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) w[i] = v[i];
+    }
+    __device__ __forceinline__ void to_f32(float (&v)[VEC]) const {
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) v[i] = w[i];
+    }
+};
+
 template <int VEC>
 __device__ __forceinline__ void store_cols(float* p, const float (&v)[VEC]) {
     if constexpr (VEC == 4) *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
@@ -48,11 +82,33 @@ __device__ __forceinline__ void store_cols(float* p, const float (&v)[VEC]) {
     else *p = v[0];
 }
 
+// Most tokens per chunk: the chunk's dz and dp rows stay within 32 KB of LDS.
+template <int EMAX> struct ChunkMax {
+    static constexpr int value = EMAX <= 16 ? 256 : (EMAX <= 32 ? 128 : 64);
+};
+static_assert(ChunkMax<64>::value >= kMinChunk, "chunk bounds");
+
 // Columns per lane: a lane keeps E x VEC router weights and E x VEC gradient
 // partials in registers.
 template <int EMAX> struct ColsPerLane {
     static constexpr int value = EMAX <= 8 ? 4 : (EMAX <= 16 ? 2 : 1);
 };
+
+// Barrier for LDS traffic only: this wave's LDS accesses are complete
+// (lgkmcnt 0) while its global loads may stay in flight (__syncthreads would
+// also wait for those). The signal fences keep the compiler from moving
+// memory accesses across it.
+__device__ __forceinline__ void lds_barrier() {
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0); vmcnt, expcnt not waited for
+    __builtin_amdgcn_s_barrier();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+// global loads per thread issued together when forming dz: assignments,
+// probabilities
+constexpr int kBatch = 4;
+constexpr int kProbBatch = 16;
 
 // A token's dz row from LDS into registers (broadcast 16-byte reads).
 template <int EMAX>
@@ -84,12 +140,13 @@ __global__ __launch_bounds__(256) void route_bwd_kernel(
     constexpr int VEC = ColsPerLane<EMAX>::value;
     constexpr int COLS = 64 * VEC;
     constexpr int U = EMAX <= 8 ? 4 : 8;  // tokens per wave in flight
-    // dz of the chunk while streaming; afterwards waves 1..3 hand their
-    // partials to wave 0 through the same LDS
-    constexpr int DZ_FLOATS = kMaxChunk * EMAX, RED_FLOATS = DW ? 3 * EMAX * COLS : 0;
-    __shared__ __attribute__((aligned(16))) float lds[DZ_FLOATS > RED_FLOATS ? DZ_FLOATS : RED_FLOATS];
-    __shared__ float pdp_s[kMaxChunk];
-    __shared__ uint64_t kept_s[kMaxChunk];
+    // LDS: dz (and, while it is formed, dp) of the chunk; afterwards waves
+    // 1..3 hand their partials to wave 0 through the same space
+    constexpr int CH = ChunkMax<EMAX>::value;
+    constexpr int DZ_FLOATS = CH * EMAX, RED_FLOATS = DW ? 3 * EMAX * COLS : 0;
+    __shared__ __attribute__((aligned(16)))
+    float lds[2 * DZ_FLOATS > RED_FLOATS ? 2 * DZ_FLOATS : RED_FLOATS];
+    __shared__ float pdp_s[CH];
     float (*dzs)[EMAX] = reinterpret_cast<float (*)[EMAX]>(lds);
     const int c = blockIdx.x, g = blockIdx.z;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -108,51 +165,83 @@ __global__ __launch_bounds__(256) void route_bwd_kernel(
 #pragma unroll
         for (int v = 0; v < VEC; ++v) w[e][v] = (e < E && live) ? w[e][v] : 0.0f;
     }
-    auto load_round = [&](int r0, float (&xv)[U][VEC], float (&dv)[U][VEC]) {
+    using RX = RawCols<T, VEC>;
+    using RD = RawCols<float, VEC>;
+    // (token indices clamp to the chunk, so a wave past its last token reloads it)
+    auto load_round = [&](int r0, RX (&xv)[U], RD (&dv)[U]) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const size_t t = tok0 + min(r0 + 4 * u, ntok - 1);
-            if constexpr (DW) load_cols<VEC>(x + t * d + ic, xv[u]);
-            load_cols<VEC>(dx + t * d + ic, dv[u]);
+            if constexpr (DW) xv[u].load(x + t * d + ic);
+            dv[u].load(dx + t * d + ic);
         }
     };
-    float xa[U][VEC], da[U][VEC], xb[U][VEC], db[U][VEC];
-    if (wave < ntok) load_round(wave, xa, da);
+    RX xa[U], xb[U];
+    RD da[U], db[U];
 
-    // 1. dz of the chunk
-    for (int q = tid; q < ntok * EMAX; q += 256) dzs[q / EMAX][q % EMAX] = 0.0f;
-    __syncthreads();
+    // 1. dz of the chunk. The first batch of its inputs (assignments and
+    // probability rows, clamped indices, no branches) is requested before the
+    // first round of x and dx rows, so waiting for it leaves those in flight;
+    // the barriers of this phase wait for LDS only. dps holds dp, NaN where
+    // the expert was not kept.
+    const int na = ntok * k, np = ntok * E;
+    const size_t q0 = tok0 * k, p0 = tok0 * E;
+    int sl[kBatch], ex[kBatch];
+    float gv[kBatch], pv[kProbBatch];
+    auto fetch_assign = [&](int b0) {
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            const size_t q = q0 + min(b0 + u * 256 + tid, na - 1);
+            sl[u] = slot[q];
+            ex[u] = idx[q];
+            gv[u] = dgate[q];
+        }
+    };
+    // the chunk's probability rows are one contiguous run of ntok * E floats
+    auto fetch_probs = [&](int b0) {
+#pragma unroll
+        for (int u = 0; u < kProbBatch; ++u) pv[u] = probs[p0 + min(b0 + u * 256 + tid, np - 1)];
+    };
+    fetch_assign(0);
+    fetch_probs(0);
+    load_round(wave, xa, da);
+    float (*dps)[EMAX] = reinterpret_cast<float (*)[EMAX]>(lds + DZ_FLOATS);
+    for (int q = tid; q < ntok * EMAX; q += 256) dps[q / EMAX][q % EMAX] = __builtin_nanf("");
+    lds_barrier();
+    for (int b0 = 0; b0 < na; b0 += kBatch * 256) {
+        if (b0 > 0) fetch_assign(b0);
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            const int q = b0 + u * 256 + tid;
+            if (q < na && sl[u] >= 0) dps[q / k][ex[u]] = gv[u];
+        }
+    }
+    for (int b0 = 0; b0 < np; b0 += kProbBatch * 256) {
+        if (b0 > 0) fetch_probs(b0);
+#pragma unroll
+        for (int u = 0; u < kProbBatch; ++u) {
+            const int q = b0 + u * 256 + tid;
+            if (q < np) dzs[q / E][q % E] = pv[u];  // columns E..EMAX are never read
+        }
+    }
+    lds_barrier();
     if (tid < ntok) {
-        const size_t t = tok0 + tid;
-        const float* pr = probs + t * E;
+        // <p, dp> over the kept experts, e ascending
         float pdp = 0.0f;
-        uint64_t kept = 0;
-#pragma unroll 2
-        for (int j = 0; j < k; ++j) {
-            const size_t a = t * k + j;
-            if (slot[a] >= 0) {
-                const int ej = idx[a];
-                const float gj = dgate[a];
-                pdp = __builtin_fmaf(pr[ej], gj, pdp);
-                kept |= 1ull << ej;
-                dzs[tid][ej] = gj;
-            }
+        for (int e = 0; e < E; ++e) {
+            const float dp = dps[tid][e];
+            if (dp == dp) pdp = __builtin_fmaf(dzs[tid][e], dp, pdp);
         }
         pdp_s[tid] = pdp;
-        kept_s[tid] = kept;
     }
-    __syncthreads();
+    lds_barrier();
     for (int q = tid; q < ntok * EMAX; q += 256) {
         const int t = q / EMAX, e = q % EMAX;
-        float z = 0.0f;
-        if (e < E) {
-            const float p = probs[(tok0 + t) * E + e], pdp = pdp_s[t];
-            // kept: p (dgate - <p, dp>); other experts: -p <p, dp>
-            z = ((kept_s[t] >> e) & 1ull) ? p * (dzs[t][e] - pdp) : -p * pdp;
-        }
-        dzs[t][e] = z;
+        const float p = dzs[t][e], dp = dps[t][e], pdp = pdp_s[t];
+        // kept: p (dgate - <p, dp>); other experts: -p <p, dp>
+        dzs[t][e] = e >= E ? 0.0f : (dp == dp ? p * (dp - pdp) : -p * pdp);
     }
-    __syncthreads();
+    lds_barrier();
 
     // 2. stream the chunk's tokens
     float acc[DW ? EMAX : 1][VEC];
@@ -160,8 +249,7 @@ __global__ __launch_bounds__(256) void route_bwd_kernel(
     for (int e = 0; e < (DW ? EMAX : 1); ++e)
 #pragma unroll
         for (int v = 0; v < VEC; ++v) acc[e][v] = 0.0f;
-    auto step = [&](int r0, float (&xc)[U][VEC], float (&dc)[U][VEC], float (&xn)[U][VEC],
-                    float (&dn)[U][VEC]) {
+    auto step = [&](int r0, RX (&xc)[U], RD (&dc)[U], RX (&xn)[U], RD (&dn)[U]) {
         if (r0 + 4 * U < ntok) load_round(r0 + 4 * U, xn, dn);
 #pragma unroll
         for (int u = 0; u < U; ++u) {
@@ -169,22 +257,25 @@ __global__ __launch_bounds__(256) void route_bwd_kernel(
             if (tt < ntok) {
                 float z[EMAX];
                 read_dz<EMAX>(dzs, tt, z);
-                float out[VEC];
+                float dv[VEC], out[VEC];
+                dc[u].to_f32(dv);
 #pragma unroll
                 for (int v = 0; v < VEC; ++v) {
                     float s = 0.0f;
 #pragma unroll
                     for (int e = 0; e < EMAX; ++e)
                         if (e < E) s = __builtin_fmaf(z[e], w[e][v], s);
-                    out[v] = dc[u][v] + s;
+                    out[v] = dv[v] + s;
                 }
                 store_cols<VEC>(dx + (tok0 + tt) * d + i0, out);
                 if constexpr (DW) {
+                    float xv[VEC];
+                    xc[u].to_f32(xv);
 #pragma unroll
                     for (int e = 0; e < EMAX; ++e)
 #pragma unroll
                         for (int v = 0; v < VEC; ++v)
-                            acc[e][v] = __builtin_fmaf(z[e], xc[u][v], acc[e][v]);
+                            acc[e][v] = __builtin_fmaf(z[e], xv[v], acc[e][v]);
                 }
             }
         }
@@ -264,7 +355,11 @@ ChunkPlan plan(const Dims& D) {
     int target = 1024 / (D.G * colblocks);
     if (target < 1) target = 1;
     int tch = D.Ng > 0 ? static_cast<int>(cdiv(D.Ng, target)) : 1;
-    tch = tch < kMinChunk ? kMinChunk : (tch > kMaxChunk ? kMaxChunk : tch);
+    const int tmax = D.E <= 8    ? ChunkMax<8>::value
+                     : D.E <= 16 ? ChunkMax<16>::value
+                     : D.E <= 32 ? ChunkMax<32>::value
+                                 : ChunkMax<64>::value;
+    tch = tch < kMinChunk ? kMinChunk : (tch > tmax ? tmax : tch);
     return ChunkPlan{tch, D.Ng > 0 ? static_cast<int>(cdiv(D.Ng, tch)) : 0};
 }
 

@@ -84,15 +84,4 @@ inline vmoe_status launch_status() {
 
 inline unsigned cdiv(long long a, long long b) { return static_cast<unsigned>((a + b - 1) / b); }
 
-// Row of assignment (t, j) in the [E, G*C, width] buffers, or -1 if dropped.
-__device__ __forceinline__ long long assignment_row(int t, int j, const int32_t* idx,
-                                                    const int32_t* slot, const int32_t* row_base,
-                                                    int k, int Ng, int E, int C, int G) {
-    int s = slot[static_cast<size_t>(t) * k + j];
-    if (s < 0) return -1;
-    int e = idx[static_cast<size_t>(t) * k + j];
-    int g = t / Ng;
-    return static_cast<long long>(e) * G * C + row_base[g * E + e] + s;
-}
-
 }  // namespace vmoe

@@ -3,6 +3,8 @@
 // All four are HBM-bound gathers / scatters keyed by the routing metadata,
 // moving rows in 16-byte vectors (fully coalesced). Float sums run in a fixed
 // order (j ascending, then a fixed butterfly), so results are deterministic.
+#include <type_traits>
+
 #include "common.h"
 
 namespace vmoe {
@@ -46,20 +48,45 @@ struct RouteMeta {
     const int32_t* slot;
     const int32_t* row_base;
     int N, Ng, E, k, C, G;
-    __device__ __forceinline__ long long row(int t, int j) const {
-        return assignment_row(t, j, idx, slot, row_base, k, Ng, E, C, G);
+};
+
+// Rows of assignments j0 .. j0 + J - 1 of token t (-1: dropped or past k).
+// The loads run in three independent rounds (slot and expert of every j,
+// then the row bases, then the caller's rows), with indices clamped instead
+// of branches, so the compiler issues each round at once.
+template <int J>
+struct Rows {
+    long long r[J];
+    __device__ __forceinline__ void fetch(const RouteMeta& m, int t, int j0) {
+        const size_t a0 = static_cast<size_t>(t) * m.k;
+        int s[J], e[J], rb[J];
+#pragma unroll
+        for (int jj = 0; jj < J; ++jj) {
+            const int j = min(j0 + jj, m.k - 1);
+            s[jj] = m.slot[a0 + j];
+            e[jj] = m.idx[a0 + j];  // a valid expert for every assignment
+        }
+        const int g = t / m.Ng;
+#pragma unroll
+        for (int jj = 0; jj < J; ++jj) rb[jj] = m.row_base[g * m.E + e[jj]];
+#pragma unroll
+        for (int jj = 0; jj < J; ++jj)
+            r[jj] = (j0 + jj < m.k && s[jj] >= 0)
+                        ? static_cast<long long>(e[jj]) * m.G * m.C + rb[jj] + s[jj]
+                        : -1;
     }
 };
 
 // Flat element-wise mapping for the row moves without a reduction: item i is
 // 16-byte vector v = i mod nvec of token t = i / nvec, so consecutive lanes
 // touch consecutive bytes of a row and every lane is busy whatever d is. Each
-// thread takes kItems items kBlock apart and issues all their loads before any
-// store.
+// thread takes kItems items kBlock apart; every load of both items (data,
+// then metadata) is issued before the first store.
 constexpr int kBlock = 256;
 constexpr int kItems = 2;
+// J: assignments per pass (2 when k <= 2, else 4; larger k loops)
 
-template <typename T>
+template <typename T, int kJ>
 __global__ __launch_bounds__(kBlock) void dispatch_kernel(const T* __restrict__ x,
                                                           T* __restrict__ xe, RouteMeta m,
                                                           int nvec) {
@@ -67,65 +94,76 @@ __global__ __launch_bounds__(kBlock) void dispatch_kernel(const T* __restrict__ 
     const long long i0 = static_cast<long long>(blockIdx.x) * kBlock * kItems + threadIdx.x;
     const uint4* src = reinterpret_cast<const uint4*>(x);
     uint4* dst = reinterpret_cast<uint4*>(xe);
-    auto item = [&](long long i) { return i < total ? src[i] : make_uint4(0u, 0u, 0u, 0u); };
-    auto place = [&](long long i, const uint4 v) {
-        if (i >= total) return;
-        const int t = static_cast<int>(i / nvec);
-        const int c = static_cast<int>(i - static_cast<long long>(t) * nvec);
-        for (int j = 0; j < m.k; ++j) {
-            const long long row = m.row(t, j);
-            if (row >= 0) dst[row * nvec + c] = v;
-        }
-    };
     static_assert(kItems == 2, "two items per thread");
-    const uint4 v0 = item(i0), v1 = item(i0 + kBlock);
-    place(i0, v0);
-    place(i0 + kBlock, v1);
+    const long long ia = min(i0, total - 1), ib = min(i0 + kBlock, total - 1);
+    const uint4 va = src[ia], vb = src[ib];
+    const int ta = static_cast<int>(ia / nvec), tb = static_cast<int>(ib / nvec);
+    const int ca = static_cast<int>(ia - static_cast<long long>(ta) * nvec);
+    const int cb = static_cast<int>(ib - static_cast<long long>(tb) * nvec);
+    for (int j0 = 0; j0 < m.k; j0 += kJ) {
+        Rows<kJ> ra, rb;
+        ra.fetch(m, ta, j0);
+        rb.fetch(m, tb, j0);
+#pragma unroll
+        for (int jj = 0; jj < kJ; ++jj) {
+            if (i0 < total && ra.r[jj] >= 0) dst[ra.r[jj] * nvec + ca] = va;
+            if (i0 + kBlock < total && rb.r[jj] >= 0) dst[rb.r[jj] * nvec + cb] = vb;
+        }
+    }
 }
 
-template <typename T>
+// y[t] = sum over kept j (ascending) of gate[t, j] ye[row(t, j)], f32 sums.
+template <typename T, int kJ>
 __global__ __launch_bounds__(kBlock) void combine_fwd_kernel(const T* __restrict__ ye,
                                                              const float* __restrict__ gate,
                                                              T* __restrict__ y, RouteMeta m,
                                                              int nvec) {
     constexpr int VN = Vec<T>::n;
-    constexpr int KMAX = 4;  // rows gathered per pass; more assignments loop
     const long long total = static_cast<long long>(m.N) * nvec;
     const long long i0 = static_cast<long long>(blockIdx.x) * kBlock * kItems + threadIdx.x;
     const uint4* src = reinterpret_cast<const uint4*>(ye);
     uint4* dst = reinterpret_cast<uint4*>(y);
+    long long it[kItems];
+    int tt[kItems], cc[kItems];
+    float acc[kItems][VN];
 #pragma unroll
     for (int u = 0; u < kItems; ++u) {
-        const long long i = i0 + u * kBlock;
-        if (i >= total) break;
-        const int t = static_cast<int>(i / nvec), c = static_cast<int>(i - static_cast<long long>(t) * nvec);
-        float acc[VN];
+        it[u] = min(i0 + u * kBlock, total - 1);
+        tt[u] = static_cast<int>(it[u] / nvec);
+        cc[u] = static_cast<int>(it[u] - static_cast<long long>(tt[u]) * nvec);
 #pragma unroll
-        for (int q = 0; q < VN; ++q) acc[q] = 0.0f;
-        for (int j0 = 0; j0 < m.k; j0 += KMAX) {
-            uint4 r[KMAX];
-            float gj[KMAX];
-            bool kept[KMAX];
-#pragma unroll
-            for (int jj = 0; jj < KMAX; ++jj) {
-                const int j = j0 + jj;
-                const long long row = j < m.k ? m.row(t, j) : -1;
-                kept[jj] = row >= 0;
-                gj[jj] = row >= 0 ? gate[static_cast<size_t>(t) * m.k + j] : 0.0f;
-                r[jj] = row >= 0 ? src[row * nvec + c] : make_uint4(0u, 0u, 0u, 0u);
-            }
-            // j ascending over the kept assignments
-#pragma unroll
-            for (int jj = 0; jj < KMAX; ++jj) {
-                if (!kept[jj]) continue;
-                float f[VN];
-                Vec<T>::unpack(r[jj], f);
-#pragma unroll
-                for (int q = 0; q < VN; ++q) acc[q] = __builtin_fmaf(gj[jj], f[q], acc[q]);
-            }
-        }
-        dst[i] = Vec<T>::pack(acc);
+        for (int q = 0; q < VN; ++q) acc[u][q] = 0.0f;
     }
+    for (int j0 = 0; j0 < m.k; j0 += kJ) {
+        Rows<kJ> rows[kItems];
+        float gj[kItems][kJ];
+        uint4 r[kItems][kJ];
+#pragma unroll
+        for (int u = 0; u < kItems; ++u) {
+            rows[u].fetch(m, tt[u], j0);
+#pragma unroll
+            for (int jj = 0; jj < kJ; ++jj)
+                gj[u][jj] = gate[static_cast<size_t>(tt[u]) * m.k + min(j0 + jj, m.k - 1)];
+        }
+#pragma unroll
+        for (int u = 0; u < kItems; ++u)
+#pragma unroll
+            for (int jj = 0; jj < kJ; ++jj)
+                r[u][jj] = src[(rows[u].r[jj] >= 0 ? rows[u].r[jj] : 0) * nvec + cc[u]];
+#pragma unroll
+        for (int u = 0; u < kItems; ++u)
+#pragma unroll
+            for (int jj = 0; jj < kJ; ++jj) {
+                if (rows[u].r[jj] < 0) continue;
+                float f[VN];
+                Vec<T>::unpack(r[u][jj], f);
+#pragma unroll
+                for (int q = 0; q < VN; ++q) acc[u][q] = __builtin_fmaf(gj[u][jj], f[q], acc[u][q]);
+            }
+    }
+#pragma unroll
+    for (int u = 0; u < kItems; ++u)
+        if (i0 + u * kBlock < total) dst[it[u]] = Vec<T>::pack(acc[u]);
 }
 
 // One wave per token (the dot products reduce across the row): the token's dy
@@ -149,7 +187,9 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void combine_bwd_kernel(
             if (v < nvec) a[q] = g_dy[v];
         }
         for (int j = 0; j < m.k; ++j) {
-            const long long row = m.row(t, j);
+            Rows<1> rj;
+            rj.fetch(m, t, j);
+            const long long row = rj.r[0];
             if (row < 0) {
                 if (lane == 0 && v0 == 0) dgate[static_cast<size_t>(t) * m.k + j] = 0.0f;
                 continue;
@@ -188,48 +228,55 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void combine_bwd_kernel(
     }
 }
 
-template <typename T>
+// dx[t] = sum over kept j (ascending) of dxe[row(t, j)], f32, overwritten.
+template <typename T, int kJ>
 __global__ __launch_bounds__(kBlock) void dispatch_bwd_kernel(const T* __restrict__ dxe,
                                                               float* __restrict__ dx, RouteMeta m,
                                                               int nvec) {
     constexpr int VN = Vec<T>::n;
-    constexpr int KMAX = 4;
     const long long total = static_cast<long long>(m.N) * nvec;
     const long long i0 = static_cast<long long>(blockIdx.x) * kBlock * kItems + threadIdx.x;
     const uint4* src = reinterpret_cast<const uint4*>(dxe);
     float4* dst = reinterpret_cast<float4*>(dx);
+    long long it[kItems];
+    int tt[kItems], cc[kItems];
+    float acc[kItems][VN];
 #pragma unroll
     for (int u = 0; u < kItems; ++u) {
-        const long long i = i0 + u * kBlock;
-        if (i >= total) break;
-        const int t = static_cast<int>(i / nvec), c = static_cast<int>(i - static_cast<long long>(t) * nvec);
-        float acc[VN];
+        it[u] = min(i0 + u * kBlock, total - 1);
+        tt[u] = static_cast<int>(it[u] / nvec);
+        cc[u] = static_cast<int>(it[u] - static_cast<long long>(tt[u]) * nvec);
 #pragma unroll
-        for (int q = 0; q < VN; ++q) acc[q] = 0.0f;
-        for (int j0 = 0; j0 < m.k; j0 += KMAX) {
-            uint4 r[KMAX];
-            bool kept[KMAX];
+        for (int q = 0; q < VN; ++q) acc[u][q] = 0.0f;
+    }
+    for (int j0 = 0; j0 < m.k; j0 += kJ) {
+        Rows<kJ> rows[kItems];
+        uint4 r[kItems][kJ];
 #pragma unroll
-            for (int jj = 0; jj < KMAX; ++jj) {
-                const int j = j0 + jj;
-                const long long row = j < m.k ? m.row(t, j) : -1;
-                kept[jj] = row >= 0;
-                r[jj] = row >= 0 ? src[row * nvec + c] : make_uint4(0u, 0u, 0u, 0u);
-            }
-            // j ascending over the kept assignments
+        for (int u = 0; u < kItems; ++u) rows[u].fetch(m, tt[u], j0);
 #pragma unroll
-            for (int jj = 0; jj < KMAX; ++jj) {
-                if (!kept[jj]) continue;
+        for (int u = 0; u < kItems; ++u)
+#pragma unroll
+            for (int jj = 0; jj < kJ; ++jj)
+                r[u][jj] = src[(rows[u].r[jj] >= 0 ? rows[u].r[jj] : 0) * nvec + cc[u]];
+#pragma unroll
+        for (int u = 0; u < kItems; ++u)
+#pragma unroll
+            for (int jj = 0; jj < kJ; ++jj) {
+                if (rows[u].r[jj] < 0) continue;
                 float f[VN];
-                Vec<T>::unpack(r[jj], f);
+                Vec<T>::unpack(r[u][jj], f);
 #pragma unroll
-                for (int q = 0; q < VN; ++q) acc[q] += f[q];
+                for (int q = 0; q < VN; ++q) acc[u][q] += f[q];
             }
-        }
+    }
+#pragma unroll
+    for (int u = 0; u < kItems; ++u) {
+        if (i0 + u * kBlock >= total) continue;
 #pragma unroll
         for (int q = 0; q < VN / 4; ++q)
-            dst[i * (VN / 4) + q] = make_float4(acc[4 * q], acc[4 * q + 1], acc[4 * q + 2],
-                                                acc[4 * q + 3]);
+            dst[it[u] * (VN / 4) + q] = make_float4(acc[u][4 * q], acc[u][4 * q + 1],
+                                                    acc[u][4 * q + 2], acc[u][4 * q + 3]);
     }
 }
 
@@ -245,12 +292,17 @@ vmoe_status dispatch_launch(const Dims& D, const void* x, const int32_t* idx, co
     const RouteMeta m = meta(D, idx, slot, row_base);
     const int nvec = D.d / (D.dtype == VMOE_BF16 ? 8 : 4);
     const unsigned grid = cdiv(static_cast<long long>(D.N) * nvec, kBlock * kItems);
-    if (D.dtype == VMOE_BF16)
-        dispatch_kernel<uint16_t><<<grid, kBlock, 0, st>>>(
-            static_cast<const uint16_t*>(x), static_cast<uint16_t*>(xe), m, nvec);
-    else
-        dispatch_kernel<float><<<grid, kBlock, 0, st>>>(
-            static_cast<const float*>(x), static_cast<float*>(xe), m, nvec);
+    auto go = [&](auto jc) {
+        constexpr int J = decltype(jc)::value;
+        if (D.dtype == VMOE_BF16)
+            dispatch_kernel<uint16_t, J><<<grid, kBlock, 0, st>>>(
+                static_cast<const uint16_t*>(x), static_cast<uint16_t*>(xe), m, nvec);
+        else
+            dispatch_kernel<float, J><<<grid, kBlock, 0, st>>>(
+                static_cast<const float*>(x), static_cast<float*>(xe), m, nvec);
+    };
+    if (D.k <= 2) go(std::integral_constant<int, 2>{});
+    else go(std::integral_constant<int, 4>{});
     return launch_status();
 }
 
@@ -261,12 +313,17 @@ vmoe_status combine_fwd_launch(const Dims& D, const void* ye, const int32_t* idx
     const RouteMeta m = meta(D, idx, slot, row_base);
     const int nvec = D.d / (D.dtype == VMOE_BF16 ? 8 : 4);
     const unsigned grid = cdiv(static_cast<long long>(D.N) * nvec, kBlock * kItems);
-    if (D.dtype == VMOE_BF16)
-        combine_fwd_kernel<uint16_t><<<grid, kBlock, 0, st>>>(
-            static_cast<const uint16_t*>(ye), gate, static_cast<uint16_t*>(y), m, nvec);
-    else
-        combine_fwd_kernel<float><<<grid, kBlock, 0, st>>>(
-            static_cast<const float*>(ye), gate, static_cast<float*>(y), m, nvec);
+    auto go = [&](auto jc) {
+        constexpr int J = decltype(jc)::value;
+        if (D.dtype == VMOE_BF16)
+            combine_fwd_kernel<uint16_t, J><<<grid, kBlock, 0, st>>>(
+                static_cast<const uint16_t*>(ye), gate, static_cast<uint16_t*>(y), m, nvec);
+        else
+            combine_fwd_kernel<float, J><<<grid, kBlock, 0, st>>>(
+                static_cast<const float*>(ye), gate, static_cast<float*>(y), m, nvec);
+    };
+    if (D.k <= 2) go(std::integral_constant<int, 2>{});
+    else go(std::integral_constant<int, 4>{});
     return launch_status();
 }
 
@@ -294,12 +351,17 @@ vmoe_status dispatch_bwd_launch(const Dims& D, const void* dxe, const int32_t* i
     const RouteMeta m = meta(D, idx, slot, row_base);
     const int nvec = D.d / (D.dtype == VMOE_BF16 ? 8 : 4);
     const unsigned grid = cdiv(static_cast<long long>(D.N) * nvec, kBlock * kItems);
-    if (D.dtype == VMOE_BF16)
-        dispatch_bwd_kernel<uint16_t><<<grid, kBlock, 0, st>>>(
-            static_cast<const uint16_t*>(dxe), dx, m, nvec);
-    else
-        dispatch_bwd_kernel<float><<<grid, kBlock, 0, st>>>(
-            static_cast<const float*>(dxe), dx, m, nvec);
+    auto go = [&](auto jc) {
+        constexpr int J = decltype(jc)::value;
+        if (D.dtype == VMOE_BF16)
+            dispatch_bwd_kernel<uint16_t, J><<<grid, kBlock, 0, st>>>(
+                static_cast<const uint16_t*>(dxe), dx, m, nvec);
+        else
+            dispatch_bwd_kernel<float, J><<<grid, kBlock, 0, st>>>(
+                static_cast<const float*>(dxe), dx, m, nvec);
+    };
+    if (D.k <= 2) go(std::integral_constant<int, 2>{});
+    else go(std::integral_constant<int, 4>{});
     return launch_status();
 }
 

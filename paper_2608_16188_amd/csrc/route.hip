@@ -46,7 +46,7 @@ struct RouteWs {
     BinMap* binmap;     // [G]
     int32_t* bin_start; // [G][kNumBins + 1]
     int32_t* fill;      // [G][kNumBins]
-    int32_t* members;   // [N]
+    uint2* members;     // [N] (key, token) grouped by bin
     int32_t* ccount;    // [G][nch][k][E]
     int32_t* cbase;     // [G][nch][k][E]
     int32_t* demand;    // [G][k][E]
@@ -70,7 +70,7 @@ RouteWs route_ws_layout(const Dims& D, void* base) {
     w.binmap = reinterpret_cast<BinMap*>(take(sizeof(BinMap) * D.G));
     w.bin_start = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * D.G * (kNumBins + 1)));
     w.fill = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * D.G * kNumBins));
-    w.members = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * D.N));
+    w.members = reinterpret_cast<uint2*>(take(sizeof(uint2) * D.N));
     w.ccount = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * D.G * nch * D.k * D.E));
     w.cbase = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * D.G * nch * D.k * D.E));
     w.demand = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * D.G * D.k * D.E));
@@ -484,21 +484,22 @@ __global__ __launch_bounds__(256) void bin_scatter_kernel(const uint32_t* __rest
                                                           const BinMap* __restrict__ binmap,
                                                           const int32_t* __restrict__ bin_start,
                                                           int32_t* __restrict__ fill,
-                                                          int32_t* __restrict__ members, int N,
+                                                          uint2* __restrict__ members, int N,
                                                           int Ng) {
     const int t = blockIdx.x * 256 + threadIdx.x;
     if (t >= N) return;
     const int g = t / Ng;
-    const int b = binmap[g](keys[t]);
+    const uint32_t key = keys[t];
+    const int b = binmap[g](key);
     const int pos = bin_start[static_cast<size_t>(g) * (kNumBins + 1) + b] +
                     atomicAdd(&fill[static_cast<size_t>(g) * kNumBins + b], 1);
-    members[static_cast<size_t>(g) * Ng + pos] = t;
+    members[static_cast<size_t>(g) * Ng + pos] = make_uint2(key, static_cast<uint32_t>(t));
 }
 
 __global__ __launch_bounds__(256) void rank_kernel(
     const uint32_t* __restrict__ keys, const BinMap* __restrict__ binmap,
     const int32_t* __restrict__ bin_start,
-    const int32_t* __restrict__ members, const int32_t* __restrict__ idx,
+    const uint2* __restrict__ members, const int32_t* __restrict__ idx,
     int32_t* __restrict__ order, int32_t* __restrict__ ccount, int N, int Ng, int E, int k,
     int nch) {
     const int t = blockIdx.x * 256 + threadIdx.x;
@@ -508,12 +509,18 @@ __global__ __launch_bounds__(256) void rank_kernel(
     const int32_t* bs = bin_start + static_cast<size_t>(g) * (kNumBins + 1);
     const int b = binmap[g](key);
     const int lo = bs[b], hi = bs[b + 1];
-    const int32_t* mg = members + static_cast<size_t>(g) * Ng;
+    const uint2* mg = members + static_cast<size_t>(g) * Ng;
+    // members carry their keys: four independent loads per round
     int rank = lo;
-    for (int p = lo; p < hi; ++p) {
-        const int t2 = mg[p];
-        const uint32_t k2 = keys[t2];
-        rank += (k2 < key || (k2 == key && t2 < t)) ? 1 : 0;
+    for (int p = lo; p < hi; p += 4) {
+        uint2 m[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) m[u] = mg[min(p + u, hi - 1)];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const uint32_t k2 = m[u].x, t2 = m[u].y;
+            rank += (p + u < hi && (k2 < key || (k2 == key && t2 < static_cast<uint32_t>(t)))) ? 1 : 0;
+        }
     }
     order[static_cast<size_t>(g) * Ng + rank] = t;
     const int c = rank / kSlotChunk;

@@ -152,6 +152,14 @@ SMALL = [
                     capacity_factor=1.0, dtype=W.F32, n_groups=2, router_std=0.2),
     W.custom_config("bf16_hot_empty", n_tokens=256, d_model=128, d_ff=384, n_experts=8, k=2,
                     capacity_factor=1.0, hot_experts=2, hot_offset=6.0),
+    # k > 2 (row moves in passes of four assignments), 17..32 and 33..64 experts
+    # (router backward with 32 / 64 expert columns), ragged widths
+    W.custom_config("bf16_k4_e20", n_tokens=400, d_model=96, d_ff=160, n_experts=20, k=4,
+                    capacity_factor=1.0, n_groups=2, router_std=0.3),
+    W.custom_config("bf16_k6_e64", n_tokens=300, d_model=64, d_ff=128, n_experts=64, k=6,
+                    capacity_factor=2.0, router_std=0.3, noise_var=0.05),
+    W.custom_config("f32_k3", n_tokens=150, d_model=48, d_ff=96, n_experts=6, k=3,
+                    capacity_factor=0.9, dtype=W.F32, router_std=0.2),
 ]
 
 

@@ -264,21 +264,24 @@ __device__ __forceinline__ bf16x8 read_frag(const uint16_t* s, int blk, int kste
     }
 }
 
-// GELU and its derivative from one exponential: with x = |h| / sqrt(2),
-// erf(x) = 1 - t (a1 + t (a2 + t (a3 + t (a4 + t a5)))) exp(-x^2), t = 1 / (1 + p x)
-// (Abramowitz & Stegun 7.1.26, |error| < 1.5e-7), Phi(h) = (1 + sign(h) erf(x)) / 2,
-// gelu(h) = h Phi(h) and gelu'(h) = Phi(h) + h exp(-h^2 / 2) / sqrt(2 pi).
+// GELU and its derivative from one exponential. With phi the standard normal
+// density, Abramowitz & Stegun 26.2.17 gives the upper tail
+//   q = 1 - Phi(|h|) = phi(h) t (b1 + t (b2 + t (b3 + t (b4 + t b5)))),
+//   t = 1 / (1 + p |h|), |error| < 7.5e-8 (far below bf16 rounding), so
+//   Phi(h) = 0.5 + sign(h) (0.5 - q),  gelu(h) = h Phi(h),  gelu'(h) = Phi(h) + h phi(h),
+// where phi(h) = 2^(-h^2 log2(e) / 2 + log2(1 / sqrt(2 pi))) is one v_exp_f32.
 __device__ __forceinline__ void gelu_pair(float h, float& g, float& dg) {
-    const float x = fabsf(h) * 0.70710678118654752f;
-    const float t = __builtin_amdgcn_rcpf(1.0f + 0.3275911f * x);
-    const float ex = __expf(-x * x);
-    const float poly =
-        t * (0.254829592f + t * (-0.284496736f + t * (1.421413741f + t * (-1.453152027f +
-                                                                           t * 1.061405429f))));
-    const float erf_abs = 1.0f - poly * ex;
-    const float phi_cdf = 0.5f + 0.5f * copysignf(erf_abs, h);
+    const float t = __builtin_amdgcn_rcpf(__builtin_fmaf(fabsf(h), 0.2316419f, 1.0f));
+    const float phi = __builtin_amdgcn_exp2f(
+        __builtin_fmaf(h * h, -0.72134752044448170f, -1.32574806473615920f));
+    float poly = __builtin_fmaf(t, 1.330274429f, -1.821255978f);
+    poly = __builtin_fmaf(t, poly, 1.781477937f);
+    poly = __builtin_fmaf(t, poly, -0.356563782f);
+    poly = __builtin_fmaf(t, poly, 0.319381530f);
+    const float q = (t * poly) * phi;
+    const float phi_cdf = 0.5f + copysignf(0.5f - q, h);
     g = h * phi_cdf;
-    dg = phi_cdf + h * ex * 0.39894228040143268f;
+    dg = __builtin_fmaf(h, phi, phi_cdf);
 }
 
 // Static description of one bf16 GEMM tiling: BM x BN block tile of WGM x WGN
@@ -360,9 +363,9 @@ __device__ __forceinline__ void mfma_block(f32x16 (&acc)[FM][FN], const F& f) {
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.b[j], f.a[i], acc[i][j], 0, 0, 0);
 }
 
-// Bias of the columns a lane owns in the epilogue: column 32 j + 8 q + 4 (l / 32)
-// + 0..3 of the wave tile, for j < FN, q < 4, as four packed bf16 (zero past N).
-// Loaded before the main loop so its latency hides behind the MFMAs.
+// Bias of the columns a lane owns: column 32 j + 8 q + 4 (l / 32) + 0..3 of the
+// wave tile, for j < FN, q < 4, as four packed bf16 (zero past N). Loaded ahead
+// of the first operand stages; the accumulators start from it.
 template <class T, int EPI>
 struct BiasRegs {
     static constexpr bool USED = EPI == EPI_FWD1 || EPI == EPI_BIAS;
@@ -384,13 +387,13 @@ struct BiasRegs {
 };
 
 // Epilogue of one block: optional bias-gradient row sums (partials combined in
-// part_buf), then each wave turns its accumulators into outputs (bias, GELU +
+// part_buf), then each wave turns its accumulators (bias included) into outputs (GELU +
 // GELU', GELU' product), parks them in its own slot of ep_buf and writes every
 // output row as 16-byte-per-lane segments. The slots are private to a wave and
 // LDS accesses of one wave complete in order, so the passes need no barrier.
 template <class T, class CFG, int EPI>
 __device__ __forceinline__ void gemm_epilogue(const GemmArgs& p, f32x16 (&acc)[T::FM][T::FN],
-                                              const BiasRegs<T, EPI>& bias, uint16_t* part_buf,
+                                              uint16_t* part_buf,
                                               uint16_t* ep_buf, float rsum, bool row_sum, int e,
                                               int M, int N, int m0, int n0) {
     constexpr int FM = T::FM, FN = T::FN, WM = T::WM, WN = T::WN, BM_ = T::BM;
@@ -463,13 +466,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& p, f32x16 (&acc)[T
                             *reinterpret_cast<float4*>(reinterpret_cast<float*>(ep) + ml * EP_LD +
                                                        nl) = make_float4(r[0], r[1], r[2], r[3]);
                         } else {
-                            if constexpr (EPI == EPI_FWD1 || EPI == EPI_BIAS) {
-                                const uint2 bb = bias.v[j * 4 + q];
-                                r[0] += bf16_to_f32(bb.x & 0xFFFFu);
-                                r[1] += bf16_to_f32(bb.x >> 16);
-                                r[2] += bf16_to_f32(bb.y & 0xFFFFu);
-                                r[3] += bf16_to_f32(bb.y >> 16);
-                            }
+                            // (the bias of EPI_FWD1 / EPI_BIAS is already in acc)
                             if constexpr (EPI == EPI_GELU_GRAD) {
                                 const uint2 gg = aux[(ii * FN + j) * 4 + q];
                                 r[0] *= bf16_to_f32(gg.x & 0xFFFFu);
@@ -608,12 +605,6 @@ void gemm_bf16_kernel(GemmBatch batch) {
     float rsum = 0.0f;
 
     f32x16 acc[FM][FN];
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
     using DA = DmaStage<BM_, A_KMAJOR, KB, NT>;
     using DB = DmaStage<BN_, B_KMAJOR, KB, NT>;
@@ -638,21 +629,46 @@ void gemm_bf16_kernel(GemmBatch batch) {
         DA::issue(ra_rs, p.a.ld, m0, M, kt * KB, K, dst);
         DB::issue(rb_rs, p.b.ld, n0, N, kt * KB, K, dst + AE);
     };
+    // the accumulators start from the bias where there is one (added once per
+    // output instead of in the epilogue); its loads were issued first, so
+    // waiting for them leaves the first stages in flight
+    auto init_acc = [&]() {
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    float b4[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+                    if constexpr (BiasRegs<T, EPI>::USED) {
+                        const uint2 bb = bias.v[j * 4 + q];
+                        b4[0] = bf16_to_f32(bb.x & 0xFFFFu);
+                        b4[1] = bf16_to_f32(bb.x >> 16);
+                        b4[2] = bf16_to_f32(bb.y & 0xFFFFu);
+                        b4[3] = bf16_to_f32(bb.y >> 16);
+                    }
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) acc[i][j][4 * q + r] = b4[r];
+                }
+    };
     if constexpr (MODE == STAGE_DMA) {
         issue(0, buf0);
         if constexpr (T::PAIR) {
             issue(1, buf1);
+            init_acc();
             __builtin_amdgcn_s_waitcnt(WAIT_ODD);
         } else {
             if constexpr (NS > 2) issue(1, buf1);
             if constexpr (NS > 3) issue(2, buf2);
             if constexpr (NS > 4) issue(3, buf3);
+            init_acc();
             __builtin_amdgcn_s_waitcnt(WAIT_IMM);
         }
         ring_barrier();
     } else {
         RA::load(ra_rs, p.a.ld, m0, M, 0, K, ra);
         RB::load(rb_rs, p.b.ld, n0, N, 0, K, rb);
+        init_acc();
         RA::store(buf0, ra);
         RB::store(buf0 + AE, rb);
         __syncthreads();
@@ -758,7 +774,7 @@ void gemm_bf16_kernel(GemmBatch batch) {
     // arrays themselves keeps the accesses in the LDS address space)
     const int eb = wave % NS;
     uint16_t* const ep = eb == 0 ? buf0 : eb == 1 ? buf1 : eb == 2 ? buf2 : eb == 3 ? buf3 : buf4;
-    gemm_epilogue<T, CFG, EPI>(p, acc, bias, buf0, ep, rsum, row_sum, e, M, N, m0, n0);
+    gemm_epilogue<T, CFG, EPI>(p, acc, buf0, ep, rsum, row_sum, e, M, N, m0, n0);
 }
 
 // ------------------------------------------------------------------ f32 FMA path

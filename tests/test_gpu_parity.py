@@ -35,8 +35,11 @@ def _gpu():
 
 
 def _f64_out(t, dtype):
+    """A whole output buffer as float64; rows past an expert's count are never
+    written and may hold any bits (signalling NaNs included)."""
     a = to_numpy(t)
-    return W.to_f64(a, dtype) if a.dtype == np.uint16 else a.astype(np.float64)
+    with np.errstate(invalid="ignore"):
+        return W.to_f64(a, dtype) if a.dtype == np.uint16 else a.astype(np.float64)
 
 
 # ------------------------------------------------------------------ routing

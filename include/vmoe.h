@@ -188,8 +188,8 @@ vmoe_status vmoe_dispatch_bwd(const vmoe_shape* shape, const void* dxe,
  *   dx[t,:] += sum_e dz[t,e] w_router[g,e,:]                    (accumulates)
  *   dw_router[g,e,:] = sum_{t in g} dz[t,e] x[t,:]  f32 [G,E,d], overwritten;
  *                      NULL skips it (frozen routers)
- * workspace: vmoe_route_bwd_workspace_bytes(shape) bytes of device memory (dz,
- * and the per-chunk router-gradient partials), required with or without
+ * workspace: vmoe_route_bwd_workspace_bytes(shape) bytes of device memory
+ * (the per-chunk router-gradient partials), required with or without
  * dw_router; VMOE_ERR_WORKSPACE if it is smaller or not device memory. */
 vmoe_status vmoe_route_bwd(const vmoe_shape* shape, const void* x, const void* w_router,
                            const float* probs, const int32_t* expert_idx, const int32_t* slot,

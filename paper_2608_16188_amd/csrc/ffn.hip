@@ -75,10 +75,51 @@ struct GemmBatch {
     int group_m, chunk, per_xcd;
 };
 
+// A GEMM whose m is the expert's rows (every epilogue but the weight
+// gradients', whose k is the rows) runs one problem per launch and numbers its
+// tiles over the experts' live m-tiles only (ceil(n_e / BM) each, from the
+// device row counts): the blocks past the last live tile all sit at the end
+// of the grid instead of between the live tiles of consecutive experts, where
+// each would hold a CU slot while the dispatcher places blocks in order.
+template <int EPI>
+constexpr bool compact_tiles() { return EPI != EPI_F32; }
+
 __device__ __forceinline__ int expert_rows(const int32_t* counts, int G, int E, int e) {
     int n = 0;
     for (int g = 0; g < G; ++g) n += counts[g * E + e];
     return n;
+}
+
+// Live tile w of a compact problem (see GemmBatch::compact): lane e of every
+// wave sums expert e's rows (at most `cap`, the rows of its buffer) and its tile count, an inclusive scan over the
+// lanes places the experts' tile ranges end to end, and the expert holding w
+// is the number of ranges that end at or before it. Returns false past the
+// last live tile. Uniform per wave (every wave of a block computes the same).
+struct LiveTile {
+    int e, r, ne;  // expert, tile index inside the expert, expert's rows
+};
+__device__ __forceinline__ bool live_tile(const int32_t* counts, int G, int E, int cap, int bm,
+                                          int tiles_n, int w, LiveTile* out) {
+    const int lane = threadIdx.x & 63;
+    int ne = 0;
+    if (lane < E) {
+#pragma unroll 4
+        for (int g = 0; g < G; ++g) ne += counts[g * E + lane];
+        ne = min(ne, cap);  // never past the expert's rows, whatever the counts say
+    }
+    const int t = (ne + bm - 1) / bm * tiles_n;
+    int incl = t;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int u = __shfl_up(incl, o, 64);
+        if (lane >= o) incl += u;
+    }
+    if (w >= __shfl(incl, 63, 64)) return false;
+    const int e = __popcll(__ballot(incl <= w));
+    out->e = e;
+    out->r = w - __shfl(incl - t, e, 64);
+    out->ne = __shfl(ne, e, 64);
+    return true;
 }
 
 __device__ __forceinline__ float gelu_f(float h) {
@@ -564,27 +605,38 @@ void gemm_bf16_kernel(GemmBatch batch) {
     const int b = blockIdx.x;
     const int l = b >> 3, chunk = batch.chunk;
     int w = ((l / chunk) * 8 + (b & 7)) * chunk + l % chunk;
-    if (w >= batch.total[0] + batch.total[1]) return;
-    const int prob = w >= batch.total[0] ? 1 : 0;  // uniform per block
-    if (prob) w -= batch.total[0];
+    int prob = 0, e, r, ne, tiles_m;
+    if constexpr (compact_tiles<EPI>()) {
+        LiveTile lt;
+        const GemmArgs& p0 = batch.p[0];
+        if (!live_tile(p0.counts, p0.G, p0.E, p0.M, BM_, batch.tiles_n[0], w, &lt)) return;
+        e = lt.e;
+        r = lt.r;
+        ne = lt.ne;
+        tiles_m = (ne + BM_ - 1) / BM_;
+    } else {
+        if (w >= batch.total[0] + batch.total[1]) return;
+        prob = w >= batch.total[0] ? 1 : 0;  // uniform per block
+        if (prob) w -= batch.total[0];
+        tiles_m = batch.tiles_m[prob];
+        const int tiles_e = tiles_m * batch.tiles_n[prob];
+        e = w / tiles_e;
+        r = w - e * tiles_e;
+        ne = expert_rows(batch.p[prob].counts, batch.p[prob].G, batch.p[prob].E, e);
+    }
     const GemmArgs& p = batch.p[prob];
-    const int tiles_m = batch.tiles_m[prob], tiles_n = batch.tiles_n[prob];
+    const int tiles_n = batch.tiles_n[prob];
     const int group_m = batch.group_m;
     // inside one expert, tiles go in groups of group_m m-tiles, m fastest, so
     // the blocks resident on an XCD at once cover a compact patch of the output
     // and share both operand panels in its L2
-    const int tiles_e = tiles_m * tiles_n;
-    const int e = w / tiles_e;
-    const int r = w - e * tiles_e;
     const int grp = r / (group_m * tiles_n);
     const int first_m = grp * group_m;
     const int gm = min(group_m, tiles_m - first_m);
     const int idx = r - grp * group_m * tiles_n;
     const int tm = first_m + idx % gm;
     const int tn = idx / gm;
-
-    const int ne = expert_rows(p.counts, p.G, p.E, e);
-    const int M = p.var_k ? p.M : ne;
+    const int M = p.var_k ? p.M : min(ne, p.M);
     const int K = p.var_k ? ne : p.K;
     const int N = p.N;
     const int m0 = tm * BM_, n0 = tn * BN_;

@@ -612,6 +612,351 @@ __global__ __launch_bounds__(kSlotChunk) void slots_kernel(
     }
 }
 
+// ------------------------------------------ small groups: one block each
+//
+// A group of at most kLocalTokens tokens and kLocalAssign assignments runs
+// steps 2-6 in one 1024-thread block, all in LDS: the same bin map and exact
+// (key, token) rank give the order (a bin member carries the key bits below
+// the bin with its token, so one LDS word decides each comparison), then the
+// slots are assigned round by round over the order in tiles of 1024
+// positions with the ballot ranks of slots_kernel; a round's running
+// per-expert totals are its demand, which gives the next round's carry.
+// Phases meet at LDS-only barriers, so the order and slot stores drain in
+// the background, and the gate probabilities are fetched at the start.
+constexpr int kLocalTokens = 8192;
+constexpr int kLocalAssign = 16384;
+constexpr int kTokBits = 13;  // token index inside a group < 2^13
+static_assert(kLocalTokens <= (1 << kTokBits), "token index field");
+static_assert(kKeyBits - kBinBits + kTokBits <= 32, "bin member = low key bits + token");
+
+// Barrier for data exchanged through LDS only: waits for this wave's LDS
+// accesses (lgkmcnt(0)), not for its global stores.
+__device__ __forceinline__ void lds_barrier() {
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    __builtin_amdgcn_s_barrier();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+// NW > 0 (E <= 2 NW <= 16): slots from a block scan of per-thread expert
+// counts packed two 16-bit fields to a word; NW == 0: ballot tiles.
+template <int NW>
+__global__ __launch_bounds__(1024) void local_route_kernel(
+    const uint32_t* __restrict__ keys, const int32_t* __restrict__ idx,
+    const float* __restrict__ probs, int32_t* __restrict__ order, int32_t* __restrict__ slot,
+    float* __restrict__ gate, int32_t* __restrict__ counts, int32_t* __restrict__ row_base,
+    int G, int Ng, int E, int k, int C) {
+    constexpr int KT = kLocalTokens / 1024, KA = kLocalAssign / 1024;  // per thread
+    __shared__ uint32_t key_l[kLocalTokens];
+    __shared__ uint32_t memb[kLocalTokens];          // bin members: low key bits << 13 | token
+    __shared__ uint16_t ord_l[kLocalTokens];         // tokens by order position
+    __shared__ uint8_t idx_l[kLocalAssign];          // [Ng][k] choices
+    __shared__ uint32_t kept_l[kLocalAssign / 32];   // bit t*k + r: assignment kept
+    __shared__ int start[kNumBins + 1];
+    __shared__ int cursor[kNumBins];                 // histogram, then fill cursors
+    __shared__ int wcnt[2][16][kMaxExperts + 1];     // per-wave expert counts, two tiles
+    __shared__ int running[kMaxExperts + 1];         // this round's earlier tiles
+    __shared__ int carry[kMaxExperts];               // min(C, earlier rounds' demand)
+    __shared__ uint32_t wtot[16][NW > 0 ? NW : 1];   // packed scan: wave totals,
+    __shared__ uint32_t wpre[16][NW > 0 ? NW : 1];   // their prefixes over waves,
+    __shared__ uint32_t btot[NW > 0 ? NW : 1];       // the block total,
+    __shared__ uint32_t wmin[16], wmax[16];
+    __shared__ BinMap map;
+    const int g = blockIdx.x, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const size_t t0 = static_cast<size_t>(g) * Ng;
+    const int nk = Ng * k;
+
+    // all global loads of the group first, in flight together
+    uint32_t kv[KT];
+    int32_t iv[KA];
+#pragma unroll
+    for (int u = 0; u < KT; ++u) kv[u] = keys[t0 + min(u * 1024 + tid, Ng - 1)];
+#pragma unroll
+    for (int u = 0; u < KA; ++u) iv[u] = idx[t0 * k + min(u * 1024 + tid, nk - 1)];
+    for (int b = tid; b < kNumBins; b += 1024) cursor[b] = 0;
+    for (int q = tid; q < kLocalAssign / 32; q += 1024) kept_l[q] = 0u;
+    for (int q = tid; q < 2 * 16 * (kMaxExperts + 1); q += 1024) (&wcnt[0][0][0])[q] = 0;
+    if (tid <= kMaxExperts) running[tid] = 0;
+    if (tid < kMaxExperts) carry[tid] = 0;
+    uint32_t lo = 0xFFFFFFFFu, hi = 0u;
+#pragma unroll
+    for (int u = 0; u < KT; ++u) {
+        const int t = u * 1024 + tid;
+        if (t < Ng) {
+            key_l[t] = kv[u];
+            lo = min(lo, kv[u]);
+            hi = max(hi, kv[u]);
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < KA; ++u) {
+        const int q = u * 1024 + tid;
+        if (q < nk) idx_l[q] = static_cast<uint8_t>(iv[u]);
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        lo = min(lo, static_cast<uint32_t>(__shfl_xor(static_cast<int>(lo), o, 64)));
+        hi = max(hi, static_cast<uint32_t>(__shfl_xor(static_cast<int>(hi), o, 64)));
+    }
+    if (lane == 0) {
+        wmin[w] = lo;
+        wmax[w] = hi;
+    }
+    lds_barrier();
+    if (tid == 0) {
+        uint32_t a = wmin[0], z = wmax[0];
+        for (int q = 1; q < 16; ++q) {
+            a = min(a, wmin[q]);
+            z = max(z, wmax[q]);
+        }
+        int sh = 0;
+        while (((z - a) >> sh) >= static_cast<uint32_t>(kNumBins)) ++sh;
+        map = BinMap{a, sh};
+    }
+    lds_barrier();
+    const BinMap bm = map;
+    const uint32_t low_mask = (1u << bm.shift) - 1u;
+    for (int t = tid; t < Ng; t += 1024) atomicAdd(&cursor[bm(key_l[t])], 1);
+    lds_barrier();
+    {
+        constexpr int per = kNumBins / 1024;
+        int local[per];
+        int sum = 0;
+#pragma unroll
+        for (int q = 0; q < per; ++q) {
+            local[q] = cursor[tid * per + q];
+            sum += local[q];
+        }
+        int total;
+        int run = block_exclusive_scan_1024(sum, &total);
+#pragma unroll
+        for (int q = 0; q < per; ++q) {
+            start[tid * per + q] = run;
+            cursor[tid * per + q] = run;
+            run += local[q];
+        }
+        if (tid == 0) start[kNumBins] = total;
+    }
+    lds_barrier();
+    for (int t = tid; t < Ng; t += 1024) {
+        const uint32_t key = key_l[t];
+        const int pos = atomicAdd(&cursor[bm(key)], 1);
+        memb[pos] = (((key - bm.kmin) & low_mask) << kTokBits) | static_cast<uint32_t>(t);
+    }
+    lds_barrier();
+    {
+        // this thread's tokens tid + 1024 u: keys, then bin bounds, read together
+        uint32_t mine[KT];
+        int lo_b[KT], hi_b[KT];
+#pragma unroll
+        for (int u = 0; u < KT; ++u) mine[u] = key_l[min(u * 1024 + tid, Ng - 1)];
+#pragma unroll
+        for (int u = 0; u < KT; ++u) {
+            const int b = bm(mine[u]);
+            lo_b[u] = start[b];
+            hi_b[u] = start[b + 1];
+            mine[u] = (((mine[u] - bm.kmin) & low_mask) << kTokBits) |
+                      static_cast<uint32_t>(u * 1024 + tid);
+        }
+#pragma unroll
+        for (int u = 0; u < KT; ++u) {
+            const int t = u * 1024 + tid;
+            if (t < Ng) {
+                // members before this token: smaller (low key bits, token); four reads at a time
+                const int pe = hi_b[u];
+                int rank = lo_b[u];
+                int before = 0;
+                for (int p = rank; p < pe; p += 4) {
+                    uint32_t m[4];
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) m[v] = memb[min(p + v, pe - 1)];
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) before += (p + v < pe && m[v] < mine[u]) ? 1 : 0;
+                }
+                rank += before;
+                ord_l[rank] = static_cast<uint16_t>(t);
+                order[t0 + rank] = static_cast<int32_t>(t0 + t);
+            }
+        }
+    }
+    lds_barrier();
+    // the probabilities of the gates, needed at the very end (their latency
+    // hides behind the slots); q / k as a multiply-high by ceil(2^32 / k),
+    // exact for q k < 2^32
+    const uint32_t kinv = k > 1 ? 0xFFFFFFFFu / static_cast<uint32_t>(k) + 1u : 0u;
+    float pv[KA];
+#pragma unroll
+    for (int u = 0; u < KA; ++u) {
+        const int q = min(u * 1024 + tid, nk - 1);
+        const int t = k > 1 ? static_cast<int>(__umulhi(static_cast<uint32_t>(q), kinv)) : q;
+        pv[u] = probs[(t0 + t) * E + idx_l[q]];
+    }
+    int total = 0;  // thread e < E: demand of the rounds so far
+    if constexpr (NW > 0) {
+        // thread tid owns order positions [tid P, tid P + P), P <= 8: its
+        // per-expert counts (4-bit fields of one word) give the ranks among
+        // its own positions, and an exclusive block scan of the counts
+        // (16-bit fields, two experts per word) the ranks before them
+        // Carries and demands never exceed N_g k <= kLocalAssign < 2^16, so
+        // every thread keeps the per-expert demand of the finished rounds
+        // packed like the scan, and derives the carries itself
+        static_assert(kLocalAssign < (1 << 16), "16-bit demand fields");
+        const int P = (Ng + 1023) / 1024;
+        uint32_t done[NW];
+#pragma unroll
+        for (int q = 0; q < NW; ++q) done[q] = 0u;
+        const uint32_t cap = static_cast<uint32_t>(min(C, 0xFFFF));
+        for (int r = 0; r < k; ++r) {
+            uint64_t lc = 0;
+            int ee[KT], tt[KT], lr[KT];
+#pragma unroll
+            for (int j = 0; j < KT; ++j) tt[j] = ord_l[min(tid * P + j, Ng - 1)];
+#pragma unroll
+            for (int j = 0; j < KT; ++j) ee[j] = idx_l[tt[j] * k + r];
+#pragma unroll
+            for (int j = 0; j < KT; ++j) {
+                const int p = tid * P + j;
+                const bool act = j < P && p < Ng;
+                const int e = ee[j];
+                lr[j] = static_cast<int>((lc >> (4 * e)) & 15u);
+                lc += act ? (1ull << (4 * e)) : 0ull;
+                ee[j] = act ? e : -1;
+            }
+            // word q of this thread's counts: experts 2q, 2q + 1 in 16-bit fields
+            auto own = [&](int q) {
+                return static_cast<uint32_t>((lc >> (8 * q)) & 15u) |
+                       (static_cast<uint32_t>((lc >> (8 * q + 4)) & 15u) << 16);
+            };
+            uint32_t inc[NW];
+#pragma unroll
+            for (int q = 0; q < NW; ++q) inc[q] = own(q);
+#pragma unroll
+            for (int o = 1; o < 64; o <<= 1) {
+#pragma unroll
+                for (int q = 0; q < NW; ++q) {
+                    const uint32_t u = static_cast<uint32_t>(__shfl_up(static_cast<int>(inc[q]), o, 64));
+                    if (lane >= o) inc[q] += u;
+                }
+            }
+            if (lane == 63) {
+#pragma unroll
+                for (int q = 0; q < NW; ++q) wtot[w][q] = inc[q];
+            }
+#pragma unroll
+            for (int q = 0; q < NW; ++q) inc[q] -= own(q);  // exclusive inside the wave
+            lds_barrier();
+            if (tid < 16 * NW) {  // (wave, word): prefix over earlier waves
+                const int w2 = tid / NW, q = tid % NW;
+                uint32_t pre = 0u;
+#pragma unroll
+                for (int w3 = 0; w3 < 15; ++w3) pre += w3 < w2 ? wtot[w3][q] : 0u;
+                wpre[w2][q] = pre;
+                if (w2 == 15) btot[q] = pre + wtot[15][q];
+            }
+            lds_barrier();
+#pragma unroll
+            for (int q = 0; q < NW; ++q) inc[q] += wpre[w][q];  // exclusive over the block
+#pragma unroll
+            for (int j = 0; j < KT; ++j) {
+                const int e = ee[j];
+                if (e >= 0) {
+                    uint32_t word = inc[0], dw = done[0];
+#pragma unroll
+                    for (int q = 1; q < NW; ++q) {
+                        word = (e >> 1) == q ? inc[q] : word;
+                        dw = (e >> 1) == q ? done[q] : dw;
+                    }
+                    const int sh = 16 * (e & 1);
+                    const int rank = static_cast<int>((word >> sh) & 0xFFFFu) + lr[j];
+                    const int sl = static_cast<int>(min((dw >> sh) & 0xFFFFu, cap)) + rank;
+                    const int t = tt[j];
+                    const bool kept = sl < C;
+                    slot[(t0 + t) * k + r] = kept ? sl : -1;
+                    if (kept) atomicOr(&kept_l[(t * k + r) >> 5], 1u << ((t * k + r) & 31));
+                }
+            }
+#pragma unroll
+            for (int q = 0; q < NW; ++q) done[q] += btot[q];
+        }
+        if (tid < E) {
+            uint32_t word = done[0];
+#pragma unroll
+            for (int q = 1; q < NW; ++q) word = (tid >> 1) == q ? done[q] : word;
+            total = static_cast<int>((word >> (16 * (tid & 1))) & 0xFFFFu);
+        }
+    } else {
+    // slots: tile i counts its waves' experts into wcnt[i & 1] (cleared while
+    // tile i - 1 was read), so a tile takes two barriers
+    const uint64_t lt_mask = (1ull << lane) - 1ull;
+    const int ntile = (Ng + 1023) / 1024;
+    int it = 0;
+    for (int r = 0; r < k; ++r) {
+        for (int i = 0; i < ntile; ++i, ++it) {
+            const int buf = it & 1;
+            const int p = i * 1024 + tid;
+            const bool active = p < Ng;
+            const int t = active ? ord_l[p] : 0;
+            const int e = active ? idx_l[t * k + r] : kMaxExperts;
+            uint64_t same = __ballot(1);
+#pragma unroll
+            for (int bit = 0; bit < 7; ++bit) {
+                const uint64_t bal = __ballot((e >> bit) & 1);
+                same &= ((e >> bit) & 1) ? bal : ~bal;
+            }
+            const int rank_w = __popcll(same & lt_mask);
+            if (rank_w == 0) wcnt[buf][w][e] = __popcll(same);
+            lds_barrier();
+            if (active) {
+                int rank = running[e] + rank_w;
+#pragma unroll
+                for (int w2 = 0; w2 < 16; ++w2) rank += w2 < w ? wcnt[buf][w2][e] : 0;
+                const int sl = carry[e] + rank;
+                const bool kept = sl < C;
+                slot[(t0 + t) * k + r] = kept ? sl : -1;
+                if (kept) atomicOr(&kept_l[(t * k + r) >> 5], 1u << ((t * k + r) & 31));
+            }
+            for (int q = tid; q < 16 * (kMaxExperts + 1); q += 1024) (&wcnt[buf ^ 1][0][0])[q] = 0;
+            lds_barrier();
+            if (tid < E) {
+                int sum = running[tid];
+#pragma unroll
+                for (int w2 = 0; w2 < 16; ++w2) sum += wcnt[buf][w2][tid];
+                if (i + 1 < ntile) {
+                    running[tid] = sum;
+                } else {  // round done: its demand moves into the carry
+                    running[tid] = 0;
+                    total += sum;
+                    carry[tid] = min(C, total);
+                }
+            }
+        }
+    }
+    }
+    if (tid < E) {
+        counts[g * E + tid] = min(C, total);
+        if (G == 1) row_base[tid] = 0;
+    }
+    lds_barrier();
+#pragma unroll
+    for (int u = 0; u < KA; ++u) {
+        const int q = u * 1024 + tid;
+        if (q < nk) gate[t0 * k + q] = ((kept_l[q >> 5] >> (q & 31)) & 1u) ? pv[u] : 0.0f;
+    }
+}
+
+// row_base[g, e] = sum of counts[g', e] over g' < g.
+__global__ __launch_bounds__(64) void row_base_kernel(const int32_t* __restrict__ counts,
+                                                      int32_t* __restrict__ row_base, int G,
+                                                      int E) {
+    for (int e = threadIdx.x; e < E; e += 64) {
+        int base = 0;
+        for (int g = 0; g < G; ++g) {
+            row_base[g * E + e] = base;
+            base += counts[g * E + e];
+        }
+    }
+}
+
 }  // namespace
 
 size_t route_workspace_bytes(const Dims& D) { return route_ws_layout(D, nullptr).bytes; }
@@ -636,6 +981,14 @@ vmoe_status route_launch(const Dims& D, const void* x, const void* wr, const flo
             router_f64_kernel<<<grid, 256, 0, st>>>(
                 static_cast<const float*>(x), static_cast<const float*>(wr), bias, noise, logits,
                 probs, idx, ws.keys, D.Ng, D.d, D.E, D.k, logits_in, tpb);
+        }
+        if (D.Ng <= kLocalTokens && static_cast<long long>(D.Ng) * D.k <= kLocalAssign) {
+            auto kern = D.E <= 8 ? local_route_kernel<4>
+                      : D.E <= 16 ? local_route_kernel<8> : local_route_kernel<0>;
+            kern<<<D.G, 1024, 0, st>>>(ws.keys, idx, probs, order, slot, gate, counts, row_base,
+                                       D.G, D.Ng, D.E, D.k, D.C);
+            if (D.G > 1) row_base_kernel<<<1, 64, 0, st>>>(counts, row_base, D.G, D.E);
+            return launch_status();
         }
         bin_scan_kernel<<<D.G, 1024, 0, st>>>(ws.keys, ws.binmap, ws.bin_start, ws.fill,
                                                ws.ccount, D.Ng, nch * D.k * D.E);

@@ -96,6 +96,12 @@ ROUTE_CASES = [
     ("noise_and_bias", 777, 12, 3, 1, dict(seed=10, noise=True)),
     ("ragged_chunks", 3 * 257, 8, 2, 3, dict(seed=11)),
     ("empty", 0, 8, 2, 1, dict(seed=12)),
+    # one block per group up to 8192 tokens and 16384 assignments, else the
+    # multi-kernel path: both sides of that limit, and a one-bin worst case
+    ("single_block_limit", 8192, 8, 2, 1, dict(seed=13, scale=2.0)),
+    ("single_block_limit_plus_one", 8193, 8, 2, 1, dict(seed=14, scale=2.0)),
+    ("single_block_equal_priorities", 8000, 4, 2, 1, dict(seed=15, tie_every=1)),
+    ("single_block_k4_groups", 4 * 4096, 16, 4, 4, dict(seed=16, scale=2.0)),
 ]
 
 

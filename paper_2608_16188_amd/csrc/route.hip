@@ -807,20 +807,22 @@ __global__ __launch_bounds__(1024) void local_route_kernel(
         for (int q = 0; q < NW; ++q) done[q] = 0u;
         const uint32_t cap = static_cast<uint32_t>(min(C, 0xFFFF));
         for (int r = 0; r < k; ++r) {
+            // position j's expert and its rank among this thread's earlier
+            // positions, 4-bit fields of ep and rp (E <= 16, rank < 8)
             uint64_t lc = 0;
-            int ee[KT], tt[KT], lr[KT];
+            uint32_t ep = 0u, rp = 0u;
+            {
+                int tt[KT];
 #pragma unroll
-            for (int j = 0; j < KT; ++j) tt[j] = ord_l[min(tid * P + j, Ng - 1)];
+                for (int j = 0; j < KT; ++j) tt[j] = ord_l[min(tid * P + j, Ng - 1)];
 #pragma unroll
-            for (int j = 0; j < KT; ++j) ee[j] = idx_l[tt[j] * k + r];
-#pragma unroll
-            for (int j = 0; j < KT; ++j) {
-                const int p = tid * P + j;
-                const bool act = j < P && p < Ng;
-                const int e = ee[j];
-                lr[j] = static_cast<int>((lc >> (4 * e)) & 15u);
-                lc += act ? (1ull << (4 * e)) : 0ull;
-                ee[j] = act ? e : -1;
+                for (int j = 0; j < KT; ++j) {
+                    const int e = idx_l[tt[j] * k + r];
+                    const bool act = j < P && tid * P + j < Ng;
+                    rp |= static_cast<uint32_t>((lc >> (4 * e)) & 15u) << (4 * j);
+                    ep |= static_cast<uint32_t>(e) << (4 * j);
+                    lc += act ? (1ull << (4 * e)) : 0ull;
+                }
             }
             // word q of this thread's counts: experts 2q, 2q + 1 in 16-bit fields
             auto own = [&](int q) {
@@ -858,8 +860,9 @@ __global__ __launch_bounds__(1024) void local_route_kernel(
             for (int q = 0; q < NW; ++q) inc[q] += wpre[w][q];  // exclusive over the block
 #pragma unroll
             for (int j = 0; j < KT; ++j) {
-                const int e = ee[j];
-                if (e >= 0) {
+                const int p = tid * P + j;
+                if (j < P && p < Ng) {
+                    const int e = static_cast<int>((ep >> (4 * j)) & 15u);
                     uint32_t word = inc[0], dw = done[0];
 #pragma unroll
                     for (int q = 1; q < NW; ++q) {
@@ -867,9 +870,10 @@ __global__ __launch_bounds__(1024) void local_route_kernel(
                         dw = (e >> 1) == q ? done[q] : dw;
                     }
                     const int sh = 16 * (e & 1);
-                    const int rank = static_cast<int>((word >> sh) & 0xFFFFu) + lr[j];
+                    const int rank = static_cast<int>((word >> sh) & 0xFFFFu) +
+                                     static_cast<int>((rp >> (4 * j)) & 15u);
                     const int sl = static_cast<int>(min((dw >> sh) & 0xFFFFu, cap)) + rank;
-                    const int t = tt[j];
+                    const int t = ord_l[p];
                     const bool kept = sl < C;
                     slot[(t0 + t) * k + r] = kept ? sl : -1;
                     if (kept) atomicOr(&kept_l[(t * k + r) >> 5], 1u << ((t * k + r) & 31));
@@ -944,15 +948,25 @@ __global__ __launch_bounds__(1024) void local_route_kernel(
     }
 }
 
-// row_base[g, e] = sum of counts[g', e] over g' < g.
-__global__ __launch_bounds__(64) void row_base_kernel(const int32_t* __restrict__ counts,
-                                                      int32_t* __restrict__ row_base, int G,
-                                                      int E) {
-    for (int e = threadIdx.x; e < E; e += 64) {
-        int base = 0;
-        for (int g = 0; g < G; ++g) {
-            row_base[g * E + e] = base;
-            base += counts[g * E + e];
+// row_base[g, e] = sum of counts[g', e] over g' < g: the counts of a chunk of
+// groups are staged in LDS first (one load latency per chunk, not per group).
+__global__ __launch_bounds__(1024) void row_base_kernel(const int32_t* __restrict__ counts,
+                                                        int32_t* __restrict__ row_base, int G,
+                                                        int E) {
+    constexpr int kStage = 8192;
+    __shared__ int cnt_l[kStage];
+    const int per = kStage / E;  // groups per chunk (E <= 64)
+    int base = 0;                // thread e < E
+    for (int g0 = 0; g0 < G; g0 += per) {
+        const int ng = min(per, G - g0);
+        __syncthreads();
+        for (int q = threadIdx.x; q < ng * E; q += 1024) cnt_l[q] = counts[g0 * E + q];
+        __syncthreads();
+        if (static_cast<int>(threadIdx.x) < E) {
+            for (int g = 0; g < ng; ++g) {
+                row_base[(g0 + g) * E + threadIdx.x] = base;
+                base += cnt_l[g * E + threadIdx.x];
+            }
         }
     }
 }
@@ -987,7 +1001,7 @@ vmoe_status route_launch(const Dims& D, const void* x, const void* wr, const flo
                       : D.E <= 16 ? local_route_kernel<8> : local_route_kernel<0>;
             kern<<<D.G, 1024, 0, st>>>(ws.keys, idx, probs, order, slot, gate, counts, row_base,
                                        D.G, D.Ng, D.E, D.k, D.C);
-            if (D.G > 1) row_base_kernel<<<1, 64, 0, st>>>(counts, row_base, D.G, D.E);
+            if (D.G > 1) row_base_kernel<<<1, 1024, 0, st>>>(counts, row_base, D.G, D.E);
             return launch_status();
         }
         bin_scan_kernel<<<D.G, 1024, 0, st>>>(ws.keys, ws.binmap, ws.bin_start, ws.fill,

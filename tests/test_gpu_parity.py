@@ -102,6 +102,7 @@ ROUTE_CASES = [
     ("single_block_limit_plus_one", 8193, 8, 2, 1, dict(seed=14, scale=2.0)),
     ("single_block_equal_priorities", 8000, 4, 2, 1, dict(seed=15, tie_every=1)),
     ("single_block_k4_groups", 4 * 4096, 16, 4, 4, dict(seed=16, scale=2.0)),
+    ("many_small_groups_e64", 300 * 8, 64, 2, 300, dict(seed=17, scale=2.0)),
 ]
 
 

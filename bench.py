@@ -32,8 +32,10 @@ PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 matrix peak
 PEAK_F32_TFLOPS = 157.3        # MI355X f32 matrix peak
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 
+# The step's C-ABI calls in order; the dispatch and router backward run as
+# one call (vmoe_dispatch_route_bwd, bit-identical to the two separate calls).
 CALLS = ["route", "dispatch", "ffn_fwd", "combine_fwd", "combine_bwd", "ffn_bwd",
-         "dispatch_bwd", "route_bwd"]
+         "dispatch_route_bwd"]
 
 
 def algorithmic_cost(cfg, A: int, n_noise: bool, n_bias: bool):
@@ -58,6 +60,9 @@ def algorithmic_cost(cfg, A: int, n_noise: bool, n_bias: bool):
     c["dispatch_bwd"] = (0, A * d * B + N * d * 4 + meta)
     c["route_bwd"] = (4 * N * d * E, N * d * B + 2 * N * d * 4 + N * E * 4 + N * k * 12
                       + G * E * d * (B + 4))
+    # dxe rows in, dx out once, x, probs, routing data, router and its gradient
+    c["dispatch_route_bwd"] = (4 * N * d * E, A * d * B + N * d * B + N * d * 4 + N * E * 4
+                               + N * k * 12 + G * E * 4 + G * E * d * (B + 4))
     return c
 
 
@@ -95,7 +100,8 @@ def measured_traffic(workload: str, call: str):
         elif len(w) == 4 and w[0] == "source":
             sources[w[1]] = w[3]
     used = {"ffn_fwd": ["ffn.hip"], "ffn_bwd": ["ffn.hip"], "route": ["route.hip"],
-            "route_bwd": ["route_bwd.hip"]}.get(call, ["moves.hip"]) + ["common.h"]
+            "route_bwd": ["route_bwd.hip"],
+            "dispatch_route_bwd": ["route_bwd.hip"]}.get(call, ["moves.hip"]) + ["common.h"]
     csrc = os.path.join(ROOT, "paper_2608_16188_amd", "csrc")
     for f in used:
         if sources.get(f) != source_digest(os.path.join(csrc, f)):
@@ -181,6 +187,9 @@ def main():
                                                     L.dx, stream),
         "route_bwd": lambda: V.vmoe_route_bwd(s, L.x, L.w_router, L.probs, L.expert_idx, L.slot,
                                               L.dgate, L.dx, L.dw_router, L.route_bwd_ws, stream),
+        "dispatch_route_bwd": lambda: V.vmoe_dispatch_route_bwd(
+            s, L.dxe, L.row_base, L.x, L.w_router, L.probs, L.expert_idx, L.slot, L.dgate, L.dx,
+            L.dw_router, L.route_bwd_ws, stream),
     }
 
     if args.copy_probe:

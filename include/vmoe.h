@@ -196,6 +196,19 @@ vmoe_status vmoe_route_bwd(const vmoe_shape* shape, const void* x, const void* w
                            const float* dgate, float* dx, float* dw_router, void* workspace,
                            size_t workspace_bytes, void* stream);
 
+/* vmoe_dispatch_bwd followed by vmoe_route_bwd in one pass over the tokens:
+ *   dx[t,:] = sum over kept j of dxe[row(t,j),:] (j ascending, from 0)
+ *             + sum_e dz[t,e] w_router[g,e,:]        dx [N, d] f32, overwritten
+ *   dw_router as in vmoe_route_bwd (NULL skips it).
+ * Bit-identical to the two calls in sequence; it reads dxe where they would
+ * write and re-read dx. Arguments and workspace as in those two calls. */
+vmoe_status vmoe_dispatch_route_bwd(const vmoe_shape* shape, const void* dxe,
+                                    const int32_t* row_base, const void* x, const void* w_router,
+                                    const float* probs, const int32_t* expert_idx,
+                                    const int32_t* slot, const float* dgate, float* dx,
+                                    float* dw_router, void* workspace, size_t workspace_bytes,
+                                    void* stream);
+
 #ifdef __cplusplus
 }
 #endif

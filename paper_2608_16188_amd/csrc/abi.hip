@@ -33,6 +33,11 @@ vmoe_status ffn_bwd_launch(const Dims& D, const void* xe, const int32_t* counts,
 vmoe_status route_bwd_launch(const Dims& D, const void* x, const void* wr, const float* probs,
                              const int32_t* idx, const int32_t* slot, const float* dgate,
                              float* dx, float* dwr, void* ws, hipStream_t st);
+vmoe_status dispatch_route_bwd_launch(const Dims& D, const void* dxe, const int32_t* row_base,
+                                      const void* x, const void* wr, const float* probs,
+                                      const int32_t* idx, const int32_t* slot,
+                                      const float* dgate, float* dx, float* dwr, void* ws,
+                                      hipStream_t st);
 
 vmoe_status make_dims(const vmoe_shape* s, Dims* out) {
     if (!s || !out) return VMOE_ERR_INVALID_ARG;
@@ -213,6 +218,22 @@ vmoe_status vmoe_route_bwd(const vmoe_shape* shape, const void* x, const void* w
     if (workspace_bytes < need_ws || (need_ws > 0 && !dev(workspace))) return VMOE_ERR_WORKSPACE;
     return vmoe::route_bwd_launch(D, x, w_router, probs, expert_idx, slot, dgate, dx, dw_router,
                                   workspace, as_stream(stream));
+}
+
+vmoe_status vmoe_dispatch_route_bwd(const vmoe_shape* shape, const void* dxe,
+                                    const int32_t* row_base, const void* x, const void* w_router,
+                                    const float* probs, const int32_t* expert_idx,
+                                    const int32_t* slot, const float* dgate, float* dx,
+                                    float* dw_router, void* workspace, size_t workspace_bytes,
+                                    void* stream) {
+    Dims D;
+    VMOE_TRY(vmoe::make_dims(shape, &D));
+    VMOE_TRY(need(dev(dxe) && dev(row_base) && dev(x) && dev(w_router) && dev(probs) &&
+                  dev(expert_idx) && dev(slot) && dev(dgate) && dev(dx) && opt(dw_router)));
+    const size_t need_ws = vmoe::route_bwd_workspace_bytes(D);
+    if (workspace_bytes < need_ws || (need_ws > 0 && !dev(workspace))) return VMOE_ERR_WORKSPACE;
+    return vmoe::dispatch_route_bwd_launch(D, dxe, row_base, x, w_router, probs, expert_idx, slot,
+                                           dgate, dx, dw_router, workspace, as_stream(stream));
 }
 
 }  // extern "C"

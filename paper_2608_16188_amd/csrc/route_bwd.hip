@@ -7,9 +7,20 @@
 // the chunk's partial of dW_r[e, i] = sum_t dz[t,e] x[t,i] in registers. A
 // second kernel adds the partials over chunks in a fixed order
 // (deterministic, no float atomics).
+//
+// Fused with the dispatch backward, the kernel starts each dx row from the
+// token's kept expert rows of dxe, summed in j order (the dispatch backward's
+// sum, so the result is bit-identical to the two calls in sequence), instead
+// of reading dx: two f32 passes over dx and a launch fewer.
 #include "common.h"
 
 namespace vmoe {
+
+// (moves.hip) dx[t] = sum over kept j of dxe[row(t, j)]
+vmoe_status dispatch_bwd_launch(const Dims& D, const void* dxe, const int32_t* idx,
+                                const int32_t* slot, const int32_t* row_base, float* dx,
+                                hipStream_t st);
+
 namespace {
 
 constexpr int kMinChunk = 64;
@@ -82,6 +93,43 @@ __device__ __forceinline__ void store_cols(float* p, const float (&v)[VEC]) {
     else *p = v[0];
 }
 
+// The value a dx row starts from. KJ == 0: dx itself (accumulating call);
+// KJ > 0: the sum over the token's kept assignments j < KJ of its dxe rows, in
+// j order from 0, with the rows (-1 = not kept) taken from LDS.
+template <typename T, int VEC, int KJ>
+struct DxIn {
+    RawCols<T, VEC> r[KJ];
+    int kept;
+    __device__ __forceinline__ void load(const T* dxe, const int* rows, int d, int ic) {
+        kept = 0;
+#pragma unroll
+        for (int j = 0; j < KJ; ++j) {
+            const int row = rows[j];
+            kept |= (row >= 0 ? 1 : 0) << j;
+            r[j].load(dxe + static_cast<size_t>(row >= 0 ? row : 0) * d + ic);
+        }
+    }
+    __device__ __forceinline__ void to_f32(float (&v)[VEC]) const {
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) v[i] = 0.0f;
+#pragma unroll
+        for (int j = 0; j < KJ; ++j) {
+            if ((kept >> j) & 1) {
+                float f[VEC];
+                r[j].to_f32(f);
+#pragma unroll
+                for (int i = 0; i < VEC; ++i) v[i] += f[i];
+            }
+        }
+    }
+};
+template <typename T, int VEC>
+struct DxIn<T, VEC, 0> {
+    RawCols<float, VEC> r;
+    __device__ __forceinline__ void load(const float* dx, const int*, int, int) { r.load(dx); }
+    __device__ __forceinline__ void to_f32(float (&v)[VEC]) const { r.to_f32(v); }
+};
+
 // Most tokens per chunk: the chunk's dz and dp rows stay within 32 KB of LDS.
 template <int EMAX> struct ChunkMax {
     static constexpr int value = EMAX <= 16 ? 256 : (EMAX <= 32 ? 128 : 64);
@@ -131,11 +179,14 @@ __device__ __forceinline__ void read_dz(const float (*dzs)[EMAX], int t, float (
 //      acc[e, cols] += dz[t,e] x[t, cols];
 //   3. (DW) the four waves' partials are added in wave order through LDS and
 //      written to the chunk's slot of `partial`.
-template <typename T, int EMAX, bool DW>
+//   (KJ > 0: the chunk's dxe row indices are formed with dz in step 1 and
+//   the first round's loads follow it)
+template <typename T, int EMAX, bool DW, int KJ>
 __global__ __launch_bounds__(256) void route_bwd_kernel(
     const T* __restrict__ x, const T* __restrict__ wr, const float* __restrict__ probs,
     const int32_t* __restrict__ idx, const int32_t* __restrict__ slot,
-    const float* __restrict__ dgate, float* __restrict__ dx, float* __restrict__ partial, int Ng,
+    const float* __restrict__ dgate, float* __restrict__ dx, float* __restrict__ partial,
+    const T* __restrict__ dxe, const int32_t* __restrict__ row_base, long long gc, int Ng,
     int d, int E, int k, int tch, int nch) {
     constexpr int VEC = ColsPerLane<EMAX>::value;
     constexpr int COLS = 64 * VEC;
@@ -147,6 +198,8 @@ __global__ __launch_bounds__(256) void route_bwd_kernel(
     __shared__ __attribute__((aligned(16)))
     float lds[2 * DZ_FLOATS > RED_FLOATS ? 2 * DZ_FLOATS : RED_FLOATS];
     __shared__ float pdp_s[CH];
+    __shared__ int rows_s[KJ > 0 ? CH : 1][KJ > 0 ? KJ : 1];  // dxe rows, -1 = not kept
+    __shared__ int rb_s[KJ > 0 ? EMAX : 1];                  // row_base[g, :]
     float (*dzs)[EMAX] = reinterpret_cast<float (*)[EMAX]>(lds);
     const int c = blockIdx.x, g = blockIdx.z;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -166,14 +219,16 @@ __global__ __launch_bounds__(256) void route_bwd_kernel(
         for (int v = 0; v < VEC; ++v) w[e][v] = (e < E && live) ? w[e][v] : 0.0f;
     }
     using RX = RawCols<T, VEC>;
-    using RD = RawCols<float, VEC>;
+    using RD = DxIn<T, VEC, KJ>;
     // (token indices clamp to the chunk, so a wave past its last token reloads it)
     auto load_round = [&](int r0, RX (&xv)[U], RD (&dv)[U]) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const size_t t = tok0 + min(r0 + 4 * u, ntok - 1);
+            const int tl = min(r0 + 4 * u, ntok - 1);
+            const size_t t = tok0 + tl;
             if constexpr (DW) xv[u].load(x + t * d + ic);
-            dv[u].load(dx + t * d + ic);
+            if constexpr (KJ > 0) dv[u].load(dxe, &rows_s[tl][0], d, ic);
+            else dv[u].load(dx + t * d + ic, nullptr, d, ic);
         }
     };
     RX xa[U], xb[U];
@@ -204,16 +259,25 @@ __global__ __launch_bounds__(256) void route_bwd_kernel(
     };
     fetch_assign(0);
     fetch_probs(0);
-    load_round(wave, xa, da);
+    if constexpr (KJ == 0) load_round(wave, xa, da);
     float (*dps)[EMAX] = reinterpret_cast<float (*)[EMAX]>(lds + DZ_FLOATS);
     for (int q = tid; q < ntok * EMAX; q += 256) dps[q / EMAX][q % EMAX] = __builtin_nanf("");
+    if constexpr (KJ > 0) {
+        for (int q = tid; q < ntok * KJ; q += 256) rows_s[q / KJ][q % KJ] = -1;
+        if (tid < E) rb_s[tid] = row_base[static_cast<size_t>(g) * E + tid];
+    }
     lds_barrier();
     for (int b0 = 0; b0 < na; b0 += kBatch * 256) {
         if (b0 > 0) fetch_assign(b0);
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {
             const int q = b0 + u * 256 + tid;
-            if (q < na && sl[u] >= 0) dps[q / k][ex[u]] = gv[u];
+            if (q < na && sl[u] >= 0) {
+                dps[q / k][ex[u]] = gv[u];
+                // row(t, j) = e G C + row_base[g, e] + slot (k <= KJ)
+                if constexpr (KJ > 0)
+                    rows_s[q / k][q % k] = static_cast<int>(ex[u] * gc + rb_s[ex[u]] + sl[u]);
+            }
         }
     }
     for (int b0 = 0; b0 < np; b0 += kProbBatch * 256) {
@@ -242,6 +306,7 @@ __global__ __launch_bounds__(256) void route_bwd_kernel(
         dzs[t][e] = e >= E ? 0.0f : (dp == dp ? p * (dp - pdp) : -p * pdp);
     }
     lds_barrier();
+    if constexpr (KJ > 0) load_round(wave, xa, da);
 
     // 2. stream the chunk's tokens
     float acc[DW ? EMAX : 1][VEC];
@@ -363,34 +428,66 @@ ChunkPlan plan(const Dims& D) {
     return ChunkPlan{tch, D.Ng > 0 ? static_cast<int>(cdiv(D.Ng, tch)) : 0};
 }
 
-template <typename T, int EMAX>
-void launch_main(const Dims& D, const ChunkPlan& P, const void* x, const void* wr,
-                 const float* probs, const int32_t* idx, const int32_t* slot, const float* dgate,
-                 float* dx, float* partial, hipStream_t st) {
+// Inputs of one launch of the main kernel (dxe, row_base, gc: fused only).
+struct BwdArgs {
+    const void *x, *wr;
+    const float* probs;
+    const int32_t *idx, *slot;
+    const float* dgate;
+    float *dx, *partial;
+    const void* dxe;
+    const int32_t* row_base;
+};
+
+template <typename T, int EMAX, int KJ>
+void launch_main(const Dims& D, const ChunkPlan& P, const BwdArgs& a, hipStream_t st) {
     constexpr int COLS = 64 * ColsPerLane<EMAX>::value;
     const dim3 grid(P.nch, cdiv(D.d, COLS), D.G);
-    if (partial)
-        route_bwd_kernel<T, EMAX, true><<<grid, 256, 0, st>>>(
-            static_cast<const T*>(x), static_cast<const T*>(wr), probs, idx, slot, dgate, dx,
-            partial, D.Ng, D.d, D.E, D.k, P.tch, P.nch);
-    else
-        route_bwd_kernel<T, EMAX, false><<<grid, 256, 0, st>>>(
-            static_cast<const T*>(x), static_cast<const T*>(wr), probs, idx, slot, dgate, dx,
-            nullptr, D.Ng, D.d, D.E, D.k, P.tch, P.nch);
+    const long long gc = static_cast<long long>(D.G) * D.C;
+    auto go = [&](auto kern) {
+        kern<<<grid, 256, 0, st>>>(static_cast<const T*>(a.x), static_cast<const T*>(a.wr),
+                                   a.probs, a.idx, a.slot, a.dgate, a.dx, a.partial,
+                                   static_cast<const T*>(a.dxe), a.row_base, gc, D.Ng, D.d, D.E,
+                                   D.k, P.tch, P.nch);
+    };
+    if (a.partial) go(route_bwd_kernel<T, EMAX, true, KJ>);
+    else go(route_bwd_kernel<T, EMAX, false, KJ>);
 }
 
-template <typename T>
-void launch_main_e(const Dims& D, const ChunkPlan& P, const void* x, const void* wr,
-                   const float* probs, const int32_t* idx, const int32_t* slot,
-                   const float* dgate, float* dx, float* partial, hipStream_t st) {
-    if (D.E <= 8)
-        launch_main<T, 8>(D, P, x, wr, probs, idx, slot, dgate, dx, partial, st);
-    else if (D.E <= 16)
-        launch_main<T, 16>(D, P, x, wr, probs, idx, slot, dgate, dx, partial, st);
-    else if (D.E <= 32)
-        launch_main<T, 32>(D, P, x, wr, probs, idx, slot, dgate, dx, partial, st);
-    else
-        launch_main<T, 64>(D, P, x, wr, probs, idx, slot, dgate, dx, partial, st);
+template <typename T, int KJ>
+void launch_main_e(const Dims& D, const ChunkPlan& P, const BwdArgs& a, hipStream_t st) {
+    if (D.E <= 8) launch_main<T, 8, KJ>(D, P, a, st);
+    else if (D.E <= 16) launch_main<T, 16, KJ>(D, P, a, st);
+    else if (D.E <= 32) launch_main<T, 32, KJ>(D, P, a, st);
+    else launch_main<T, 64, KJ>(D, P, a, st);
+}
+
+template <int KJ>
+void launch_main_t(const Dims& D, const ChunkPlan& P, const BwdArgs& a, hipStream_t st) {
+    if (D.dtype == VMOE_BF16) launch_main_e<uint16_t, KJ>(D, P, a, st);
+    else launch_main_e<float, KJ>(D, P, a, st);
+}
+
+// The main kernel (fused: KJ = 2 or 4) and the reduction of the partials.
+vmoe_status run_route_bwd(const Dims& D, BwdArgs a, float* dwr, void* ws, int kj,
+                          hipStream_t st) {
+    const ChunkPlan P = plan(D);
+    const long long total = static_cast<long long>(D.G) * D.E * D.d;
+    if (D.N == 0) {
+        // no tokens: the router gradient is zero (written by the reducer, nch = 0)
+        if (dwr && total > 0)
+            route_bwd_reduce_kernel<<<cdiv(total, 32), 256, 0, st>>>(nullptr, dwr, D.E, D.d, 0,
+                                                                      total);
+        return launch_status();
+    }
+    a.partial = dwr ? static_cast<float*>(ws) : nullptr;
+    if (kj == 0) launch_main_t<0>(D, P, a, st);
+    else if (kj == 2) launch_main_t<2>(D, P, a, st);
+    else launch_main_t<4>(D, P, a, st);
+    if (dwr)
+        route_bwd_reduce_kernel<<<cdiv(total, 32), 256, 0, st>>>(a.partial, dwr, D.E, D.d,
+                                                                  P.nch, total);
+    return launch_status();
 }
 
 }  // namespace
@@ -404,24 +501,27 @@ size_t route_bwd_workspace_bytes(const Dims& D) {
 vmoe_status route_bwd_launch(const Dims& D, const void* x, const void* wr, const float* probs,
                              const int32_t* idx, const int32_t* slot, const float* dgate,
                              float* dx, float* dwr, void* ws, hipStream_t st) {
-    const ChunkPlan P = plan(D);
-    const long long total = static_cast<long long>(D.G) * D.E * D.d;
-    if (D.N == 0) {
-        // no tokens: the router gradient is zero (written by the reducer, nch = 0)
-        if (dwr && total > 0)
-            route_bwd_reduce_kernel<<<cdiv(total, 32), 256, 0, st>>>(nullptr, dwr, D.E, D.d, 0,
-                                                                      total);
-        return launch_status();
+    const BwdArgs a{x, wr, probs, idx, slot, dgate, dx, nullptr, nullptr, nullptr};
+    return run_route_bwd(D, a, dwr, ws, 0, st);
+}
+
+vmoe_status dispatch_route_bwd_launch(const Dims& D, const void* dxe, const int32_t* row_base,
+                                      const void* x, const void* wr, const float* probs,
+                                      const int32_t* idx, const int32_t* slot,
+                                      const float* dgate, float* dx, float* dwr, void* ws,
+                                      hipStream_t st) {
+    // the gathered rows are indexed in int and kept in LDS for k <= 4, and
+    // a lane gathers at least two columns per row only for E <= 16 (with one,
+    // the 2-byte gathers measured slower than the separate dispatch pass);
+    // otherwise the two passes run one after the other (same result)
+    const long long rows = static_cast<long long>(D.E) * D.G * D.C;
+    if (D.k > 4 || D.E > 16 || rows >= (1ll << 31) || D.N == 0) {
+        const vmoe_status s = dispatch_bwd_launch(D, dxe, idx, slot, row_base, dx, st);
+        if (s != VMOE_OK) return s;
+        return route_bwd_launch(D, x, wr, probs, idx, slot, dgate, dx, dwr, ws, st);
     }
-    float* partial = dwr ? static_cast<float*>(ws) : nullptr;
-    if (D.dtype == VMOE_BF16)
-        launch_main_e<uint16_t>(D, P, x, wr, probs, idx, slot, dgate, dx, partial, st);
-    else
-        launch_main_e<float>(D, P, x, wr, probs, idx, slot, dgate, dx, partial, st);
-    if (dwr)
-        route_bwd_reduce_kernel<<<cdiv(total, 32), 256, 0, st>>>(partial, dwr, D.E, D.d, P.nch,
-                                                                  total);
-    return launch_status();
+    const BwdArgs a{x, wr, probs, idx, slot, dgate, dx, nullptr, dxe, row_base};
+    return run_route_bwd(D, a, dwr, ws, D.k <= 2 ? 2 : 4, st);
 }
 
 }  // namespace vmoe

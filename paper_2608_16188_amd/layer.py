@@ -108,13 +108,20 @@ class LayerBuffers:
         V.vmoe_combine_fwd(s, self.ye, self.expert_idx, self.slot, self.row_base, self.gate,
                            self.y, stream)
 
-    def backward(self, stream=None):
+    def backward(self, stream=None, fused: bool = True):
+        """fused: dispatch and router backward in one call (bit-identical to
+        vmoe_dispatch_bwd followed by vmoe_route_bwd, which fused=False runs)."""
         s = self.shape
         V.vmoe_combine_bwd(s, self.dy, self.ye, self.expert_idx, self.slot, self.row_base,
                            self.gate, self.dye, self.dgate, stream)
         V.vmoe_expert_ffn_bwd(s, self.xe, self.counts, self.w1, self.w2, self.a, self.a_grad,
                               self.dye, self.dh, self.dxe, self.dw1, self.db1, self.dw2, self.db2,
                               stream)
+        if fused:
+            V.vmoe_dispatch_route_bwd(s, self.dxe, self.row_base, self.x, self.w_router,
+                                      self.probs, self.expert_idx, self.slot, self.dgate, self.dx,
+                                      self.dw_router, self.route_bwd_ws, stream)
+            return
         V.vmoe_dispatch_bwd(s, self.dxe, self.expert_idx, self.slot, self.row_base, self.dx,
                             stream)
         V.vmoe_route_bwd(s, self.x, self.w_router, self.probs, self.expert_idx, self.slot,

@@ -69,6 +69,7 @@ def _load():
         "vmoe_expert_ffn_bwd": [S] + [P] * 14,
         "vmoe_dispatch_bwd": [S] + [P] * 6,
         "vmoe_route_bwd": [S] + [P] * 9 + [ctypes.c_size_t, P],
+        "vmoe_dispatch_route_bwd": [S] + [P] * 11 + [ctypes.c_size_t, P],
     }
     for name, args in sigs.items():
         f = getattr(lib, name)
@@ -167,6 +168,15 @@ def vmoe_dispatch_bwd(shape, dxe, expert_idx, slot, row_base, dx, stream=None):
     _check("vmoe_dispatch_bwd", _lib.vmoe_dispatch_bwd(
         ctypes.byref(shape), _ptr(dxe), _ptr(expert_idx), _ptr(slot), _ptr(row_base), _ptr(dx),
         _stream(stream)))
+
+
+def vmoe_dispatch_route_bwd(shape, dxe, row_base, x, w_router, probs, expert_idx, slot, dgate,
+                            dx, dw_router, workspace, stream=None):
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check("vmoe_dispatch_route_bwd", _lib.vmoe_dispatch_route_bwd(
+        ctypes.byref(shape), _ptr(dxe), _ptr(row_base), _ptr(x), _ptr(w_router), _ptr(probs),
+        _ptr(expert_idx), _ptr(slot), _ptr(dgate), _ptr(dx), _ptr(dw_router), _ptr(workspace),
+        ws_bytes, _stream(stream)))
 
 
 def vmoe_route_bwd(shape, x, w_router, probs, expert_idx, slot, dgate, dx, dw_router, workspace,

@@ -17,7 +17,7 @@ FAKE = 0x10000  # 16-byte aligned, never dereferenced: validation fails first
 
 def test_every_declared_symbol_is_exported():
     declared = V.header_symbols()
-    assert len(declared) == 13, declared
+    assert len(declared) == 14, declared
     out = subprocess.check_output(["nm", "-D", "--defined-only", V.LIB_PATH], text=True)
     exported = {line.split()[-1] for line in out.splitlines() if line.strip()}
     missing = [s for s in declared if s not in exported]
@@ -102,6 +102,11 @@ def test_null_and_misaligned_pointers_rejected():
     # route_bwd: missing probs
     assert L.vmoe_route_bwd(b, FAKE, FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30,
                             None) == V.VMOE_ERR_INVALID_ARG
+    # dispatch + route backward: missing dxe, then a misaligned row_base
+    assert L.vmoe_dispatch_route_bwd(b, None, *([FAKE] * 10), 1 << 30, None) == \
+        V.VMOE_ERR_INVALID_ARG
+    assert L.vmoe_dispatch_route_bwd(b, FAKE, FAKE + 4, *([FAKE] * 9), 1 << 30, None) == \
+        V.VMOE_ERR_INVALID_ARG
 
 
 def test_workspace_too_small_rejected():
@@ -117,6 +122,8 @@ def test_workspace_too_small_rejected():
     need_b = V.vmoe_route_bwd_workspace_bytes(s)
     assert need_b > 0
     assert V._lib.vmoe_route_bwd(b, *([FAKE] * 8), FAKE, need_b - 1, None) == \
+        V.VMOE_ERR_WORKSPACE
+    assert V._lib.vmoe_dispatch_route_bwd(b, *([FAKE] * 10), FAKE, need_b - 1, None) == \
         V.VMOE_ERR_WORKSPACE
 
 

@@ -316,6 +316,32 @@ def test_layer_full_size_sampled(name):
             assert_close(f"{nm}[e={e}]", gotv[sl], refv[sl], tol)
 
 
+FUSED_CASES = [c.name for c in SMALL] + ["vitb16_bf16", "vitl16_384_bf16"]
+
+
+@pytest.mark.parametrize("name", FUSED_CASES)
+def test_dispatch_route_bwd_matches_two_calls(name):
+    """The fused dispatch + router backward is bit-identical to the two calls
+    (k <= 4 gathers in the router kernel; larger k runs the two passes)."""
+    cfg = next((c for c in SMALL if c.name == name), None) or W.CONFIGS[name]
+    say("dispatch+route bwd", name)
+    inp = W.make_inputs(cfg)
+    L = LayerBuffers(cfg, inp)
+    L.forward()
+    L.backward(fused=False)
+    torch.cuda.synchronize()
+    dx2 = L.dx.clone()
+    dw2 = None if L.dw_router is None else L.dw_router.clone()
+    L.dx.fill_(float("nan"))
+    if dw2 is not None:
+        L.dw_router.fill_(float("nan"))
+    L.backward(fused=True)
+    torch.cuda.synchronize()
+    assert torch.equal(L.dx.view(torch.int32), dx2.view(torch.int32)), "dx differs"
+    if dw2 is not None:
+        assert torch.equal(L.dw_router.view(torch.int32), dw2.view(torch.int32)), "dW_r differs"
+
+
 def test_route_bwd_full_size_per_call():
     """Router backward alone at the ViT-L/16 size, fed the oracle's routing."""
     cfg, inp = workload_inputs("vitl16_384_bf16", with_experts=False)

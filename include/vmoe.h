@@ -209,6 +209,41 @@ vmoe_status vmoe_dispatch_route_bwd(const vmoe_shape* shape, const void* dxe,
                                     float* dw_router, void* workspace, size_t workspace_bytes,
                                     void* stream);
 
+/* ---------------------------------------------------------------------------
+ * Cross-task expert grouping (paper Sec. 3.2.1). HOST routines: every pointer
+ * below is host memory, nothing runs on the GPU.
+ * ------------------------------------------------------------------------- */
+
+/* Temporary DRAM of one expert: M_tmp = B_p (theta1 T d_k + theta2 T^2) + m_f
+ * bytes for T = tokens routed to it (m_c, the compute-dependent buffers, plus
+ * m_f, the profiled per-call overhead). Evaluated as written, left to right. */
+double vmoe_expert_mtmp(int64_t tokens, int32_t d_k, double bytes_per_elem, double theta1,
+                        double theta2, double m_f);
+
+/* Host scratch bytes for vmoe_group_experts (0 on invalid arguments). */
+size_t vmoe_group_experts_workspace_bytes(int32_t n, double mem_budget, double mem_static,
+                                          double unit_bytes);
+
+/* Ordered time slices of n experts under a DRAM budget: slice s is the 0/1
+ * knapsack optimum over the experts not in slices 0..s-1, with weight
+ * w_i = ceil(mtmp[i] / unit_bytes), value v_i = mtmp[i] / mem_budget -
+ * eta * lifespan[i], capacity floor((mem_budget - mem_static) / unit_bytes),
+ * by dp[i][j] = max(dp[i-1][j], dp[i-1][j - w_i] + v_i) over the remaining
+ * experts in index order (an expert enters only if strictly better; the set
+ * is read back from full capacity). A slice with no gain takes the remaining
+ * expert of shortest lifespan (lower index on ties), so every expert is placed.
+ *   mtmp, lifespan [n] f64 (>= 0)   in
+ *   slice_of       [n] i32          out: slice of each expert, 0-based
+ *   n_slices       i32              out
+ *   workspace      host memory of vmoe_group_experts_workspace_bytes(...)
+ * VMOE_ERR_INVALID_ARG: n outside [0, 65536], unit_bytes <= 0, mem_budget <=
+ * mem_static, a capacity above 2^24 units, a negative input, or an expert
+ * whose weight alone exceeds the capacity; VMOE_ERR_WORKSPACE: too small. */
+vmoe_status vmoe_group_experts(int32_t n, const double* mtmp, const double* lifespan,
+                               double mem_budget, double mem_static, double eta,
+                               double unit_bytes, int32_t* slice_of, int32_t* n_slices,
+                               void* workspace, size_t workspace_bytes);
+
 #ifdef __cplusplus
 }
 #endif

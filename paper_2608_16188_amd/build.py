@@ -3,8 +3,9 @@
     python -m paper_2608_16188_amd.build
 
 Each source compiles on its own (in parallel) into _build/, then links into
-paper_2608_16188_amd/libvmoe.so. route.hip is compiled without floating-point
-contraction: its gate arithmetic is specified operation by operation.
+paper_2608_16188_amd/libvmoe.so. route.hip and grouping.cpp (host code) are
+compiled without floating-point contraction: their arithmetic is specified
+operation by operation.
 """
 from __future__ import annotations
 
@@ -19,10 +20,10 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libvmoe.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = ["abi.hip", "route.hip", "moves.hip", "ffn.hip", "route_bwd.hip"]
+SOURCES = ["abi.hip", "route.hip", "moves.hip", "ffn.hip", "route_bwd.hip", "grouping.cpp"]
 COMMON = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
-PER_FILE = {"route.hip": ["-ffp-contract=off"]}
+PER_FILE = {"route.hip": ["-ffp-contract=off"], "grouping.cpp": ["-ffp-contract=off"]}
 
 
 def build(verbose: bool = False) -> str:
@@ -30,7 +31,7 @@ def build(verbose: bool = False) -> str:
     procs = []
     objs = []
     for src in SOURCES:
-        obj = os.path.join(BUILD, src.replace(".hip", ".o"))
+        obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
         cmd = [HIPCC, *COMMON, *PER_FILE.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
         if verbose:
             print(" ".join(cmd), flush=True)

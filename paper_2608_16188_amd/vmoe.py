@@ -75,6 +75,13 @@ def _load():
         f = getattr(lib, name)
         f.restype = ctypes.c_int32
         f.argtypes = args
+    D = ctypes.c_double
+    lib.vmoe_expert_mtmp.restype = D
+    lib.vmoe_expert_mtmp.argtypes = [ctypes.c_int64, ctypes.c_int32, D, D, D, D]
+    lib.vmoe_group_experts_workspace_bytes.restype = ctypes.c_size_t
+    lib.vmoe_group_experts_workspace_bytes.argtypes = [ctypes.c_int32, D, D, D]
+    lib.vmoe_group_experts.restype = ctypes.c_int32
+    lib.vmoe_group_experts.argtypes = [ctypes.c_int32, P, P, D, D, D, D, P, P, P, ctypes.c_size_t]
     return lib
 
 
@@ -185,3 +192,31 @@ def vmoe_route_bwd(shape, x, w_router, probs, expert_idx, slot, dgate, dx, dw_ro
     _check("vmoe_route_bwd", _lib.vmoe_route_bwd(
         ctypes.byref(shape), _ptr(x), _ptr(w_router), _ptr(probs), _ptr(expert_idx), _ptr(slot),
         _ptr(dgate), _ptr(dx), _ptr(dw_router), _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+# ---------------------------------------------------- expert grouping (host)
+
+def vmoe_expert_mtmp(tokens, d_k, bytes_per_elem, theta1, theta2, m_f) -> float:
+    """Temporary DRAM estimate of one expert, bytes (host)."""
+    return _lib.vmoe_expert_mtmp(int(tokens), int(d_k), float(bytes_per_elem), float(theta1),
+                                 float(theta2), float(m_f))
+
+
+def vmoe_group_experts(mtmp, lifespan, mem_budget, mem_static, eta, unit_bytes):
+    """Ordered time slices of the experts (host arrays in, numpy out):
+    returns (slice_of int32 [n], n_slices)."""
+    import numpy as np
+    m = np.ascontiguousarray(mtmp, dtype=np.float64)
+    r = np.ascontiguousarray(lifespan, dtype=np.float64)
+    n = int(m.size)
+    if r.size != n:
+        raise ValueError("mtmp and lifespan differ in length")
+    ws_bytes = _lib.vmoe_group_experts_workspace_bytes(n, float(mem_budget), float(mem_static),
+                                                       float(unit_bytes))
+    ws = np.empty(max(ws_bytes, 8), dtype=np.uint8)
+    out = np.empty(max(n, 1), dtype=np.int32)
+    ns = ctypes.c_int32(0)
+    _check("vmoe_group_experts", _lib.vmoe_group_experts(
+        n, m.ctypes.data, r.ctypes.data, float(mem_budget), float(mem_static), float(eta),
+        float(unit_bytes), out.ctypes.data, ctypes.addressof(ns), ws.ctypes.data, ws_bytes))
+    return out[:n], int(ns.value)

@@ -127,3 +127,74 @@ def test_mtmp_estimator_scaling():
     # bytes scale with the element width B_p
     assert OG.expert_mtmp(50, 64, 4.0, 3.0, 1.0, 0.0) == 2 * OG.expert_mtmp(50, 64, 2.0, 3.0,
                                                                             1.0, 0.0)
+
+
+# ------------------------------------------- the library's host routine
+
+def _lib():
+    from paper_2608_16188_amd import vmoe as V
+    return V
+
+
+def test_library_matches_oracle():
+    V = _lib()
+    rng = random.Random(4)
+    for trial in range(300):
+        n = rng.randint(0, 40)
+        mt, life = _random_instance(rng, n)
+        unit = rng.choice([MB, MB // 4, 3 * MB])
+        budget, static = rng.randint(60, 200) * MB, rng.randint(0, 20) * MB
+        eta = rng.choice([0.0, 1e-3, 1e-2, 0.05, 1.0])
+        try:
+            ref = OG.group_experts(mt, life, budget, static, eta, unit)
+        except ValueError:
+            with pytest.raises(V.VmoeError):
+                V.vmoe_group_experts(mt, life, budget, static, eta, unit)
+            continue
+        so, ns = V.vmoe_group_experts(mt, life, budget, static, eta, unit)
+        assert (list(so), ns) == ref, f"trial {trial}"
+
+
+def test_library_hand_worked_example():
+    V = _lib()
+    h = _hand()
+    mt = [u * h["unit_bytes"] for u in h["mtmp_units"]]
+    so, ns = V.vmoe_group_experts(mt, h["lifespan"], h["mem_budget"], h["mem_static"], h["eta"],
+                                  h["unit_bytes"])
+    assert (list(so), ns) == (h["slice_of"], h["n_slices"])
+    fb = h["fallback_case"]
+    mt = [u * h["unit_bytes"] for u in fb["mtmp_units"]]
+    so, ns = V.vmoe_group_experts(mt, fb["lifespan"], h["mem_budget"], h["mem_static"], fb["eta"],
+                                  h["unit_bytes"])
+    assert (list(so), ns) == (fb["slice_of"], fb["n_slices"])
+
+
+def test_library_errors():
+    import ctypes
+    import numpy as np
+    V = _lib()
+    with pytest.raises(V.VmoeError):          # an expert alone over the budget
+        V.vmoe_group_experts([5 * MB, 11 * MB], [1, 1], 12 * MB, 2 * MB, 0.0, MB)
+    with pytest.raises(V.VmoeError):          # no room
+        V.vmoe_group_experts([MB], [1], 2 * MB, 2 * MB, 0.0, MB)
+    with pytest.raises(V.VmoeError):          # negative lifespan
+        V.vmoe_group_experts([MB], [-1.0], 8 * MB, 0, 0.0, MB)
+    need = V._lib.vmoe_group_experts_workspace_bytes(2, 8.0 * MB, 0.0, float(MB))
+    assert need > 0
+    m = np.array([MB, MB], np.float64)
+    ws = np.empty(need, np.uint8)
+    out = np.empty(2, np.int32)
+    ns = ctypes.c_int32(0)
+    assert V._lib.vmoe_group_experts(2, m.ctypes.data, m.ctypes.data, 8.0 * MB, 0.0, 0.0,
+                                     float(MB), out.ctypes.data, ctypes.addressof(ns),
+                                     ws.ctypes.data, need - 1) == V.VMOE_ERR_WORKSPACE
+    assert V._lib.vmoe_group_experts_workspace_bytes(2, 1.0, 2.0, 1.0) == 0
+
+
+def test_library_mtmp_matches_oracle():
+    V = _lib()
+    rng = random.Random(5)
+    for _ in range(200):
+        args = (rng.randint(0, 100000), rng.choice([32, 64, 768, 1024]), rng.choice([1.0, 2.0, 4.0]),
+                rng.uniform(0, 8), rng.uniform(0, 2), rng.uniform(0, 1e7))
+        assert V.vmoe_expert_mtmp(*args) == OG.expert_mtmp(*args)

@@ -12,6 +12,8 @@
 // token's kept expert rows of dxe, summed in j order (the dispatch backward's
 // sum, so the result is bit-identical to the two calls in sequence), instead
 // of reading dx: two f32 passes over dx and a launch fewer.
+#include <type_traits>
+
 #include "common.h"
 
 namespace vmoe {
@@ -168,6 +170,103 @@ __device__ __forceinline__ void read_dz(const float (*dzs)[EMAX], int t, float (
     }
 }
 
+// Step 1 of a chunk: dz[t][e] = p (dp - <p, dp>) for its ntok tokens into
+// dzs (row stride LD floats; columns E..EMAX-1 are zero), with dps (same
+// shape) as scratch for dp (NaN where the expert was not kept) and pdp_s for
+// <p, dp>; with KJ > 0 also the dxe row of each kept assignment into rows_s
+// [tokens][KJ] (-1 = not kept; row_base[g] staged in rb_s). The first batch
+// of inputs (assignments and probability rows, clamped indices, no
+// branches) is requested before `issue()` runs the caller's first streaming
+// loads, so waiting for it leaves those in flight; the barriers wait for
+// LDS traffic only.
+template <int EMAX, int LD, int KJ, typename Issue>
+__device__ __forceinline__ void form_dz(float* dzs, float* dps, float* pdp_s, int* rows_s,
+                                        int* rb_s, const float* __restrict__ probs,
+                                        const int32_t* __restrict__ idx,
+                                        const int32_t* __restrict__ slot,
+                                        const float* __restrict__ dgate,
+                                        const int32_t* __restrict__ row_base, size_t tok0,
+                                        int ntok, int E, int k, int g, long long gc,
+                                        Issue issue) {
+    const int tid = threadIdx.x;
+    const int na = ntok * k, np = ntok * E;
+    const size_t q0 = tok0 * k, p0 = tok0 * E;
+    int sl[kBatch], ex[kBatch];
+    float gv[kBatch], pv[kProbBatch];
+    auto fetch_assign = [&](int b0) {
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            const size_t q = q0 + min(b0 + u * 256 + tid, na - 1);
+            sl[u] = slot[q];
+            ex[u] = idx[q];
+            gv[u] = dgate[q];
+        }
+    };
+    // the chunk's probability rows are one contiguous run of ntok * E floats
+    auto fetch_probs = [&](int b0) {
+#pragma unroll
+        for (int u = 0; u < kProbBatch; ++u) pv[u] = probs[p0 + min(b0 + u * 256 + tid, np - 1)];
+    };
+    fetch_assign(0);
+    fetch_probs(0);
+    issue();
+    for (int q = tid; q < ntok * EMAX; q += 256) dps[(q / EMAX) * LD + q % EMAX] = __builtin_nanf("");
+    if constexpr (KJ > 0) {
+        for (int q = tid; q < ntok * KJ; q += 256) rows_s[q] = -1;
+        if (tid < E) rb_s[tid] = row_base[static_cast<size_t>(g) * E + tid];
+    }
+    lds_barrier();
+    for (int b0 = 0; b0 < na; b0 += kBatch * 256) {
+        if (b0 > 0) fetch_assign(b0);
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            const int q = b0 + u * 256 + tid;
+            if (q < na && sl[u] >= 0) {
+                dps[(q / k) * LD + ex[u]] = gv[u];
+                // row(t, j) = e G C + row_base[g, e] + slot (k <= KJ)
+                if constexpr (KJ > 0)
+                    rows_s[(q / k) * KJ + q % k] =
+                        static_cast<int>(ex[u] * gc + rb_s[ex[u]] + sl[u]);
+            }
+        }
+    }
+    for (int b0 = 0; b0 < np; b0 += kProbBatch * 256) {
+        if (b0 > 0) fetch_probs(b0);
+#pragma unroll
+        for (int u = 0; u < kProbBatch; ++u) {
+            const int q = b0 + u * 256 + tid;
+            if (q < np) dzs[(q / E) * LD + q % E] = pv[u];  // columns E..EMAX set below
+        }
+    }
+    lds_barrier();
+    if (tid < ntok) {
+        // <p, dp> over the kept experts, e ascending (eight entries read at a
+        // time; dp is NaN at every column not kept, E..EMAX included)
+        float pdp = 0.0f;
+        for (int e0 = 0; e0 < E; e0 += 8) {
+            float dpv[8], pv8[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const int e = min(e0 + u, EMAX - 1);
+                dpv[u] = dps[tid * LD + e];
+                pv8[u] = dzs[tid * LD + e];
+            }
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                if (e0 + u < E && dpv[u] == dpv[u]) pdp = __builtin_fmaf(pv8[u], dpv[u], pdp);
+        }
+        pdp_s[tid] = pdp;
+    }
+    lds_barrier();
+    for (int q = tid; q < ntok * EMAX; q += 256) {
+        const int t = q / EMAX, e = q % EMAX;
+        const float p = dzs[t * LD + e], dp = dps[t * LD + e], pdp = pdp_s[t];
+        // kept: p (dgate - <p, dp>); other experts: -p <p, dp>
+        dzs[t * LD + e] = e >= E ? 0.0f : (dp == dp ? p * (dp - pdp) : -p * pdp);
+    }
+    lds_barrier();
+}
+
 // Block = a chunk of tch tokens of group g (blockIdx.x, .z) times 64 * VEC
 // columns (blockIdx.y), four waves; wave w takes the chunk's tokens w, w + 4,
 // ..., with the x and dx rows of U tokens in flight.
@@ -234,78 +333,13 @@ __global__ __launch_bounds__(256) void route_bwd_kernel(
     RX xa[U], xb[U];
     RD da[U], db[U];
 
-    // 1. dz of the chunk. The first batch of its inputs (assignments and
-    // probability rows, clamped indices, no branches) is requested before the
-    // first round of x and dx rows, so waiting for it leaves those in flight;
-    // the barriers of this phase wait for LDS only. dps holds dp, NaN where
-    // the expert was not kept.
-    const int na = ntok * k, np = ntok * E;
-    const size_t q0 = tok0 * k, p0 = tok0 * E;
-    int sl[kBatch], ex[kBatch];
-    float gv[kBatch], pv[kProbBatch];
-    auto fetch_assign = [&](int b0) {
-#pragma unroll
-        for (int u = 0; u < kBatch; ++u) {
-            const size_t q = q0 + min(b0 + u * 256 + tid, na - 1);
-            sl[u] = slot[q];
-            ex[u] = idx[q];
-            gv[u] = dgate[q];
-        }
-    };
-    // the chunk's probability rows are one contiguous run of ntok * E floats
-    auto fetch_probs = [&](int b0) {
-#pragma unroll
-        for (int u = 0; u < kProbBatch; ++u) pv[u] = probs[p0 + min(b0 + u * 256 + tid, np - 1)];
-    };
-    fetch_assign(0);
-    fetch_probs(0);
-    if constexpr (KJ == 0) load_round(wave, xa, da);
-    float (*dps)[EMAX] = reinterpret_cast<float (*)[EMAX]>(lds + DZ_FLOATS);
-    for (int q = tid; q < ntok * EMAX; q += 256) dps[q / EMAX][q % EMAX] = __builtin_nanf("");
-    if constexpr (KJ > 0) {
-        for (int q = tid; q < ntok * KJ; q += 256) rows_s[q / KJ][q % KJ] = -1;
-        if (tid < E) rb_s[tid] = row_base[static_cast<size_t>(g) * E + tid];
-    }
-    lds_barrier();
-    for (int b0 = 0; b0 < na; b0 += kBatch * 256) {
-        if (b0 > 0) fetch_assign(b0);
-#pragma unroll
-        for (int u = 0; u < kBatch; ++u) {
-            const int q = b0 + u * 256 + tid;
-            if (q < na && sl[u] >= 0) {
-                dps[q / k][ex[u]] = gv[u];
-                // row(t, j) = e G C + row_base[g, e] + slot (k <= KJ)
-                if constexpr (KJ > 0)
-                    rows_s[q / k][q % k] = static_cast<int>(ex[u] * gc + rb_s[ex[u]] + sl[u]);
-            }
-        }
-    }
-    for (int b0 = 0; b0 < np; b0 += kProbBatch * 256) {
-        if (b0 > 0) fetch_probs(b0);
-#pragma unroll
-        for (int u = 0; u < kProbBatch; ++u) {
-            const int q = b0 + u * 256 + tid;
-            if (q < np) dzs[q / E][q % E] = pv[u];  // columns E..EMAX are never read
-        }
-    }
-    lds_barrier();
-    if (tid < ntok) {
-        // <p, dp> over the kept experts, e ascending
-        float pdp = 0.0f;
-        for (int e = 0; e < E; ++e) {
-            const float dp = dps[tid][e];
-            if (dp == dp) pdp = __builtin_fmaf(dzs[tid][e], dp, pdp);
-        }
-        pdp_s[tid] = pdp;
-    }
-    lds_barrier();
-    for (int q = tid; q < ntok * EMAX; q += 256) {
-        const int t = q / EMAX, e = q % EMAX;
-        const float p = dzs[t][e], dp = dps[t][e], pdp = pdp_s[t];
-        // kept: p (dgate - <p, dp>); other experts: -p <p, dp>
-        dzs[t][e] = e >= E ? 0.0f : (dp == dp ? p * (dp - pdp) : -p * pdp);
-    }
-    lds_barrier();
+    // 1. dz of the chunk; the first round of x and dx rows is issued behind
+    // the first batch of routing inputs (fused: after the dxe rows are known)
+    float* dps = lds + DZ_FLOATS;
+    form_dz<EMAX, EMAX, KJ>(lds, dps, pdp_s, &rows_s[0][0], rb_s, probs, idx, slot, dgate,
+                            row_base, tok0, ntok, E, k, g, gc, [&] {
+                                if constexpr (KJ == 0) load_round(wave, xa, da);
+                            });
     if constexpr (KJ > 0) load_round(wave, xa, da);
 
     // 2. stream the chunk's tokens
@@ -381,6 +415,206 @@ __global__ __launch_bounds__(256) void route_bwd_kernel(
     }
 }
 
+// ---------------------------------------------------------------- E > 16
+//
+// With many experts the two products of a chunk are small GEMMs of f32
+// operands, dx[t, c] += sum_e dz[t, e] W[e, c] (k = E) and
+// P[e, c] = sum_t dz[t, e] x[t, c] (k = the chunk's tokens), and run on the
+// f32 matrix cores (v_mfma_f32_32x32x2_f32: products and sums in f32). Block
+// = kMfmaTok tokens x kMfmaCols columns of one group, four waves: wave w
+// computes dx for tokens [32 w, 32 w + 32) over all the block's columns and
+// P for columns [32 w, 32 w + 32) over all experts, so no wave waits for
+// another. W[:, cols] (as f32) and x[tokens, cols] are staged in LDS with
+// rows padded so the two rows a fragment reads fall on different banks; dz
+// rows have an odd stride, so a column of dz is read without conflicts.
+typedef float f32x16_m __attribute__((ext_vector_type(16)));
+constexpr int kMfmaTok = 128, kMfmaCols = 128;
+constexpr int kXLd = kMfmaCols + 32;  // bf16 per staged x row
+constexpr int kWLd = kMfmaCols + 16;  // f32 per staged W row
+
+// KJ > 0 (fused with the dispatch backward): dx starts from the token's kept
+// dxe rows, summed in j order from 0, instead of from dx.
+template <int EMAX, bool DW, int KJ>
+__global__ __launch_bounds__(256) void route_bwd_mfma_kernel(
+    const uint16_t* __restrict__ x, const uint16_t* __restrict__ wr,
+    const float* __restrict__ probs, const int32_t* __restrict__ idx,
+    const int32_t* __restrict__ slot, const float* __restrict__ dgate, float* __restrict__ dx,
+    float* __restrict__ partial, const uint16_t* __restrict__ dxe,
+    const int32_t* __restrict__ row_base, long long gc, int Ng, int d, int E, int k, int nch) {
+    constexpr int LD = EMAX + 1, TCH = kMfmaTok, COLS = kMfmaCols;
+    constexpr int XV = TCH * COLS / 8 / 256;    // 16-byte x vectors per thread
+    constexpr int WV = EMAX * COLS / 8 / 256;   // 16-byte W vectors per thread
+    constexpr int DPS = TCH * LD > TCH * kXLd / 2 ? TCH * LD : TCH * kXLd / 2;
+    __shared__ __attribute__((aligned(16))) float dzs[TCH * LD];
+    __shared__ __attribute__((aligned(16))) float xdp[DPS];  // dp while forming dz, then x
+    __shared__ __attribute__((aligned(16))) float ws[EMAX * kWLd];
+    __shared__ float pdp_s[TCH];
+    __shared__ int rows_s[KJ > 0 ? TCH * KJ : 1];  // dxe rows, -1 = not kept
+    __shared__ int rb_s[KJ > 0 ? EMAX : 1];        // row_base[g, :]
+    const int c = blockIdx.x, g = blockIdx.z;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int t0 = c * TCH;
+    const int ntok = min(TCH, Ng - t0);
+    const size_t tok0 = static_cast<size_t>(g) * Ng + t0;
+    const int c0 = blockIdx.y * COLS;
+    const uint16_t* wg = wr + static_cast<size_t>(g) * E * d;
+
+    // x and W tiles: 16-byte vectors, zero past the chunk, the experts or d
+    uint4 xv[XV], wv[WV];
+    auto issue = [&] {
+#pragma unroll
+        for (int u = 0; u < XV; ++u) {
+            const int q = u * 256 + tid, r = q / (COLS / 8), col = c0 + (q % (COLS / 8)) * 8;
+            xv[u] = (r < ntok && col < d)
+                        ? *reinterpret_cast<const uint4*>(x + (tok0 + r) * d + col)
+                        : make_uint4(0u, 0u, 0u, 0u);
+        }
+#pragma unroll
+        for (int u = 0; u < WV; ++u) {
+            const int q = u * 256 + tid, e = q / (COLS / 8), col = c0 + (q % (COLS / 8)) * 8;
+            wv[u] = (e < E && col < d)
+                        ? *reinterpret_cast<const uint4*>(wg + static_cast<size_t>(e) * d + col)
+                        : make_uint4(0u, 0u, 0u, 0u);
+        }
+    };
+    for (int q = ntok * LD + tid; q < TCH * LD; q += 256) dzs[q] = 0.0f;  // rows past the chunk
+    form_dz<EMAX, LD, KJ>(dzs, xdp, pdp_s, rows_s, rb_s, probs, idx, slot, dgate, row_base,
+                          tok0, ntok, E, k, g, gc, issue);
+    // dp is no longer needed: its space takes the x tile
+    uint16_t* xs = reinterpret_cast<uint16_t*>(xdp);
+#pragma unroll
+    for (int u = 0; u < XV; ++u) {
+        const int q = u * 256 + tid, r = q / (COLS / 8), v = q % (COLS / 8);
+        *reinterpret_cast<uint4*>(xs + r * kXLd + v * 8) = xv[u];
+    }
+#pragma unroll
+    for (int u = 0; u < WV; ++u) {
+        const int q = u * 256 + tid, e = q / (COLS / 8), v = q % (COLS / 8);
+        const uint32_t h[4] = {wv[u].x, wv[u].y, wv[u].z, wv[u].w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            ws[e * kWLd + v * 8 + 2 * i] = bf16_to_f32(static_cast<uint16_t>(h[i] & 0xFFFFu));
+            ws[e * kWLd + v * 8 + 2 * i + 1] = bf16_to_f32(static_cast<uint16_t>(h[i] >> 16));
+        }
+    }
+    lds_barrier();
+
+    const int m = lane & 31, kh = lane >> 5;
+    // The products are formed transposed (dx^T = W^T dz^T, P^T = x^T dz), so
+    // register 4 q + r of lane l holds output column 8 q + 4 (l / 32) + r of
+    // the 32 x 32 block and token (or expert) l % 32: four consecutive
+    // columns, one 16-byte access.
+    const int tl = 32 * wave + m;               // this lane's token in the chunk
+    const size_t trow = (tok0 + min(tl, ntok - 1)) * d;
+    // the incoming dx first (its latency hides behind the products): dx
+    // itself, or (fused) the kept dxe rows, 8 bytes of each per access
+    float4 din[4][4];
+    if constexpr (KJ == 0) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int col = c0 + 32 * j + 8 * q + 4 * kh;  // d is a multiple of 8
+                din[j][q] = col < d ? *reinterpret_cast<const float4*>(dx + trow + col)
+                                    : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+            }
+    } else {
+        int rr[KJ];
+#pragma unroll
+        for (int jj = 0; jj < KJ; ++jj) rr[jj] = rows_s[min(tl, ntok - 1) * KJ + jj];
+        uint2 h[KJ][4][4];
+#pragma unroll
+        for (int jj = 0; jj < KJ; ++jj)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int col = min(c0 + 32 * j + 8 * q + 4 * kh, d - 4);
+                    h[jj][j][q] = *reinterpret_cast<const uint2*>(
+                        dxe + static_cast<size_t>(rr[jj] >= 0 ? rr[jj] : 0) * d + col);
+                }
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                float v[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+                for (int jj = 0; jj < KJ; ++jj) {
+                    if (rr[jj] < 0) continue;
+                    v[0] += bf16_to_f32(static_cast<uint16_t>(h[jj][j][q].x & 0xFFFFu));
+                    v[1] += bf16_to_f32(static_cast<uint16_t>(h[jj][j][q].x >> 16));
+                    v[2] += bf16_to_f32(static_cast<uint16_t>(h[jj][j][q].y & 0xFFFFu));
+                    v[3] += bf16_to_f32(static_cast<uint16_t>(h[jj][j][q].y >> 16));
+                }
+                din[j][q] = make_float4(v[0], v[1], v[2], v[3]);
+            }
+    }
+    f32x16_m acc[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc[j][i] = 0.0f;
+    // A[col m][e = 2 s + kh] = W, B[e][token m] = dz
+#pragma unroll 4
+    for (int s2 = 0; s2 < EMAX / 2; ++s2) {
+        const float b = dzs[(32 * wave + m) * LD + 2 * s2 + kh];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            acc[j] = __builtin_amdgcn_mfma_f32_32x32x2f32(ws[(2 * s2 + kh) * kWLd + 32 * j + m], b,
+                                                          acc[j], 0, 0, 0);
+    }
+    if (tl < ntok) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int col = c0 + 32 * j + 8 * q + 4 * kh;
+                if (col < d)
+                    *reinterpret_cast<float4*>(dx + trow + col) =
+                        make_float4(din[j][q].x + acc[j][4 * q], din[j][q].y + acc[j][4 * q + 1],
+                                    din[j][q].z + acc[j][4 * q + 2],
+                                    din[j][q].w + acc[j][4 * q + 3]);
+            }
+    }
+
+    if constexpr (DW) {
+        // P[e][col] over the chunk's tokens: A[e m][token 2 s + kh] = dz,
+        // B[token][col m] = x (columns 32 w .. 32 w + 31 of the block)
+        constexpr int MB = EMAX / 32;
+        f32x16_m pacc[MB];
+#pragma unroll
+        for (int b = 0; b < MB; ++b)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) pacc[b][i] = 0.0f;
+        const int nks = (ntok + 1) / 2;
+        // A[col m][token 2 s + kh] = x, B[token][expert m] = dz
+#pragma unroll 4
+        for (int s2 = 0; s2 < nks; ++s2) {
+            const int t = 2 * s2 + kh;
+            const float ax = bf16_to_f32(xs[t * kXLd + 32 * wave + m]);
+#pragma unroll
+            for (int b = 0; b < MB; ++b)
+                pacc[b] = __builtin_amdgcn_mfma_f32_32x32x2f32(ax, dzs[t * LD + 32 * b + m],
+                                                               pacc[b], 0, 0, 0);
+        }
+        float* pg = partial + (static_cast<size_t>(g) * nch + c) * E * d;
+#pragma unroll
+        for (int b = 0; b < MB; ++b) {
+            const int e = 32 * b + m;
+            if (e < E) {
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int col = c0 + 32 * wave + 8 * q + 4 * kh;
+                    if (col < d)
+                        *reinterpret_cast<float4*>(pg + static_cast<size_t>(e) * d + col) =
+                            make_float4(pacc[b][4 * q], pacc[b][4 * q + 1], pacc[b][4 * q + 2],
+                                        pacc[b][4 * q + 3]);
+                }
+            }
+        }
+    }
+}
+
 // dW_r = sum over chunks of the partials. A block owns 32 outputs; 8 lane
 // groups each add every 8th chunk (coalesced 128-byte rows), then the 8
 // partial sums are added in a fixed order.
@@ -412,6 +646,9 @@ struct ChunkPlan {
 };
 
 ChunkPlan plan(const Dims& D) {
+    // bf16 with E > 16: the matrix-core kernel's fixed chunk
+    if (D.dtype == VMOE_BF16 && D.E > 16)
+        return ChunkPlan{kMfmaTok, D.Ng > 0 ? static_cast<int>(cdiv(D.Ng, kMfmaTok)) : 0};
     // about 1024 blocks over (chunks, column blocks, groups)
     const int cols = 64 * (D.E <= 8    ? ColsPerLane<8>::value
                            : D.E <= 16 ? ColsPerLane<16>::value
@@ -441,6 +678,20 @@ struct BwdArgs {
 
 template <typename T, int EMAX, int KJ>
 void launch_main(const Dims& D, const ChunkPlan& P, const BwdArgs& a, hipStream_t st) {
+    if constexpr (std::is_same<T, uint16_t>::value && EMAX >= 32) {
+        const dim3 grid(P.nch, cdiv(D.d, kMfmaCols), D.G);
+        const long long gc = static_cast<long long>(D.G) * D.C;
+        auto go = [&](auto kern) {
+            kern<<<grid, 256, 0, st>>>(static_cast<const uint16_t*>(a.x),
+                                       static_cast<const uint16_t*>(a.wr), a.probs, a.idx, a.slot,
+                                       a.dgate, a.dx, a.partial,
+                                       static_cast<const uint16_t*>(a.dxe), a.row_base, gc, D.Ng,
+                                       D.d, D.E, D.k, P.nch);
+        };
+        if (a.partial) go(route_bwd_mfma_kernel<EMAX, true, KJ>);
+        else go(route_bwd_mfma_kernel<EMAX, false, KJ>);
+        return;
+    }
     constexpr int COLS = 64 * ColsPerLane<EMAX>::value;
     const dim3 grid(P.nch, cdiv(D.d, COLS), D.G);
     const long long gc = static_cast<long long>(D.G) * D.C;
@@ -510,12 +761,13 @@ vmoe_status dispatch_route_bwd_launch(const Dims& D, const void* dxe, const int3
                                       const int32_t* idx, const int32_t* slot,
                                       const float* dgate, float* dx, float* dwr, void* ws,
                                       hipStream_t st) {
-    // the gathered rows are indexed in int and kept in LDS for k <= 4, and
-    // a lane gathers at least two columns per row only for E <= 16 (with one,
-    // the 2-byte gathers measured slower than the separate dispatch pass);
-    // otherwise the two passes run one after the other (same result)
+    // the gathered rows are indexed in int and kept in LDS for k <= 4, and a
+    // lane gathers at least two columns per row (E <= 16, or the matrix-core
+    // kernel of bf16 layers with more experts; f32 with E > 16 would gather
+    // one column per lane, which measured slower than the separate dispatch
+    // pass); otherwise the two passes run one after the other (same result)
     const long long rows = static_cast<long long>(D.E) * D.G * D.C;
-    if (D.k > 4 || D.E > 16 || rows >= (1ll << 31) || D.N == 0) {
+    if (D.k > 4 || (D.E > 16 && D.dtype != VMOE_BF16) || rows >= (1ll << 31) || D.N == 0) {
         const vmoe_status s = dispatch_bwd_launch(D, dxe, idx, slot, row_base, dx, st);
         if (s != VMOE_OK) return s;
         return route_bwd_launch(D, x, wr, probs, idx, slot, dgate, dx, dwr, ws, st);

@@ -19,6 +19,8 @@
 //                    carry + rank, kept while slot < C
 // This file must be compiled with -ffp-contract=off: the gate's float
 // arithmetic is specified operation by operation.
+#include <type_traits>
+
 #include "common.h"
 
 namespace vmoe {
@@ -147,51 +149,16 @@ __device__ __forceinline__ void gate_token(float* z, size_t t, const float* __re
     keys[t] = priority_key(__fdiv_rn(exp_spec(z[first] - m), s));
 }
 
-// The same gate with one lane per expert: the tokens of a block in groups of
-// L = next power of two >= E lanes (L divides 64, so a group never straddles a
-// wave and every lane of a group follows the same path). Every element is
-// computed by the same operations as in gate_token: the maximum is exact in
-// any order, the sum runs e = 0..E-1 through lane broadcasts, and the top-k
-// butterflies keep the larger value, then the lower expert.
-__device__ __forceinline__ void gate_lanes(const float* zrow, size_t t, int sub, int L,
-                                           const float* __restrict__ bias,
-                                           const float* __restrict__ noise,
-                                           float* __restrict__ probs, int32_t* __restrict__ idx,
-                                           uint32_t* __restrict__ keys, int E, int k) {
-    const bool real = sub < E;
-    float v = real ? zrow[sub] : 0.0f;
-    if (real && bias) v = v + bias[sub];
-    if (real && noise) v = v + noise[t * E + sub];
-    float m = real ? v : -__builtin_inff();
-    for (int o = L >> 1; o > 0; o >>= 1) {
-        const float u = __shfl_xor(m, o, L);
-        m = u > m ? u : m;
-    }
-    const float q = real ? exp_spec(v - m) : 0.0f;
-    float s = 0.0f;
-    for (int e = 0; e < E; ++e) s = s + __shfl(q, e, L);
-    const float p = __fdiv_rn(q, s);
-    if (real) probs[t * E + sub] = p;
-    bool taken = !real;
-    for (int j = 0; j < k; ++j) {
-        // candidate (valid, value, expert); the better one has the larger
-        // value, then the lower expert
-        int ok = taken ? 0 : 1, be = sub;
-        float bv = v;
-        for (int o = L >> 1; o > 0; o >>= 1) {
-            const int ok2 = __shfl_xor(ok, o, L), be2 = __shfl_xor(be, o, L);
-            const float bv2 = __shfl_xor(bv, o, L);
-            const bool better = ok2 && (!ok || bv2 > bv || (bv2 == bv && be2 < be));
-            ok = better ? ok2 : ok;
-            be = better ? be2 : be;
-            bv = better ? bv2 : bv;
-        }
-        if (sub == be) {
-            taken = true;
-            idx[t * k + j] = be;
-            if (j == 0) keys[t] = priority_key(p);
-        }
-    }
+// The gate of a block's tokens, by the same operations in the same order as
+// gate_token, split so that no lane repeats another's work: per (token,
+// expert) pair the noisy logit, the exp term and the probability (lane e of a
+// group of L = next power of two >= E lanes); per token (one thread) the
+// maximum, the top-k scan and, once the terms are in, their sum in expert
+// order. A token's row is read into EMAX >= E registers (independent reads).
+template <int EMAX>
+__device__ __forceinline__ void row_to_regs(const float* row, float (&r)[EMAX]) {
+#pragma unroll
+    for (int e = 0; e < EMAX; ++e) r[e] = row[e];  // entries past E are never used
 }
 
 // ---------------------------------------------------------------- bf16: MFMA
@@ -201,10 +168,22 @@ __device__ __forceinline__ void gate_lanes(const float* zrow, size_t t, int sub,
 // d range split in four contiguous quarters, one per wave, whose partial
 // products are added in wave order; A and B fragments are 16-byte loads of
 // x rows and W_r rows straight from memory (both k-contiguous), eight k-steps
-// in flight. Then one thread per token runs the gate.
+// in flight. Then the gate, in phases that meet at LDS-only barriers: per
+// (token, expert) pair the noisy logit, per token the maximum and top-k, per
+// pair the exp terms, per token their sum and the priority key, per pair the
+// probabilities — each element by gate_token's operations in its order.
 typedef __bf16 bf16x8_r __attribute__((ext_vector_type(8)));
 typedef float f32x16_r __attribute__((ext_vector_type(16)));
 constexpr int kMfmaTokens = 32;
+
+// Barrier for data exchanged through LDS only: waits for this wave's LDS
+// accesses (lgkmcnt(0)), not for its global stores.
+__device__ __forceinline__ void lds_barrier() {
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    __builtin_amdgcn_s_barrier();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
 
 template <bool WIDE>
 __global__ __launch_bounds__(256) void router_mfma_kernel(
@@ -270,22 +249,88 @@ __global__ __launch_bounds__(256) void router_mfma_kernel(
             }
     }
     __syncthreads();
-    for (int q = tid; q < ntok * E; q += 256) {
-        const int t = q / E, e = q % E;
-        float v;
-        if (logits_in) {
-            v = logits[(tok0 + t) * E + e];
-        } else {
-            v = ((red[0][t][e] + red[1][t][e]) + red[2][t][e]) + red[3][t][e];
-            logits[(tok0 + t) * E + e] = v;
+    // pairs (token t, expert e): lane e of a group of L lanes, 256 / L tokens a pass
+    int lsh = 0;
+    while ((1 << lsh) < E) ++lsh;
+    const int sub = tid & ((1 << lsh) - 1), tg = tid >> lsh, tp = 256 >> lsh;
+    __shared__ float m_s[kMfmaTokens], s_s[kMfmaTokens];
+    __shared__ int first_s[kMfmaTokens];
+    // 1. the logit (the four waves' partials in wave order, or the input),
+    //    then the noisy logit z = (logit + bias) + noise in place of wave 1's partial
+    for (int t = tg; t < ntok; t += tp) {
+        if (sub < E) {
+            float v;
+            if (logits_in) {
+                v = logits[(tok0 + t) * E + sub];
+            } else {
+                v = ((red[0][t][sub] + red[1][t][sub]) + red[2][t][sub]) + red[3][t][sub];
+                logits[(tok0 + t) * E + sub] = v;
+            }
+            if (bias) v = v + bias[sub];
+            if (noise) v = v + noise[(tok0 + t) * E + sub];
+            red[1][t][sub] = v;
         }
-        red[1][t][e] = v;  // staged in wave 1's slot, no reader of it remains
     }
-    __syncthreads();
-    int L = 1;
-    while (L < E) L <<= 1;
-    for (int t = tid / L; t < ntok; t += 256 / L)
-        gate_lanes(&red[1][t][0], tok0 + t, tid % L, L, bias, noise, probs, idx, keys, E, k);
+    lds_barrier();
+    // 2. per token: the maximum and the top-k choices (larger z, then lower expert)
+    auto choose = [&](auto emax) {
+        constexpr int EM = decltype(emax)::value;
+        float z[EM];
+        row_to_regs<EM>(&red[1][tid][0], z);
+        float m = z[0];
+#pragma unroll
+        for (int e = 1; e < EM; ++e)
+            if (e < E) m = z[e] > m ? z[e] : m;
+        uint64_t taken = 0;
+        for (int j = 0; j < k; ++j) {
+            int best = -1;
+            float bz = 0.0f;
+#pragma unroll
+            for (int e = 0; e < EM; ++e) {
+                if (e < E && !((taken >> e) & 1ull) && (best < 0 || z[e] > bz)) {
+                    best = e;
+                    bz = z[e];
+                }
+            }
+            taken |= 1ull << best;
+            idx[(tok0 + tid) * k + j] = best;
+            if (j == 0) first_s[tid] = best;
+        }
+        m_s[tid] = m;
+    };
+    if (tid < ntok) {
+        if (E <= 8) choose(std::integral_constant<int, 8>{});
+        else if (E <= 16) choose(std::integral_constant<int, 16>{});
+        else if (E <= 32 || !WIDE) choose(std::integral_constant<int, 32>{});
+        else choose(std::integral_constant<int, 64>{});
+    }
+    lds_barrier();
+    // 3. the exp terms q = exp(z - m), in place of wave 2's partial
+    for (int t = tg; t < ntok; t += tp)
+        if (sub < E) red[2][t][sub] = exp_spec(red[1][t][sub] - m_s[t]);
+    lds_barrier();
+    // 4. per token: s = sum of the terms in expert order; the priority key
+    auto total = [&](auto emax) {
+        constexpr int EM = decltype(emax)::value;
+        float q[EM];
+        row_to_regs<EM>(&red[2][tid][0], q);
+        float sum = 0.0f;
+#pragma unroll
+        for (int e = 0; e < EM; ++e)
+            if (e < E) sum = sum + q[e];
+        s_s[tid] = sum;
+        keys[tok0 + tid] = priority_key(__fdiv_rn(red[2][tid][first_s[tid]], sum));
+    };
+    if (tid < ntok) {
+        if (E <= 8) total(std::integral_constant<int, 8>{});
+        else if (E <= 16) total(std::integral_constant<int, 16>{});
+        else if (E <= 32 || !WIDE) total(std::integral_constant<int, 32>{});
+        else total(std::integral_constant<int, 64>{});
+    }
+    lds_barrier();
+    // 5. the probabilities p = q / s (IEEE division)
+    for (int t = tg; t < ntok; t += tp)
+        if (sub < E) probs[(tok0 + t) * E + sub] = __fdiv_rn(red[2][t][sub], s_s[t]);
 }
 
 // ------------------------------------------------------------ f32: f64 sums
@@ -628,15 +673,6 @@ constexpr int kLocalAssign = 16384;
 constexpr int kTokBits = 13;  // token index inside a group < 2^13
 static_assert(kLocalTokens <= (1 << kTokBits), "token index field");
 static_assert(kKeyBits - kBinBits + kTokBits <= 32, "bin member = low key bits + token");
-
-// Barrier for data exchanged through LDS only: waits for this wave's LDS
-// accesses (lgkmcnt(0)), not for its global stores.
-__device__ __forceinline__ void lds_barrier() {
-    __atomic_signal_fence(__ATOMIC_SEQ_CST);
-    __builtin_amdgcn_s_waitcnt(0xC07F);
-    __builtin_amdgcn_s_barrier();
-    __atomic_signal_fence(__ATOMIC_SEQ_CST);
-}
 
 // NW > 0 (E <= 2 NW <= 16): slots from a block scan of per-thread expert
 // counts packed two 16-bit fields to a word; NW == 0: ballot tiles.

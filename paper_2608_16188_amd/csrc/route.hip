@@ -471,10 +471,16 @@ __global__ __launch_bounds__(1024) void bin_scan_kernel(const uint32_t* __restri
     for (int b = threadIdx.x; b < kNumBins; b += 1024) hist[b] = 0;
     const uint32_t* kg = keys + static_cast<size_t>(g) * Ng;
     uint32_t lo = 0xFFFFFFFFu, hi = 0u;
-    for (int t = threadIdx.x; t < Ng; t += 1024) {
-        const uint32_t key = kg[t];
-        lo = min(lo, key);
-        hi = max(hi, key);
+    // eight keys per thread in flight at a time (clamped indices, repeats are harmless)
+    for (int b0 = 0; b0 < Ng; b0 += 8 * 1024) {
+        uint32_t v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = kg[min(b0 + u * 1024 + static_cast<int>(threadIdx.x), Ng - 1)];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            lo = min(lo, v[u]);
+            hi = max(hi, v[u]);
+        }
     }
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) {
@@ -500,7 +506,14 @@ __global__ __launch_bounds__(1024) void bin_scan_kernel(const uint32_t* __restri
     }
     __syncthreads();
     const BinMap bm = map;
-    for (int t = threadIdx.x; t < Ng; t += 1024) atomicAdd(&hist[bm(kg[t])], 1);
+    for (int b0 = 0; b0 < Ng; b0 += 8 * 1024) {
+        uint32_t v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = kg[min(b0 + u * 1024 + static_cast<int>(threadIdx.x), Ng - 1)];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            if (b0 + u * 1024 + static_cast<int>(threadIdx.x) < Ng) atomicAdd(&hist[bm(v[u])], 1);
+    }
     __syncthreads();
     constexpr int per = kNumBins / 1024;
     int local[per];
@@ -580,22 +593,30 @@ __global__ __launch_bounds__(1024) void chunk_scan_kernel(
     int G, int E, int k, int C, int nch) {
     const int kE = k * E;
     const int lane = threadIdx.x & 63;
-    // one wave per (group, round, expert): exclusive scan over the chunks, 64 at a time
+    // one wave per (group, round, expert): exclusive scan over the chunks, 64 at
+    // a time, with the counts of up to four 64-chunk spans requested together
     for (int q = threadIdx.x >> 6; q < G * kE; q += 16) {
         const int g = q / kE, re = q % kE;
         int run = 0;
-        for (int c0 = 0; c0 < nch; c0 += 64) {
-            const int c = c0 + lane;
-            const size_t at = (static_cast<size_t>(g) * nch + c) * kE + re;
-            const int v = c < nch ? ccount[at] : 0;
-            int inc = v;
+        for (int c0 = 0; c0 < nch; c0 += 4 * 64) {
+            int v[4];
 #pragma unroll
-            for (int o = 1; o < 64; o <<= 1) {
-                const int u = __shfl_up(inc, o, 64);
-                if (lane >= o) inc += u;
+            for (int u = 0; u < 4; ++u) {
+                const int c = c0 + u * 64 + lane;
+                v[u] = c < nch ? ccount[(static_cast<size_t>(g) * nch + c) * kE + re] : 0;
             }
-            if (c < nch) cbase[at] = run + inc - v;
-            run += __shfl(inc, 63, 64);
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int c = c0 + u * 64 + lane;
+                int inc = v[u];
+#pragma unroll
+                for (int o = 1; o < 64; o <<= 1) {
+                    const int w = __shfl_up(inc, o, 64);
+                    if (lane >= o) inc += w;
+                }
+                if (c < nch) cbase[(static_cast<size_t>(g) * nch + c) * kE + re] = run + inc - v[u];
+                run += __shfl(inc, 63, 64);
+            }
         }
         if (lane == 0) demand[q] = run;
     }

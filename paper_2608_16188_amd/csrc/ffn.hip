@@ -831,11 +831,38 @@ void gemm_bf16_kernel(GemmBatch batch) {
 
 // ------------------------------------------------------------------ f32 FMA path
 
-constexpr int FT = 64, FK = 16;
+// f32 activations: 64 x 64 output tiles, four waves, each a 32 x 32 block on
+// v_mfma_f32_32x32x2_f32 (f32 products and sums); FK-deep k stages staged in
+// LDS as [k][mn] (rows padded by one float), read so that consecutive
+// threads load consecutive addresses whatever the operand's layout.
+constexpr int FT = 64, FK = 32;
+typedef float f32x16_f __attribute__((ext_vector_type(16)));
 
 template <bool KMAJOR>
 __device__ __forceinline__ float f32_elem(const float* base, int ld, int mn, int k) {
     return KMAJOR ? base[static_cast<size_t>(mn) * ld + k] : base[static_cast<size_t>(k) * ld + mn];
+}
+
+// One FK x FT operand stage into S[k][mn] (zero outside the operand): k-major
+// operands are walked k fastest, mn-major ones mn fastest.
+template <bool KMAJOR>
+__device__ __forceinline__ void stage_f32(float (*S)[FT + 1], const float* base, int ld, int mn0,
+                                          int mn_lim, int k0, int k_lim) {
+    constexpr int PER = FK * FT / 256;
+    float v[PER];
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+        const int q = u * 256 + static_cast<int>(threadIdx.x);
+        const int kk = KMAJOR ? q % FK : q / FT, mn = KMAJOR ? q / FK : q % FT;
+        v[u] = (mn0 + mn < mn_lim && k0 + kk < k_lim) ? f32_elem<KMAJOR>(base, ld, mn0 + mn, k0 + kk)
+                                                      : 0.0f;
+    }
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+        const int q = u * 256 + static_cast<int>(threadIdx.x);
+        const int kk = KMAJOR ? q % FK : q / FT, mn = KMAJOR ? q / FK : q % FT;
+        S[kk][mn] = v[u];
+    }
 }
 
 template <bool A_KMAJOR, bool B_KMAJOR, int EPI>
@@ -844,51 +871,46 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs p) {
     __shared__ float Bs[FK][FT + 1];
     const int e = blockIdx.z;
     const int ne = expert_rows(p.counts, p.G, p.E, e);
-    const int M = p.var_k ? p.M : ne;
+    const int M = p.var_k ? p.M : min(ne, p.M);
     const int K = p.var_k ? ne : p.K;
     const int N = p.N;
     const int m0 = blockIdx.y * FT, n0 = blockIdx.x * FT;
     if (m0 >= M) return;
     const float* A = static_cast<const float*>(p.a.base) + e * p.a.estride;
     const float* B = static_cast<const float*>(p.b.base) + e * p.b.estride;
-    const int tm = (threadIdx.x >> 4) * 4, tn = (threadIdx.x & 15) * 4;
-    float acc[4][4] = {};
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, wm = w >> 1, wn = w & 1;
+    const int r = lane & 31, kh = lane >> 5;
+    f32x16_f acc;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) acc[i] = 0.0f;
     for (int k0 = 0; k0 < K; k0 += FK) {
-        for (int q = threadIdx.x; q < FK * FT; q += 256) {
-            const int kk = q / FT, mn = q % FT;
-            As[kk][mn] = (m0 + mn < M && k0 + kk < K)
-                             ? f32_elem<A_KMAJOR>(A, p.a.ld, m0 + mn, k0 + kk) : 0.0f;
-            Bs[kk][mn] = (n0 + mn < N && k0 + kk < K)
-                             ? f32_elem<B_KMAJOR>(B, p.b.ld, n0 + mn, k0 + kk) : 0.0f;
-        }
+        stage_f32<A_KMAJOR>(As, A, p.a.ld, m0, M, k0, K);
+        stage_f32<B_KMAJOR>(Bs, B, p.b.ld, n0, N, k0, K);
         __syncthreads();
+        // A[m][k = 2 s + kh], B[k][n]: lane l supplies row / column l % 32
 #pragma unroll
-        for (int kk = 0; kk < FK; ++kk)
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    acc[i][j] = __builtin_fmaf(As[kk][tm + i], Bs[kk][tn + j], acc[i][j]);
+        for (int s2 = 0; s2 < FK / 2; ++s2)
+            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(As[2 * s2 + kh][32 * wm + r],
+                                                       Bs[2 * s2 + kh][32 * wn + r], acc, 0, 0, 0);
         __syncthreads();
     }
-    for (int i = 0; i < 4; ++i) {
-        const int m = m0 + tm + i;
-        if (m >= M) continue;
-        for (int j = 0; j < 4; ++j) {
-            const int n = n0 + tn + j;
-            if (n >= N) continue;
-            const size_t o = e * p.out_estride + static_cast<size_t>(m) * p.ldo + n;
-            float v = acc[i][j];
-            float* out = static_cast<float*>(p.out);
-            if (EPI == EPI_FWD1 || EPI == EPI_BIAS)
-                v += static_cast<const float*>(p.bias)[e * p.bias_estride + n];
-            if (EPI == EPI_GELU_GRAD) v *= static_cast<const float*>(p.aux)[o];
-            if (EPI == EPI_FWD1) {
-                out[o] = gelu_f(v);
-                static_cast<float*>(p.out2)[o] = gelu_grad_f(v);
-            } else {
-                out[o] = v;
-            }
+    // register i of lane l: row 8 (i / 4) + 4 (l / 32) + i % 4, column l % 32
+    const int n = n0 + 32 * wn + r;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+        const int m = m0 + 32 * wm + 8 * (i / 4) + 4 * kh + (i % 4);
+        if (m >= M || n >= N) continue;
+        const size_t o = e * p.out_estride + static_cast<size_t>(m) * p.ldo + n;
+        float v = acc[i];
+        float* out = static_cast<float*>(p.out);
+        if (EPI == EPI_FWD1 || EPI == EPI_BIAS)
+            v += static_cast<const float*>(p.bias)[e * p.bias_estride + n];
+        if (EPI == EPI_GELU_GRAD) v *= static_cast<const float*>(p.aux)[o];
+        if (EPI == EPI_FWD1) {
+            out[o] = gelu_f(v);
+            static_cast<float*>(p.out2)[o] = gelu_grad_f(v);
+        } else {
+            out[o] = v;
         }
     }
 }

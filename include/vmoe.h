@@ -43,7 +43,9 @@
  *   required pointer, N % G != 0, k outside [1, E], E > 64, d or f not a
  *   multiple of 8, a non-positive capacity factor, an unknown dtype or
  *   misaligned pointer -> VMOE_ERR_INVALID_ARG; a too-small workspace ->
- *   VMOE_ERR_WORKSPACE; a failed kernel launch -> VMOE_ERR_HIP. Nothing
+ *   VMOE_ERR_WORKSPACE; a failed kernel launch -> VMOE_ERR_HIP. Required
+ *   pointers are checked whatever the sizes: with N = 0 they still point to
+ *   an allocation (nothing is read from it). Nothing
  *   throws across the ABI. All entry points are thread-safe (stateless).
  */
 #ifndef VMOE_H

@@ -56,6 +56,9 @@ class LayerBuffers:
         self.x, self.w_router = up("x"), up("w_router")
         self.w1, self.b1, self.w2, self.b2 = up("w1"), up("b1"), up("w2"), up("b2")
         self.dy = up("dy")
+        if cfg.n_tokens == 0:  # an empty batch still hands over allocated rows
+            self.x = torch.zeros(1, d, dtype=act, device=dev)
+            self.dy = torch.zeros(1, d, dtype=act, device=dev)
         self.logit_bias = None if inputs.get("logit_bias") is None else \
             torch.from_numpy(inputs["logit_bias"]).to(dev)
         self.noise = None if inputs.get("noise") is None else \

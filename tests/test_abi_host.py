@@ -109,6 +109,21 @@ def test_null_and_misaligned_pointers_rejected():
         V.VMOE_ERR_INVALID_ARG
 
 
+def test_null_pointers_rejected_with_zero_tokens():
+    """An empty batch is a valid shape, but required pointers are still
+    checked: sizes never waive them."""
+    s = V.make_shape(0, 1, 64, 128, 8, 2, 1.0, 1)
+    assert V.vmoe_capacity(s) >= 1
+    b, L = ctypes.byref(s), V._lib
+    r = [FAKE] * 8
+    assert L.vmoe_route(b, None, FAKE, None, None, 0, *r, FAKE, 1 << 30, None) == \
+        V.VMOE_ERR_INVALID_ARG
+    assert L.vmoe_dispatch(b, None, FAKE, FAKE, FAKE, FAKE, None) == V.VMOE_ERR_INVALID_ARG
+    assert L.vmoe_combine_bwd(b, None, *([FAKE] * 6), FAKE, None) == V.VMOE_ERR_INVALID_ARG
+    assert L.vmoe_dispatch_route_bwd(b, *([FAKE] * 7), None, FAKE, FAKE, FAKE, 1 << 30,
+                                     None) == V.VMOE_ERR_INVALID_ARG
+
+
 def test_workspace_too_small_rejected():
     s = _shape()
     b = ctypes.byref(s)

@@ -170,6 +170,14 @@ SMALL = [
                     capacity_factor=2.0, router_std=0.3, noise_var=0.05),
     W.custom_config("f32_k3", n_tokens=150, d_model=48, d_ff=96, n_experts=6, k=3,
                     capacity_factor=0.9, dtype=W.F32, router_std=0.2),
+    # degenerate layers: one expert (a plain MLP on every token), every token
+    # on every expert, and a capacity of 2 that drops almost every assignment
+    W.custom_config("bf16_single_expert", n_tokens=128, d_model=64, d_ff=128, n_experts=1, k=1,
+                    capacity_factor=1.0, router_std=0.2),
+    W.custom_config("bf16_k_equals_e", n_tokens=96, d_model=64, d_ff=96, n_experts=4, k=4,
+                    capacity_factor=1.0, router_std=0.3),
+    W.custom_config("f32_capacity_two", n_tokens=200, d_model=32, d_ff=64, n_experts=4, k=2,
+                    capacity_factor=0.02, dtype=W.F32, router_std=0.2),
 ]
 
 
@@ -314,6 +322,23 @@ def test_layer_full_size_sampled(name):
         for q, nm in enumerate(["dW1", "dW2", "db1", "db2"]):
             sl = slice(q * ns, (q + 1) * ns)
             assert_close(f"{nm}[e={e}]", gotv[sl], refv[sl], tol)
+
+
+@pytest.mark.parametrize("dtype", [W.BF16, W.F32])
+def test_layer_empty_batch(dtype):
+    """No tokens: every call runs, the weight, bias and router gradients are
+    exactly zero (the closed form of an empty sum)."""
+    cfg = W.custom_config(f"empty_{dtype}", n_tokens=0, d_model=64, d_ff=128, n_experts=4, k=2,
+                          capacity_factor=1.0, dtype=dtype)
+    say("layer empty", dtype)
+    L = LayerBuffers(cfg, W.make_inputs(cfg))
+    for t in (L.dw1, L.db1, L.dw2, L.db2, L.dw_router):
+        t.fill_(float("nan"))
+    L.step()
+    torch.cuda.synchronize()
+    for name in ("dw1", "db1", "dw2", "db2", "dw_router"):
+        assert torch.all(getattr(L, name) == 0), name
+    assert int(L.counts.sum()) == 0
 
 
 FUSED_CASES = [c.name for c in SMALL] + ["vitb16_bf16", "vitl16_384_bf16"]

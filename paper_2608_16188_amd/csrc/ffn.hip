@@ -26,8 +26,9 @@
 // XCD's L2. The tile shape is chosen per launch by a cost model: rounds of
 // 256 CUs times the tile area, scaled by a per-shape efficiency.
 //
-// f32 path: a plain LDS-tiled FMA kernel with the same operand and epilogue
-// description (small widths; accuracy path).
+// f32 path: 64 x 64 tiles on the f32 matrix cores (v_mfma_f32_32x32x2f32, one
+// 32 x 32 block per wave) with coalesced operand staging through LDS and the
+// same operand and epilogue description (the accuracy path).
 #include <type_traits>
 
 #include "common.h"

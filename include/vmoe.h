@@ -211,6 +211,54 @@ vmoe_status vmoe_dispatch_route_bwd(const vmoe_shape* shape, const void* dxe,
                                     float* dw_router, void* workspace, size_t workspace_bytes,
                                     void* stream);
 
+/* vmoe_dispatch_route_bwd with an extra gradient with respect to the router
+ * logits added before the router products (chain rule: the logits also feed
+ * an auxiliary loss, e.g. the dlogits of vmoe_balance_loss):
+ *   dz[t,e] = probs[t,e] (dp[t,e] - <p, dp>) + dlogits[t,e]
+ *   dx, dw_router from that dz as in vmoe_dispatch_route_bwd.
+ * dlogits [N, E] f32 (required). Other arguments and workspace as there. */
+vmoe_status vmoe_dispatch_route_bwd_dlogits(const vmoe_shape* shape, const void* dxe,
+                                            const int32_t* row_base, const void* x,
+                                            const void* w_router, const float* probs,
+                                            const int32_t* expert_idx, const int32_t* slot,
+                                            const float* dgate, const float* dlogits, float* dx,
+                                            float* dw_router, void* workspace,
+                                            size_t workspace_bytes, void* stream);
+
+/* Bytes of scratch that vmoe_balance_loss needs (0 on an invalid shape). */
+size_t vmoe_balance_loss_workspace_bytes(const vmoe_shape* shape);
+
+/* Auxiliary balance losses on the gate, per routing group, and their gradient
+ * with respect to the router logits. The paper cites such losses (Sec. 1,
+ * Sec. 2.3) as the alternative to capacity limits without defining them;
+ * this is the published noisy top-k gating form:
+ *   importance[g,e] = sum over the group's tokens of probs[t,e]
+ *   load[g,e]       = sum over tokens of Phi((l[t,e] - thr[t,e]) / noise_std),
+ *                     l = logits + bias, thr = the k-th largest noisy logit
+ *                     z = (logits + bias) + noise among the OTHER experts
+ *                     (ties: lower index first; -inf if fewer than k): the
+ *                     chance that e stays in the top-k when only its own
+ *                     noise is drawn again (Phi: standard normal CDF)
+ *   losses[g,0|1]   = CV^2 = var / mean^2 over the experts of importance[g]
+ *                     and load[g] (population variance; 0 for a zero sum)
+ *   dlogits[t,e]    = d/dlogits of sum_g w_importance losses[g,0]
+ *                     + w_load losses[g,1]; pass it to
+ *                     vmoe_dispatch_route_bwd_dlogits
+ *   logits, probs   [N, E] f32   vmoe_route's outputs (z is rebuilt in f32
+ *                                 exactly as vmoe_route forms it)
+ *   logit_bias [E], noise [N, E] f32 or NULL, as given to vmoe_route
+ *   noise_std  > 0, the standard deviation the noise was drawn with
+ *   losses [G, 2], dlogits [N, E] f32 out; importance, load [G, E] f32 out
+ *   or NULL; workspace: vmoe_balance_loss_workspace_bytes(shape) bytes.
+ * Sums over tokens are f32 within a 256-token chunk and double across chunks
+ * in chunk order (deterministic); VMOE_ERR_INVALID_ARG for a non-positive or
+ * non-finite noise_std or non-finite weights. */
+vmoe_status vmoe_balance_loss(const vmoe_shape* shape, const float* logits,
+                              const float* logit_bias, const float* noise, const float* probs,
+                              float noise_std, float w_importance, float w_load, float* losses,
+                              float* importance, float* load, float* dlogits, void* workspace,
+                              size_t workspace_bytes, void* stream);
+
 /* ---------------------------------------------------------------------------
  * Cross-task expert grouping (paper Sec. 3.2.1). HOST routines: every pointer
  * below is host memory, nothing runs on the GPU.

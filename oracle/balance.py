@@ -140,10 +140,9 @@ def balance_loss(logits, k, n_groups, sigma, w_imp=1.0, w_load=1.0, bias=None, n
         dl[s] = pg * (c_imp[None, :] - (pg @ c_imp)[:, None])
         a = c_load[None, :] * dens[s]
         dl[s] += a
-        for t in range(s.start, s.stop):
-            for e in range(E):
-                if tgt[t, e] >= 0:
-                    dl[t, tgt[t, e]] -= a[t - s.start, e]
+        # the same amount leaves at each (t, e)'s threshold expert
+        tt, ee = np.nonzero(tgt[s] >= 0)
+        np.subtract.at(dl, (s.start + tt, tgt[s][tt, ee]), a[tt, ee])
     total = float((w_imp * losses[:, 0] + w_load * losses[:, 1]).sum())
     return dict(losses=losses, imp=imp, load=load, dlogits=dl, total=total)
 

@@ -20,7 +20,8 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libvmoe.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = ["abi.hip", "route.hip", "moves.hip", "ffn.hip", "route_bwd.hip", "grouping.cpp"]
+SOURCES = ["abi.hip", "route.hip", "moves.hip", "ffn.hip", "route_bwd.hip", "balance.hip",
+           "grouping.cpp"]
 COMMON = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 PER_FILE = {"route.hip": ["-ffp-contract=off"], "grouping.cpp": ["-ffp-contract=off"]}

@@ -32,12 +32,18 @@ vmoe_status ffn_bwd_launch(const Dims& D, const void* xe, const int32_t* counts,
                            hipStream_t st);
 vmoe_status route_bwd_launch(const Dims& D, const void* x, const void* wr, const float* probs,
                              const int32_t* idx, const int32_t* slot, const float* dgate,
-                             float* dx, float* dwr, void* ws, hipStream_t st);
+                             const float* dz_add, float* dx, float* dwr, void* ws,
+                             hipStream_t st);
 vmoe_status dispatch_route_bwd_launch(const Dims& D, const void* dxe, const int32_t* row_base,
                                       const void* x, const void* wr, const float* probs,
                                       const int32_t* idx, const int32_t* slot,
-                                      const float* dgate, float* dx, float* dwr, void* ws,
-                                      hipStream_t st);
+                                      const float* dgate, const float* dz_add, float* dx,
+                                      float* dwr, void* ws, hipStream_t st);
+size_t balance_workspace_bytes(const Dims& D);
+vmoe_status balance_launch(const Dims& D, const float* logits, const float* bias,
+                           const float* noise, const float* probs, float sigma, float w_imp,
+                           float w_load, float* losses, float* imp, float* load, float* dlogits,
+                           void* ws, hipStream_t st);
 
 vmoe_status make_dims(const vmoe_shape* s, Dims* out) {
     if (!s || !out) return VMOE_ERR_INVALID_ARG;
@@ -216,8 +222,8 @@ vmoe_status vmoe_route_bwd(const vmoe_shape* shape, const void* x, const void* w
                   dev(dgate) && dev(dx) && opt(dw_router)));
     const size_t need_ws = vmoe::route_bwd_workspace_bytes(D);
     if (workspace_bytes < need_ws || (need_ws > 0 && !dev(workspace))) return VMOE_ERR_WORKSPACE;
-    return vmoe::route_bwd_launch(D, x, w_router, probs, expert_idx, slot, dgate, dx, dw_router,
-                                  workspace, as_stream(stream));
+    return vmoe::route_bwd_launch(D, x, w_router, probs, expert_idx, slot, dgate, nullptr, dx,
+                                  dw_router, workspace, as_stream(stream));
 }
 
 vmoe_status vmoe_dispatch_route_bwd(const vmoe_shape* shape, const void* dxe,
@@ -233,7 +239,50 @@ vmoe_status vmoe_dispatch_route_bwd(const vmoe_shape* shape, const void* dxe,
     const size_t need_ws = vmoe::route_bwd_workspace_bytes(D);
     if (workspace_bytes < need_ws || (need_ws > 0 && !dev(workspace))) return VMOE_ERR_WORKSPACE;
     return vmoe::dispatch_route_bwd_launch(D, dxe, row_base, x, w_router, probs, expert_idx, slot,
-                                           dgate, dx, dw_router, workspace, as_stream(stream));
+                                           dgate, nullptr, dx, dw_router, workspace,
+                                           as_stream(stream));
+}
+
+vmoe_status vmoe_dispatch_route_bwd_dlogits(const vmoe_shape* shape, const void* dxe,
+                                            const int32_t* row_base, const void* x,
+                                            const void* w_router, const float* probs,
+                                            const int32_t* expert_idx, const int32_t* slot,
+                                            const float* dgate, const float* dlogits, float* dx,
+                                            float* dw_router, void* workspace,
+                                            size_t workspace_bytes, void* stream) {
+    Dims D;
+    VMOE_TRY(vmoe::make_dims(shape, &D));
+    VMOE_TRY(need(dev(dxe) && dev(row_base) && dev(x) && dev(w_router) && dev(probs) &&
+                  dev(expert_idx) && dev(slot) && dev(dgate) && dev(dlogits) && dev(dx) &&
+                  opt(dw_router)));
+    const size_t need_ws = vmoe::route_bwd_workspace_bytes(D);
+    if (workspace_bytes < need_ws || (need_ws > 0 && !dev(workspace))) return VMOE_ERR_WORKSPACE;
+    return vmoe::dispatch_route_bwd_launch(D, dxe, row_base, x, w_router, probs, expert_idx, slot,
+                                           dgate, dlogits, dx, dw_router, workspace,
+                                           as_stream(stream));
+}
+
+size_t vmoe_balance_loss_workspace_bytes(const vmoe_shape* shape) {
+    Dims D;
+    return vmoe::make_dims(shape, &D) == VMOE_OK ? vmoe::balance_workspace_bytes(D) : 0;
+}
+
+vmoe_status vmoe_balance_loss(const vmoe_shape* shape, const float* logits,
+                              const float* logit_bias, const float* noise, const float* probs,
+                              float noise_std, float w_importance, float w_load, float* losses,
+                              float* importance, float* load, float* dlogits, void* workspace,
+                              size_t workspace_bytes, void* stream) {
+    Dims D;
+    VMOE_TRY(vmoe::make_dims(shape, &D));
+    VMOE_TRY(need(dev(logits) && dev(probs) && dev(losses) && dev(dlogits) && opt(logit_bias) &&
+                  opt(noise) && opt(importance) && opt(load)));
+    VMOE_TRY(need(noise_std > 0.0f && isfinite(noise_std) && isfinite(w_importance) &&
+                  isfinite(w_load)));
+    const size_t need_ws = vmoe::balance_workspace_bytes(D);
+    if (workspace_bytes < need_ws || (need_ws > 0 && !dev(workspace))) return VMOE_ERR_WORKSPACE;
+    return vmoe::balance_launch(D, logits, logit_bias, noise, probs, noise_std, w_importance,
+                                w_load, losses, importance, load, dlogits, workspace,
+                                as_stream(stream));
 }
 
 }  // extern "C"

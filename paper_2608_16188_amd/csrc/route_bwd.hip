@@ -185,7 +185,8 @@ __device__ __forceinline__ void form_dz(float* dzs, float* dps, float* pdp_s, in
                                         const int32_t* __restrict__ idx,
                                         const int32_t* __restrict__ slot,
                                         const float* __restrict__ dgate,
-                                        const int32_t* __restrict__ row_base, size_t tok0,
+                                        const int32_t* __restrict__ row_base,
+                                        const float* __restrict__ dz_add, size_t tok0,
                                         int ntok, int E, int k, int g, long long gc,
                                         Issue issue) {
     const int tid = threadIdx.x;
@@ -258,11 +259,32 @@ __device__ __forceinline__ void form_dz(float* dzs, float* dps, float* pdp_s, in
         pdp_s[tid] = pdp;
     }
     lds_barrier();
-    for (int q = tid; q < ntok * EMAX; q += 256) {
-        const int t = q / EMAX, e = q % EMAX;
-        const float p = dzs[t * LD + e], dp = dps[t * LD + e], pdp = pdp_s[t];
-        // kept: p (dgate - <p, dp>); other experts: -p <p, dp>
-        dzs[t * LD + e] = e >= E ? 0.0f : (dp == dp ? p * (dp - pdp) : -p * pdp);
+    if (dz_add == nullptr) {
+        for (int q = tid; q < ntok * EMAX; q += 256) {
+            const int t = q / EMAX, e = q % EMAX;
+            const float p = dzs[t * LD + e], dp = dps[t * LD + e], pdp = pdp_s[t];
+            // kept: p (dgate - <p, dp>); other experts: -p <p, dp>
+            dzs[t * LD + e] = e >= E ? 0.0f : (dp == dp ? p * (dp - pdp) : -p * pdp);
+        }
+    } else {
+        // the same, plus an extra gradient with respect to the logits (four
+        // of its values requested before any is used)
+        for (int q0 = tid; q0 < ntok * EMAX; q0 += 4 * 256) {
+            float av[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int q = q0 + u * 256, t = q / EMAX, e = q % EMAX;
+                av[u] = (q < ntok * EMAX && e < E) ? dz_add[(tok0 + t) * E + e] : 0.0f;
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int q = q0 + u * 256, t = q / EMAX, e = q % EMAX;
+                if (q >= ntok * EMAX) break;
+                const float p = dzs[t * LD + e], dp = dps[t * LD + e], pdp = pdp_s[t];
+                const float v = dp == dp ? p * (dp - pdp) : -p * pdp;
+                dzs[t * LD + e] = e >= E ? 0.0f : v + av[u];
+            }
+        }
     }
     lds_barrier();
 }
@@ -285,8 +307,9 @@ __global__ __launch_bounds__(256) void route_bwd_kernel(
     const T* __restrict__ x, const T* __restrict__ wr, const float* __restrict__ probs,
     const int32_t* __restrict__ idx, const int32_t* __restrict__ slot,
     const float* __restrict__ dgate, float* __restrict__ dx, float* __restrict__ partial,
-    const T* __restrict__ dxe, const int32_t* __restrict__ row_base, long long gc, int Ng,
-    int d, int E, int k, int tch, int nch) {
+    const T* __restrict__ dxe, const int32_t* __restrict__ row_base,
+    const float* __restrict__ dz_add, long long gc, int Ng, int d, int E, int k, int tch,
+    int nch) {
     constexpr int VEC = ColsPerLane<EMAX>::value;
     constexpr int COLS = 64 * VEC;
     constexpr int U = EMAX <= 8 ? 4 : 8;  // tokens per wave in flight
@@ -337,7 +360,7 @@ __global__ __launch_bounds__(256) void route_bwd_kernel(
     // the first batch of routing inputs (fused: after the dxe rows are known)
     float* dps = lds + DZ_FLOATS;
     form_dz<EMAX, EMAX, KJ>(lds, dps, pdp_s, &rows_s[0][0], rb_s, probs, idx, slot, dgate,
-                            row_base, tok0, ntok, E, k, g, gc, [&] {
+                            row_base, dz_add, tok0, ntok, E, k, g, gc, [&] {
                                 if constexpr (KJ == 0) load_round(wave, xa, da);
                             });
     if constexpr (KJ > 0) load_round(wave, xa, da);
@@ -440,7 +463,8 @@ __global__ __launch_bounds__(256) void route_bwd_mfma_kernel(
     const float* __restrict__ probs, const int32_t* __restrict__ idx,
     const int32_t* __restrict__ slot, const float* __restrict__ dgate, float* __restrict__ dx,
     float* __restrict__ partial, const uint16_t* __restrict__ dxe,
-    const int32_t* __restrict__ row_base, long long gc, int Ng, int d, int E, int k, int nch) {
+    const int32_t* __restrict__ row_base, const float* __restrict__ dz_add, long long gc, int Ng,
+    int d, int E, int k, int nch) {
     constexpr int LD = EMAX + 1, TCH = kMfmaTok, COLS = kMfmaCols;
     constexpr int XV = TCH * COLS / 8 / 256;    // 16-byte x vectors per thread
     constexpr int WV = EMAX * COLS / 8 / 256;   // 16-byte W vectors per thread
@@ -479,7 +503,7 @@ __global__ __launch_bounds__(256) void route_bwd_mfma_kernel(
     };
     for (int q = ntok * LD + tid; q < TCH * LD; q += 256) dzs[q] = 0.0f;  // rows past the chunk
     form_dz<EMAX, LD, KJ>(dzs, xdp, pdp_s, rows_s, rb_s, probs, idx, slot, dgate, row_base,
-                          tok0, ntok, E, k, g, gc, issue);
+                          dz_add, tok0, ntok, E, k, g, gc, issue);
     // dp is no longer needed: its space takes the x tile
     uint16_t* xs = reinterpret_cast<uint16_t*>(xdp);
 #pragma unroll
@@ -674,6 +698,7 @@ struct BwdArgs {
     float *dx, *partial;
     const void* dxe;
     const int32_t* row_base;
+    const float* dz_add;  // extra gradient with respect to the logits, or null
 };
 
 template <typename T, int EMAX, int KJ>
@@ -685,8 +710,8 @@ void launch_main(const Dims& D, const ChunkPlan& P, const BwdArgs& a, hipStream_
             kern<<<grid, 256, 0, st>>>(static_cast<const uint16_t*>(a.x),
                                        static_cast<const uint16_t*>(a.wr), a.probs, a.idx, a.slot,
                                        a.dgate, a.dx, a.partial,
-                                       static_cast<const uint16_t*>(a.dxe), a.row_base, gc, D.Ng,
-                                       D.d, D.E, D.k, P.nch);
+                                       static_cast<const uint16_t*>(a.dxe), a.row_base, a.dz_add,
+                                       gc, D.Ng, D.d, D.E, D.k, P.nch);
         };
         if (a.partial) go(route_bwd_mfma_kernel<EMAX, true, KJ>);
         else go(route_bwd_mfma_kernel<EMAX, false, KJ>);
@@ -698,8 +723,8 @@ void launch_main(const Dims& D, const ChunkPlan& P, const BwdArgs& a, hipStream_
     auto go = [&](auto kern) {
         kern<<<grid, 256, 0, st>>>(static_cast<const T*>(a.x), static_cast<const T*>(a.wr),
                                    a.probs, a.idx, a.slot, a.dgate, a.dx, a.partial,
-                                   static_cast<const T*>(a.dxe), a.row_base, gc, D.Ng, D.d, D.E,
-                                   D.k, P.tch, P.nch);
+                                   static_cast<const T*>(a.dxe), a.row_base, a.dz_add, gc, D.Ng,
+                                   D.d, D.E, D.k, P.tch, P.nch);
     };
     if (a.partial) go(route_bwd_kernel<T, EMAX, true, KJ>);
     else go(route_bwd_kernel<T, EMAX, false, KJ>);
@@ -751,16 +776,17 @@ size_t route_bwd_workspace_bytes(const Dims& D) {
 
 vmoe_status route_bwd_launch(const Dims& D, const void* x, const void* wr, const float* probs,
                              const int32_t* idx, const int32_t* slot, const float* dgate,
-                             float* dx, float* dwr, void* ws, hipStream_t st) {
-    const BwdArgs a{x, wr, probs, idx, slot, dgate, dx, nullptr, nullptr, nullptr};
+                             const float* dz_add, float* dx, float* dwr, void* ws,
+                             hipStream_t st) {
+    const BwdArgs a{x, wr, probs, idx, slot, dgate, dx, nullptr, nullptr, nullptr, dz_add};
     return run_route_bwd(D, a, dwr, ws, 0, st);
 }
 
 vmoe_status dispatch_route_bwd_launch(const Dims& D, const void* dxe, const int32_t* row_base,
                                       const void* x, const void* wr, const float* probs,
                                       const int32_t* idx, const int32_t* slot,
-                                      const float* dgate, float* dx, float* dwr, void* ws,
-                                      hipStream_t st) {
+                                      const float* dgate, const float* dz_add, float* dx,
+                                      float* dwr, void* ws, hipStream_t st) {
     // the gathered rows are indexed in int and kept in LDS for k <= 4, and a
     // lane gathers at least two columns per row (E <= 16, or the matrix-core
     // kernel of bf16 layers with more experts; f32 with E > 16 would gather
@@ -770,9 +796,9 @@ vmoe_status dispatch_route_bwd_launch(const Dims& D, const void* dxe, const int3
     if (D.k > 4 || (D.E > 16 && D.dtype != VMOE_BF16) || rows >= (1ll << 31) || D.N == 0) {
         const vmoe_status s = dispatch_bwd_launch(D, dxe, idx, slot, row_base, dx, st);
         if (s != VMOE_OK) return s;
-        return route_bwd_launch(D, x, wr, probs, idx, slot, dgate, dx, dwr, ws, st);
+        return route_bwd_launch(D, x, wr, probs, idx, slot, dgate, dz_add, dx, dwr, ws, st);
     }
-    const BwdArgs a{x, wr, probs, idx, slot, dgate, dx, nullptr, dxe, row_base};
+    const BwdArgs a{x, wr, probs, idx, slot, dgate, dx, nullptr, dxe, row_base, dz_add};
     return run_route_bwd(D, a, dwr, ws, D.k <= 2 ? 2 : 4, st);
 }
 

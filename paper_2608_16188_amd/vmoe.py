@@ -57,7 +57,8 @@ def _load():
     lib.vmoe_status_string.argtypes = [ctypes.c_int32]
     lib.vmoe_capacity.restype = ctypes.c_int32
     lib.vmoe_capacity.argtypes = [S]
-    for name in ("vmoe_route_workspace_bytes", "vmoe_route_bwd_workspace_bytes"):
+    for name in ("vmoe_route_workspace_bytes", "vmoe_route_bwd_workspace_bytes",
+                 "vmoe_balance_loss_workspace_bytes"):
         getattr(lib, name).restype = ctypes.c_size_t
         getattr(lib, name).argtypes = [S]
     sigs = {
@@ -70,6 +71,8 @@ def _load():
         "vmoe_dispatch_bwd": [S] + [P] * 6,
         "vmoe_route_bwd": [S] + [P] * 9 + [ctypes.c_size_t, P],
         "vmoe_dispatch_route_bwd": [S] + [P] * 11 + [ctypes.c_size_t, P],
+        "vmoe_dispatch_route_bwd_dlogits": [S] + [P] * 12 + [ctypes.c_size_t, P],
+        "vmoe_balance_loss": [S] + [P] * 4 + [ctypes.c_float] * 3 + [P] * 5 + [ctypes.c_size_t, P],
     }
     for name, args in sigs.items():
         f = getattr(lib, name)
@@ -184,6 +187,28 @@ def vmoe_dispatch_route_bwd(shape, dxe, row_base, x, w_router, probs, expert_idx
         ctypes.byref(shape), _ptr(dxe), _ptr(row_base), _ptr(x), _ptr(w_router), _ptr(probs),
         _ptr(expert_idx), _ptr(slot), _ptr(dgate), _ptr(dx), _ptr(dw_router), _ptr(workspace),
         ws_bytes, _stream(stream)))
+
+
+def vmoe_dispatch_route_bwd_dlogits(shape, dxe, row_base, x, w_router, probs, expert_idx, slot,
+                                    dgate, dlogits, dx, dw_router, workspace, stream=None):
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check("vmoe_dispatch_route_bwd_dlogits", _lib.vmoe_dispatch_route_bwd_dlogits(
+        ctypes.byref(shape), _ptr(dxe), _ptr(row_base), _ptr(x), _ptr(w_router), _ptr(probs),
+        _ptr(expert_idx), _ptr(slot), _ptr(dgate), _ptr(dlogits), _ptr(dx), _ptr(dw_router),
+        _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def vmoe_balance_loss_workspace_bytes(shape: Shape) -> int:
+    return int(_lib.vmoe_balance_loss_workspace_bytes(ctypes.byref(shape)))
+
+
+def vmoe_balance_loss(shape, logits, logit_bias, noise, probs, noise_std, w_importance, w_load,
+                      losses, importance, load, dlogits, workspace, stream=None):
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check("vmoe_balance_loss", _lib.vmoe_balance_loss(
+        ctypes.byref(shape), _ptr(logits), _ptr(logit_bias), _ptr(noise), _ptr(probs),
+        float(noise_std), float(w_importance), float(w_load), _ptr(losses), _ptr(importance),
+        _ptr(load), _ptr(dlogits), _ptr(workspace), ws_bytes, _stream(stream)))
 
 
 def vmoe_route_bwd(shape, x, w_router, probs, expert_idx, slot, dgate, dx, dw_router, workspace,

@@ -138,6 +138,59 @@ def cpu_baseline(cfg, inputs, C_full, budget_s=20.0):
                       f"single-threaded C oracle, double precision; {dt:.1f} s"}
 
 
+def balance_losses(L, V, stream, K):
+    """The auxiliary balance losses (importance and load CV^2 per group, with
+    their logit gradient) and the router backward that takes that gradient,
+    timed after the layer step on the same buffers (not part of the step)."""
+    import torch
+    s, cfg = L.shape, L.cfg
+    N, G, E = cfg.n_tokens, cfg.n_groups, cfg.n_experts
+    sigma = 1.0 / E
+    f32 = torch.float32
+    losses = torch.empty(G, 2, dtype=f32, device="cuda")
+    dl = torch.empty(max(N, 1), E, dtype=f32, device="cuda")
+    ws = torch.empty(max(V.vmoe_balance_loss_workspace_bytes(s), 16), dtype=torch.uint8,
+                     device="cuda")
+
+    def loss():
+        V.vmoe_balance_loss(s, L.logits, L.logit_bias, L.noise, L.probs, sigma, 0.01, 0.01,
+                            losses, None, None, dl, ws, stream)
+
+    def bwd(with_dl):
+        if with_dl:
+            V.vmoe_dispatch_route_bwd_dlogits(s, L.dxe, L.row_base, L.x, L.w_router, L.probs,
+                                              L.expert_idx, L.slot, L.dgate, dl, L.dx,
+                                              L.dw_router, L.route_bwd_ws, stream)
+        else:
+            V.vmoe_dispatch_route_bwd(s, L.dxe, L.row_base, L.x, L.w_router, L.probs,
+                                      L.expert_idx, L.slot, L.dgate, L.dx, L.dw_router,
+                                      L.route_bwd_ws, stream)
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(K):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / K
+
+    ms = timed(loss)
+    ms_bwd = timed(lambda: bwd(False))
+    ms_bwd_dl = timed(lambda: bwd(True))
+    # two passes read logits and probs (and noise), the second writes dlogits
+    rows = 2 + (L.noise is not None)
+    nbytes = (2 * rows + 1) * N * E * 4
+    return {"ms": round(ms, 4), "gbs": round(nbytes / (ms * 1e-3) / 1e9, 1),
+            "algorithmic_bytes": nbytes, "noise_std": sigma,
+            "dispatch_route_bwd_ms": round(ms_bwd, 4),
+            "dispatch_route_bwd_dlogits_ms": round(ms_bwd_dl, 4),
+            "note": "vmoe_balance_loss, then the fused router backward without and with its "
+                    "logit gradient; timed after the step, not part of it"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -242,6 +295,8 @@ def main():
                 for c, name in enumerate(CALLS)}
     step_ms_events = float(np.mean([evc[i][0].elapsed_time(evc[i][-1]) for i in range(K)]))
 
+    balance = balance_losses(L, V, stream, K)
+
     counts = L.counts.cpu().numpy()
     A = int(counts.sum())
     cost = algorithmic_cost(cfg, A, L.noise is not None, L.logit_bias is not None)
@@ -290,6 +345,7 @@ def main():
         "per_call": breakdown,
         "per_call_note": "diagnostic pass after the timed region, every call bracketed by events",
         "step_ms_events": step_ms_events,
+        "balance_losses": balance,
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, inputs, L.C)

@@ -10,9 +10,9 @@
 //              only its own noise is drawn again;
 //   losses     CV^2 = var / mean^2 over the experts (0 for a zero sum), and
 //   dlogits    = d/dlogits of sum_g w_imp CV^2(imp[g]) + w_load CV^2(load[g]).
-// Three launches: per-chunk sums (one thread per token, wave-shuffle sums),
-// a per-group finalisation in double (fixed order), and the per-token
-// gradient row. Every pass reads the [N, E] rows once; N x E is small next to
+// Two launches: per-chunk sums (one thread per token, wave-shuffle sums), then
+// the per-token gradient row, each block of which first forms its group's
+// losses and coefficients from the chunk sums in double (fixed order). Every pass reads the [N, E] rows once; N x E is small next to
 // the layer's activations, so the launches are latency-bound.
 #include <type_traits>
 
@@ -134,22 +134,36 @@ __global__ __launch_bounds__(kBalTok) void balance_partial_kernel(
 }
 
 // Per group: the chunk sums in double (chunk order), both CV^2 values and the
-// gradient coefficients c[e] = w 2 / (E mu^2) (v_e - mu - var / mu).
-__global__ __launch_bounds__(128) void balance_finalize_kernel(
-    const float* __restrict__ partial, int nch, int E, float w_imp, float w_load,
-    float* __restrict__ coef, float* __restrict__ losses, float* __restrict__ imp_out,
-    float* __restrict__ load_out) {
-    __shared__ double v[2][kMaxExperts];
-    __shared__ double stat[2][3];  // mean, variance, loss
-    const int g = blockIdx.x, tid = threadIdx.x;
+// gradient coefficients c[e] = w 2 / (E mu^2) (v_e - mu - var / mu) into cs
+// (every block of the group forms the same values; block 0 writes the losses
+// and the optional sums).
+template <int EMAX>
+__device__ __forceinline__ void balance_coefficients(const float* __restrict__ partial, int nch,
+                                                     int E, int g, float w_imp, float w_load,
+                                                     float (&cs)[2][EMAX], bool writer,
+                                                     float* __restrict__ losses,
+                                                     float* __restrict__ imp_out,
+                                                     float* __restrict__ load_out) {
+    __shared__ double v[2][EMAX];
+    __shared__ double stat[2][2];  // mean, variance
+    const int tid = threadIdx.x;
     if (tid < 2 * E) {
         const int which = tid / E, e = tid % E;
+        const float* src = partial + (static_cast<size_t>(g) * nch * 2 + which) * E + e;
         double s = 0.0;
-        for (int c = 0; c < nch; ++c)
-            s += partial[((static_cast<size_t>(g) * nch + c) * 2 + which) * E + e];
+        int c = 0;
+        for (; c + 4 <= nch; c += 4) {  // four chunk values in flight, summed in chunk order
+            const float a0 = src[(c + 0) * 2 * E], a1 = src[(c + 1) * 2 * E];
+            const float a2 = src[(c + 2) * 2 * E], a3 = src[(c + 3) * 2 * E];
+            s += a0;
+            s += a1;
+            s += a2;
+            s += a3;
+        }
+        for (; c < nch; ++c) s += src[c * 2 * E];
         v[which][e] = s;
         float* out = which == 0 ? imp_out : load_out;
-        if (out) out[static_cast<size_t>(g) * E + e] = static_cast<float>(s);
+        if (writer && out) out[static_cast<size_t>(g) * E + e] = static_cast<float>(s);
     }
     __syncthreads();
     if (tid < 2) {
@@ -161,8 +175,9 @@ __global__ __launch_bounds__(128) void balance_finalize_kernel(
         var /= E;
         stat[tid][0] = mu;
         stat[tid][1] = var;
-        stat[tid][2] = sum == 0.0 ? 0.0 : var / (mu * mu);
-        losses[static_cast<size_t>(g) * 2 + tid] = static_cast<float>(stat[tid][2]);
+        if (writer)
+            losses[static_cast<size_t>(g) * 2 + tid] =
+                static_cast<float>(sum == 0.0 ? 0.0 : var / (mu * mu));
     }
     __syncthreads();
     if (tid < 2 * E) {
@@ -170,8 +185,9 @@ __global__ __launch_bounds__(128) void balance_finalize_kernel(
         const double mu = stat[which][0], var = stat[which][1];
         const double w = which == 0 ? w_imp : w_load;
         const double c = mu == 0.0 ? 0.0 : w * 2.0 / (E * mu * mu) * (v[which][e] - mu - var / mu);
-        coef[(static_cast<size_t>(g) * 2 + which) * E + e] = static_cast<float>(c);
+        cs[which][e] = static_cast<float>(c);
     }
+    __syncthreads();
 }
 
 // dlogits[t,e] = p_e (ci_e - sum p ci) + cl_e phi(u_e) / sigma, minus at the
@@ -181,12 +197,13 @@ template <int EMAX>
 __global__ __launch_bounds__(kBalTok) void balance_grad_kernel(
     const float* __restrict__ logits, const float* __restrict__ bias,
     const float* __restrict__ noise, const float* __restrict__ probs,
-    const float* __restrict__ coef, float sigma, int Ng, int E, int k,
-    float* __restrict__ dlogits) {
+    const float* __restrict__ partial, int nch, float sigma, float w_imp, float w_load, int Ng,
+    int E, int k, float* __restrict__ losses, float* __restrict__ imp_out,
+    float* __restrict__ load_out, float* __restrict__ dlogits) {
     __shared__ float cs[2][EMAX];
     const int g = blockIdx.y, tid = threadIdx.x;
-    if (tid < 2 * E) cs[tid / E][tid % E] = coef[(static_cast<size_t>(g) * 2) * E + tid];
-    __syncthreads();
+    balance_coefficients<EMAX>(partial, nch, E, g, w_imp, w_load, cs, blockIdx.x == 0, losses,
+                               imp_out, load_out);
     const int tl = blockIdx.x * kBalTok + tid;
     if (tl >= Ng) return;
     const size_t t = static_cast<size_t>(g) * Ng + tl;
@@ -225,36 +242,33 @@ unsigned balance_chunks(const Dims& D) { return cdiv(D.Ng, kBalTok); }
 template <int EMAX>
 void launch_balance(const Dims& D, const float* logits, const float* bias, const float* noise,
                     const float* probs, float sigma, float w_imp, float w_load, float* losses,
-                    float* imp, float* load, float* dlogits, float* partial, float* coef,
-                    hipStream_t st) {
+                    float* imp, float* load, float* dlogits, float* partial, hipStream_t st) {
+    // nch = 0 (no tokens) still runs one block per group to write zero losses
     const unsigned nch = balance_chunks(D);
     if (nch > 0)
         balance_partial_kernel<EMAX><<<dim3(nch, D.G), kBalTok, 0, st>>>(
             logits, bias, noise, probs, sigma, D.Ng, D.E, D.k, nch, partial);
-    balance_finalize_kernel<<<D.G, 128, 0, st>>>(partial, nch, D.E, w_imp, w_load, coef, losses,
-                                                 imp, load);
-    if (nch > 0)
-        balance_grad_kernel<EMAX><<<dim3(nch, D.G), kBalTok, 0, st>>>(
-            logits, bias, noise, probs, coef, sigma, D.Ng, D.E, D.k, dlogits);
+    balance_grad_kernel<EMAX><<<dim3(nch > 0 ? nch : 1, D.G), kBalTok, 0, st>>>(
+        logits, bias, noise, probs, partial, static_cast<int>(nch), sigma, w_imp, w_load, D.Ng,
+        D.E, D.k, losses, imp, load, dlogits);
 }
 
 }  // namespace
 
-// Workspace: per-chunk sums [G, chunks, 2, E] and coefficients [G, 2, E], f32.
+// Workspace: per-chunk sums [G, chunks, 2, E] f32.
 size_t balance_workspace_bytes(const Dims& D) {
-    return sizeof(float) * static_cast<size_t>(D.G) * 2 * D.E * (balance_chunks(D) + 1);
+    return sizeof(float) * static_cast<size_t>(D.G) * 2 * D.E * balance_chunks(D);
 }
 
 vmoe_status balance_launch(const Dims& D, const float* logits, const float* bias,
                            const float* noise, const float* probs, float sigma, float w_imp,
                            float w_load, float* losses, float* imp, float* load, float* dlogits,
                            void* ws, hipStream_t st) {
-    float* coef = static_cast<float*>(ws);
-    float* partial = coef + static_cast<size_t>(D.G) * 2 * D.E;
+    float* partial = static_cast<float*>(ws);
     auto go = [&](auto tag) {
         constexpr int EM = decltype(tag)::value;
         launch_balance<EM>(D, logits, bias, noise, probs, sigma, w_imp, w_load, losses, imp, load,
-                           dlogits, partial, coef, st);
+                           dlogits, partial, st);
     };
     if (D.E <= 8) go(std::integral_constant<int, 8>{});
     else if (D.E <= 16) go(std::integral_constant<int, 16>{});

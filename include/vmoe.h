@@ -294,6 +294,28 @@ vmoe_status vmoe_group_experts(int32_t n, const double* mtmp, const double* life
                                double unit_bytes, int32_t* slice_of, int32_t* n_slices,
                                void* workspace, size_t workspace_bytes);
 
+/* Lifespan aligning within a slice (paper Sec. 3.2.2): fill-clamp-refill
+ * allocation of `budget` whole compute units (or workgroup slots) among n
+ * experts. Every expert starts from min_units[i]; the rest is split among the
+ * experts below saturation in proportion to coef[i] (>= 0; an expert with
+ * coef 0 keeps its minimum); an expert pushed past sat_units[i] is clamped
+ * there and its excess is split again among the others, until nothing is
+ * returned (at most n rounds). Budget beyond the saturations stays unused.
+ *   alloc [n] f64        out: the real shares; they equal
+ *                        min(sat_i, min_i + lambda coef_i) with one lambda
+ *   alloc_units [n] i32  out: largest-remainder rounding of alloc to
+ *                        floor(sum alloc) units (each share rounded down or
+ *                        up, ties to the lower index)
+ *   n_rounds             out: share-clamp rounds taken
+ *   workspace            host memory of at least 4 n bytes
+ * HOST routine. VMOE_ERR_INVALID_ARG for n outside [0, 65536], a negative
+ * minimum, sat < min, a negative or non-finite coefficient or a budget below
+ * the sum of the minima; VMOE_ERR_WORKSPACE for a small workspace. */
+vmoe_status vmoe_fill_clamp_refill(int32_t n, const int32_t* min_units, const int32_t* sat_units,
+                                   const double* coef, int64_t budget, double* alloc,
+                                   int32_t* alloc_units, int32_t* n_rounds, void* workspace,
+                                   size_t workspace_bytes);
+
 #ifdef __cplusplus
 }
 #endif

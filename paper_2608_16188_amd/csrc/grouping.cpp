@@ -121,4 +121,81 @@ vmoe_status vmoe_group_experts(int32_t n, const double* mtmp, const double* life
     return VMOE_OK;
 }
 
+// Fill-clamp-refill allocation of compute units within a slice (paper
+// Sec. 3.2.2): minima first, the rest in proportion to the coefficients among
+// the unsaturated experts, saturated experts clamped and their excess shared
+// again, until nothing is returned. Real shares in `alloc`, their
+// largest-remainder rounding to floor(sum) whole units in `alloc_units`
+// (ties to the lower index); `n_rounds` counts the share-clamp rounds.
+vmoe_status vmoe_fill_clamp_refill(int32_t n, const int32_t* min_units, const int32_t* sat_units,
+                                   const double* coef, int64_t budget, double* alloc,
+                                   int32_t* alloc_units, int32_t* n_rounds, void* workspace,
+                                   size_t workspace_bytes) {
+    if (n < 0 || n > kMaxExpertsGrouped || !n_rounds ||
+        (n > 0 && (!min_units || !sat_units || !coef || !alloc || !alloc_units)))
+        return VMOE_ERR_INVALID_ARG;
+    if (workspace_bytes < sizeof(int32_t) * static_cast<size_t>(n) || (n > 0 && !workspace))
+        return VMOE_ERR_WORKSPACE;
+    int64_t need = 0;
+    for (int32_t i = 0; i < n; ++i) {
+        if (min_units[i] < 0 || sat_units[i] < min_units[i] || !(coef[i] >= 0.0) ||
+            !isfinite(coef[i]))
+            return VMOE_ERR_INVALID_ARG;
+        need += min_units[i];
+    }
+    if (budget < need) return VMOE_ERR_INVALID_ARG;
+    int32_t* active = static_cast<int32_t*>(workspace);
+    int32_t na = 0;
+    for (int32_t i = 0; i < n; ++i) {
+        alloc[i] = static_cast<double>(min_units[i]);
+        if (alloc[i] < sat_units[i] && coef[i] > 0.0) active[na++] = i;
+    }
+    double left = static_cast<double>(budget - need);
+    int32_t rounds = 0;
+    while (left > 0.0 && na > 0) {
+        double W = 0.0;
+        for (int32_t r = 0; r < na; ++r) W += coef[active[r]];
+        for (int32_t r = 0; r < na; ++r) alloc[active[r]] += left * coef[active[r]] / W;
+        ++rounds;
+        left = 0.0;
+        int32_t kept = 0;
+        for (int32_t r = 0; r < na; ++r) {
+            const int32_t i = active[r];
+            if (alloc[i] > sat_units[i]) {
+                left += alloc[i] - sat_units[i];
+                alloc[i] = static_cast<double>(sat_units[i]);
+            } else {
+                active[kept++] = i;
+            }
+        }
+        na = kept;
+    }
+    // whole units: floor of each share, then the remaining units to the
+    // largest fractional parts (lower index first on ties)
+    double sum = 0.0;
+    int64_t base = 0;
+    for (int32_t i = 0; i < n; ++i) {
+        alloc_units[i] = static_cast<int32_t>(floor(alloc[i]));
+        base += alloc_units[i];
+        sum += alloc[i];
+    }
+    int64_t extra = static_cast<int64_t>(floor(sum + 1e-9)) - base;
+    while (extra > 0) {
+        int32_t best = -1;
+        double bf = 0.0;  // only shares with a fractional part round up
+        for (int32_t i = 0; i < n; ++i) {
+            const double fr = alloc[i] - floor(alloc[i]);
+            if (alloc_units[i] == static_cast<int32_t>(floor(alloc[i])) && fr > bf) {
+                best = i;
+                bf = fr;
+            }
+        }
+        if (best < 0) break;
+        ++alloc_units[best];
+        --extra;
+    }
+    *n_rounds = rounds;
+    return VMOE_OK;
+}
+
 }  // extern "C"

@@ -85,6 +85,9 @@ def _load():
     lib.vmoe_group_experts_workspace_bytes.argtypes = [ctypes.c_int32, D, D, D]
     lib.vmoe_group_experts.restype = ctypes.c_int32
     lib.vmoe_group_experts.argtypes = [ctypes.c_int32, P, P, D, D, D, D, P, P, P, ctypes.c_size_t]
+    lib.vmoe_fill_clamp_refill.restype = ctypes.c_int32
+    lib.vmoe_fill_clamp_refill.argtypes = [ctypes.c_int32, P, P, P, ctypes.c_int64, P, P, P, P,
+                                           ctypes.c_size_t]
     return lib
 
 
@@ -245,3 +248,25 @@ def vmoe_group_experts(mtmp, lifespan, mem_budget, mem_static, eta, unit_bytes):
         n, m.ctypes.data, r.ctypes.data, float(mem_budget), float(mem_static), float(eta),
         float(unit_bytes), out.ctypes.data, ctypes.addressof(ns), ws.ctypes.data, ws_bytes))
     return out[:n], int(ns.value)
+
+
+def vmoe_fill_clamp_refill(min_units, sat_units, coef, budget):
+    """Host routine: fill-clamp-refill shares of `budget` units; returns
+    (alloc f64 array, alloc_units i32 array, rounds)."""
+    import numpy as np
+    mn = np.ascontiguousarray(min_units, dtype=np.int32)
+    sat = np.ascontiguousarray(sat_units, dtype=np.int32)
+    w = np.ascontiguousarray(coef, dtype=np.float64)
+    n = len(mn)
+    if len(sat) != n or len(w) != n:
+        raise ValueError("min_units, sat_units and coef must have one entry per expert")
+    alloc = np.zeros(n, np.float64)
+    units = np.zeros(n, np.int32)
+    ws = np.zeros(max(n, 1), np.int32)
+    rounds = ctypes.c_int32(0)
+    c = ctypes.c_void_p
+    _check("vmoe_fill_clamp_refill", _lib.vmoe_fill_clamp_refill(
+        n, c(mn.ctypes.data), c(sat.ctypes.data), c(w.ctypes.data), int(budget),
+        c(alloc.ctypes.data), c(units.ctypes.data), ctypes.cast(ctypes.byref(rounds), c),
+        c(ws.ctypes.data), ws.nbytes))
+    return alloc, units, int(rounds.value)

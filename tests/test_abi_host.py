@@ -124,6 +124,33 @@ def test_null_pointers_rejected_with_zero_tokens():
                                      None) == V.VMOE_ERR_INVALID_ARG
 
 
+def test_balance_and_dlogits_entry_points_validate():
+    b, L = ctypes.byref(_shape()), V._lib
+    f = [FAKE] * 4
+    # logits, bias, noise, probs, noise_std, w_imp, w_load, losses, imp, load, dlogits, ws
+    ok_tail = [FAKE, None, None, FAKE, FAKE, 1 << 30, None]
+    assert L.vmoe_balance_loss(b, None, None, None, FAKE, 0.1, 1.0, 1.0, *ok_tail) == \
+        V.VMOE_ERR_INVALID_ARG
+    assert L.vmoe_balance_loss(b, FAKE, FAKE + 4, None, FAKE, 0.1, 1.0, 1.0, *ok_tail) == \
+        V.VMOE_ERR_INVALID_ARG
+    for bad in (0.0, -0.5, float("inf"), float("nan")):
+        assert L.vmoe_balance_loss(b, FAKE, None, None, FAKE, bad, 1.0, 1.0, *ok_tail) == \
+            V.VMOE_ERR_INVALID_ARG
+    assert L.vmoe_balance_loss(b, FAKE, None, None, FAKE, 0.1, float("nan"), 1.0, *ok_tail) == \
+        V.VMOE_ERR_INVALID_ARG
+    need = V.vmoe_balance_loss_workspace_bytes(_shape())
+    assert need > 0
+    assert L.vmoe_balance_loss(b, FAKE, None, None, FAKE, 0.1, 1.0, 1.0, FAKE, None, None, FAKE,
+                               FAKE, need - 1, None) == V.VMOE_ERR_WORKSPACE
+    # the fused backward with dlogits: a NULL dlogits is an error
+    assert L.vmoe_dispatch_route_bwd_dlogits(b, *([FAKE] * 8), None, FAKE, FAKE, FAKE, 1 << 30,
+                                             None) == V.VMOE_ERR_INVALID_ARG
+    need_b = V.vmoe_route_bwd_workspace_bytes(_shape())
+    assert L.vmoe_dispatch_route_bwd_dlogits(b, *([FAKE] * 12), need_b - 1, None) == \
+        V.VMOE_ERR_WORKSPACE
+    del f
+
+
 def test_workspace_too_small_rejected():
     s = _shape()
     b = ctypes.byref(s)

@@ -844,26 +844,40 @@ __device__ __forceinline__ float f32_elem(const float* base, int ld, int mn, int
     return KMAJOR ? base[static_cast<size_t>(mn) * ld + k] : base[static_cast<size_t>(k) * ld + mn];
 }
 
-// One FK x FT operand stage into S[k][mn] (zero outside the operand): k-major
-// operands are walked k fastest, mn-major ones mn fastest.
+// One FK x FT operand stage (zero outside the operand), in two halves: the
+// loads into registers, then the stores into S[k][mn]. k-major operands are
+// walked k fastest, mn-major ones mn fastest.
+constexpr int kF32Per = FK * FT / 256;
+
 template <bool KMAJOR>
-__device__ __forceinline__ void stage_f32(float (*S)[FT + 1], const float* base, int ld, int mn0,
-                                          int mn_lim, int k0, int k_lim) {
-    constexpr int PER = FK * FT / 256;
-    float v[PER];
+__device__ __forceinline__ void load_f32(float (&v)[kF32Per], const float* base, int ld, int mn0,
+                                         int mn_lim, int k0, int k_lim) {
 #pragma unroll
-    for (int u = 0; u < PER; ++u) {
+    for (int u = 0; u < kF32Per; ++u) {
         const int q = u * 256 + static_cast<int>(threadIdx.x);
         const int kk = KMAJOR ? q % FK : q / FT, mn = KMAJOR ? q / FK : q % FT;
         v[u] = (mn0 + mn < mn_lim && k0 + kk < k_lim) ? f32_elem<KMAJOR>(base, ld, mn0 + mn, k0 + kk)
                                                       : 0.0f;
     }
+}
+
+template <bool KMAJOR>
+__device__ __forceinline__ void store_f32(float (*S)[FT + 1], const float (&v)[kF32Per]) {
 #pragma unroll
-    for (int u = 0; u < PER; ++u) {
+    for (int u = 0; u < kF32Per; ++u) {
         const int q = u * 256 + static_cast<int>(threadIdx.x);
         const int kk = KMAJOR ? q % FK : q / FT, mn = KMAJOR ? q / FK : q % FT;
         S[kk][mn] = v[u];
     }
+}
+
+// A barrier that waits for this wave's LDS accesses only: the next stage's
+// global loads stay in flight across it.
+__device__ __forceinline__ void f32_lds_barrier() {
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0); vmcnt, expcnt not waited for
+    __builtin_amdgcn_s_barrier();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
 template <bool A_KMAJOR, bool B_KMAJOR, int EPI>
@@ -884,16 +898,25 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs p) {
     f32x16_f acc;
 #pragma unroll
     for (int i = 0; i < 16; ++i) acc[i] = 0.0f;
+    // the next stage's loads are issued before this stage's products and
+    // land in registers while they run
+    float va[kF32Per], vb[kF32Per];
+    load_f32<A_KMAJOR>(va, A, p.a.ld, m0, M, 0, K);
+    load_f32<B_KMAJOR>(vb, B, p.b.ld, n0, N, 0, K);
     for (int k0 = 0; k0 < K; k0 += FK) {
-        stage_f32<A_KMAJOR>(As, A, p.a.ld, m0, M, k0, K);
-        stage_f32<B_KMAJOR>(Bs, B, p.b.ld, n0, N, k0, K);
-        __syncthreads();
+        store_f32<A_KMAJOR>(As, va);
+        store_f32<B_KMAJOR>(Bs, vb);
+        f32_lds_barrier();
+        if (k0 + FK < K) {
+            load_f32<A_KMAJOR>(va, A, p.a.ld, m0, M, k0 + FK, K);
+            load_f32<B_KMAJOR>(vb, B, p.b.ld, n0, N, k0 + FK, K);
+        }
         // A[m][k = 2 s + kh], B[k][n]: lane l supplies row / column l % 32
 #pragma unroll
         for (int s2 = 0; s2 < FK / 2; ++s2)
             acc = __builtin_amdgcn_mfma_f32_32x32x2f32(As[2 * s2 + kh][32 * wm + r],
                                                        Bs[2 * s2 + kh][32 * wn + r], acc, 0, 0, 0);
-        __syncthreads();
+        f32_lds_barrier();
     }
     // register i of lane l: row 8 (i / 4) + 4 (l / 32) + i % 4, column l % 32
     const int n = n0 + 32 * wn + r;

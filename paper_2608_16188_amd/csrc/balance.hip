@@ -14,8 +14,9 @@
 // first forms its group's losses and coefficients from the chunk sums in
 // double (fixed order). Up to 8 experts a thread holds a whole token; beyond,
 // lanes run over experts (a token's E values on consecutive lanes), so no
-// thread keeps an E-wide array and every row access is contiguous. Every pass reads the [N, E] rows once; N x E is small next to
-// the layer's activations, so the launches are latency-bound.
+// thread keeps an E-wide array and every row access is contiguous. Each
+// launch reads the [N, E] rows once; N x E is small next to the layer's
+// activations, so both are latency-bound.
 #include <type_traits>
 
 #include "common.h"

@@ -143,3 +143,47 @@ def test_dispatch_route_bwd_dlogits(cfg):
     tol = TOL[cfg.dtype]
     assert_close("dx", to_numpy(L.dx), ref["dx"] + ex_dx, tol)
     assert_close("dW_router", to_numpy(L.dw_router), ref["dw_router"] + ex_dwr, tol)
+
+
+def test_balance_loss_and_router_backward_full_size():
+    """ViT-B/16 (6304 tokens, E = 8) as the bench runs it: the losses and
+    dlogits from the layer's own routing, and the change that dlogits makes to
+    dx and dW_router, against the oracle (its gate re-run on the layer's f32
+    logits gives the probabilities)."""
+    cfg = W.CONFIGS["vitb16_bf16"]
+    say("balance loss full size", cfg.name)
+    inp = W.make_inputs(cfg)
+    L = LayerBuffers(cfg, inp)
+    L.step()
+    torch.cuda.synchronize()
+    s, N, G, E, k = L.shape, cfg.n_tokens, cfg.n_groups, cfg.n_experts, cfg.k
+    # weights of the order of the token count, so that the logit gradient
+    # moves dx well above its f32 rounding
+    sigma, w_imp, w_load = 1.0 / E, float(N), float(N)
+    logits = to_numpy(L.logits)
+    bias = inp.get("logit_bias")
+    noise = inp.get("noise")
+    probs = oracle.gate(logits, k, bias, noise)["probs"]
+    assert bits_equal(to_numpy(L.probs), probs), "router probabilities differ from the oracle's"
+    ref = OB.balance_loss(logits, k, G, sigma, w_imp, w_load, bias=bias, noise=noise,
+                          probs=probs)
+    f32 = torch.float32
+    losses = torch.empty(G, 2, dtype=f32, device="cuda")
+    dl = torch.empty(N, E, dtype=f32, device="cuda")
+    ws = torch.empty(max(V.vmoe_balance_loss_workspace_bytes(s), 16), dtype=torch.uint8,
+                     device="cuda")
+    V.vmoe_balance_loss(s, L.logits, L.logit_bias, L.noise, L.probs, sigma, w_imp, w_load,
+                        losses, None, None, dl, ws)
+    dx0, dwr0 = L.dx.clone(), L.dw_router.clone()
+    V.vmoe_dispatch_route_bwd_dlogits(s, L.dxe, L.row_base, L.x, L.w_router, L.probs,
+                                      L.expert_idx, L.slot, L.dgate, dl, L.dx, L.dw_router,
+                                      L.route_bwd_ws)
+    torch.cuda.synchronize()
+    np.testing.assert_allclose(to_numpy(losses), ref["losses"], rtol=1e-4, atol=1e-7)
+    assert_close("dlogits", to_numpy(dl), ref["dlogits"], TOL[W.F32])
+    ex_dx, ex_dwr = OB.router_grad_extra(as_f64(inp["x"], cfg.dtype),
+                                         as_f64(inp["w_router"], cfg.dtype), ref["dlogits"], G)
+    tol = TOL[cfg.dtype]
+    assert_close("dx change", to_numpy(L.dx).astype(np.float64) - to_numpy(dx0), ex_dx, tol)
+    assert_close("dW_router change", to_numpy(L.dw_router).astype(np.float64) - to_numpy(dwr0),
+                 ex_dwr, tol)

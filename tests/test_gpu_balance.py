@@ -25,6 +25,8 @@ CASES = [
     ("e33_k3", 513, 1, 33, 3, 0.05, True, True, 0),
     ("e64_k8", 700, 1, 64, 8, 1 / 64, False, True, 0),
     ("k_equals_e", 300, 1, 4, 4, 0.25, False, True, 0),
+    ("e8_bias_no_noise", 512, 2, 8, 2, 0.125, True, False, 0),
+    ("e24_bias_no_noise_hot", 480, 1, 24, 2, 0.1, True, False, 2),
     ("single_expert", 128, 2, 1, 1, 1.0, False, True, 0),
     ("empty", 0, 1, 8, 2, 0.125, False, True, 0),
     ("vitb16_6304_e8", 6304, 1, 8, 2, 1 / 8, False, True, 0),

@@ -1,11 +1,14 @@
 """Benchmark: one V-MoE layer forward + backward on one MI355X.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+                    [--flush-mall]
 
 A step is one pass of the whole layer: routing (router product, noisy top-k,
 batch-prioritized capacity), dispatch, expert MLP forward, combine, and the
-backward of all of them, on synthetic ViT-B/16-shaped tokens already resident
-in HBM. W untimed warm-up steps, then K timed steps between device
+backward of all of them, on synthetic ViT-shaped tokens already resident in
+HBM. The default workload is the largest: ViT-L/16 at 384 px, 64 images x 577
+tokens, d_model 1024, d_ff 4096, 32 experts (four hot), top-2, capacity
+factor 1.05. W untimed warm-up steps, then K timed steps between device
 synchronisations. Prints ONE JSON line.
 
 Inside the timed steps only the dominant call, the expert-MLP backward, is
@@ -109,33 +112,40 @@ def measured_traffic(workload: str, call: str):
     return calls.get(call)
 
 
-def cpu_baseline(cfg, inputs, C_full, budget_s=20.0):
-    """The oracle as it stands, single-threaded, on a bounded token sample."""
+def _cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(cfg, inputs, C_full):
+    """The oracle as it stands (the one the full-size parity tests use) on the
+    whole workload, the same inputs and routing as the GPU step: routing,
+    moves and router backward in the plain-loop C oracle (OpenMP over
+    tokens), the expert MLP in float64 matrix products (multi-threaded BLAS).
+    Input widening to float64 is not timed."""
     import oracle
+    from oracle.layer_full import layer_packed
     from paper_2608_16188_amd import workloads as W
     oracle.load()
     f = {key: W.to_f64(inputs[key], cfg.dtype) for key in ("x", "w_router", "w1", "b1", "w2",
                                                             "b2", "dy")}
-    G = cfg.n_groups
-    ng = cfg.n_tokens // G
-    n_s = 16
-    while True:
-        # first n_s tokens of group 0 as one routing group, capacity scaled to n_s
-        C = max(1, int(np.floor(cfg.k * n_s * cfg.capacity_factor / cfg.n_experts + 0.5)))
-        sl = slice(0, n_s)
-        bias = inputs["logit_bias"]
-        noise = None if inputs["noise"] is None else inputs["noise"][sl]
-        t0 = time.perf_counter()
-        oracle.layer(f["x"][sl], f["w_router"][:1], f["w1"], f["b1"], f["w2"], f["b2"], f["dy"][sl],
-                     k=cfg.k, C=C, n_groups=1, bias=bias, noise=noise)
-        dt = time.perf_counter() - t0
-        if dt >= budget_s / 4 or n_s * 2 > ng:
-            break
-        n_s *= 2
-    return {"value": n_s / dt, "unit": "tokens/s", "cores": 1, "kind": "oracle",
-            "sample": f"first {n_s} tokens of the workload as one routing group "
-                      f"(capacity {C}), full layer fwd+bwd incl. all expert weight gradients, "
-                      f"single-threaded C oracle, double precision; {dt:.1f} s"}
+    threads = int(os.environ.get("OMP_NUM_THREADS") or os.cpu_count() or 1)
+    t0 = time.perf_counter()
+    layer_packed(f["x"], f["w_router"], f["w1"], f["b1"], f["w2"], f["b2"], f["dy"], k=cfg.k,
+                 C=C_full, n_groups=cfg.n_groups, bias=inputs["logit_bias"],
+                 noise=inputs["noise"], want_dwr=not cfg.routers_frozen)
+    dt = time.perf_counter() - t0
+    return {"value": cfg.n_tokens / dt, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"the whole workload ({cfg.n_tokens} tokens, its own routing), one "
+                      f"forward + backward in float64: C oracle (OpenMP) for routing, moves "
+                      f"and router backward, float64 BLAS products for the expert MLP; "
+                      f"{dt:.1f} s on {threads} threads",
+            "nproc": os.cpu_count(), "cpu_model": _cpu_model()}
 
 
 def balance_losses(L, V, stream, K):
@@ -145,7 +155,10 @@ def balance_losses(L, V, stream, K):
     import torch
     s, cfg = L.shape, L.cfg
     N, G, E = cfg.n_tokens, cfg.n_groups, cfg.n_experts
-    sigma = 1.0 / E
+    # the load term's width is the standard deviation the gating noise was
+    # drawn with; a noise-free workload takes 1/E as its smoothing width
+    noisy = L.noise is not None
+    sigma = float(np.sqrt(cfg.noise_var)) if noisy else 1.0 / E
     f32 = torch.float32
     losses = torch.empty(G, 2, dtype=f32, device="cuda")
     dl = torch.empty(max(N, 1), E, dtype=f32, device="cuda")
@@ -184,7 +197,8 @@ def balance_losses(L, V, stream, K):
     rows = 2 + (L.noise is not None)
     nbytes = (2 * rows + 1) * N * E * 4
     return {"ms": round(ms, 4), "gbs": round(nbytes / (ms * 1e-3) / 1e9, 1),
-            "algorithmic_bytes": nbytes, "noise_std": sigma,
+            "algorithmic_bytes": nbytes,
+            ("noise_std" if noisy else "smoothing_width_no_noise"): sigma,
             "dispatch_route_bwd_ms": round(ms_bwd, 4),
             "dispatch_route_bwd_dlogits_ms": round(ms_bwd_dl, 4),
             "note": "vmoe_balance_loss, then the fused router backward without and with its "
@@ -196,8 +210,11 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="vitb16_bf16")
+    ap.add_argument("--workload", default="vitl16_384_bf16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--flush-mall", action="store_true",
+                    help="after the timed region, time every call again with a 512 MiB "
+                         "buffer written before each step (the 256 MB MALL holds no inputs)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="before warm-up, copy one 256 MiB buffer (a plain copy kernel of known "
                          "size, to calibrate the HBM byte counters of a profiler run)")
@@ -295,6 +312,24 @@ def main():
                 for c, name in enumerate(CALLS)}
     step_ms_events = float(np.mean([evc[i][0].elapsed_time(evc[i][-1]) for i in range(K)]))
 
+    flushed = None
+    if args.flush_mall:
+        # per-call times with the MALL flushed before every step: a 512 MiB
+        # buffer is written between steps, outside the events
+        scratch = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+        evf = [[torch.cuda.Event(enable_timing=True) for _ in range(len(CALLS) + 1)]
+               for _ in range(K)]
+        for i in range(K):
+            scratch.fill_(i & 0xFF)
+            evf[i][0].record(stream)
+            for c, name in enumerate(CALLS):
+                calls[name]()
+                evf[i][c + 1].record(stream)
+        torch.cuda.synchronize()
+        del scratch
+        flushed = {name: float(np.mean([evf[i][c].elapsed_time(evf[i][c + 1])
+                                        for i in range(K)])) for c, name in enumerate(CALLS)}
+
     balance = balance_losses(L, V, stream, K)
 
     counts = L.counts.cpu().numpy()
@@ -303,6 +338,19 @@ def main():
     peak_mfma = PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_F32_TFLOPS
     fl, by = cost[dom]
     ach = fl / (dom_ms * 1e-3) / 1e12
+    ach_gbs = by / (dom_ms * 1e-3) / 1e9
+    # the call's binding roof: the larger of its matrix-core time at peak and
+    # its algorithmic HBM bytes at peak bandwidth
+    hbm_bound = by / (PEAK_HBM_GBS * 1e9) > fl / (peak_mfma * 1e12)
+    if hbm_bound:
+        roof = {"bound": "hbm", "kernel": f"vmoe_expert_{dom}", "achieved": ach_gbs,
+                "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": ach_gbs / PEAK_HBM_GBS}
+    else:
+        roof = {"bound": "mfma", "kernel": f"vmoe_expert_{dom}", "achieved": ach,
+                "peak": peak_mfma, "unit": "TFLOP/s", "frac": ach / peak_mfma}
+    roof.update({"traffic": measured_traffic(args.workload, dom), "algorithmic_bytes": by,
+                 "algorithmic_flops": fl, "mfma_frac": ach / peak_mfma,
+                 "hbm_frac": ach_gbs / PEAK_HBM_GBS, "ms": dom_ms})
     # the expert-MLP summary: the backward from the timed region, the forward
     # from the per-call pass
     ffn_total_ms = per_call["ffn_fwd"] + dom_ms
@@ -333,10 +381,7 @@ def main():
                                f"{cfg.capacity_factor}, groups {cfg.n_groups}",
                    "global_batch": cfg.images, "seq_len": cfg.tokens_per_image,
                    "capacity": L.C, "kept_assignments": A, "parallelism": "single GPU"},
-        "roofline": {"bound": "mfma", "kernel": f"vmoe_expert_{dom}",
-                     "achieved": ach, "peak": peak_mfma, "unit": "TFLOP/s",
-                     "frac": ach / peak_mfma, "traffic": measured_traffic(args.workload, dom),
-                     "algorithmic_bytes": by},
+        "roofline": roof,
         "expert_gemms": {"tflops": ffn_tflops, "frac_of_peak": ffn_tflops / peak_mfma,
                          "ms": ffn_total_ms},
         "route_dispatch_combine": {"gbs": moves_bytes / (moves_ms * 1e-3) / 1e9,
@@ -347,6 +392,15 @@ def main():
         "step_ms_events": step_ms_events,
         "balance_losses": balance,
     }
+    if flushed is not None:
+        fb = sum(cost[n][1] for n in moves)
+        fm = sum(flushed[n] for n in moves)
+        out["mall_flushed"] = {
+            "per_call_ms": {n: round(v, 4) for n, v in flushed.items()},
+            "route_dispatch_combine_gbs": fb / (fm * 1e-3) / 1e9,
+            "route_dispatch_combine_frac_of_hbm": fb / (fm * 1e-3) / 1e9 / PEAK_HBM_GBS,
+            "ffn_bwd_gbs": by / (flushed[dom] * 1e-3) / 1e9,
+            "note": "a 512 MiB buffer written before each step, outside the events"}
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, inputs, L.C)
     print(json.dumps(out), flush=True)

@@ -42,8 +42,12 @@
  * - Errors are status codes, checked before anything is enqueued: a NULL
  *   required pointer, N % G != 0, k outside [1, E], E > 64, d or f not a
  *   multiple of 8, a non-positive capacity factor, an unknown dtype or
- *   misaligned pointer -> VMOE_ERR_INVALID_ARG; a too-small workspace ->
- *   VMOE_ERR_WORKSPACE; a failed kernel launch -> VMOE_ERR_HIP. Required
+ *   misaligned pointer -> VMOE_ERR_INVALID_ARG; a shape beyond the kernels'
+ *   32-bit addressing (one expert's [G*C, d or f] operand or [f, d] weight of
+ *   2 GiB or more, or 2^31 or more elements in the pooled expert buffers or
+ *   the token-major tensors) -> VMOE_ERR_UNSUPPORTED (vmoe_capacity returns
+ *   -1 for it); a too-small workspace -> VMOE_ERR_WORKSPACE; a failed kernel
+ *   launch -> VMOE_ERR_HIP. Required
  *   pointers are checked whatever the sizes: with N = 0 they still point to
  *   an allocation (nothing is read from it). Nothing
  *   throws across the ABI. All entry points are thread-safe (stateless).
@@ -250,8 +254,9 @@ size_t vmoe_balance_loss_workspace_bytes(const vmoe_shape* shape);
  *   noise_std  > 0, the standard deviation the noise was drawn with
  *   losses [G, 2], dlogits [N, E] f32 out; importance, load [G, E] f32 out
  *   or NULL; workspace: vmoe_balance_loss_workspace_bytes(shape) bytes.
- * Sums over tokens are f32 within a 256-token chunk and double across chunks
- * in chunk order (deterministic); VMOE_ERR_INVALID_ARG for a non-positive or
+ * Sums over tokens are f32 within a chunk of tokens and double across chunks
+ * in chunk order (deterministic); the chunk is 256 tokens for E <= 16, 128
+ * for E <= 32 and 64 for E <= 64. VMOE_ERR_INVALID_ARG for a non-positive or
  * non-finite noise_std or non-finite weights. */
 vmoe_status vmoe_balance_loss(const vmoe_shape* shape, const float* logits,
                               const float* logit_bias, const float* noise, const float* probs,

@@ -31,6 +31,11 @@
  *
  * Array conventions: row-major; float64 arrays hold values that are exactly
  * representable in the layer's dtype (bf16 or f32), widened by the caller.
+ *
+ * Threads. Built with OpenMP, loops over independent outputs (tokens, rows,
+ * weight entries) are shared among threads; every output is still computed
+ * by one thread with the sums in the order written, so results do not depend
+ * on the thread count.
  */
 #include <math.h>
 #include <stdint.h>
@@ -93,6 +98,7 @@ float orc_exp(float u) {
 void orc_router_logits(int N, int G, int d, int E, const double* x, const double* wr,
                        float* logits) {
     int ng = N / G;
+#pragma omp parallel for schedule(static)
     for (int t = 0; t < N; ++t) {
         const double* w = wr + (size_t)(t / ng) * E * d;
         for (int e = 0; e < E; ++e) {
@@ -220,6 +226,7 @@ static long row_of(int t, int j, int ng, int E, int k, int C, int G, const int32
 void orc_dispatch(int N, int G, int d, int E, int k, int C, const double* x, const int32_t* idx,
                   const int32_t* slot, const int32_t* row_base, double* xe) {
     int ng = N / G;
+#pragma omp parallel for schedule(static)
     for (int t = 0; t < N; ++t)
         for (int j = 0; j < k; ++j) {
             long row = row_of(t, j, ng, E, k, C, G, idx, slot, row_base);
@@ -234,6 +241,7 @@ void orc_combine_fwd(int N, int G, int d, int E, int k, int C, const double* ye,
                      const int32_t* idx, const int32_t* slot, const int32_t* row_base,
                      const float* gate, double* y) {
     int ng = N / G;
+#pragma omp parallel for schedule(static)
     for (int t = 0; t < N; ++t) {
         for (int i = 0; i < d; ++i) y[(size_t)t * d + i] = 0.0;
         for (int j = 0; j < k; ++j) {
@@ -251,6 +259,7 @@ void orc_combine_bwd(int N, int G, int d, int E, int k, int C, const double* dy,
                      const double* ye, const int32_t* idx, const int32_t* slot,
                      const int32_t* row_base, const float* gate, double* dye, double* dgate) {
     int ng = N / G;
+#pragma omp parallel for schedule(static)
     for (int t = 0; t < N; ++t)
         for (int j = 0; j < k; ++j) {
             long row = row_of(t, j, ng, E, k, C, G, idx, slot, row_base);
@@ -273,6 +282,7 @@ void orc_dispatch_bwd(int N, int G, int d, int E, int k, int C, const double* dx
                       const int32_t* idx, const int32_t* slot, const int32_t* row_base,
                       double* dx) {
     int ng = N / G;
+#pragma omp parallel for schedule(static)
     for (int t = 0; t < N; ++t) {
         for (int i = 0; i < d; ++i) dx[(size_t)t * d + i] = 0.0;
         for (int j = 0; j < k; ++j) {
@@ -301,8 +311,11 @@ static double gelu_grad(double h) {
 void orc_ffn_fwd(int rows, int d, int f, const double* xe, const double* w1, const double* b1,
                  const double* w2, const double* b2, double* H, double* A, double* G,
                  double* ye) {
+#pragma omp parallel
+    {
     double* h = (double*)malloc(sizeof(double) * f);
     double* a = (double*)malloc(sizeof(double) * f);
+#pragma omp for schedule(static)
     for (int r = 0; r < rows; ++r) {
         for (int j = 0; j < f; ++j) {
             double acc = b1[j];
@@ -321,6 +334,7 @@ void orc_ffn_fwd(int rows, int d, int f, const double* xe, const double* w1, con
     }
     free(h);
     free(a);
+    }
 }
 
 /* Per-row backward of one expert's MLP (H is recomputed from xe):
@@ -331,7 +345,10 @@ void orc_ffn_fwd(int rows, int d, int f, const double* xe, const double* w1, con
 void orc_ffn_bwd_rows(int rows, int d, int f, const double* xe, const double* w1,
                       const double* b1, const double* w2, const double* dye, double* dxe,
                       double* dH) {
+#pragma omp parallel
+    {
     double* dh = (double*)malloc(sizeof(double) * f);
+#pragma omp for schedule(static)
     for (int r = 0; r < rows; ++r) {
         for (int j = 0; j < f; ++j) {
             double h = b1[j];
@@ -348,6 +365,7 @@ void orc_ffn_bwd_rows(int rows, int d, int f, const double* xe, const double* w1
         }
     }
     free(dh);
+    }
 }
 
 /* Weight gradients of one expert's MLP over its `rows` kept rows:
@@ -360,6 +378,7 @@ void orc_ffn_bwd_weights(int rows, int d, int f, const double* xe, const double*
                          double* db1, double* dw2, double* db2) {
     double* A = (double*)malloc(sizeof(double) * ((size_t)rows * f + 1));
     double* dH = (double*)malloc(sizeof(double) * ((size_t)rows * f + 1));
+#pragma omp parallel for schedule(static)
     for (int r = 0; r < rows; ++r)
         for (int j = 0; j < f; ++j) {
             double h = b1[j];
@@ -369,6 +388,7 @@ void orc_ffn_bwd_weights(int rows, int d, int f, const double* xe, const double*
             A[(size_t)r * f + j] = gelu(h);
             dH[(size_t)r * f + j] = da * gelu_grad(h);
         }
+#pragma omp parallel for schedule(static)
     for (int o = 0; o < d; ++o) {
         double sb = 0.0;
         for (int r = 0; r < rows; ++r) sb += dye[(size_t)r * d + o];
@@ -379,6 +399,7 @@ void orc_ffn_bwd_weights(int rows, int d, int f, const double* xe, const double*
             dw2[(size_t)o * f + j] = acc;
         }
     }
+#pragma omp parallel for schedule(static)
     for (int j = 0; j < f; ++j) {
         double sb = 0.0;
         for (int r = 0; r < rows; ++r) sb += dH[(size_t)r * f + j];
@@ -400,6 +421,7 @@ void orc_ffn_bwd_weight_entries(int rows, int d, int f, const double* xe, const 
                                 const double* b1, const double* w2, const double* dye,
                                 int n_samples, const int32_t* which, const int32_t* row,
                                 const int32_t* col, double* out) {
+#pragma omp parallel for schedule(dynamic)
     for (int s = 0; s < n_samples; ++s) {
         int w = which[s];
         /* column j of H / dH is needed by dW1, db1 (j = row) and dW2 (j = col) */
@@ -438,8 +460,11 @@ void orc_route_bwd(int N, int G, int d, int E, int k, const double* x, const dou
                    const float* probs, const int32_t* idx, const int32_t* slot,
                    const double* dgate, double* dx, double* dwr, double* dz_out) {
     int ng = N / G;
-    double* dp = (double*)malloc(sizeof(double) * E);
     double* dz = (double*)malloc(sizeof(double) * (size_t)N * E);
+#pragma omp parallel
+    {
+    double* dp = (double*)malloc(sizeof(double) * E);
+#pragma omp for schedule(static)
     for (int t = 0; t < N; ++t) {
         for (int e = 0; e < E; ++e) dp[e] = 0.0;
         for (int j = 0; j < k; ++j)
@@ -449,6 +474,9 @@ void orc_route_bwd(int N, int G, int d, int E, int k, const double* x, const dou
         for (int e = 0; e < E; ++e)
             dz[(size_t)t * E + e] = (double)probs[(size_t)t * E + e] * (dp[e] - pdp);
     }
+    free(dp);
+    }
+#pragma omp parallel for schedule(static)
     for (int t = 0; t < N; ++t) {
         const double* w = wr + (size_t)(t / ng) * E * d;
         for (int i = 0; i < d; ++i) {
@@ -458,6 +486,7 @@ void orc_route_bwd(int N, int G, int d, int E, int k, const double* x, const dou
         }
     }
     if (dwr) {
+#pragma omp parallel for collapse(3) schedule(static)
         for (int g = 0; g < G; ++g)
             for (int e = 0; e < E; ++e)
                 for (int i = 0; i < d; ++i) {
@@ -468,6 +497,5 @@ void orc_route_bwd(int N, int G, int d, int E, int k, const double* x, const dou
                 }
     }
     if (dz_out) memcpy(dz_out, dz, sizeof(double) * (size_t)N * E);
-    free(dp);
     free(dz);
 }

@@ -77,6 +77,22 @@ vmoe_status make_dims(const vmoe_shape* s, Dims* out) {
     }
     // every buffer index must fit comfortably in 64 bits and rows in 31 bits
     if (static_cast<long long>(D.G) * D.C > 0x7FFFFFFFLL) return VMOE_ERR_INVALID_ARG;
+    // 32-bit addressing limits of the kernels (a legal shape beyond them is
+    // refused rather than computed wrongly):
+    // - a buffer resource spans one expert's operand and reads zeros at byte
+    //   offsets >= 2^31 (the tail-mask offset), so every per-expert operand
+    //   ([G*C, d or f] activations, [f, d] weights) stays below 2^31 bytes;
+    // - expert-buffer rows (E*G*C) and element indices into the expert buffers
+    //   and the token-major tensors ([N, d], [N, E]) are 32-bit integers.
+    const long long lim = 0x7FFFFFFFLL;
+    const long long elem = D.dtype == VMOE_BF16 ? 2 : 4;
+    const long long rows = static_cast<long long>(D.G) * D.C;
+    const long long wide = D.d > D.f ? D.d : D.f;
+    const long long er = rows * D.E;
+    if (rows * wide * elem > lim || static_cast<long long>(D.f) * D.d * elem > lim ||
+        er > lim || er * wide > lim ||
+        static_cast<long long>(D.N) * (wide > D.E ? wide : D.E) > lim)
+        return VMOE_ERR_UNSUPPORTED;
     *out = D;
     return VMOE_OK;
 }

@@ -106,3 +106,83 @@ def rows_of_expert(r: dict, e: int, C: int, G: int):
         toks[row], js[row] = t, j
     assert (toks >= 0).all()
     return toks, js
+
+
+# ------------------------------------------------------------------ every element
+
+def elementwise_rel(got, ref) -> float:
+    """max over elements of |a - b| / max(|b|, 1e-3 max|b|): the element-wise
+    form of the relative error, reported beside the per-tensor one."""
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    if ref.size == 0:
+        return 0.0
+    floor = 1e-3 * float(np.max(np.abs(ref)))
+    if floor == 0.0:
+        return float(np.max(np.abs(got)))
+    return float(np.max(np.abs(got - ref) / np.maximum(np.abs(ref), floor)))
+
+
+class Report:
+    """Per-tensor metrics of one parity case: the per-tensor error
+    max|a - b| / max|b|, the worst row's error against that row's own largest
+    magnitude, and the element-wise form. Tensors checked in parts (one
+    expert at a time) are merged by taking the worst part."""
+
+    def __init__(self, case: str):
+        self.case = case
+        self.m = {}
+
+    def add(self, name, tensor_rel, row_rel, elem_rel):
+        old = self.m.get(name)
+        new = dict(tensor=tensor_rel, worst_row=row_rel, elementwise=elem_rel)
+        if old is not None:
+            new = {k: max(old[k], new[k]) for k in new}
+        self.m[name] = new
+
+    def write(self):
+        import json
+        import os
+        out = os.environ.get("VMOE_PARITY_REPORT_DIR")
+        if out:
+            os.makedirs(out, exist_ok=True)
+            with open(os.path.join(out, f"{self.case}.json"), "w") as fh:
+                json.dump(self.m, fh, indent=1, sort_keys=True)
+        say(self.case, " ".join(f"{k}:{v['tensor']:.1e}/{v['worst_row']:.1e}/"
+                                f"{v['elementwise']:.1e}" for k, v in sorted(self.m.items())))
+
+
+def assert_rows_close(name, got, ref, tol, report=None, block=1):
+    """Every row (leading index) of `got` within tol of `ref`, relative to
+    that row's largest reference magnitude; a row whose reference is all zero
+    must be exactly zero. Catches a wrong row far below the tensor's maximum
+    (a light expert's, a dropped token's), which the per-tensor metric alone
+    would let pass. Also checks the per-tensor metric and finiteness.
+    block > 1 takes rows `block` at a time (a weight gradient's row is the
+    same few coefficients times different vectors, so a single row's scale can
+    sit far below its rounding error; 32 rows is one matrix-core block)."""
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    assert got.shape == ref.shape, (name, got.shape, ref.shape)
+    if ref.size == 0:
+        return
+    assert np.all(np.isfinite(got)), f"{name}: non-finite values"
+    g2 = got.reshape(got.shape[0], -1)
+    r2 = ref.reshape(ref.shape[0], -1)
+    scale = np.max(np.abs(r2), axis=1)
+    err = np.max(np.abs(g2 - r2), axis=1)
+    if block > 1:
+        starts = np.arange(0, len(scale), block)
+        scale = np.maximum.reduceat(scale, starts)
+        err = np.maximum.reduceat(err, starts)
+    zero = scale == 0.0
+    assert np.all(err[zero] == 0.0), f"{name}: rows {np.nonzero(zero & (err > 0))[0][:8]} " \
+                                      "should be exactly zero"
+    row_rel = err[~zero] / scale[~zero]
+    worst = float(np.max(row_rel)) if row_rel.size else 0.0
+    tensor = rel_err(got, ref)
+    if report is not None:
+        report.add(name, tensor, worst, elementwise_rel(got, ref))
+    assert tensor <= tol, f"{name}: max rel err {tensor:.3e} > {tol:.1e}"
+    bad = np.nonzero(~zero)[0][row_rel > tol]
+    assert worst <= tol, f"{name}: rows {bad[:8]} off by up to {worst:.3e} of their magnitude"

@@ -175,3 +175,36 @@ def test_workspace_sizes_are_modest_for_workloads():
                          c.capacity_factor, 1)
         assert 0 < V.vmoe_route_workspace_bytes(s) < 8 << 20
         assert 0 < V.vmoe_route_bwd_workspace_bytes(s) < 64 << 20
+
+
+@pytest.mark.parametrize("kw", [
+    # one expert's [G*C, f] activations pass 2 GiB (bf16): 350 000 rows x 4096
+    dict(n_tokens=350_000, d_model=1024, d_ff=4096, n_experts=2, k=2, capacity_factor=1.0),
+    # the same rows in f32 pass it at half the width
+    dict(n_tokens=300_000, d_model=1024, d_ff=2048, n_experts=2, k=2, capacity_factor=1.0,
+         dtype=0),
+    # every expert fits, but the pooled buffers' element index passes 2^31
+    dict(n_tokens=100_000, d_model=8, d_ff=4096, n_experts=64, k=8, capacity_factor=1.0),
+    # one expert's [f, d] weight passes 2 GiB
+    dict(n_tokens=64, d_model=32768, d_ff=32768, n_experts=2, k=1, capacity_factor=1.0),
+])
+def test_shapes_beyond_32bit_addressing_unsupported(kw):
+    """Shapes the kernels' 32-bit buffer offsets cannot address are refused
+    with VMOE_ERR_UNSUPPORTED before anything is enqueued."""
+    base = dict(n_groups=1, dtype=1)
+    base.update(kw)
+    s = V.make_shape(**base)
+    b, L = ctypes.byref(s), V._lib
+    assert V.vmoe_capacity(s) == -1
+    assert V.vmoe_route_workspace_bytes(s) == 0
+    assert L.vmoe_dispatch(b, FAKE, FAKE, FAKE, FAKE, FAKE, None) == V.VMOE_ERR_UNSUPPORTED
+    assert L.vmoe_expert_ffn_fwd(b, *([FAKE] * 9), None) == V.VMOE_ERR_UNSUPPORTED
+    assert L.vmoe_expert_ffn_bwd(b, *([FAKE] * 13), None) == V.VMOE_ERR_UNSUPPORTED
+
+
+def test_largest_workload_within_addressing_limits():
+    for c in W.CONFIGS.values():
+        s = V.make_shape(c.n_tokens, c.n_groups, c.d_model, c.d_ff, c.n_experts, c.k,
+                         c.capacity_factor, 1 if c.dtype == W.BF16 else 0)
+        assert V.vmoe_capacity(s) > 0
+

@@ -20,7 +20,7 @@ from paper_2608_16188_amd import workloads as W
 from paper_2608_16188_amd.layer import LayerBuffers, to_numpy
 
 from .gpu_common import (TOL, as_f64, assert_close, assert_router_logits, bits_equal,
-                         oracle_capacity, rows_of_expert, say, workload_inputs)
+                         oracle_capacity, say, workload_inputs)
 
 pytestmark = pytest.mark.gpu
 
@@ -178,6 +178,13 @@ SMALL = [
                     capacity_factor=1.0, router_std=0.3),
     W.custom_config("f32_capacity_two", n_tokens=200, d_model=32, d_ff=64, n_experts=4, k=2,
                     capacity_factor=0.02, dtype=W.F32, router_std=0.2),
+    # several 256-row m-tiles per expert, every element: ten (the forward
+    # GEMMs' patches of four m-tiles and a partial last patch) and eight (one
+    # whole m-column per XCD chunk), with ragged n-tiles and k tails
+    W.custom_config("bf16_ten_mtiles", n_tokens=2400, d_model=72, d_ff=264, n_experts=2, k=2,
+                    capacity_factor=1.0, router_std=0.05),
+    W.custom_config("bf16_eight_mtiles", n_tokens=3000, d_model=136, d_ff=520, n_experts=3,
+                    k=2, capacity_factor=0.9, router_std=0.1),
 ]
 
 
@@ -231,97 +238,6 @@ def test_layer_small_every_element(cfg):
     for e in np.nonzero(n_e == 0)[0]:
         assert np.all(to_numpy(L.dw1)[e] == 0) and np.all(to_numpy(L.dw2)[e] == 0)
         assert np.all(to_numpy(L.db1)[e] == 0) and np.all(to_numpy(L.db2)[e] == 0)
-
-
-# ------------------------------------------------------------------ whole layer, full size
-
-FULL = ["vitb16_bf16", "wide_e32_bf16", "multitask17_bf16", "vitl16_384_bf16"]
-
-
-def _token_reference(t, ref, f, cfg, probs):
-    """y[t] and dx[t] of one token, by the oracle, from the token alone."""
-    G, ng = cfg.n_groups, cfg.n_tokens // cfg.n_groups
-    g = t // ng
-    x_t = f["x"][t:t + 1]
-    y = np.zeros(cfg.d_model)
-    dx = np.zeros((1, cfg.d_model))
-    dgate = np.zeros((1, cfg.k))
-    for j in range(cfg.k):
-        if ref["slot"][t, j] < 0:
-            continue
-        e = ref["idx"][t, j]
-        gj = float(ref["gate"][t, j])
-        _, _, ye = oracle.ffn_fwd(x_t, f["w1"][e], f["b1"][e], f["w2"][e], f["b2"][e])
-        y += gj * ye[0]
-        dxe, _ = oracle.ffn_bwd_rows(x_t, f["w1"][e], f["b1"][e], f["w2"][e], gj * f["dy"][t:t + 1])
-        dx += dxe
-        dgate[0, j] = float(np.dot(f["dy"][t], ye[0]))
-    dx, _, _ = oracle.route_bwd(x_t, f["w_router"][g:g + 1], probs[t:t + 1], ref["idx"][t:t + 1],
-                                ref["slot"][t:t + 1], dgate, 1, dx_in=dx, want_dwr=False)
-    return y, dx[0], dgate[0]
-
-
-@pytest.mark.parametrize("name", FULL)
-def test_layer_full_size_sampled(name):
-    cfg, inp = workload_inputs(name)
-    say("layer full", name)
-    L = LayerBuffers(cfg, inp)
-    L.step()
-    torch.cuda.synchronize()
-    C = oracle_capacity(cfg)
-    f = {key: as_f64(inp[key], cfg.dtype) for key in ("x", "w_router", "w1", "b1", "w2", "b2", "dy")}
-    logits = to_numpy(L.logits)
-    assert_router_logits(logits, f["x"], f["w_router"], cfg.n_groups, cfg.dtype)
-    ref = oracle.route(logits, cfg.k, C, cfg.n_groups, inp["logit_bias"], inp["noise"])
-    got_r = dict(idx=to_numpy(L.expert_idx), slot=to_numpy(L.slot), order=to_numpy(L.order),
-                 counts=to_numpy(L.counts), row_base=to_numpy(L.row_base),
-                 probs=to_numpy(L.probs), gate=to_numpy(L.gate))
-    _compare_routing(got_r, ref, name)
-    tol = TOL[cfg.dtype]
-    rng = np.random.default_rng(0)
-    kept_any = (ref["slot"] >= 0).any(1)
-    toks = list(rng.choice(cfg.n_tokens, 14, replace=False))
-    toks += list(rng.choice(np.nonzero(~kept_any)[0], 2)) if (~kept_any).any() else []
-    toks += list(rng.choice(np.nonzero((ref["slot"] < 0).any(1) & kept_any)[0], 2)) \
-        if ((ref["slot"] < 0).any(1) & kept_any).any() else []
-    y_gpu, dx_gpu, dg_gpu = _f64_out(L.y, cfg.dtype), to_numpy(L.dx), to_numpy(L.dgate)
-    ys, dxs, dgs, yr, dxr, dgr = [], [], [], [], [], []
-    for t in toks:
-        y, dx, dg = _token_reference(t, ref, f, cfg, ref["probs"])
-        ys.append(y_gpu[t]), dxs.append(dx_gpu[t]), dgs.append(dg_gpu[t])
-        yr.append(y), dxr.append(dx), dgr.append(dg)
-    assert_close("y[sampled]", np.array(ys), np.array(yr), tol)
-    assert_close("dx[sampled]", np.array(dxs), np.array(dxr), tol)
-    assert_close("dgate[sampled]", np.array(dgs), np.array(dgr), tol)
-    # weight gradients: sampled entries of the busiest, the least busy non-empty
-    # and (if any) an empty expert
-    n_e = ref["counts"].sum(0)
-    order_e = np.argsort(n_e)
-    experts = {int(order_e[-1]), int(order_e[np.searchsorted(n_e[order_e], 1)])}
-    if (n_e == 0).any():
-        experts.add(int(np.nonzero(n_e == 0)[0][0]))
-    dw1, dw2, db1, db2 = (to_numpy(t) for t in (L.dw1, L.dw2, L.db1, L.db2))
-    d, ff = cfg.d_model, cfg.d_ff
-    for e in sorted(experts):
-        tok_e, j_e = rows_of_expert(ref, e, C, cfg.n_groups)
-        xe_rows = f["x"][tok_e]
-        dye_rows = ref["gate"][tok_e, j_e][:, None].astype(np.float64) * f["dy"][tok_e]
-        ns = 24
-        which = np.repeat([1, 2, 3, 4], ns)
-        row = np.concatenate([rng.integers(0, ff, ns), rng.integers(0, d, ns),
-                              rng.integers(0, ff, ns), rng.integers(0, d, ns)])
-        col = np.concatenate([rng.integers(0, d, ns), rng.integers(0, ff, ns),
-                              np.zeros(2 * ns, np.int64)])
-        refv = oracle.ffn_bwd_weight_entries(xe_rows, f["w1"][e], f["b1"][e], f["w2"][e],
-                                             dye_rows, which, row, col)
-        gotv = np.concatenate([dw1[e][row[:ns], col[:ns]], dw2[e][row[ns:2 * ns], col[ns:2 * ns]],
-                               db1[e][row[2 * ns:3 * ns]], db2[e][row[3 * ns:]]])
-        if n_e[e] == 0:
-            assert np.all(gotv == 0.0) and np.all(refv == 0.0)
-            continue
-        for q, nm in enumerate(["dW1", "dW2", "db1", "db2"]):
-            sl = slice(q * ns, (q + 1) * ns)
-            assert_close(f"{nm}[e={e}]", gotv[sl], refv[sl], tol)
 
 
 @pytest.mark.parametrize("dtype", [W.BF16, W.F32])

@@ -136,6 +136,27 @@ vmoe_status vmoe_route(const vmoe_shape* shape, const void* x, const void* w_rou
                        int32_t* order, int32_t* counts, int32_t* row_base, void* workspace,
                        size_t workspace_bytes, void* stream);
 
+/* Scratch held by vmoe_route_noalloc on each GPU it runs on (16 MiB). */
+#define VMOE_ROUTE_NOALLOC_SCRATCH_BYTES (16u << 20)
+
+/* vmoe_route for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation): the
+ * same routing with the same outputs, bit for bit, but no workspace
+ * argument. Its scratch is a static device array of
+ * VMOE_ROUTE_NOALLOC_SCRATCH_BYTES on each GPU, placed when the library's
+ * code is loaded there and held until the process ends; the call allocates
+ * and frees nothing. Shapes whose vmoe_route_workspace_bytes exceeds that size
+ * get VMOE_ERR_WORKSPACE (before anything is enqueued); VMOE_ERR_HIP if the
+ * array's device address cannot be looked up. Every call on one GPU shares
+ * that GPU's array: calls that overlap on one GPU (on any streams, from any
+ * threads) race on it, and the caller must serialise them. Other arguments
+ * and errors as vmoe_route. */
+vmoe_status vmoe_route_noalloc(const vmoe_shape* shape, const void* x, const void* w_router,
+                               const float* logit_bias, const float* noise, int32_t flags,
+                               float* logits, float* probs, int32_t* expert_idx, int32_t* slot,
+                               float* gate, int32_t* order, int32_t* counts, int32_t* row_base,
+                               void* stream);
+
 /* Dispatch (permutation) of kept tokens into per-expert buffers:
  * xe[row(t, j), :] = x[t, :] for every kept (t, j). x [N, d], xe [E, G*C, d]. */
 vmoe_status vmoe_dispatch(const vmoe_shape* shape, const void* x, const int32_t* expert_idx,

@@ -1,6 +1,8 @@
 // extern "C" entry points of libvmoe: argument validation, then launches.
 #include <math.h>
 
+#include <mutex>
+
 #include "common.h"
 
 namespace vmoe {
@@ -103,6 +105,33 @@ using vmoe::Dims;
 using vmoe::aligned16;
 using vmoe::as_stream;
 
+// Routing scratch of vmoe_route_noalloc: one static array per GPU, which the
+// runtime places when it loads the library's code on that GPU and holds until
+// the process ends. Host code never passes `scratch` itself to a kernel (on
+// the host it only names the symbol); its device address is looked up once
+// per GPU with that GPU current and kept in scratch_ptr.
+static __device__ __align__(256) unsigned char scratch[VMOE_ROUTE_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex scratch_mu;
+void* scratch_ptr[kMaxDevices] = {};
+
+// The current GPU's copy of `scratch`, or nullptr on a HIP error.
+void* scratch_on_current_device() {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    std::lock_guard<std::mutex> lock(scratch_mu);
+    if (scratch_ptr[dev] == nullptr) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr)
+            return nullptr;
+        scratch_ptr[dev] = p;
+    }
+    return scratch_ptr[dev];
+}
+}  // namespace
+
 #define VMOE_TRY(expr)                       \
     do {                                     \
         vmoe_status _s = (expr);             \
@@ -163,6 +192,29 @@ vmoe_status vmoe_route(const vmoe_shape* shape, const void* x, const void* w_rou
     if (workspace_bytes < need_ws || (need_ws > 0 && !dev(workspace))) return VMOE_ERR_WORKSPACE;
     return vmoe::route_launch(D, x, w_router, logit_bias, noise, flags, logits, probs, expert_idx,
                               slot, gate, order, counts, row_base, workspace, as_stream(stream));
+}
+
+vmoe_status vmoe_route_noalloc(const vmoe_shape* shape, const void* x, const void* w_router,
+                               const float* logit_bias, const float* noise, int32_t flags,
+                               float* logits, float* probs, int32_t* expert_idx, int32_t* slot,
+                               float* gate, int32_t* order, int32_t* counts, int32_t* row_base,
+                               void* stream) {
+    Dims D;
+    VMOE_TRY(vmoe::make_dims(shape, &D));
+    VMOE_TRY(need((flags & ~VMOE_ROUTE_LOGITS_IN) == 0));
+    const bool logits_in = (flags & VMOE_ROUTE_LOGITS_IN) != 0;
+    VMOE_TRY(need(logits_in || (dev(x) && dev(w_router))));
+    VMOE_TRY(need(opt(logit_bias) && opt(noise)));
+    VMOE_TRY(need(dev(logits) && dev(probs) && dev(expert_idx) && dev(slot) && dev(gate) &&
+                  dev(order) && dev(counts) && dev(row_base)));
+    // the routing kernels leave no state in the scratch between calls and
+    // need none of it cleared: each pass writes what it later reads
+    if (vmoe::route_workspace_bytes(D) > VMOE_ROUTE_NOALLOC_SCRATCH_BYTES)
+        return VMOE_ERR_WORKSPACE;
+    void* ws = scratch_on_current_device();
+    if (ws == nullptr) return VMOE_ERR_HIP;
+    return vmoe::route_launch(D, x, w_router, logit_bias, noise, flags, logits, probs, expert_idx,
+                              slot, gate, order, counts, row_base, ws, as_stream(stream));
 }
 
 vmoe_status vmoe_dispatch(const vmoe_shape* shape, const void* x, const int32_t* expert_idx,

@@ -63,6 +63,7 @@ def _load():
         getattr(lib, name).argtypes = [S]
     sigs = {
         "vmoe_route": [S, P, P, P, P, ctypes.c_int32] + [P] * 8 + [P, ctypes.c_size_t, P],
+        "vmoe_route_noalloc": [S, P, P, P, P, ctypes.c_int32] + [P] * 8 + [P],
         "vmoe_dispatch": [S] + [P] * 6,
         "vmoe_expert_ffn_fwd": [S] + [P] * 10,
         "vmoe_combine_fwd": [S] + [P] * 7,
@@ -142,6 +143,15 @@ def vmoe_route(shape, x, w_router, logit_bias, noise, flags, logits, probs, expe
         ctypes.byref(shape), _ptr(x), _ptr(w_router), _ptr(logit_bias), _ptr(noise), flags,
         _ptr(logits), _ptr(probs), _ptr(expert_idx), _ptr(slot), _ptr(gate), _ptr(order),
         _ptr(counts), _ptr(row_base), _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def vmoe_route_noalloc(shape, x, w_router, logit_bias, noise, flags, logits, probs, expert_idx,
+                       slot, gate, order, counts, row_base, stream=None):
+    """vmoe_route with the library's static per-GPU scratch (no workspace)."""
+    _check("vmoe_route_noalloc", _lib.vmoe_route_noalloc(
+        ctypes.byref(shape), _ptr(x), _ptr(w_router), _ptr(logit_bias), _ptr(noise), flags,
+        _ptr(logits), _ptr(probs), _ptr(expert_idx), _ptr(slot), _ptr(gate), _ptr(order),
+        _ptr(counts), _ptr(row_base), _stream(stream)))
 
 
 def vmoe_dispatch(shape, x, expert_idx, slot, row_base, xe, stream=None):

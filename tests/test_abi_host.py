@@ -17,7 +17,7 @@ FAKE = 0x10000  # 16-byte aligned, never dereferenced: validation fails first
 
 def test_every_declared_symbol_is_exported():
     declared = V.header_symbols()
-    assert len(declared) == 21, declared
+    assert len(declared) == 22, declared
     out = subprocess.check_output(["nm", "-D", "--defined-only", V.LIB_PATH], text=True)
     exported = {line.split()[-1] for line in out.splitlines() if line.strip()}
     missing = [s for s in declared if s not in exported]
@@ -208,3 +208,23 @@ def test_largest_workload_within_addressing_limits():
                          c.capacity_factor, 1 if c.dtype == W.BF16 else 0)
         assert V.vmoe_capacity(s) > 0
 
+
+def test_route_noalloc_validates_before_touching_the_gpu():
+    """The no-allocation routing call checks its arguments and that the shape's
+    scratch fits the static array before any HIP call."""
+    L = V._lib
+    r = [FAKE] * 8
+    b = ctypes.byref(_shape())
+    assert L.vmoe_route_noalloc(b, None, FAKE, None, None, 0, *r, None) == \
+        V.VMOE_ERR_INVALID_ARG
+    assert L.vmoe_route_noalloc(b, FAKE, FAKE, None, None, 4, *r, None) == \
+        V.VMOE_ERR_INVALID_ARG
+    # 2M tokens need about 24 MiB of routing scratch: more than the 16 MiB array
+    big = V.make_shape(2_000_000, 1, 8, 8, 8, 2, 1.0, 1)
+    assert V.vmoe_route_workspace_bytes(big) > 16 << 20
+    assert L.vmoe_route_noalloc(ctypes.byref(big), FAKE, FAKE, None, None, 0, *r, None) == \
+        V.VMOE_ERR_WORKSPACE
+    for c in W.CONFIGS.values():
+        s = V.make_shape(c.n_tokens, c.n_groups, c.d_model, c.d_ff, c.n_experts, c.k,
+                         c.capacity_factor, 1)
+        assert V.vmoe_route_workspace_bytes(s) <= 16 << 20

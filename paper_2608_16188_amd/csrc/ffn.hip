@@ -383,26 +383,34 @@ template <class T, bool A_KMAJOR, bool B_KMAJOR, int MODE>
 struct Frags {
     static constexpr int FM = T::FM, FN = T::FN;
     bf16x8 a[FM], b[FN];
+    // fm_live: the wave's 32-row blocks that hold rows of the output (wave-
+    // uniform); the A fragments of the others are not read
     __device__ __forceinline__ void read(const uint16_t* As, const uint16_t* Bs, int wm, int wn,
-                                         int ks, int lane) {
+                                         int ks, int lane, int fm_live) {
 #pragma unroll
         for (int i = 0; i < FM; ++i)
-            a[i] = read_frag<T::BM, A_KMAJOR, T::KB, MODE>(As, wm * FM + i, ks, lane);
+            if (i < fm_live)
+                a[i] = read_frag<T::BM, A_KMAJOR, T::KB, MODE>(As, wm * FM + i, ks, lane);
 #pragma unroll
         for (int j = 0; j < FN; ++j)
             b[j] = read_frag<T::BN, B_KMAJOR, T::KB, MODE>(Bs, wn * FN + j, ks, lane);
     }
 };
 
-// acc[i][j] += A-block i x B-block j; the operands are swapped inside the
-// MFMA so that register 4q + r of lane l holds C[m = l % 32][n = 8q + 4 (l / 32) + r].
+// acc[i][j] += A-block i x B-block j for the live row blocks i < fm_live (a
+// wave-uniform scalar, so the skipped products are branches, not masks); the
+// operands are swapped inside the MFMA so that register 4q + r of lane l
+// holds C[m = l % 32][n = 8q + 4 (l / 32) + r].
 template <int FM, int FN, typename F>
-__device__ __forceinline__ void mfma_block(f32x16 (&acc)[FM][FN], const F& f) {
+__device__ __forceinline__ void mfma_block(f32x16 (&acc)[FM][FN], const F& f, int fm_live) {
 #pragma unroll
     for (int i = 0; i < FM; ++i)
+        if (i < fm_live) {
 #pragma unroll
-        for (int j = 0; j < FN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.b[j], f.a[i], acc[i][j], 0, 0, 0);
+            for (int j = 0; j < FN; ++j)
+                acc[i][j] =
+                    __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.b[j], f.a[i], acc[i][j], 0, 0, 0);
+        }
 }
 
 // Bias of the columns a lane owns: column 32 j + 8 q + 4 (l / 32) + 0..3 of the
@@ -437,7 +445,7 @@ template <class T, class CFG, int EPI>
 __device__ __forceinline__ void gemm_epilogue(const GemmArgs& p, f32x16 (&acc)[T::FM][T::FN],
                                               uint16_t* part_buf,
                                               uint16_t* ep_buf, float rsum, bool row_sum, int e,
-                                              int M, int N, int m0, int n0) {
+                                              int M, int N, int m0, int n0, int fm_live) {
     constexpr int FM = T::FM, FN = T::FN, WM = T::WM, WN = T::WN, BM_ = T::BM;
     constexpr int EP_LD = CFG::EP_LD, ELEM = CFG::ELEM, EP_TILE = CFG::EP_TILE;
     constexpr int IPP = CFG::IPP, OUTS = CFG::OUTS, EPO = CFG::EP_OUTS_AT_ONCE;
@@ -470,6 +478,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& p, f32x16 (&acc)[T
 
 #pragma unroll
     for (int i0 = 0; i0 < FM; i0 += IPP) {
+        if (i0 >= fm_live) break;  // the wave's remaining rows are past M
         // saved gelu'(H) of this pass's rows, all loads in flight together
         uint2 aux[EPI == EPI_GELU_GRAD ? IPP * FN * 4 : 1];
         if constexpr (EPI == EPI_GELU_GRAD) {
@@ -650,6 +659,11 @@ void gemm_bf16_kernel(GemmBatch batch) {
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int wm = wave / T::WGN, wn = wave % T::WGN;
+    // 32-row blocks of this wave's rows that lie inside M: an expert with a
+    // few rows (a light expert under a skewed load) runs the matrix-core
+    // products, fragment reads and epilogue of those blocks only
+    const int fm_live = __builtin_amdgcn_readfirstlane(
+        min(FM, max(0, (M - m0 - wm * T::WM + 31) / 32)));
     // weight-gradient GEMMs: the first n-tile also sums its A rows (bias grad);
     // thread t adds row t % BM over k slice t / BM of each stage
     const bool row_sum = CFG::F32_OUT && p.bsum != nullptr && tn == 0;
@@ -667,6 +681,14 @@ void gemm_bf16_kernel(GemmBatch batch) {
     // NS - 2 later stages are still in flight
     constexpr int L = DA::PER + DB::PER;
     constexpr int WAIT_IMM = VmWait<MODE == STAGE_DMA && !T::PAIR ? (NS - 2) * L : 0>::imm;
+    // A k-major A operand's DMA blocks of wave w hold rows [w BM / NW, (w + 1)
+    // BM / NW) of the tile: a wave whose rows all lie past M (an expert with
+    // few rows) issues none of its A loads (those rows are never read: their
+    // products are skipped) and counts only its B loads in its waits
+    constexpr bool SKIP_A = A_KMAJOR && MODE == STAGE_DMA && !T::PAIR;
+    constexpr int WAIT_IMM_B = VmWait<SKIP_A ? (NS - 2) * DB::PER : 0>::imm;
+    const bool skip_a =
+        SKIP_A && __builtin_amdgcn_readfirstlane(m0 + wave * (BM_ / T::NW)) >= M;
     // paired fetch: after an even stage the pair issued in it is in flight,
     // after an odd stage the second half of the previous pair
     constexpr int WAIT_EVEN = VmWait<T::PAIR ? 2 * L : 0>::imm;
@@ -679,8 +701,13 @@ void gemm_bf16_kernel(GemmBatch batch) {
     uint4 ra[MODE == STAGE_REG ? RA::V : 1], rb[MODE == STAGE_REG ? RB::V : 1];
 
     auto issue = [&](int kt, uint16_t* dst) {
-        DA::issue(ra_rs, p.a.ld, m0, M, kt * KB, K, dst);
+        if (!skip_a) DA::issue(ra_rs, p.a.ld, m0, M, kt * KB, K, dst);
         DB::issue(rb_rs, p.b.ld, n0, N, kt * KB, K, dst + AE);
+    };
+    // wait until stage kt + 1 has landed (this wave's share of it)
+    auto wait_ring = [&]() {
+        if (skip_a) __builtin_amdgcn_s_waitcnt(WAIT_IMM_B);
+        else __builtin_amdgcn_s_waitcnt(WAIT_IMM);
     };
     // the accumulators start from the bias where there is one (added once per
     // output instead of in the epilogue); its loads were issued first, so
@@ -715,7 +742,7 @@ void gemm_bf16_kernel(GemmBatch batch) {
             if constexpr (NS > 3) issue(2, buf2);
             if constexpr (NS > 4) issue(3, buf3);
             init_acc();
-            __builtin_amdgcn_s_waitcnt(WAIT_IMM);
+            wait_ring();
         }
         ring_barrier();
     } else {
@@ -726,7 +753,7 @@ void gemm_bf16_kernel(GemmBatch batch) {
         RB::store(buf0 + AE, rb);
         __syncthreads();
     }
-    f0.read(buf0, buf0 + AE, wm, wn, 0, lane);
+    f0.read(buf0, buf0 + AE, wm, wn, 0, lane, fm_live);
 
     // stage kt computes from `cur`, refills `tgt` (the buffer of stage kt - 1;
     // paired fetch: at even kt, `tgt` and `tgt2` with stages kt + 2 and kt + 3)
@@ -758,13 +785,13 @@ void gemm_bf16_kernel(GemmBatch batch) {
 #pragma unroll
             for (int s = 0; s < KSTEPS - 1; ++s) {
                 if (s % 2 == 0) {
-                    f1.read(cur, cur + AE, wm, wn, s + 1, lane);
+                    f1.read(cur, cur + AE, wm, wn, s + 1, lane, fm_live);
                     __builtin_amdgcn_sched_barrier(0);
-                    mfma_block(acc, f0);
+                    mfma_block(acc, f0, fm_live);
                 } else {
-                    f0.read(cur, cur + AE, wm, wn, s + 1, lane);
+                    f0.read(cur, cur + AE, wm, wn, s + 1, lane, fm_live);
                     __builtin_amdgcn_sched_barrier(0);
-                    mfma_block(acc, f1);
+                    mfma_block(acc, f1, fm_live);
                 }
                 __builtin_amdgcn_sched_barrier(0);
             }
@@ -773,7 +800,7 @@ void gemm_bf16_kernel(GemmBatch batch) {
             __builtin_amdgcn_s_waitcnt(EVEN ? WAIT_EVEN : WAIT_ODD);
             ring_barrier();
         } else if constexpr (MODE == STAGE_DMA) {
-            __builtin_amdgcn_s_waitcnt(WAIT_IMM);
+            wait_ring();
             ring_barrier();
         } else {
             RA::store(nxt, ra);
@@ -782,9 +809,9 @@ void gemm_bf16_kernel(GemmBatch batch) {
         }
         if (live) {
             // KSTEPS is even: the last step's fragments are in f1
-            f0.read(nxt, nxt + AE, wm, wn, 0, lane);
+            f0.read(nxt, nxt + AE, wm, wn, 0, lane, fm_live);
             __builtin_amdgcn_sched_barrier(0);
-            mfma_block(acc, f1);
+            mfma_block(acc, f1, fm_live);
             __builtin_amdgcn_sched_barrier(0);
         }
     };
@@ -827,7 +854,7 @@ void gemm_bf16_kernel(GemmBatch batch) {
     // arrays themselves keeps the accesses in the LDS address space)
     const int eb = wave % NS;
     uint16_t* const ep = eb == 0 ? buf0 : eb == 1 ? buf1 : eb == 2 ? buf2 : eb == 3 ? buf3 : buf4;
-    gemm_epilogue<T, CFG, EPI>(p, acc, buf0, ep, rsum, row_sum, e, M, N, m0, n0);
+    gemm_epilogue<T, CFG, EPI>(p, acc, buf0, ep, rsum, row_sum, e, M, N, m0, n0, fm_live);
 }
 
 // ------------------------------------------------------------------ f32 FMA path
@@ -965,6 +992,8 @@ __global__ __launch_bounds__(256) void colsum_kernel(const T* __restrict__ src,
                                                   part[2][c & 63]) + part[3][c & 63];
 }
 
+constexpr int kNumCUs = 256;
+
 // One launch over `n` (1 or 2) problems; grid_m_rows[i] bounds problem i's m.
 template <class T, bool AK, bool BK_, int EPI>
 void launch_bf16(const Dims& D, const GemmArgs* a, const int* grid_m_rows, int n, hipStream_t st) {
@@ -997,8 +1026,6 @@ void launch_bf16(const Dims& D, const GemmArgs& a, int grid_m_rows, hipStream_t 
 using TileBig = Tile<256, 256, 2, 4, 32, 4, STAGE_DMA>;    // 8 waves, one block per CU
 using TileNarrow = Tile<256, 192, 4, 2, 64, 2, STAGE_DMA>; // 8 waves, 3/4 of TileBig's columns
 using TileSmall = Tile<128, 128, 2, 2, 32, 4, STAGE_DMA>;  // 4 waves, two blocks per CU
-
-constexpr int kNumCUs = 256;
 
 // Work of a launch in units of one CU's time: rounds of one-block-per-CU
 // waves times the tile's area (relative cost per tile area `eff`).

@@ -440,41 +440,167 @@ __global__ __launch_bounds__(256) void route_bwd_kernel(
 
 // ---------------------------------------------------------------- E > 16
 //
-// With many experts the two products of a chunk are small GEMMs of f32
-// operands, dx[t, c] += sum_e dz[t, e] W[e, c] (k = E) and
-// P[e, c] = sum_t dz[t, e] x[t, c] (k = the chunk's tokens), and run on the
-// f32 matrix cores (v_mfma_f32_32x32x2_f32: products and sums in f32). Block
-// = kMfmaTok tokens x kMfmaCols columns of one group, four waves: wave w
-// computes dx for tokens [32 w, 32 w + 32) over all the block's columns and
-// P for columns [32 w, 32 w + 32) over all experts, so no wave waits for
-// another. W[:, cols] (as f32) and x[tokens, cols] are staged in LDS with
-// rows padded so the two rows a fragment reads fall on different banks; dz
-// rows have an odd stride, so a column of dz is read without conflicts.
-typedef float f32x16_m __attribute__((ext_vector_type(16)));
-constexpr int kMfmaTok = 128, kMfmaCols = 128;
-constexpr int kXLd = kMfmaCols + 32;  // bf16 per staged x row
-constexpr int kWLd = kMfmaCols + 16;  // f32 per staged W row
+// With many experts (bf16 layers) the two products of a token chunk are small
+// GEMMs, dx[t, c] += sum_e dz[t, e] W[e, c] (k = E) and
+// P[e, c] = sum_t dz[t, e] x[t, c] (k = the chunk's tokens), run on the bf16
+// matrix cores (v_mfma_f32_32x32x16_bf16, f32 sums). x and W are bf16 already;
+// dz (f32) enters as three bf16 terms dz = hi + mid + lo (each the rounded
+// remainder of the previous), which carry its 24 significant bits, so every
+// product dz W or dz x is formed as three exact bf16 products summed in f32.
+//
+// dz is formed first, once per token, by its own kernel (rbwd_dz_kernel) into
+// the workspace, so the product kernel starts streaming at once: a block =
+// kRbTok tokens x kRbCols columns of one group, four waves; dz rows (f32), W
+// columns (transposed to [column][expert] bf16) and x rows are staged in LDS,
+// wave w computes dx for tokens [32 w, 32 w + 32) over the block's columns and
+// the partial P for columns [32 w, 32 w + 32) over all experts.
+constexpr int kRbTok = 128, kRbCols = 128;
+constexpr int kRbXLd = kRbCols + 16;  // bf16 per staged x row (rows 32 bytes apart in banks)
 
-// KJ > 0 (fused with the dispatch backward): dx starts from the token's kept
-// dxe rows, summed in j order from 0, instead of from dx.
-template <int EMAX, bool DW, int KJ>
-__global__ __launch_bounds__(256) void route_bwd_mfma_kernel(
-    const uint16_t* __restrict__ x, const uint16_t* __restrict__ wr,
+typedef __bf16 bf16x8_r __attribute__((ext_vector_type(8)));
+typedef float f32x16_r __attribute__((ext_vector_type(16)));
+typedef short s16x4_r __attribute__((ext_vector_type(4)));
+typedef short s16x8_r __attribute__((ext_vector_type(8)));
+
+// dz[t, e] = p (dp - <p, dp>) (+ dz_add) for every token, f32 [N, E]: EL lanes
+// per token (EL = the power of two >= E), lane e holding expert e; <p, dp> is
+// summed over the kept experts in ascending e with fused multiply-adds (the
+// order the fused kernel of fewer experts uses). With rows != null also the
+// expert-buffer row of each kept assignment, rows [N, k] (-1 = dropped).
+template <int EL>
+__global__ __launch_bounds__(256) void rbwd_dz_kernel(
     const float* __restrict__ probs, const int32_t* __restrict__ idx,
-    const int32_t* __restrict__ slot, const float* __restrict__ dgate, float* __restrict__ dx,
-    float* __restrict__ partial, const uint16_t* __restrict__ dxe,
-    const int32_t* __restrict__ row_base, const float* __restrict__ dz_add, long long gc, int Ng,
-    int d, int E, int k, int nch) {
-    constexpr int LD = EMAX + 1, TCH = kMfmaTok, COLS = kMfmaCols;
-    constexpr int XV = TCH * COLS / 8 / 256;    // 16-byte x vectors per thread
-    constexpr int WV = EMAX * COLS / 8 / 256;   // 16-byte W vectors per thread
-    constexpr int DPS = TCH * LD > TCH * kXLd / 2 ? TCH * LD : TCH * kXLd / 2;
-    __shared__ __attribute__((aligned(16))) float dzs[TCH * LD];
-    __shared__ __attribute__((aligned(16))) float xdp[DPS];  // dp while forming dz, then x
-    __shared__ __attribute__((aligned(16))) float ws[EMAX * kWLd];
-    __shared__ float pdp_s[TCH];
-    __shared__ int rows_s[KJ > 0 ? TCH * KJ : 1];  // dxe rows, -1 = not kept
-    __shared__ int rb_s[KJ > 0 ? EMAX : 1];        // row_base[g, :]
+    const int32_t* __restrict__ slot, const float* __restrict__ dgate,
+    const float* __restrict__ dz_add, const int32_t* __restrict__ row_base,
+    float* __restrict__ dz, int32_t* __restrict__ rows, long long gc, int N, int Ng, int E,
+    int k) {
+    constexpr int TPB = 256 / EL, KB = 8;
+    const int sub = threadIdx.x % EL;
+    const int t = blockIdx.x * TPB + static_cast<int>(threadIdx.x) / EL;
+    if (t >= N) return;  // uniform per group of EL lanes (EL divides 64)
+    const size_t te = static_cast<size_t>(t) * E, tk = static_cast<size_t>(t) * k;
+    const int g = t / Ng;
+    // every input of the token requested together: its probabilities (lane e),
+    // its first KB assignments (every lane), the group's row bases (lane e)
+    const float p = sub < E ? probs[te + sub] : 0.0f;
+    const float add = (dz_add != nullptr && sub < E) ? dz_add[te + sub] : 0.0f;
+    const int rb = (rows != nullptr && sub < E) ? row_base[static_cast<size_t>(g) * E + sub] : 0;
+    int ej[KB], sj[KB];
+    float gj[KB];
+#pragma unroll
+    for (int u = 0; u < KB; ++u) {
+        const size_t q = tk + min(u, k - 1);
+        ej[u] = idx[q];
+        sj[u] = slot[q];
+        gj[u] = dgate[q];
+    }
+    float dp = 0.0f;
+    int kept = 0;
+    for (int j0 = 0; j0 < k; j0 += KB) {
+        if (j0 > 0) {
+#pragma unroll
+            for (int u = 0; u < KB; ++u) {
+                const size_t q = tk + min(j0 + u, k - 1);
+                ej[u] = idx[q];
+                sj[u] = slot[q];
+                gj[u] = dgate[q];
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < KB; ++u) {
+            if (j0 + u < k && ej[u] == sub && sj[u] >= 0) {  // top-k experts are distinct
+                dp = gj[u];
+                kept = 1;
+            }
+        }
+    }
+    float pdp = 0.0f;
+    if (k <= KB) {
+        // the kept assignments' p[e_j] dgate_j, added in ascending e_j
+        float pe[KB];
+#pragma unroll
+        for (int u = 0; u < KB; ++u) pe[u] = __shfl(p, ej[u] & (EL - 1), EL);
+        int last = -1;
+        for (int r = 0; r < k; ++r) {
+            int best = 1 << 30, bu = -1;
+#pragma unroll
+            for (int u = 0; u < KB; ++u)
+                if (u < k && sj[u] >= 0 && ej[u] > last && ej[u] < best) {
+                    best = ej[u];
+                    bu = u;
+                }
+            if (bu < 0) break;
+            float pv = 0.0f, gv = 0.0f;
+#pragma unroll
+            for (int u = 0; u < KB; ++u)
+                if (u == bu) {
+                    pv = pe[u];
+                    gv = gj[u];
+                }
+            pdp = __builtin_fmaf(pv, gv, pdp);
+            last = best;
+        }
+    } else {
+        for (int e = 0; e < E; ++e) {
+            const float pe = __shfl(p, e, EL), de = __shfl(dp, e, EL);
+            if (__shfl(kept, e, EL)) pdp = __builtin_fmaf(pe, de, pdp);
+        }
+    }
+    if (sub < E) {
+        float v = kept ? p * (dp - pdp) : -p * pdp;
+        if (dz_add != nullptr) v = v + add;
+        dz[te + sub] = v;
+    }
+    if (rows != nullptr) {
+        // lane j < k: the expert-buffer row of assignment j (k <= KB here: the
+        // fused call runs for k <= 4)
+        int e = 0, sl = -1;
+#pragma unroll
+        for (int u = 0; u < KB; ++u)
+            if (u == sub) {
+                e = ej[u];
+                sl = sj[u];
+            }
+        const int rbe = __shfl(rb, e & (EL - 1), EL);
+        if (sub < k)
+            rows[tk + sub] = sl >= 0 ? static_cast<int>(e * gc + rbe + sl) : -1;
+    }
+}
+
+// Eight f32 values as three bf16x8 terms hi + mid + lo (round to nearest even
+// at each step; each remainder is exact in f32).
+__device__ __forceinline__ void split3(const float (&v)[8], bf16x8_r& hi, bf16x8_r& mid,
+                                       bf16x8_r& lo) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const __bf16 h = static_cast<__bf16>(v[i]);
+        const float r1 = v[i] - static_cast<float>(h);
+        const __bf16 m = static_cast<__bf16>(r1);
+        const float r2 = r1 - static_cast<float>(m);
+        hi[i] = h;
+        mid[i] = m;
+        lo[i] = static_cast<__bf16>(r2);
+    }
+}
+
+// ds_read_b64_tr_b16: within each 16-lane group, lane j reads 4 bf16 at its
+// address and lane i receives element i % 4 of lanes i/4, i/4+4, i/4+8, i/4+12.
+__device__ __forceinline__ s16x4_r rb_read_tr(const uint16_t* p) {
+    typedef __attribute__((address_space(3))) s16x4_r* lds_s16x4;
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4)(p));
+}
+
+template <int EMAX, bool DW, int KJ>
+__global__ __launch_bounds__(512) void route_bwd_mma_kernel(
+    const uint16_t* __restrict__ x, const uint16_t* __restrict__ wr,
+    const float* __restrict__ dz, const int32_t* __restrict__ rows,
+    const uint16_t* __restrict__ dxe, float* __restrict__ dx, float* __restrict__ partial,
+    int Ng, int d, int E, int k, int nch) {
+    constexpr int TCH = kRbTok, COLS = kRbCols, DZLD = EMAX + 1, WLD = EMAX + 8;
+    constexpr int KS = EMAX / 16;  // k-steps of the dx product
+    __shared__ __attribute__((aligned(16))) float dzs[TCH * DZLD];
+    __shared__ __attribute__((aligned(16))) uint16_t wts[COLS * WLD];
+    __shared__ __attribute__((aligned(16))) uint16_t xs[TCH * kRbXLd];
     const int c = blockIdx.x, g = blockIdx.z;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int t0 = c * TCH;
@@ -483,144 +609,195 @@ __global__ __launch_bounds__(256) void route_bwd_mfma_kernel(
     const int c0 = blockIdx.y * COLS;
     const uint16_t* wg = wr + static_cast<size_t>(g) * E * d;
 
-    // x and W tiles: 16-byte vectors, zero past the chunk, the experts or d
-    uint4 xv[XV], wv[WV];
-    auto issue = [&] {
+    const int m = lane & 31, kh = lane >> 5;
+    // waves 0-3 form dx, waves 4-7 the router-gradient partial, at the same
+    // time once the tiles are staged
+    const bool dx_wave = wave < 4;
+    const int rw = wave & 3;
+    // the dx rows of a dx wave's lane: tokens [32 w, 32 w + 32) of the chunk;
+    // register 4 q + r of lane l will hold token 32 w + l % 32, column
+    // 32 j + 8 q + 4 (l / 32) + r
+    const int tl = 32 * rw + m;
+    const bool tok_ok = tl < ntok;
+    const size_t trow = (tok0 + min(tl, ntok - 1)) * d;
+    constexpr int NJ = COLS / 32;
+    // stage 1, all requested before any is used, in this order (the waits
+    // count in issue order): (fused) the token's expert-buffer rows; the dz
+    // rows, W columns and x rows of the tiles, zero past the chunk, the
+    // experts or d; then the incoming value of each dx element, dx itself or
+    // (fused) the kept dxe rows, which stay in flight through the staging
+    // and the products
+    int rr[KJ > 0 ? KJ : 1];
+    if constexpr (KJ > 0) {
+#pragma unroll
+        for (int jj = 0; jj < KJ; ++jj)
+            rr[jj] = (dx_wave && jj < k) ? rows[(tok0 + min(tl, ntok - 1)) * k + jj] : -1;
+    }
+    constexpr int NT = 512;
+    constexpr int DZV = TCH * EMAX / NT;      // dz values per thread
+    constexpr int WV = EMAX * COLS / 8 / NT;  // 16-byte W vectors per thread
+    constexpr int XV = TCH * COLS / 8 / NT;   // 16-byte x vectors per thread
+    static_assert(DZV * NT == TCH * EMAX && WV * NT * 8 == EMAX * COLS &&
+                      XV * NT * 8 == TCH * COLS, "tiles split evenly over the threads");
+    float dzv[DZV];
+    uint4 wv[WV], xv[XV];
+#pragma unroll
+    for (int u = 0; u < DZV; ++u) {
+        const int q = u * NT + tid, r = q / EMAX, e = q % EMAX;
+        dzv[u] = (r < ntok && e < E) ? dz[(tok0 + r) * E + e] : 0.0f;
+    }
+#pragma unroll
+    for (int u = 0; u < WV; ++u) {
+        const int q = u * NT + tid, e = q / (COLS / 8), col = c0 + (q % (COLS / 8)) * 8;
+        wv[u] = (e < E && col < d)
+                    ? *reinterpret_cast<const uint4*>(wg + static_cast<size_t>(e) * d + col)
+                    : make_uint4(0u, 0u, 0u, 0u);
+    }
+    if constexpr (DW) {
 #pragma unroll
         for (int u = 0; u < XV; ++u) {
-            const int q = u * 256 + tid, r = q / (COLS / 8), col = c0 + (q % (COLS / 8)) * 8;
+            const int q = u * NT + tid, r = q / (COLS / 8), col = c0 + (q % (COLS / 8)) * 8;
             xv[u] = (r < ntok && col < d)
                         ? *reinterpret_cast<const uint4*>(x + (tok0 + r) * d + col)
                         : make_uint4(0u, 0u, 0u, 0u);
         }
-#pragma unroll
-        for (int u = 0; u < WV; ++u) {
-            const int q = u * 256 + tid, e = q / (COLS / 8), col = c0 + (q % (COLS / 8)) * 8;
-            wv[u] = (e < E && col < d)
-                        ? *reinterpret_cast<const uint4*>(wg + static_cast<size_t>(e) * d + col)
-                        : make_uint4(0u, 0u, 0u, 0u);
-        }
-    };
-    for (int q = ntok * LD + tid; q < TCH * LD; q += 256) dzs[q] = 0.0f;  // rows past the chunk
-    form_dz<EMAX, LD, KJ>(dzs, xdp, pdp_s, rows_s, rb_s, probs, idx, slot, dgate, row_base,
-                          dz_add, tok0, ntok, E, k, g, gc, issue);
-    // dp is no longer needed: its space takes the x tile
-    uint16_t* xs = reinterpret_cast<uint16_t*>(xdp);
-#pragma unroll
-    for (int u = 0; u < XV; ++u) {
-        const int q = u * 256 + tid, r = q / (COLS / 8), v = q % (COLS / 8);
-        *reinterpret_cast<uint4*>(xs + r * kXLd + v * 8) = xv[u];
     }
-#pragma unroll
-    for (int u = 0; u < WV; ++u) {
-        const int q = u * 256 + tid, e = q / (COLS / 8), v = q % (COLS / 8);
-        const uint32_t h[4] = {wv[u].x, wv[u].y, wv[u].z, wv[u].w};
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            ws[e * kWLd + v * 8 + 2 * i] = bf16_to_f32(static_cast<uint16_t>(h[i] & 0xFFFFu));
-            ws[e * kWLd + v * 8 + 2 * i + 1] = bf16_to_f32(static_cast<uint16_t>(h[i] >> 16));
-        }
-    }
-    lds_barrier();
-
-    const int m = lane & 31, kh = lane >> 5;
-    // The products are formed transposed (dx^T = W^T dz^T, P^T = x^T dz), so
-    // register 4 q + r of lane l holds output column 8 q + 4 (l / 32) + r of
-    // the 32 x 32 block and token (or expert) l % 32: four consecutive
-    // columns, one 16-byte access.
-    const int tl = 32 * wave + m;               // this lane's token in the chunk
-    const size_t trow = (tok0 + min(tl, ntok - 1)) * d;
-    // the incoming dx first (its latency hides behind the products): dx
-    // itself, or (fused) the kept dxe rows, 8 bytes of each per access
-    float4 din[4][4];
+    float4 dxin[KJ == 0 ? NJ : 1][4];
+    uint2 h[KJ > 0 ? KJ : 1][NJ][4];
     if constexpr (KJ == 0) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < NJ; ++j)
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
                 const int col = c0 + 32 * j + 8 * q + 4 * kh;  // d is a multiple of 8
-                din[j][q] = col < d ? *reinterpret_cast<const float4*>(dx + trow + col)
-                                    : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+                dxin[j][q] = (dx_wave && tok_ok && col < d)
+                                 ? *reinterpret_cast<const float4*>(dx + trow + col)
+                                 : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
             }
-    } else {
-        int rr[KJ];
-#pragma unroll
-        for (int jj = 0; jj < KJ; ++jj) rr[jj] = rows_s[min(tl, ntok - 1) * KJ + jj];
-        uint2 h[KJ][4][4];
+    } else if (dx_wave) {
 #pragma unroll
         for (int jj = 0; jj < KJ; ++jj)
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
+            for (int j = 0; j < NJ; ++j)
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
                     const int col = min(c0 + 32 * j + 8 * q + 4 * kh, d - 4);
                     h[jj][j][q] = *reinterpret_cast<const uint2*>(
                         dxe + static_cast<size_t>(rr[jj] >= 0 ? rr[jj] : 0) * d + col);
                 }
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                float v[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-                for (int jj = 0; jj < KJ; ++jj) {
-                    if (rr[jj] < 0) continue;
-                    v[0] += bf16_to_f32(static_cast<uint16_t>(h[jj][j][q].x & 0xFFFFu));
-                    v[1] += bf16_to_f32(static_cast<uint16_t>(h[jj][j][q].x >> 16));
-                    v[2] += bf16_to_f32(static_cast<uint16_t>(h[jj][j][q].y & 0xFFFFu));
-                    v[3] += bf16_to_f32(static_cast<uint16_t>(h[jj][j][q].y >> 16));
-                }
-                din[j][q] = make_float4(v[0], v[1], v[2], v[3]);
-            }
     }
-    f32x16_m acc[4];
+    // stage 2: into LDS (W transposed to [column][expert])
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int u = 0; u < DZV; ++u) {
+        const int q = u * NT + tid;
+        dzs[(q / EMAX) * DZLD + q % EMAX] = dzv[u];
+    }
+#pragma unroll
+    for (int u = 0; u < WV; ++u) {
+        const int q = u * NT + tid, e = q / (COLS / 8), cl = (q % (COLS / 8)) * 8;
+        const uint32_t hw[4] = {wv[u].x, wv[u].y, wv[u].z, wv[u].w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            wts[(cl + 2 * i) * WLD + e] = static_cast<uint16_t>(hw[i] & 0xFFFFu);
+            wts[(cl + 2 * i + 1) * WLD + e] = static_cast<uint16_t>(hw[i] >> 16);
+        }
+    }
+    if constexpr (DW) {
+#pragma unroll
+        for (int u = 0; u < XV; ++u) {
+            const int q = u * NT + tid, r = q / (COLS / 8), v = q % (COLS / 8);
+            *reinterpret_cast<uint4*>(xs + r * kRbXLd + v * 8) = xv[u];
+        }
+    }
+    // LDS only: the dx inputs stay in flight
+    lds_barrier();
+
+    if (dx_wave) {
+    f32x16_r acc[NJ];
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
 #pragma unroll
         for (int i = 0; i < 16; ++i) acc[j][i] = 0.0f;
-    // A[col m][e = 2 s + kh] = W, B[e][token m] = dz
-#pragma unroll 4
-    for (int s2 = 0; s2 < EMAX / 2; ++s2) {
-        const float b = dzs[(32 * wave + m) * LD + 2 * s2 + kh];
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-            acc[j] = __builtin_amdgcn_mfma_f32_32x32x2f32(ws[(2 * s2 + kh) * kWLd + 32 * j + m], b,
-                                                          acc[j], 0, 0, 0);
+    for (int ks = 0; ks < KS; ++ks) {
+        // A: dz[token m][e = 16 ks + 8 kh .. +7] as three bf16 terms
+        float a8[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) a8[i] = dzs[tl * DZLD + 16 * ks + 8 * kh + i];
+        bf16x8_r ahi, amid, alo;
+        split3(a8, ahi, amid, alo);
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+            // B: W[e][column 32 j + m], from the transposed tile
+            const bf16x8_r b = *reinterpret_cast<const bf16x8_r*>(
+                wts + (32 * j + m) * WLD + 16 * ks + 8 * kh);
+            acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, alo, acc[j], 0, 0, 0);
+            acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, amid, acc[j], 0, 0, 0);
+            acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, ahi, acc[j], 0, 0, 0);
+        }
     }
-    if (tl < ntok) {
+    if (tok_ok) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < NJ; ++j)
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
+                float4 din;
+                if constexpr (KJ == 0) {
+                    din = dxin[j][q];
+                } else {
+                    float v[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+                    for (int jj = 0; jj < KJ; ++jj) {
+                        if (rr[jj] < 0) continue;
+                        v[0] += bf16_to_f32(static_cast<uint16_t>(h[jj][j][q].x & 0xFFFFu));
+                        v[1] += bf16_to_f32(static_cast<uint16_t>(h[jj][j][q].x >> 16));
+                        v[2] += bf16_to_f32(static_cast<uint16_t>(h[jj][j][q].y & 0xFFFFu));
+                        v[3] += bf16_to_f32(static_cast<uint16_t>(h[jj][j][q].y >> 16));
+                    }
+                    din = make_float4(v[0], v[1], v[2], v[3]);
+                }
                 const int col = c0 + 32 * j + 8 * q + 4 * kh;
                 if (col < d)
                     *reinterpret_cast<float4*>(dx + trow + col) =
-                        make_float4(din[j][q].x + acc[j][4 * q], din[j][q].y + acc[j][4 * q + 1],
-                                    din[j][q].z + acc[j][4 * q + 2],
-                                    din[j][q].w + acc[j][4 * q + 3]);
+                        make_float4(din.x + acc[j][4 * q], din.y + acc[j][4 * q + 1],
+                                    din.z + acc[j][4 * q + 2], din.w + acc[j][4 * q + 3]);
             }
     }
+    }
 
-    if constexpr (DW) {
-        // P[e][col] over the chunk's tokens: A[e m][token 2 s + kh] = dz,
-        // B[token][col m] = x (columns 32 w .. 32 w + 31 of the block)
+    if (DW && !dx_wave) {
+        // 4. P[e][column] over the chunk's tokens for columns [32 w, 32 w + 32):
+        // A = dz^T (expert m, tokens 16 s + 8 kh .. +7, three terms),
+        // B = x (column m, the same tokens), read transposed from the x tile
         constexpr int MB = EMAX / 32;
-        f32x16_m pacc[MB];
+        f32x16_r pacc[MB];
 #pragma unroll
         for (int b = 0; b < MB; ++b)
 #pragma unroll
             for (int i = 0; i < 16; ++i) pacc[b][i] = 0.0f;
-        const int nks = (ntok + 1) / 2;
-        // A[col m][token 2 s + kh] = x, B[token][expert m] = dz
-#pragma unroll 4
-        for (int s2 = 0; s2 < nks; ++s2) {
-            const int t = 2 * s2 + kh;
-            const float ax = bf16_to_f32(xs[t * kXLd + 32 * wave + m]);
+        const int gq = lane >> 4, jq = lane & 15;
+        const int ntk = (ntok + 15) / 16;  // rows past the chunk are zero in both tiles
+        for (int s = 0; s < ntk; ++s) {
+            const int kt = 16 * s + 8 * (gq >> 1) + (jq >> 2);
+            const int mn = 32 * rw + 16 * (gq & 1) + 4 * (jq & 3);
+            const s16x4_r lo4 = rb_read_tr(xs + kt * kRbXLd + mn);
+            const s16x4_r hi4 = rb_read_tr(xs + (kt + 4) * kRbXLd + mn);
+            const bf16x8_r bx = __builtin_bit_cast(
+                bf16x8_r, __builtin_shufflevector(lo4, hi4, 0, 1, 2, 3, 4, 5, 6, 7));
 #pragma unroll
-            for (int b = 0; b < MB; ++b)
-                pacc[b] = __builtin_amdgcn_mfma_f32_32x32x2f32(ax, dzs[t * LD + 32 * b + m],
-                                                               pacc[b], 0, 0, 0);
+            for (int b = 0; b < MB; ++b) {
+                float a8[8];
+#pragma unroll
+                for (int i = 0; i < 8; ++i) a8[i] = dzs[(16 * s + 8 * kh + i) * DZLD + 32 * b + m];
+                bf16x8_r ahi, amid, alo;
+                split3(a8, ahi, amid, alo);
+                pacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bx, alo, pacc[b], 0, 0, 0);
+                pacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bx, amid, pacc[b], 0, 0, 0);
+                pacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bx, ahi, pacc[b], 0, 0, 0);
+            }
         }
+        // register 4 q + r of lane l: expert 32 b + l % 32, column
+        // 32 w + 8 q + 4 (l / 32) + r
         float* pg = partial + (static_cast<size_t>(g) * nch + c) * E * d;
 #pragma unroll
         for (int b = 0; b < MB; ++b) {
@@ -628,7 +805,7 @@ __global__ __launch_bounds__(256) void route_bwd_mfma_kernel(
             if (e < E) {
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
-                    const int col = c0 + 32 * wave + 8 * q + 4 * kh;
+                    const int col = c0 + 32 * rw + 8 * q + 4 * kh;
                     if (col < d)
                         *reinterpret_cast<float4*>(pg + static_cast<size_t>(e) * d + col) =
                             make_float4(pacc[b][4 * q], pacc[b][4 * q + 1], pacc[b][4 * q + 2],
@@ -653,7 +830,16 @@ __global__ __launch_bounds__(256) void route_bwd_reduce_kernel(const float* __re
     if (q < total && nch > 0) {
         const long long g = q / ed, o = q % ed;
         const float* p = partial + g * nch * ed + o;
-        for (int c = r; c < nch; c += 8) s += p[c * ed];
+        // chunks r, r + 8, ... added in that order, eight loads in flight
+        int c = r;
+        for (; c + 56 < nch; c += 64) {
+            float v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = p[(c + 8 * u) * ed];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) s += v[u];
+        }
+        for (; c < nch; c += 8) s += p[c * ed];
     }
     part[r][ql] = s;
     __syncthreads();
@@ -672,7 +858,7 @@ struct ChunkPlan {
 ChunkPlan plan(const Dims& D) {
     // bf16 with E > 16: the matrix-core kernel's fixed chunk
     if (D.dtype == VMOE_BF16 && D.E > 16)
-        return ChunkPlan{kMfmaTok, D.Ng > 0 ? static_cast<int>(cdiv(D.Ng, kMfmaTok)) : 0};
+        return ChunkPlan{kRbTok, D.Ng > 0 ? static_cast<int>(cdiv(D.Ng, kRbTok)) : 0};
     // about 1024 blocks over (chunks, column blocks, groups)
     const int cols = 64 * (D.E <= 8    ? ColsPerLane<8>::value
                            : D.E <= 16 ? ColsPerLane<16>::value
@@ -699,22 +885,31 @@ struct BwdArgs {
     const void* dxe;
     const int32_t* row_base;
     const float* dz_add;  // extra gradient with respect to the logits, or null
+    float* dz;            // bf16 with E > 16: dz [N, E] (workspace)
+    int32_t* rows;        // bf16 with E > 16, fused: expert-buffer rows [N, k] (workspace)
 };
+
+// bf16 layers with more than 16 experts: dz (and the fused call's rows) in
+// the workspace after the partials.
+bool uses_dz_pass(const Dims& D) { return D.dtype == VMOE_BF16 && D.E > 16; }
 
 template <typename T, int EMAX, int KJ>
 void launch_main(const Dims& D, const ChunkPlan& P, const BwdArgs& a, hipStream_t st) {
     if constexpr (std::is_same<T, uint16_t>::value && EMAX >= 32) {
-        const dim3 grid(P.nch, cdiv(D.d, kMfmaCols), D.G);
         const long long gc = static_cast<long long>(D.G) * D.C;
+        constexpr int TPB = 256 / EMAX;
+        rbwd_dz_kernel<EMAX><<<cdiv(D.N, TPB), 256, 0, st>>>(
+            a.probs, a.idx, a.slot, a.dgate, a.dz_add, a.row_base, a.dz,
+            KJ > 0 ? a.rows : nullptr, gc, D.N, D.Ng, D.E, D.k);
+        const dim3 grid(P.nch, cdiv(D.d, kRbCols), D.G);
         auto go = [&](auto kern) {
-            kern<<<grid, 256, 0, st>>>(static_cast<const uint16_t*>(a.x),
-                                       static_cast<const uint16_t*>(a.wr), a.probs, a.idx, a.slot,
-                                       a.dgate, a.dx, a.partial,
-                                       static_cast<const uint16_t*>(a.dxe), a.row_base, a.dz_add,
-                                       gc, D.Ng, D.d, D.E, D.k, P.nch);
+            kern<<<grid, 512, 0, st>>>(static_cast<const uint16_t*>(a.x),
+                                       static_cast<const uint16_t*>(a.wr), a.dz, a.rows,
+                                       static_cast<const uint16_t*>(a.dxe), a.dx, a.partial,
+                                       D.Ng, D.d, D.E, D.k, P.nch);
         };
-        if (a.partial) go(route_bwd_mfma_kernel<EMAX, true, KJ>);
-        else go(route_bwd_mfma_kernel<EMAX, false, KJ>);
+        if (a.partial) go(route_bwd_mma_kernel<EMAX, true, KJ>);
+        else go(route_bwd_mma_kernel<EMAX, false, KJ>);
         return;
     }
     constexpr int COLS = 64 * ColsPerLane<EMAX>::value;
@@ -757,6 +952,12 @@ vmoe_status run_route_bwd(const Dims& D, BwdArgs a, float* dwr, void* ws, int kj
         return launch_status();
     }
     a.partial = dwr ? static_cast<float*>(ws) : nullptr;
+    if (uses_dz_pass(D)) {
+        // after the partials (whose bytes are a multiple of 16: d % 8 == 0)
+        char* p = static_cast<char*>(ws) + sizeof(float) * static_cast<size_t>(D.G) * P.nch * D.E * D.d;
+        a.dz = reinterpret_cast<float*>(p);
+        a.rows = reinterpret_cast<int32_t*>(p + sizeof(float) * static_cast<size_t>(D.N) * D.E);
+    }
     if (kj == 0) launch_main_t<0>(D, P, a, st);
     else if (kj == 2) launch_main_t<2>(D, P, a, st);
     else launch_main_t<4>(D, P, a, st);
@@ -768,17 +969,23 @@ vmoe_status run_route_bwd(const Dims& D, BwdArgs a, float* dwr, void* ws, int kj
 
 }  // namespace
 
-// Workspace: the per-chunk router-gradient partials [G, chunks, E, d] f32.
+// Workspace: the per-chunk router-gradient partials [G, chunks, E, d] f32;
+// bf16 layers with more than 16 experts also dz [N, E] f32 and rows [N, k] i32.
 size_t route_bwd_workspace_bytes(const Dims& D) {
     const ChunkPlan P = plan(D);
-    return sizeof(float) * static_cast<size_t>(D.G) * P.nch * D.E * D.d;
+    size_t b = sizeof(float) * static_cast<size_t>(D.G) * P.nch * D.E * D.d;
+    if (uses_dz_pass(D))
+        b += sizeof(float) * static_cast<size_t>(D.N) * D.E +
+             sizeof(int32_t) * static_cast<size_t>(D.N) * D.k;
+    return b;
 }
 
 vmoe_status route_bwd_launch(const Dims& D, const void* x, const void* wr, const float* probs,
                              const int32_t* idx, const int32_t* slot, const float* dgate,
                              const float* dz_add, float* dx, float* dwr, void* ws,
                              hipStream_t st) {
-    const BwdArgs a{x, wr, probs, idx, slot, dgate, dx, nullptr, nullptr, nullptr, dz_add};
+    const BwdArgs a{x, wr, probs, idx, slot, dgate, dx, nullptr, nullptr, nullptr, dz_add,
+                    nullptr, nullptr};
     return run_route_bwd(D, a, dwr, ws, 0, st);
 }
 
@@ -798,7 +1005,8 @@ vmoe_status dispatch_route_bwd_launch(const Dims& D, const void* dxe, const int3
         if (s != VMOE_OK) return s;
         return route_bwd_launch(D, x, wr, probs, idx, slot, dgate, dz_add, dx, dwr, ws, st);
     }
-    const BwdArgs a{x, wr, probs, idx, slot, dgate, dx, nullptr, dxe, row_base, dz_add};
+    const BwdArgs a{x, wr, probs, idx, slot, dgate, dx, nullptr, dxe, row_base, dz_add,
+                    nullptr, nullptr};
     return run_route_bwd(D, a, dwr, ws, D.k <= 2 ? 2 : 4, st);
 }
 

@@ -260,6 +260,12 @@ def main():
         "dispatch_route_bwd": lambda: V.vmoe_dispatch_route_bwd(
             s, L.dxe, L.row_base, L.x, L.w_router, L.probs, L.expert_idx, L.slot, L.dgate, L.dx,
             L.dw_router, L.route_bwd_ws, stream),
+        # the expert MLP through the fill-clamp-refill tile scheduler (same results)
+        "ffn_fwd_quota": lambda: V.vmoe_expert_ffn_fwd_quota(
+            s, L.xe, L.counts, L.w1, L.b1, L.w2, L.b2, L.a, L.a_grad, L.ye, stream),
+        "ffn_bwd_quota": lambda: V.vmoe_expert_ffn_bwd_quota(
+            s, L.xe, L.counts, L.w1, L.w2, L.a, L.a_grad, L.dye, L.dh, L.dxe, L.dw1, L.db1, L.dw2,
+            L.db2, stream),
     }
 
     if args.copy_probe:
@@ -311,6 +317,30 @@ def main():
     per_call = {name: float(np.mean([evc[i][c].elapsed_time(evc[i][c + 1]) for i in range(K)]))
                 for c, name in enumerate(CALLS)}
     step_ms_events = float(np.mean([evc[i][0].elapsed_time(evc[i][-1]) for i in range(K)]))
+
+    # the same step with the expert MLP calls through the fill-clamp-refill
+    # tile scheduler, each call bracketed by events (diagnostic)
+    quota = None
+    if cfg.dtype == "bf16":
+        qcalls = [("ffn_fwd_quota" if n == "ffn_fwd" else "ffn_bwd_quota" if n == "ffn_bwd"
+                   else n) for n in CALLS]
+        evq = [[torch.cuda.Event(enable_timing=True) for _ in range(len(CALLS) + 1)]
+               for _ in range(K)]
+        for i in range(K):
+            evq[i][0].record(stream)
+            for c, name in enumerate(qcalls):
+                calls[name]()
+                evq[i][c + 1].record(stream)
+        torch.cuda.synchronize()
+        qt = [float(np.mean([evq[i][c].elapsed_time(evq[i][c + 1]) for i in range(K)]))
+              for c in range(len(CALLS))]
+        quota = {"ffn_fwd_ms": round(qt[CALLS.index("ffn_fwd")], 4),
+                 "ffn_bwd_ms": round(qt[CALLS.index("ffn_bwd")], 4),
+                 "step_ms_events": float(np.mean([evq[i][0].elapsed_time(evq[i][-1])
+                                                  for i in range(K)])),
+                 "note": "vmoe_expert_ffn_fwd_quota / _bwd_quota (persistent workgroups, "
+                         "per-expert quotas by fill-clamp-refill) in place of the default "
+                         "calls; compare per_call ffn_fwd / ffn_bwd"}
 
     flushed = None
     if args.flush_mall:
@@ -391,6 +421,7 @@ def main():
         "per_call_note": "diagnostic pass after the timed region, every call bracketed by events",
         "step_ms_events": step_ms_events,
         "balance_losses": balance,
+        "ffn_quota_scheduler": quota,
     }
     if flushed is not None:
         fb = sum(cost[n][1] for n in moves)

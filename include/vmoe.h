@@ -202,6 +202,39 @@ vmoe_status vmoe_expert_ffn_bwd(const vmoe_shape* shape, const void* xe, const i
                                 const void* act_grad, const void* dye, void* dh, void* dxe,
                                 float* dw1, float* db1, float* dw2, float* db2, void* stream);
 
+/* vmoe_expert_ffn_fwd and vmoe_expert_ffn_bwd with a device-side tile
+ * scheduler (the lifespan-aware aligning of paper Sec. 3.2.2 applied to the
+ * experts of one grouped GEMM): each GEMM runs as many persistent workgroups
+ * as the GPU holds at once, and every workgroup first computes, from the
+ * device row counts, the fill-clamp-refill split of those workgroups among
+ * the experts (minimum one for an expert with tiles, saturation its tile
+ * count, work coefficient its tiles times a per-tile cost model of its rows);
+ * expert e then owns a contiguous range of units_e workgroups, each taking
+ * every units_e-th tile of e. Same arguments, same results as the two calls
+ * (each output tile is computed by the same code); bf16 layers only (f32
+ * layers run the calls above). */
+vmoe_status vmoe_expert_ffn_fwd_quota(const vmoe_shape* shape, const void* xe,
+                                      const int32_t* counts, const void* w1, const void* b1,
+                                      const void* w2, const void* b2, void* act, void* act_grad,
+                                      void* ye, void* stream);
+vmoe_status vmoe_expert_ffn_bwd_quota(const vmoe_shape* shape, const void* xe,
+                                      const int32_t* counts, const void* w1, const void* w2,
+                                      const void* act, const void* act_grad, const void* dye,
+                                      void* dh, void* dxe, float* dw1, float* db1, float* dw2,
+                                      float* db2, void* stream);
+
+/* The device implementation of vmoe_fill_clamp_refill's whole-unit shares
+ * (paper Sec. 3.2.2) that the quota-scheduled GEMMs run, on one wavefront:
+ * n <= 64 experts, min_units, sat_units [n] i32, coef [n] f64, budget
+ * units -> alloc_units [n] i32 (device memory, asynchronous on stream).
+ * Every sum is taken in ascending expert order with the host routine's
+ * operations, so for valid inputs the units equal vmoe_fill_clamp_refill's
+ * alloc_units. VMOE_ERR_INVALID_ARG for n outside [0, 64], a negative
+ * budget or a missing pointer; inputs are not otherwise validated. */
+vmoe_status vmoe_fill_clamp_refill_device(int32_t n, const int32_t* min_units,
+                                          const int32_t* sat_units, const double* coef,
+                                          int32_t budget, int32_t* alloc_units, void* stream);
+
 /* Backward of the dispatch: dx[t] = sum over kept j of dxe[row(t,j)]
  * (f32, overwritten; 0 for a token with no kept assignment). dx [N, d] f32. */
 vmoe_status vmoe_dispatch_bwd(const vmoe_shape* shape, const void* dxe,

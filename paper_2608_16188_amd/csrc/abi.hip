@@ -27,11 +27,13 @@ vmoe_status dispatch_bwd_launch(const Dims& D, const void* dxe, const int32_t* i
                                 hipStream_t st);
 vmoe_status ffn_fwd_launch(const Dims& D, const void* xe, const int32_t* counts, const void* w1,
                            const void* b1, const void* w2, const void* b2, void* act,
-                           void* act_grad, void* ye, hipStream_t st);
+                           void* act_grad, void* ye, int sched, hipStream_t st);
 vmoe_status ffn_bwd_launch(const Dims& D, const void* xe, const int32_t* counts, const void* w1,
                            const void* w2, const void* act, const void* act_grad, const void* dye,
                            void* dh, void* dxe, float* dw1, float* db1, float* dw2, float* db2,
-                           hipStream_t st);
+                           int sched, hipStream_t st);
+vmoe_status fcr_device_launch(int n, const int32_t* mn, const int32_t* sat, const double* coef,
+                              int budget, int32_t* units, hipStream_t st);
 vmoe_status route_bwd_launch(const Dims& D, const void* x, const void* wr, const float* probs,
                              const int32_t* idx, const int32_t* slot, const float* dgate,
                              const float* dz_add, float* dx, float* dwr, void* ws,
@@ -225,15 +227,41 @@ vmoe_status vmoe_dispatch(const vmoe_shape* shape, const void* x, const int32_t*
     return vmoe::dispatch_launch(D, x, expert_idx, slot, row_base, xe, as_stream(stream));
 }
 
-vmoe_status vmoe_expert_ffn_fwd(const vmoe_shape* shape, const void* xe, const int32_t* counts,
-                                const void* w1, const void* b1, const void* w2, const void* b2,
-                                void* act, void* act_grad, void* ye, void* stream) {
+static vmoe_status ffn_fwd(const vmoe_shape* shape, const void* xe, const int32_t* counts,
+                           const void* w1, const void* b1, const void* w2, const void* b2,
+                           void* act, void* act_grad, void* ye, int sched, void* stream) {
     Dims D;
     VMOE_TRY(vmoe::make_dims(shape, &D));
     VMOE_TRY(need(dev(xe) && dev(counts) && dev(w1) && dev(b1) && dev(w2) && dev(b2) &&
                   dev(act) && dev(act_grad) && dev(ye)));
-    return vmoe::ffn_fwd_launch(D, xe, counts, w1, b1, w2, b2, act, act_grad, ye,
+    return vmoe::ffn_fwd_launch(D, xe, counts, w1, b1, w2, b2, act, act_grad, ye, sched,
                                 as_stream(stream));
+}
+
+static vmoe_status ffn_bwd(const vmoe_shape* shape, const void* xe, const int32_t* counts,
+                           const void* w1, const void* w2, const void* act, const void* act_grad,
+                           const void* dye, void* dh, void* dxe, float* dw1, float* db1,
+                           float* dw2, float* db2, int sched, void* stream) {
+    Dims D;
+    VMOE_TRY(vmoe::make_dims(shape, &D));
+    VMOE_TRY(need(dev(xe) && dev(counts) && dev(w1) && dev(w2) && dev(act) && dev(act_grad) &&
+                  dev(dye) && dev(dh) && dev(dxe) && dev(dw1) && dev(db1) && dev(dw2) &&
+                  dev(db2)));
+    return vmoe::ffn_bwd_launch(D, xe, counts, w1, w2, act, act_grad, dye, dh, dxe, dw1, db1,
+                                dw2, db2, sched, as_stream(stream));
+}
+
+vmoe_status vmoe_expert_ffn_fwd(const vmoe_shape* shape, const void* xe, const int32_t* counts,
+                                const void* w1, const void* b1, const void* w2, const void* b2,
+                                void* act, void* act_grad, void* ye, void* stream) {
+    return ffn_fwd(shape, xe, counts, w1, b1, w2, b2, act, act_grad, ye, 0, stream);
+}
+
+vmoe_status vmoe_expert_ffn_fwd_quota(const vmoe_shape* shape, const void* xe,
+                                      const int32_t* counts, const void* w1, const void* b1,
+                                      const void* w2, const void* b2, void* act, void* act_grad,
+                                      void* ye, void* stream) {
+    return ffn_fwd(shape, xe, counts, w1, b1, w2, b2, act, act_grad, ye, 1, stream);
 }
 
 vmoe_status vmoe_combine_fwd(const vmoe_shape* shape, const void* ye, const int32_t* expert_idx,
@@ -262,13 +290,27 @@ vmoe_status vmoe_expert_ffn_bwd(const vmoe_shape* shape, const void* xe, const i
                                 const void* w1, const void* w2, const void* act,
                                 const void* act_grad, const void* dye, void* dh, void* dxe,
                                 float* dw1, float* db1, float* dw2, float* db2, void* stream) {
-    Dims D;
-    VMOE_TRY(vmoe::make_dims(shape, &D));
-    VMOE_TRY(need(dev(xe) && dev(counts) && dev(w1) && dev(w2) && dev(act) && dev(act_grad) &&
-                  dev(dye) && dev(dh) && dev(dxe) && dev(dw1) && dev(db1) && dev(dw2) &&
-                  dev(db2)));
-    return vmoe::ffn_bwd_launch(D, xe, counts, w1, w2, act, act_grad, dye, dh, dxe, dw1, db1,
-                                dw2, db2, as_stream(stream));
+    return ffn_bwd(shape, xe, counts, w1, w2, act, act_grad, dye, dh, dxe, dw1, db1, dw2, db2, 0,
+                   stream);
+}
+
+vmoe_status vmoe_expert_ffn_bwd_quota(const vmoe_shape* shape, const void* xe,
+                                      const int32_t* counts, const void* w1, const void* w2,
+                                      const void* act, const void* act_grad, const void* dye,
+                                      void* dh, void* dxe, float* dw1, float* db1, float* dw2,
+                                      float* db2, void* stream) {
+    return ffn_bwd(shape, xe, counts, w1, w2, act, act_grad, dye, dh, dxe, dw1, db1, dw2, db2, 1,
+                   stream);
+}
+
+vmoe_status vmoe_fill_clamp_refill_device(int32_t n, const int32_t* min_units,
+                                          const int32_t* sat_units, const double* coef,
+                                          int32_t budget, int32_t* alloc_units, void* stream) {
+    if (n < 0 || n > vmoe::kMaxExperts || budget < 0) return VMOE_ERR_INVALID_ARG;
+    if (n > 0 && !(dev(min_units) && dev(sat_units) && dev(coef) && dev(alloc_units)))
+        return VMOE_ERR_INVALID_ARG;
+    return vmoe::fcr_device_launch(n, min_units, sat_units, coef, budget, alloc_units,
+                                   as_stream(stream));
 }
 
 vmoe_status vmoe_dispatch_bwd(const vmoe_shape* shape, const void* dxe,

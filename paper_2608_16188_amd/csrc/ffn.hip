@@ -123,6 +123,131 @@ __device__ __forceinline__ bool live_tile(const int32_t* counts, int G, int E, i
     return true;
 }
 
+// ------------------------------------------------------------------ quotas
+
+// Fill-clamp-refill (the paper's lifespan aligning, Sec. 3.2.2) on one wave,
+// lane i holding expert i (n <= 64): every expert starts from its minimum,
+// the budget left is split among the unsaturated experts in proportion to
+// their coefficients, an expert pushed past its saturation is clamped and
+// its excess shared again, until nothing is returned; then the real shares
+// are rounded to floor(sum) whole units by largest remainder (ties to the
+// lower index). Every sum runs in ascending expert order with the host
+// routine's operations (vmoe_fill_clamp_refill), so the units equal its
+// units for the same inputs. Returns lane i's units (0 past n).
+__device__ int fill_clamp_refill_wave(int n, int mn, int sat, double coef, int budget) {
+    const int lane = threadIdx.x & 63;
+    const bool valid = lane < n;
+    double a = valid ? static_cast<double>(mn) : 0.0;
+    long long need = 0;
+    for (int r = 0; r < n; ++r) need += __shfl(mn, r, 64);
+    bool act = valid && a < static_cast<double>(sat) && coef > 0.0;
+    double left = static_cast<double>(budget - need);
+    while (left > 0.0 && __ballot(act) != 0ull) {
+        double W = 0.0;
+        for (int r = 0; r < n; ++r) {
+            const double c = __shfl(coef, r, 64);
+            if (__shfl(static_cast<int>(act), r, 64)) W += c;
+        }
+        if (act) a += left * coef / W;
+        left = 0.0;
+        for (int r = 0; r < n; ++r) {
+            const double ar = __shfl(a, r, 64);
+            const int sr = __shfl(sat, r, 64);
+            if (__shfl(static_cast<int>(act), r, 64) && ar > static_cast<double>(sr))
+                left += ar - static_cast<double>(sr);
+        }
+        if (act && a > static_cast<double>(sat)) {
+            a = static_cast<double>(sat);
+            act = false;
+        }
+    }
+    const double fl = floor(a);
+    int units = static_cast<int>(fl);
+    long long base = 0;
+    double sum = 0.0;
+    for (int r = 0; r < n; ++r) {
+        base += __shfl(units, r, 64);
+        sum += __shfl(a, r, 64);
+    }
+    long long extra = static_cast<long long>(floor(sum + 1e-9)) - base;
+    bool up = false;  // rounded up already
+    while (extra > 0) {
+        // the largest fractional part not yet rounded up, lowest index on ties
+        const double fr = (valid && !up) ? a - fl : 0.0;
+        int best = -1;
+        double bf = 0.0;
+        for (int r = 0; r < n; ++r) {
+            const double f = __shfl(fr, r, 64);
+            if (f > bf) {
+                best = r;
+                bf = f;
+            }
+        }
+        if (best < 0) break;
+        if (lane == best) {
+            ++units;
+            up = true;
+        }
+        --extra;
+    }
+    return valid ? units : 0;
+}
+
+// The quota plan of one launch: per expert its rows, its tiles, the first of
+// its blocks and the number of blocks it gets.
+struct QuotaPlan {
+    int ne[64], tiles[64], first[64], units[64];
+};
+
+// Work model of one expert's tiles, in relative time units: a tile of the
+// GEMMs whose m is the expert's rows costs a fixed part (streaming its
+// weight panel) plus a part in proportion to its live rows; a weight-gradient
+// tile a fixed part (its output writes) plus one in proportion to the rows it
+// reduces over (300 rows ~ the writes of a 256-column tile, as measured).
+template <int EPI>
+__device__ __forceinline__ double tile_work(int ne, int bm) {
+    if constexpr (EPI == EPI_F32) return static_cast<double>(ne) + 300.0;
+    else return 1.0 + static_cast<double>(min(ne, bm)) / bm;
+}
+
+constexpr bool compact_epi(int epi) { return epi != EPI_F32; }
+
+// Wave 0 forms the launch's plan: per expert its rows and tiles, its work
+// (tiles x tile_work) as the coefficient, its tiles as saturation, a minimum
+// of one block when it has tiles, and the fill-clamp-refill split of the
+// launch's blocks; experts own consecutive block ranges in expert order.
+template <int EPI>
+__device__ void build_quota_plan(const GemmBatch& batch, int bm, int budget, QuotaPlan* qp) {
+    const int lane = threadIdx.x & 63;
+    const GemmArgs& p0 = batch.p[0];
+    const int E = p0.E;
+    int ne = 0;
+    if (lane < E)
+        for (int g = 0; g < p0.G; ++g) ne += p0.counts[g * E + lane];
+    int tiles = 0;
+    if (lane < E) {
+        if constexpr (compact_epi(EPI)) {
+            ne = min(ne, p0.M);
+            tiles = (ne + bm - 1) / bm * batch.tiles_n[0];
+        } else {
+            tiles = batch.tiles_m[0] * batch.tiles_n[0] +
+                    (batch.total[1] > 0 ? batch.tiles_m[1] * batch.tiles_n[1] : 0);
+        }
+    }
+    const double coef = static_cast<double>(tiles) * tile_work<EPI>(ne, bm);
+    const int units = fill_clamp_refill_wave(E, tiles > 0 ? 1 : 0, tiles, coef, budget);
+    int incl = units;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int u = __shfl_up(incl, o, 64);
+        if (lane >= o) incl += u;
+    }
+    qp->ne[lane] = ne;
+    qp->tiles[lane] = tiles;
+    qp->first[lane] = incl - units;
+    qp->units[lane] = units;
+}
+
 __device__ __forceinline__ float gelu_f(float h) {
     return 0.5f * h * (1.0f + erff(h * 0.70710678118654752f));
 }
@@ -592,7 +717,11 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& p, f32x16 (&acc)[T
 // HBM latency behind NS - 1 stages of MFMAs. The stage count is rounded up to
 // a multiple of NS so the ring unrolls with static buffers; the padding
 // stages load zeros (out of range) and skip their MFMAs.
-template <class T, bool A_KMAJOR, bool B_KMAJOR, int EPI>
+// SCHED = 0: one tile per block, the grid dealt over the (live) tile list;
+// SCHED = 1: persistent blocks, each expert owning the number of blocks the
+// fill-clamp-refill quota gives it, each block taking every units-th tile
+// of its expert.
+template <class T, bool A_KMAJOR, bool B_KMAJOR, int EPI, int SCHED = 0>
 __global__ __launch_bounds__(T::NT)
 __attribute__((amdgpu_waves_per_eu(T::WAVES_PER_EU, T::WAVES_PER_EU)))
 void gemm_bf16_kernel(GemmBatch batch) {
@@ -608,14 +737,44 @@ void gemm_bf16_kernel(GemmBatch batch) {
     __shared__ __attribute__((aligned(1024))) uint16_t buf3[NS > 3 ? SZX : 8];
     __shared__ __attribute__((aligned(1024))) uint16_t buf4[NS > 4 ? SZX : 8];
 
+    const int b = blockIdx.x;
+    int qe = 0, qu = 0, qn = 0, qt = 0, qne = 0;  // quota: expert, rank, units, tiles, rows
+    if constexpr (SCHED == 1) {
+        __shared__ QuotaPlan qp;
+        if (threadIdx.x < 64) build_quota_plan<EPI>(batch, BM_, static_cast<int>(gridDim.x), &qp);
+        __syncthreads();
+        const int lane = threadIdx.x & 63;
+        const int end = qp.first[lane] + qp.units[lane];
+        const int e_b = __popcll(__ballot(end <= b));  // ends never decrease
+        if (e_b >= batch.p[0].E) return;              // past every quota
+        qe = e_b;
+        qn = qp.units[e_b];
+        qu = b - qp.first[e_b];
+        qt = qp.tiles[e_b];
+        qne = qp.ne[e_b];
+    }
+    for (int it = 0;; ++it) {
+    int prob = 0, e, r, ne, tiles_m;
+    if constexpr (SCHED == 1) {
+        r = qu + it * qn;
+        if (r >= qt) break;
+        e = qe;
+        ne = qne;
+        if constexpr (compact_tiles<EPI>()) {
+            tiles_m = (ne + BM_ - 1) / BM_;
+        } else {
+            const int t0 = batch.tiles_m[0] * batch.tiles_n[0];
+            prob = r >= t0 ? 1 : 0;
+            if (prob) r -= t0;
+            tiles_m = batch.tiles_m[prob];
+        }
+    } else {
     // Block b runs on XCD b mod 8 as that XCD's (b / 8)-th block; XCDs take
     // chunks of `chunk` consecutive tiles in turn, so the tiles resident on an
     // XCD share operand panels in its L2 while every XCD gets an even share of
     // each expert, however unevenly the rows are spread over experts.
-    const int b = blockIdx.x;
     const int l = b >> 3, chunk = batch.chunk;
     int w = ((l / chunk) * 8 + (b & 7)) * chunk + l % chunk;
-    int prob = 0, e, r, ne, tiles_m;
     if constexpr (compact_tiles<EPI>()) {
         LiveTile lt;
         const GemmArgs& p0 = batch.p[0];
@@ -634,6 +793,7 @@ void gemm_bf16_kernel(GemmBatch batch) {
         r = w - e * tiles_e;
         ne = expert_rows(batch.p[prob].counts, batch.p[prob].G, batch.p[prob].E, e);
     }
+    }
     const GemmArgs& p = batch.p[prob];
     const int tiles_n = batch.tiles_n[prob];
     const int group_m = batch.group_m;
@@ -650,7 +810,10 @@ void gemm_bf16_kernel(GemmBatch batch) {
     const int K = p.var_k ? ne : p.K;
     const int N = p.N;
     const int m0 = tm * BM_, n0 = tn * BN_;
-    if (m0 >= M) return;
+    if (m0 >= M) {
+        if constexpr (SCHED == 0) return;
+        else continue;
+    }
 
     const __amdgpu_buffer_rsrc_t ra_rs = make_rsrc(
         static_cast<const uint16_t*>(p.a.base) + e * p.a.estride, p.a.estride * 2);
@@ -855,6 +1018,15 @@ void gemm_bf16_kernel(GemmBatch batch) {
     const int eb = wave % NS;
     uint16_t* const ep = eb == 0 ? buf0 : eb == 1 ? buf1 : eb == 2 ? buf2 : eb == 3 ? buf3 : buf4;
     gemm_epilogue<T, CFG, EPI>(p, acc, buf0, ep, rsum, row_sum, e, M, N, m0, n0, fm_live);
+    if constexpr (SCHED == 0) break;
+    // the next tile's first stages land in the buffers this epilogue staged
+    // its outputs in: every wave's LDS accesses are done before any issues
+    // them (its output stores stay in flight)
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+    __builtin_amdgcn_s_barrier();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    }
 }
 
 // ------------------------------------------------------------------ f32 FMA path
@@ -996,7 +1168,8 @@ constexpr int kNumCUs = 256;
 
 // One launch over `n` (1 or 2) problems; grid_m_rows[i] bounds problem i's m.
 template <class T, bool AK, bool BK_, int EPI>
-void launch_bf16(const Dims& D, const GemmArgs* a, const int* grid_m_rows, int n, hipStream_t st) {
+void launch_bf16(const Dims& D, const GemmArgs* a, const int* grid_m_rows, int n, int sched,
+                 hipStream_t st) {
     GemmBatch b{};
     for (int i = 0; i < n; ++i) {
         b.p[i] = a[i];
@@ -1014,12 +1187,20 @@ void launch_bf16(const Dims& D, const GemmArgs* a, const int* grid_m_rows, int n
     b.group_m = one_col ? one_col : (T::WAVES_PER_EU == 2 && T::NW == 4 ? 8 : 4);
     b.chunk = 4 * b.group_m;
     b.per_xcd = static_cast<int>(cdiv(b.total[0] + b.total[1], 8 * b.chunk)) * b.chunk;
-    gemm_bf16_kernel<T, AK, BK_, EPI><<<8 * b.per_xcd, T::NT, 0, st>>>(b);
+    if (sched) {
+        // persistent blocks under quotas: as many as are resident at once
+        // (one per CU for the 8-wave tiles, two for the 4-wave ones)
+        const int resident = kNumCUs * (T::NW == 8 ? 1 : T::WAVES_PER_EU);
+        const int grid = min(8 * b.per_xcd, resident);
+        gemm_bf16_kernel<T, AK, BK_, EPI, 1><<<grid, T::NT, 0, st>>>(b);
+    } else {
+        gemm_bf16_kernel<T, AK, BK_, EPI, 0><<<8 * b.per_xcd, T::NT, 0, st>>>(b);
+    }
 }
 
 template <class T, bool AK, bool BK_, int EPI>
-void launch_bf16(const Dims& D, const GemmArgs& a, int grid_m_rows, hipStream_t st) {
-    launch_bf16<T, AK, BK_, EPI>(D, &a, &grid_m_rows, 1, st);
+void launch_bf16(const Dims& D, const GemmArgs& a, int grid_m_rows, int sched, hipStream_t st) {
+    launch_bf16<T, AK, BK_, EPI>(D, &a, &grid_m_rows, 1, sched, st);
 }
 
 // Tilings (BM, BN, waves, KB, stages, staging).
@@ -1034,13 +1215,13 @@ double tile_cost(long long tiles, int bm, int bn, double eff) {
 }
 
 template <bool AK, bool BK_, int EPI>
-void launch_gemm(const Dims& D, const GemmArgs& a, int grid_m_rows, hipStream_t st) {
+void launch_gemm(const Dims& D, const GemmArgs& a, int grid_m_rows, int sched, hipStream_t st) {
     if (D.dtype == VMOE_BF16) {
         // 256 x 256 tiles (half the operand bytes per flop of 128 x 128) for
         // the GEMMs whose m is the expert's rows; the weight gradients (k is
         // the rows, often short) run 128 x 128 tiles, two blocks per CU.
         if constexpr (EPI == EPI_F32) {
-            launch_bf16<TileSmall, AK, BK_, EPI>(D, a, grid_m_rows, st);
+            launch_bf16<TileSmall, AK, BK_, EPI>(D, a, grid_m_rows, sched, st);
         } else if constexpr (EPI == EPI_BIAS || EPI == EPI_STORE) {
             // Narrow outputs (N = d_model) give few tiles: 192-column tiles fill
             // more CUs when that saves a round (two-stage 64-deep ring, a few
@@ -1049,11 +1230,11 @@ void launch_gemm(const Dims& D, const GemmArgs& a, int grid_m_rows, hipStream_t 
             const double big = tile_cost(D.E * tm * cdiv(a.N, 256), 256, 256, 1.0);
             const double narrow = tile_cost(D.E * tm * cdiv(a.N, 192), 256, 192, 1.05);
             if (narrow < big)
-                launch_bf16<TileNarrow, AK, BK_, EPI>(D, a, grid_m_rows, st);
+                launch_bf16<TileNarrow, AK, BK_, EPI>(D, a, grid_m_rows, sched, st);
             else
-                launch_bf16<TileBig, AK, BK_, EPI>(D, a, grid_m_rows, st);
+                launch_bf16<TileBig, AK, BK_, EPI>(D, a, grid_m_rows, sched, st);
         } else {
-            launch_bf16<TileBig, AK, BK_, EPI>(D, a, grid_m_rows, st);
+            launch_bf16<TileBig, AK, BK_, EPI>(D, a, grid_m_rows, sched, st);
         }
     } else {
         dim3 grid(cdiv(a.N, FT), cdiv(grid_m_rows, FT), D.E);
@@ -1071,11 +1252,29 @@ GemmArgs base_args(const Dims& D, const int32_t* counts) {
 
 size_t esize(const Dims& D) { return D.dtype == VMOE_BF16 ? 2 : 4; }
 
+// One wave: the device fill-clamp-refill of n experts (the routine the
+// quota-scheduled GEMMs run), for comparison with the host routine.
+__global__ __launch_bounds__(64) void fcr_kernel(int n, const int32_t* __restrict__ mn,
+                                                 const int32_t* __restrict__ sat,
+                                                 const double* __restrict__ coef, int budget,
+                                                 int32_t* __restrict__ units) {
+    const int lane = threadIdx.x;
+    const int u = fill_clamp_refill_wave(n, lane < n ? mn[lane] : 0, lane < n ? sat[lane] : 0,
+                                         lane < n ? coef[lane] : 0.0, budget);
+    if (lane < n) units[lane] = u;
+}
+
 }  // namespace
+
+vmoe_status fcr_device_launch(int n, const int32_t* mn, const int32_t* sat, const double* coef,
+                              int budget, int32_t* units, hipStream_t st) {
+    if (n > 0) fcr_kernel<<<1, 64, 0, st>>>(n, mn, sat, coef, budget, units);
+    return launch_status();
+}
 
 vmoe_status ffn_fwd_launch(const Dims& D, const void* xe, const int32_t* counts, const void* w1,
                            const void* b1, const void* w2, const void* b2, void* act,
-                           void* act_grad, void* ye, hipStream_t st) {
+                           void* act_grad, void* ye, int sched, hipStream_t st) {
     const long long rows = D.rows_per_expert();
     if (rows == 0 || D.E == 0) return VMOE_OK;
     // H = xe W1^T + b1 (never stored), A = gelu(H), A' = gelu'(H)
@@ -1091,7 +1290,7 @@ vmoe_status ffn_fwd_launch(const Dims& D, const void* xe, const int32_t* counts,
     g1.ldo = D.f;
     g1.bias = b1;
     g1.bias_estride = D.f;
-    launch_gemm<true, true, EPI_FWD1>(D, g1, static_cast<int>(rows), st);
+    launch_gemm<true, true, EPI_FWD1>(D, g1, static_cast<int>(rows), sched, st);
     // ye = A W2^T + b2
     GemmArgs g2 = base_args(D, counts);
     g2.a = Operand{act, rows * D.f, D.f};
@@ -1104,14 +1303,14 @@ vmoe_status ffn_fwd_launch(const Dims& D, const void* xe, const int32_t* counts,
     g2.ldo = D.d;
     g2.bias = b2;
     g2.bias_estride = D.d;
-    launch_gemm<true, true, EPI_BIAS>(D, g2, static_cast<int>(rows), st);
+    launch_gemm<true, true, EPI_BIAS>(D, g2, static_cast<int>(rows), sched, st);
     return launch_status();
 }
 
 vmoe_status ffn_bwd_launch(const Dims& D, const void* xe, const int32_t* counts, const void* w1,
                            const void* w2, const void* act, const void* act_grad, const void* dye,
                            void* dh, void* dxe, float* dw1, float* db1, float* dw2, float* db2,
-                           hipStream_t st) {
+                           int sched, hipStream_t st) {
     const long long rows = D.rows_per_expert();
     if (D.E == 0) return VMOE_OK;
     if (rows > 0) {
@@ -1126,7 +1325,7 @@ vmoe_status ffn_bwd_launch(const Dims& D, const void* xe, const int32_t* counts,
         g.out_estride = rows * D.f;
         g.ldo = D.f;
         g.aux = act_grad;
-        launch_gemm<true, false, EPI_GELU_GRAD>(D, g, static_cast<int>(rows), st);
+        launch_gemm<true, false, EPI_GELU_GRAD>(D, g, static_cast<int>(rows), sched, st);
         // dxe = dH W1: W1 [f, d] read with k = f strided
         GemmArgs x = base_args(D, counts);
         x.a = Operand{dh, rows * D.f, D.f};
@@ -1137,7 +1336,7 @@ vmoe_status ffn_bwd_launch(const Dims& D, const void* xe, const int32_t* counts,
         x.out = dxe;
         x.out_estride = rows * D.d;
         x.ldo = D.d;
-        launch_gemm<true, false, EPI_STORE>(D, x, static_cast<int>(rows), st);
+        launch_gemm<true, false, EPI_STORE>(D, x, static_cast<int>(rows), sched, st);
     }
     // dW2 [d, f] = dye^T A, reduced over the n_e rows (k = row, strided)
     GemmArgs w = base_args(D, counts);
@@ -1177,14 +1376,14 @@ vmoe_status ffn_bwd_launch(const Dims& D, const void* xe, const int32_t* counts,
         const double narrow = tile_cost(tiles(256, 192), 256, 192, 1.05);
         const double big = tile_cost(tiles(256, 256), 256, 256, 1.0);
         if (narrow <= small && narrow <= big)
-            launch_bf16<TileNarrow, false, false, EPI_F32>(D, both, rows_m, 2, st);
+            launch_bf16<TileNarrow, false, false, EPI_F32>(D, both, rows_m, 2, sched, st);
         else if (big <= small)
-            launch_bf16<TileBig, false, false, EPI_F32>(D, both, rows_m, 2, st);
+            launch_bf16<TileBig, false, false, EPI_F32>(D, both, rows_m, 2, sched, st);
         else
-            launch_bf16<TileSmall, false, false, EPI_F32>(D, both, rows_m, 2, st);
+            launch_bf16<TileSmall, false, false, EPI_F32>(D, both, rows_m, 2, sched, st);
     } else {
-        launch_gemm<false, false, EPI_F32>(D, w, D.d, st);
-        launch_gemm<false, false, EPI_F32>(D, v, D.f, st);
+        launch_gemm<false, false, EPI_F32>(D, w, D.d, 0, st);
+        launch_gemm<false, false, EPI_F32>(D, v, D.f, 0, st);
     }
     // bias gradients (the bf16 path sums them inside the dW GEMMs)
     if (D.dtype == VMOE_F32) {

@@ -102,24 +102,29 @@ class LayerBuffers:
                      self.expert_idx, self.slot, self.gate, self.order, self.counts,
                      self.row_base, self.route_ws, stream)
 
-    def forward(self, logits_in: bool = False, stream=None):
+    def forward(self, logits_in: bool = False, stream=None, quota: bool = False):
+        """quota: the expert MLP through the fill-clamp-refill tile scheduler
+        (vmoe_expert_ffn_fwd_quota; same results)."""
         s = self.shape
         self.route(logits_in, stream)
         V.vmoe_dispatch(s, self.x, self.expert_idx, self.slot, self.row_base, self.xe, stream)
-        V.vmoe_expert_ffn_fwd(s, self.xe, self.counts, self.w1, self.b1, self.w2, self.b2, self.a,
-                              self.a_grad, self.ye, stream)
+        ffn = V.vmoe_expert_ffn_fwd_quota if quota else V.vmoe_expert_ffn_fwd
+        ffn(s, self.xe, self.counts, self.w1, self.b1, self.w2, self.b2, self.a, self.a_grad,
+            self.ye, stream)
         V.vmoe_combine_fwd(s, self.ye, self.expert_idx, self.slot, self.row_base, self.gate,
                            self.y, stream)
 
-    def backward(self, stream=None, fused: bool = True):
+    def backward(self, stream=None, fused: bool = True, quota: bool = False):
         """fused: dispatch and router backward in one call (bit-identical to
-        vmoe_dispatch_bwd followed by vmoe_route_bwd, which fused=False runs)."""
+        vmoe_dispatch_bwd followed by vmoe_route_bwd, which fused=False runs);
+        quota: the expert MLP backward through the fill-clamp-refill tile
+        scheduler."""
         s = self.shape
         V.vmoe_combine_bwd(s, self.dy, self.ye, self.expert_idx, self.slot, self.row_base,
                            self.gate, self.dye, self.dgate, stream)
-        V.vmoe_expert_ffn_bwd(s, self.xe, self.counts, self.w1, self.w2, self.a, self.a_grad,
-                              self.dye, self.dh, self.dxe, self.dw1, self.db1, self.dw2, self.db2,
-                              stream)
+        ffn = V.vmoe_expert_ffn_bwd_quota if quota else V.vmoe_expert_ffn_bwd
+        ffn(s, self.xe, self.counts, self.w1, self.w2, self.a, self.a_grad, self.dye, self.dh,
+            self.dxe, self.dw1, self.db1, self.dw2, self.db2, stream)
         if fused:
             V.vmoe_dispatch_route_bwd(s, self.dxe, self.row_base, self.x, self.w_router,
                                       self.probs, self.expert_idx, self.slot, self.dgate, self.dx,
@@ -130,6 +135,6 @@ class LayerBuffers:
         V.vmoe_route_bwd(s, self.x, self.w_router, self.probs, self.expert_idx, self.slot,
                          self.dgate, self.dx, self.dw_router, self.route_bwd_ws, stream)
 
-    def step(self, stream=None):
-        self.forward(stream=stream)
-        self.backward(stream=stream)
+    def step(self, stream=None, quota: bool = False):
+        self.forward(stream=stream, quota=quota)
+        self.backward(stream=stream, quota=quota)

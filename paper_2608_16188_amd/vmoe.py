@@ -66,6 +66,9 @@ def _load():
         "vmoe_route_noalloc": [S, P, P, P, P, ctypes.c_int32] + [P] * 8 + [P],
         "vmoe_dispatch": [S] + [P] * 6,
         "vmoe_expert_ffn_fwd": [S] + [P] * 10,
+        "vmoe_expert_ffn_fwd_quota": [S] + [P] * 10,
+        "vmoe_expert_ffn_bwd_quota": [S] + [P] * 14,
+        "vmoe_fill_clamp_refill_device": [ctypes.c_int32, P, P, P, ctypes.c_int32, P, P],
         "vmoe_combine_fwd": [S] + [P] * 7,
         "vmoe_combine_bwd": [S] + [P] * 9,
         "vmoe_expert_ffn_bwd": [S] + [P] * 14,
@@ -164,6 +167,31 @@ def vmoe_expert_ffn_fwd(shape, xe, counts, w1, b1, w2, b2, act, act_grad, ye, st
     _check("vmoe_expert_ffn_fwd", _lib.vmoe_expert_ffn_fwd(
         ctypes.byref(shape), _ptr(xe), _ptr(counts), _ptr(w1), _ptr(b1), _ptr(w2), _ptr(b2),
         _ptr(act), _ptr(act_grad), _ptr(ye), _stream(stream)))
+
+
+def vmoe_expert_ffn_fwd_quota(shape, xe, counts, w1, b1, w2, b2, act, act_grad, ye,
+                              stream=None):
+    """vmoe_expert_ffn_fwd with the fill-clamp-refill tile scheduler."""
+    _check("vmoe_expert_ffn_fwd_quota", _lib.vmoe_expert_ffn_fwd_quota(
+        ctypes.byref(shape), _ptr(xe), _ptr(counts), _ptr(w1), _ptr(b1), _ptr(w2), _ptr(b2),
+        _ptr(act), _ptr(act_grad), _ptr(ye), _stream(stream)))
+
+
+def vmoe_expert_ffn_bwd_quota(shape, xe, counts, w1, w2, act, act_grad, dye, dh, dxe, dw1, db1,
+                              dw2, db2, stream=None):
+    """vmoe_expert_ffn_bwd with the fill-clamp-refill tile scheduler."""
+    _check("vmoe_expert_ffn_bwd_quota", _lib.vmoe_expert_ffn_bwd_quota(
+        ctypes.byref(shape), _ptr(xe), _ptr(counts), _ptr(w1), _ptr(w2), _ptr(act),
+        _ptr(act_grad), _ptr(dye), _ptr(dh), _ptr(dxe), _ptr(dw1), _ptr(db1), _ptr(dw2),
+        _ptr(db2), _stream(stream)))
+
+
+def vmoe_fill_clamp_refill_device(n, min_units, sat_units, coef, budget, alloc_units,
+                                  stream=None):
+    """Device fill-clamp-refill units (one wavefront), device tensors."""
+    _check("vmoe_fill_clamp_refill_device", _lib.vmoe_fill_clamp_refill_device(
+        int(n), _ptr(min_units), _ptr(sat_units), _ptr(coef), int(budget), _ptr(alloc_units),
+        _stream(stream)))
 
 
 def vmoe_combine_fwd(shape, ye, expert_idx, slot, row_base, gate, y, stream=None):

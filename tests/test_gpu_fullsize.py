@@ -15,6 +15,8 @@ C ABI, and every output and intermediate is compared with the oracle
   |a - b| <= 2e-2 max(|b|, ||dy_t * ye_row||_2), the second term the size of
   its summands (a wrong element is off by about that much);
 - the router gradient's rows; empty experts' gradients exactly zero.
+The ViT-L/16 layer runs a second time with the expert MLP through the
+fill-clamp-refill tile scheduler (vmoe_expert_ffn_fwd_quota / _bwd_quota).
 
 With VMOE_PARITY_REPORT_DIR set, each case writes its metrics (per tensor,
 worst row, element-wise) there as JSON.
@@ -33,7 +35,9 @@ from .test_gpu_parity import _compare_routing
 
 pytestmark = pytest.mark.gpu
 
-FULL = ["vitb16_bf16", "vitl16_384_bf16", "wide_e32_bf16", "multitask17_bf16"]
+# (workload, expert MLP through the fill-clamp-refill tile scheduler)
+FULL = [("vitb16_bf16", False), ("vitl16_384_bf16", False), ("vitl16_384_bf16", True),
+        ("wide_e32_bf16", False), ("multitask17_bf16", False)]
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -50,12 +54,13 @@ def _rows(t, e, n, dtype):
     return W.to_f64(to_numpy(t[e, :n]), dtype) if n else np.zeros((0, t.shape[2]))
 
 
-@pytest.mark.parametrize("name", FULL)
-def test_layer_full_size_every_element(name):
+@pytest.mark.parametrize("name,quota", FULL,
+                         ids=[n + ("-quota" if q else "") for n, q in FULL])
+def test_layer_full_size_every_element(name, quota):
     cfg, inp = workload_inputs(name)
-    say("full size, every element:", name, "GPU step")
+    say("full size, every element:", name, "quota scheduler" if quota else "", "GPU step")
     L = LayerBuffers(cfg, inp)
-    L.step()
+    L.step(quota=quota)
     torch.cuda.synchronize()
     dt, tol = cfg.dtype, TOL[cfg.dtype]
     f = {key: as_f64(inp[key], dt) for key in ("x", "w_router", "w1", "b1", "w2", "b2", "dy")}
@@ -72,7 +77,7 @@ def test_layer_full_size_every_element(name):
                  probs=to_numpy(L.probs), gate=to_numpy(L.gate))
     _compare_routing(got_r, ref, name)
     say(name, "routing bit-exact; comparing expert rows")
-    rep = Report(name)
+    rep = Report(name + ("-quota" if quota else ""))
     n_e = ref["n_e"]
     dw1, db1, dw2, db2 = (to_numpy(t) for t in (L.dw1, L.db1, L.dw2, L.db2))
     for e in range(cfg.n_experts):

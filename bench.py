@@ -266,6 +266,13 @@ def main():
         "ffn_bwd_quota": lambda: V.vmoe_expert_ffn_bwd_quota(
             s, L.xe, L.counts, L.w1, L.w2, L.a, L.a_grad, L.dye, L.dh, L.dxe, L.dw1, L.db1, L.dw2,
             L.db2, stream),
+        # the dispatch fused into the expert MLP's loads (no xe; same results)
+        "dispatch_ffn_fwd": lambda: V.vmoe_dispatch_ffn_fwd(
+            s, L.x, L.expert_idx, L.slot, L.row_base, L.counts, L.w1, L.b1, L.w2, L.b2,
+            L.row_token, L.a, L.a_grad, L.ye, stream),
+        "ffn_bwd_gather": lambda: V.vmoe_expert_ffn_bwd_gather(
+            s, L.x, L.row_token, L.counts, L.w1, L.w2, L.a, L.a_grad, L.dye, L.dh, L.dxe, L.dw1,
+            L.db1, L.dw2, L.db2, stream),
     }
 
     if args.copy_probe:
@@ -341,6 +348,29 @@ def main():
                  "note": "vmoe_expert_ffn_fwd_quota / _bwd_quota (persistent workgroups, "
                          "per-expert quotas by fill-clamp-refill) in place of the default "
                          "calls; compare per_call ffn_fwd / ffn_bwd"}
+
+    # the step with the dispatch fused into the expert MLP's loads: the
+    # dispatch call is gone, the forward and backward read x through row_token
+    gathered = None
+    if cfg.dtype == "bf16" and L.C * cfg.n_groups <= 6144:
+        gcalls = ["route", "dispatch_ffn_fwd", "combine_fwd", "combine_bwd", "ffn_bwd_gather",
+                  "dispatch_route_bwd"]
+        evg = [[torch.cuda.Event(enable_timing=True) for _ in range(len(gcalls) + 1)]
+               for _ in range(K)]
+        for i in range(K):
+            evg[i][0].record(stream)
+            for c, name in enumerate(gcalls):
+                calls[name]()
+                evg[i][c + 1].record(stream)
+        torch.cuda.synchronize()
+        gt = {name: float(np.mean([evg[i][c].elapsed_time(evg[i][c + 1]) for i in range(K)]))
+              for c, name in enumerate(gcalls)}
+        gathered = {"per_call_ms": {n: round(v, 4) for n, v in gt.items()},
+                    "step_ms_events": float(np.mean([evg[i][0].elapsed_time(evg[i][-1])
+                                                     for i in range(K)])),
+                    "note": "vmoe_dispatch_ffn_fwd in place of vmoe_dispatch + "
+                            "vmoe_expert_ffn_fwd, vmoe_expert_ffn_bwd_gather in place of "
+                            "vmoe_expert_ffn_bwd (xe never written)"}
 
     flushed = None
     if args.flush_mall:
@@ -422,6 +452,7 @@ def main():
         "step_ms_events": step_ms_events,
         "balance_losses": balance,
         "ffn_quota_scheduler": quota,
+        "dispatch_fused_step": gathered,
     }
     if flushed is not None:
         fb = sum(cost[n][1] for n in moves)

@@ -202,6 +202,31 @@ vmoe_status vmoe_expert_ffn_bwd(const vmoe_shape* shape, const void* xe, const i
                                 const void* act_grad, const void* dye, void* dh, void* dxe,
                                 float* dw1, float* db1, float* dw2, float* db2, void* stream);
 
+/* The dispatch fused into the expert MLP's operand loads (bf16 layers): the
+ * up-projection reads each expert row straight from the token's row of x
+ * (buffer loads with per-row offsets), so xe is neither written nor read.
+ *   vmoe_dispatch_ffn_fwd = vmoe_dispatch + vmoe_expert_ffn_fwd without xe:
+ *     row_token [E, G*C] i32 out: the token of each kept expert row
+ *     (row_token[row(t, j)] = t; rows at or beyond n_e unspecified), for the
+ *     backward; act, act_grad, ye as vmoe_expert_ffn_fwd.
+ *   vmoe_expert_ffn_bwd_gather = vmoe_expert_ffn_bwd with dW1 = dH^T xe
+ *     reading xe's rows from x through row_token.
+ * Bit-identical to the unfused calls (the same bf16 values reach the same
+ * products). VMOE_ERR_UNSUPPORTED for f32 layers, for N * d * 2 > 2^31 - 16
+ * bytes of x, and (backward) for G * C > 6144 rows per expert. */
+vmoe_status vmoe_dispatch_ffn_fwd(const vmoe_shape* shape, const void* x,
+                                  const int32_t* expert_idx, const int32_t* slot,
+                                  const int32_t* row_base, const int32_t* counts, const void* w1,
+                                  const void* b1, const void* w2, const void* b2,
+                                  int32_t* row_token, void* act, void* act_grad, void* ye,
+                                  void* stream);
+vmoe_status vmoe_expert_ffn_bwd_gather(const vmoe_shape* shape, const void* x,
+                                       const int32_t* row_token, const int32_t* counts,
+                                       const void* w1, const void* w2, const void* act,
+                                       const void* act_grad, const void* dye, void* dh, void* dxe,
+                                       float* dw1, float* db1, float* dw2, float* db2,
+                                       void* stream);
+
 /* vmoe_expert_ffn_fwd and vmoe_expert_ffn_bwd with a device-side tile
  * scheduler (the lifespan-aware aligning of paper Sec. 3.2.2 applied to the
  * experts of one grouped GEMM): each GEMM runs as many persistent workgroups

@@ -27,11 +27,14 @@ vmoe_status dispatch_bwd_launch(const Dims& D, const void* dxe, const int32_t* i
                                 hipStream_t st);
 vmoe_status ffn_fwd_launch(const Dims& D, const void* xe, const int32_t* counts, const void* w1,
                            const void* b1, const void* w2, const void* b2, void* act,
-                           void* act_grad, void* ye, int sched, hipStream_t st);
+                           void* act_grad, void* ye, int sched, const int32_t* row_token,
+                           hipStream_t st);
 vmoe_status ffn_bwd_launch(const Dims& D, const void* xe, const int32_t* counts, const void* w1,
                            const void* w2, const void* act, const void* act_grad, const void* dye,
                            void* dh, void* dxe, float* dw1, float* db1, float* dw2, float* db2,
-                           int sched, hipStream_t st);
+                           int sched, const int32_t* row_token, hipStream_t st);
+vmoe_status row_token_launch(const Dims& D, const int32_t* idx, const int32_t* slot,
+                             const int32_t* row_base, int32_t* row_token, hipStream_t st);
 vmoe_status fcr_device_launch(int n, const int32_t* mn, const int32_t* sat, const double* coef,
                               int budget, int32_t* units, hipStream_t st);
 vmoe_status route_bwd_launch(const Dims& D, const void* x, const void* wr, const float* probs,
@@ -235,7 +238,7 @@ static vmoe_status ffn_fwd(const vmoe_shape* shape, const void* xe, const int32_
     VMOE_TRY(need(dev(xe) && dev(counts) && dev(w1) && dev(b1) && dev(w2) && dev(b2) &&
                   dev(act) && dev(act_grad) && dev(ye)));
     return vmoe::ffn_fwd_launch(D, xe, counts, w1, b1, w2, b2, act, act_grad, ye, sched,
-                                as_stream(stream));
+                                nullptr, as_stream(stream));
 }
 
 static vmoe_status ffn_bwd(const vmoe_shape* shape, const void* xe, const int32_t* counts,
@@ -248,7 +251,7 @@ static vmoe_status ffn_bwd(const vmoe_shape* shape, const void* xe, const int32_
                   dev(dye) && dev(dh) && dev(dxe) && dev(dw1) && dev(db1) && dev(dw2) &&
                   dev(db2)));
     return vmoe::ffn_bwd_launch(D, xe, counts, w1, w2, act, act_grad, dye, dh, dxe, dw1, db1,
-                                dw2, db2, sched, as_stream(stream));
+                                dw2, db2, sched, nullptr, as_stream(stream));
 }
 
 vmoe_status vmoe_expert_ffn_fwd(const vmoe_shape* shape, const void* xe, const int32_t* counts,
@@ -301,6 +304,48 @@ vmoe_status vmoe_expert_ffn_bwd_quota(const vmoe_shape* shape, const void* xe,
                                       float* db2, void* stream) {
     return ffn_bwd(shape, xe, counts, w1, w2, act, act_grad, dye, dh, dxe, dw1, db1, dw2, db2, 1,
                    stream);
+}
+
+// Gathered (dispatch-fused) expert MLP: bf16 only, x addressable by one
+// 32-bit buffer range, the weight gradient's token list within its LDS limit.
+static vmoe_status gather_ok(const Dims& D, bool bwd) {
+    if (D.dtype != VMOE_BF16) return VMOE_ERR_UNSUPPORTED;
+    if (static_cast<long long>(D.N) * D.d * 2 > vmoe::kGatherMaxBytes) return VMOE_ERR_UNSUPPORTED;
+    if (bwd && static_cast<long long>(D.G) * D.C > vmoe::kGatherRows) return VMOE_ERR_UNSUPPORTED;
+    return VMOE_OK;
+}
+
+vmoe_status vmoe_dispatch_ffn_fwd(const vmoe_shape* shape, const void* x,
+                                  const int32_t* expert_idx, const int32_t* slot,
+                                  const int32_t* row_base, const int32_t* counts, const void* w1,
+                                  const void* b1, const void* w2, const void* b2,
+                                  int32_t* row_token, void* act, void* act_grad, void* ye,
+                                  void* stream) {
+    Dims D;
+    VMOE_TRY(vmoe::make_dims(shape, &D));
+    VMOE_TRY(need(dev(x) && dev(expert_idx) && dev(slot) && dev(row_base) && dev(counts) &&
+                  dev(w1) && dev(b1) && dev(w2) && dev(b2) && dev(row_token) && dev(act) &&
+                  dev(act_grad) && dev(ye)));
+    VMOE_TRY(gather_ok(D, false));
+    VMOE_TRY(vmoe::row_token_launch(D, expert_idx, slot, row_base, row_token, as_stream(stream)));
+    return vmoe::ffn_fwd_launch(D, x, counts, w1, b1, w2, b2, act, act_grad, ye, 0, row_token,
+                                as_stream(stream));
+}
+
+vmoe_status vmoe_expert_ffn_bwd_gather(const vmoe_shape* shape, const void* x,
+                                       const int32_t* row_token, const int32_t* counts,
+                                       const void* w1, const void* w2, const void* act,
+                                       const void* act_grad, const void* dye, void* dh, void* dxe,
+                                       float* dw1, float* db1, float* dw2, float* db2,
+                                       void* stream) {
+    Dims D;
+    VMOE_TRY(vmoe::make_dims(shape, &D));
+    VMOE_TRY(need(dev(x) && dev(row_token) && dev(counts) && dev(w1) && dev(w2) && dev(act) &&
+                  dev(act_grad) && dev(dye) && dev(dh) && dev(dxe) && dev(dw1) && dev(db1) &&
+                  dev(dw2) && dev(db2)));
+    VMOE_TRY(gather_ok(D, true));
+    return vmoe::ffn_bwd_launch(D, x, counts, w1, w2, act, act_grad, dye, dh, dxe, dw1, db1, dw2,
+                                db2, 0, row_token, as_stream(stream));
 }
 
 vmoe_status vmoe_fill_clamp_refill_device(int32_t n, const int32_t* min_units,

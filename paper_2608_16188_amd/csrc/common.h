@@ -11,6 +11,16 @@ namespace vmoe {
 // Largest expert count the routing kernels support (one 64-bit lane mask).
 constexpr int kMaxExperts = 64;
 
+// Most rows per expert (G * C) whose token list the gathered weight-gradient
+// GEMM keeps in LDS beside its stage ring.
+constexpr int kGatherRows = 6144;
+// Byte offset marking a gathered row or column outside the operand: the sum
+// of a row's and a column's offset, either one this, lands at or past
+// kGatherSentinel (no 32-bit wrap) and so past the end of x, whose size
+// gathered calls bound by kGatherMaxBytes; the load returns zeros.
+constexpr uint32_t kGatherSentinel = 0x7FFFFFF0u;
+constexpr long long kGatherMaxBytes = kGatherSentinel;
+
 // ------------------------------------------------------------ bf16 <-> f32
 
 __device__ __forceinline__ float bf16_to_f32(uint16_t b) {

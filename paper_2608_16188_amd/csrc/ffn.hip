@@ -65,7 +65,14 @@ struct GemmArgs {
     long long bias_estride;
     const void* aux;        // EPI_GELU_GRAD: saved gelu'(H)
     float* bsum;            // EPI_F32 (bf16 path): row sums of A per expert, or null
+    // Gathered operand (kernels built with GATHER != 0): the operand's rows
+    // are token rows of x, row r of expert e being x[tok[e * tok_estride + r]];
+    // its base is x itself (estride 0) and gather_bytes the size of x.
+    const int32_t* tok;     // null: this problem's operand is not gathered
+    long long tok_estride;
+    long long gather_bytes;
 };
+
 
 // Up to two independent GEMMs of one kernel instantiation in one launch (the
 // two weight gradients): blocks [0, total[0]) work on problem 0, the rest on
@@ -380,6 +387,63 @@ struct DmaStage {
             }
             __builtin_amdgcn_raw_ptr_buffer_load_lds(
                 rs, (__attribute__((address_space(3))) void*)(s + blk * 512), 16, off, 0, 0, 0);
+        }
+    }
+    // Gathered operands (rows of x): the stage row lane L fetches in wave
+    // instruction q (k-major: an mn row of the tile; mn-major: a k row).
+    static __device__ __forceinline__ int lane_row(int q) {
+        const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+        const int byte = (wave * PER + q) * 1024 + 16 * lane;
+        return byte / (KMAJOR ? KB * 2 : ROWS * 2);
+    }
+    // k-major, gathered rows: rowoff[q] = element offset in x of the start of
+    // the row lane_row(q) stands for (-1 past the rows).
+    static __device__ __forceinline__ void issue_rows(__amdgpu_buffer_rsrc_t rs,
+                                                      const int (&rowoff)[PER], int k0,
+                                                      int k_lim, uint16_t* s) {
+        static_assert(KMAJOR, "row gather: k-major operand");
+        const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+        for (int q = 0; q < PER; ++q) {
+            const int blk = wave * PER + q;
+            const int byte = blk * 1024 + 16 * lane;
+            constexpr int RB = KB * 2, Q = KB / 8, P = 16 / Q;
+            const int r = byte / RB;
+            const int c = ((byte % RB) >> 4) ^ ((r / P) % Q);
+            const int kk = k0 + 8 * c;
+            const uint32_t off = (rowoff[q] >= 0 && kk < k_lim)
+                                     ? static_cast<uint32_t>(rowoff[q] + kk) * 2u
+                                     : kOutOfRange;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                rs, (__attribute__((address_space(3))) void*)(s + blk * 512), 16, off, 0, 0, 0);
+        }
+    }
+    // mn-major, gathered k rows: rowoff[q] = byte offset in x of the k row
+    // lane_row(q) stands for in this stage, col[q] = byte offset of the lane's
+    // 8 columns in it (krow_cols); either is kGatherSentinel outside the
+    // operand, which puts the sum past the end of x.
+    static __device__ __forceinline__ void krow_cols(int mn0, int mn_lim, uint32_t (&col)[PER]) {
+        static_assert(!KMAJOR, "k-row gather: mn-major operand");
+        const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+        for (int q = 0; q < PER; ++q) {
+            const int byte = (wave * PER + q) * 1024 + 16 * lane;
+            constexpr int RB = ROWS * 2;
+            const int r = byte / RB;
+            const int mn = mn0 + 8 * (((byte % RB) >> 4) ^ mn_swizzle<ROWS>(r));
+            col[q] = mn < mn_lim ? static_cast<uint32_t>(mn) * 2u : kGatherSentinel;
+        }
+    }
+    static __device__ __forceinline__ void issue_krows(__amdgpu_buffer_rsrc_t rs,
+                                                       const uint32_t (&rowoff)[PER],
+                                                       const uint32_t (&col)[PER], uint16_t* s) {
+        const int wave = threadIdx.x >> 6;
+#pragma unroll
+        for (int q = 0; q < PER; ++q) {
+            const int blk = wave * PER + q;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                rs, (__attribute__((address_space(3))) void*)(s + blk * 512), 16,
+                rowoff[q] + col[q], 0, 0, 0);
         }
     }
 };
@@ -721,9 +785,19 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& p, f32x16 (&acc)[T
 // SCHED = 1: persistent blocks, each expert owning the number of blocks the
 // fill-clamp-refill quota gives it, each block taking every units-th tile
 // of its expert.
-template <class T, bool A_KMAJOR, bool B_KMAJOR, int EPI, int SCHED = 0>
+// GATHER = 1: operand A's rows are gathered token rows of x (the
+// up-projection fused with the dispatch); GATHER = 2: operand B's k rows are
+// (the input-weight gradient, problems with a token list).
+// (the k-row gather's token table takes the LDS of a second 4-wave block)
+template <class T, int GATHER>
+constexpr int gemm_waves_per_eu() {
+    return GATHER == 2 && T::NW == 4 ? 1 : T::WAVES_PER_EU;
+}
+
+template <class T, bool A_KMAJOR, bool B_KMAJOR, int EPI, int SCHED = 0, int GATHER = 0>
 __global__ __launch_bounds__(T::NT)
-__attribute__((amdgpu_waves_per_eu(T::WAVES_PER_EU, T::WAVES_PER_EU)))
+__attribute__((amdgpu_waves_per_eu(gemm_waves_per_eu<T, GATHER>(),
+                                   gemm_waves_per_eu<T, GATHER>())))
 void gemm_bf16_kernel(GemmBatch batch) {
     using CFG = GemmCfg<T, A_KMAJOR, B_KMAJOR, EPI>;
     constexpr int BM_ = T::BM, BN_ = T::BN, KB = T::KB, NS = T::NS, MODE = T::MODE;
@@ -736,6 +810,8 @@ void gemm_bf16_kernel(GemmBatch batch) {
     __shared__ __attribute__((aligned(1024))) uint16_t buf2[NS > 2 ? SZX : 8];
     __shared__ __attribute__((aligned(1024))) uint16_t buf3[NS > 3 ? SZX : 8];
     __shared__ __attribute__((aligned(1024))) uint16_t buf4[NS > 4 ? SZX : 8];
+    // gathered k rows' byte offsets in x (padded by two rings of stages)
+    __shared__ uint32_t tok_s[GATHER == 2 ? kGatherRows + 2 * NS * KB : 1];
 
     const int b = blockIdx.x;
     int qe = 0, qu = 0, qn = 0, qt = 0, qne = 0;  // quota: expert, rank, units, tiles, rows
@@ -794,6 +870,12 @@ void gemm_bf16_kernel(GemmBatch batch) {
         ne = expert_rows(batch.p[prob].counts, batch.p[prob].G, batch.p[prob].E, e);
     }
     }
+    // The tile body, instantiated once per operand kind: with GS != 0 the
+    // gathered operand is known at compile time, so a problem that gathers
+    // and one that does not (the two weight gradients of one launch) each
+    // get a main loop register-allocated for its own addressing alone.
+    auto tile = [&](auto gather_kind) -> bool {
+    constexpr int GS = decltype(gather_kind)::value;
     const GemmArgs& p = batch.p[prob];
     const int tiles_n = batch.tiles_n[prob];
     const int group_m = batch.group_m;
@@ -810,15 +892,47 @@ void gemm_bf16_kernel(GemmBatch batch) {
     const int K = p.var_k ? ne : p.K;
     const int N = p.N;
     const int m0 = tm * BM_, n0 = tn * BN_;
-    if (m0 >= M) {
-        if constexpr (SCHED == 0) return;
-        else continue;
-    }
+    if (m0 >= M) return false;
 
-    const __amdgpu_buffer_rsrc_t ra_rs = make_rsrc(
-        static_cast<const uint16_t*>(p.a.base) + e * p.a.estride, p.a.estride * 2);
-    const __amdgpu_buffer_rsrc_t rb_rs = make_rsrc(
-        static_cast<const uint16_t*>(p.b.base) + e * p.b.estride, p.b.estride * 2);
+    static_assert(GS == 0 || (GS == 1 && A_KMAJOR) || (GS == 2 && !B_KMAJOR),
+                  "gathered rows: k-major A or mn-major B");
+    // gathered operands address x itself: its whole size is their range
+    const __amdgpu_buffer_rsrc_t ra_rs =
+        GS == 1 ? make_rsrc(p.a.base, p.gather_bytes)
+           : make_rsrc(static_cast<const uint16_t*>(p.a.base) + e * p.a.estride,
+                       p.a.estride * 2);
+    const __amdgpu_buffer_rsrc_t rb_rs =
+        GS == 2 ? make_rsrc(p.b.base, p.gather_bytes)
+           : make_rsrc(static_cast<const uint16_t*>(p.b.base) + e * p.b.estride,
+                       p.b.estride * 2);
+    // Gathered A rows (the tile's rows, fixed over the k loop): each lane's
+    // row offsets in x, read once. Gathered B k rows (new ones every stage):
+    // the expert's token list in LDS, each lane's offsets for the next
+    // stage read one stage ahead.
+    using DA_ = DmaStage<BM_, A_KMAJOR, KB, T::NT>;
+    using DB_ = DmaStage<BN_, B_KMAJOR, KB, T::NT>;
+    int arow[GS == 1 ? DA_::PER : 1];
+    uint32_t bk[GS == 2 ? DB_::PER : 1], bcol[GS == 2 ? DB_::PER : 1];
+    if constexpr (GS == 1) {
+#pragma unroll
+        for (int q = 0; q < DA_::PER; ++q) {
+            const int r = DA_::lane_row(q);
+            arow[q] = m0 + r < M ? p.tok[e * p.tok_estride + m0 + r] * p.a.ld : -1;
+        }
+    } else if constexpr (GS == 2) {
+        // the expert's k rows as byte offsets of their rows of x, and the
+        // sentinel past K up to the last row the ring prefetches (so the
+        // stage loop tests no bound)
+        const int kfill = ((K + NS * KB - 1) / (NS * KB) + 1) * NS * KB;
+        for (int i = threadIdx.x; i < kfill; i += T::NT)
+            tok_s[i] = i < K ? static_cast<uint32_t>(p.tok[e * p.tok_estride + i]) *
+                                   (2u * static_cast<uint32_t>(p.b.ld))
+                             : kGatherSentinel;
+        __syncthreads();
+        DB_::krow_cols(n0, N, bcol);
+#pragma unroll
+        for (int q = 0; q < DB_::PER; ++q) bk[q] = tok_s[DB_::lane_row(q)];
+    }
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int wm = wave / T::WGN, wn = wave % T::WGN;
@@ -864,8 +978,21 @@ void gemm_bf16_kernel(GemmBatch batch) {
     uint4 ra[MODE == STAGE_REG ? RA::V : 1], rb[MODE == STAGE_REG ? RB::V : 1];
 
     auto issue = [&](int kt, uint16_t* dst) {
-        if (!skip_a) DA::issue(ra_rs, p.a.ld, m0, M, kt * KB, K, dst);
-        DB::issue(rb_rs, p.b.ld, n0, N, kt * KB, K, dst + AE);
+        if (!skip_a) {
+            if constexpr (GS == 1) {
+                DA::issue_rows(ra_rs, arow, kt * KB, K, dst);
+            } else {
+                DA::issue(ra_rs, p.a.ld, m0, M, kt * KB, K, dst);
+            }
+        }
+        if constexpr (GS == 2) {
+            DB::issue_krows(rb_rs, bk, bcol, dst + AE);
+            // stages are issued in order: the next one's k rows
+#pragma unroll
+            for (int q = 0; q < DB::PER; ++q) bk[q] = tok_s[(kt + 1) * KB + DB::lane_row(q)];
+        } else {
+            DB::issue(rb_rs, p.b.ld, n0, N, kt * KB, K, dst + AE);
+        }
     };
     // wait until stage kt + 1 has landed (this wave's share of it)
     auto wait_ring = [&]() {
@@ -1018,6 +1145,16 @@ void gemm_bf16_kernel(GemmBatch batch) {
     const int eb = wave % NS;
     uint16_t* const ep = eb == 0 ? buf0 : eb == 1 ? buf1 : eb == 2 ? buf2 : eb == 3 ? buf3 : buf4;
     gemm_epilogue<T, CFG, EPI>(p, acc, buf0, ep, rsum, row_sum, e, M, N, m0, n0, fm_live);
+    return true;
+    };
+    bool ran;
+    if constexpr (GATHER == 0) ran = tile(std::integral_constant<int, 0>{});
+    else if (batch.p[prob].tok != nullptr) ran = tile(std::integral_constant<int, GATHER>{});
+    else ran = tile(std::integral_constant<int, 0>{});
+    if (!ran) {
+        if constexpr (SCHED == 0) return;
+        else continue;
+    }
     if constexpr (SCHED == 0) break;
     // the next tile's first stages land in the buffers this epilogue staged
     // its outputs in: every wave's LDS accesses are done before any issues
@@ -1167,7 +1304,7 @@ __global__ __launch_bounds__(256) void colsum_kernel(const T* __restrict__ src,
 constexpr int kNumCUs = 256;
 
 // One launch over `n` (1 or 2) problems; grid_m_rows[i] bounds problem i's m.
-template <class T, bool AK, bool BK_, int EPI>
+template <class T, bool AK, bool BK_, int EPI, int GATHER = 0>
 void launch_bf16(const Dims& D, const GemmArgs* a, const int* grid_m_rows, int n, int sched,
                  hipStream_t st) {
     GemmBatch b{};
@@ -1187,20 +1324,20 @@ void launch_bf16(const Dims& D, const GemmArgs* a, const int* grid_m_rows, int n
     b.group_m = one_col ? one_col : (T::WAVES_PER_EU == 2 && T::NW == 4 ? 8 : 4);
     b.chunk = 4 * b.group_m;
     b.per_xcd = static_cast<int>(cdiv(b.total[0] + b.total[1], 8 * b.chunk)) * b.chunk;
-    if (sched) {
+    if (sched && GATHER == 0) {
         // persistent blocks under quotas: as many as are resident at once
         // (one per CU for the 8-wave tiles, two for the 4-wave ones)
         const int resident = kNumCUs * (T::NW == 8 ? 1 : T::WAVES_PER_EU);
         const int grid = min(8 * b.per_xcd, resident);
         gemm_bf16_kernel<T, AK, BK_, EPI, 1><<<grid, T::NT, 0, st>>>(b);
     } else {
-        gemm_bf16_kernel<T, AK, BK_, EPI, 0><<<8 * b.per_xcd, T::NT, 0, st>>>(b);
+        gemm_bf16_kernel<T, AK, BK_, EPI, 0, GATHER><<<8 * b.per_xcd, T::NT, 0, st>>>(b);
     }
 }
 
-template <class T, bool AK, bool BK_, int EPI>
+template <class T, bool AK, bool BK_, int EPI, int GATHER = 0>
 void launch_bf16(const Dims& D, const GemmArgs& a, int grid_m_rows, int sched, hipStream_t st) {
-    launch_bf16<T, AK, BK_, EPI>(D, &a, &grid_m_rows, 1, sched, st);
+    launch_bf16<T, AK, BK_, EPI, GATHER>(D, &a, &grid_m_rows, 1, sched, st);
 }
 
 // Tilings (BM, BN, waves, KB, stages, staging).
@@ -1214,14 +1351,14 @@ double tile_cost(long long tiles, int bm, int bn, double eff) {
     return static_cast<double>((tiles + kNumCUs - 1) / kNumCUs) * bm * bn * eff;
 }
 
-template <bool AK, bool BK_, int EPI>
+template <bool AK, bool BK_, int EPI, int GATHER = 0>
 void launch_gemm(const Dims& D, const GemmArgs& a, int grid_m_rows, int sched, hipStream_t st) {
     if (D.dtype == VMOE_BF16) {
         // 256 x 256 tiles (half the operand bytes per flop of 128 x 128) for
         // the GEMMs whose m is the expert's rows; the weight gradients (k is
         // the rows, often short) run 128 x 128 tiles, two blocks per CU.
         if constexpr (EPI == EPI_F32) {
-            launch_bf16<TileSmall, AK, BK_, EPI>(D, a, grid_m_rows, sched, st);
+            launch_bf16<TileSmall, AK, BK_, EPI, GATHER>(D, a, grid_m_rows, sched, st);
         } else if constexpr (EPI == EPI_BIAS || EPI == EPI_STORE) {
             // Narrow outputs (N = d_model) give few tiles: 192-column tiles fill
             // more CUs when that saves a round (two-stage 64-deep ring, a few
@@ -1230,11 +1367,11 @@ void launch_gemm(const Dims& D, const GemmArgs& a, int grid_m_rows, int sched, h
             const double big = tile_cost(D.E * tm * cdiv(a.N, 256), 256, 256, 1.0);
             const double narrow = tile_cost(D.E * tm * cdiv(a.N, 192), 256, 192, 1.05);
             if (narrow < big)
-                launch_bf16<TileNarrow, AK, BK_, EPI>(D, a, grid_m_rows, sched, st);
+                launch_bf16<TileNarrow, AK, BK_, EPI, GATHER>(D, a, grid_m_rows, sched, st);
             else
-                launch_bf16<TileBig, AK, BK_, EPI>(D, a, grid_m_rows, sched, st);
+                launch_bf16<TileBig, AK, BK_, EPI, GATHER>(D, a, grid_m_rows, sched, st);
         } else {
-            launch_bf16<TileBig, AK, BK_, EPI>(D, a, grid_m_rows, sched, st);
+            launch_bf16<TileBig, AK, BK_, EPI, GATHER>(D, a, grid_m_rows, sched, st);
         }
     } else {
         dim3 grid(cdiv(a.N, FT), cdiv(grid_m_rows, FT), D.E);
@@ -1274,7 +1411,8 @@ vmoe_status fcr_device_launch(int n, const int32_t* mn, const int32_t* sat, cons
 
 vmoe_status ffn_fwd_launch(const Dims& D, const void* xe, const int32_t* counts, const void* w1,
                            const void* b1, const void* w2, const void* b2, void* act,
-                           void* act_grad, void* ye, int sched, hipStream_t st) {
+                           void* act_grad, void* ye, int sched, const int32_t* row_token,
+                           hipStream_t st) {
     const long long rows = D.rows_per_expert();
     if (rows == 0 || D.E == 0) return VMOE_OK;
     // H = xe W1^T + b1 (never stored), A = gelu(H), A' = gelu'(H)
@@ -1290,7 +1428,16 @@ vmoe_status ffn_fwd_launch(const Dims& D, const void* xe, const int32_t* counts,
     g1.ldo = D.f;
     g1.bias = b1;
     g1.bias_estride = D.f;
-    launch_gemm<true, true, EPI_FWD1>(D, g1, static_cast<int>(rows), sched, st);
+    if (row_token != nullptr) {
+        // dispatch fused into the loads: row r of expert e is x[row_token[e, r]]
+        g1.a = Operand{xe, 0, D.d};
+        g1.tok = row_token;
+        g1.tok_estride = rows;
+        g1.gather_bytes = static_cast<long long>(D.N) * D.d * 2;
+        launch_gemm<true, true, EPI_FWD1, 1>(D, g1, static_cast<int>(rows), sched, st);
+    } else {
+        launch_gemm<true, true, EPI_FWD1>(D, g1, static_cast<int>(rows), sched, st);
+    }
     // ye = A W2^T + b2
     GemmArgs g2 = base_args(D, counts);
     g2.a = Operand{act, rows * D.f, D.f};
@@ -1310,7 +1457,7 @@ vmoe_status ffn_fwd_launch(const Dims& D, const void* xe, const int32_t* counts,
 vmoe_status ffn_bwd_launch(const Dims& D, const void* xe, const int32_t* counts, const void* w1,
                            const void* w2, const void* act, const void* act_grad, const void* dye,
                            void* dh, void* dxe, float* dw1, float* db1, float* dw2, float* db2,
-                           int sched, hipStream_t st) {
+                           int sched, const int32_t* row_token, hipStream_t st) {
     const long long rows = D.rows_per_expert();
     if (D.E == 0) return VMOE_OK;
     if (rows > 0) {
@@ -1362,6 +1509,13 @@ vmoe_status ffn_bwd_launch(const Dims& D, const void* xe, const int32_t* counts,
     v.out_estride = static_cast<long long>(D.f) * D.d;
     v.ldo = D.d;
     v.bsum = D.dtype == VMOE_BF16 ? db1 : nullptr;  // db1 = row sums of dH^T
+    if (row_token != nullptr) {
+        // xe rows gathered from x: row r of expert e is x[row_token[e, r]]
+        v.b = Operand{xe, 0, D.d};
+        v.tok = row_token;
+        v.tok_estride = rows;
+        v.gather_bytes = static_cast<long long>(D.N) * D.d * 2;
+    }
     if (D.dtype == VMOE_BF16) {
         // both weight gradients in one launch (same kernel, independent tiles),
         // with the tiling of the least cost in rounds x tile area (128 x 128
@@ -1375,12 +1529,19 @@ vmoe_status ffn_bwd_launch(const Dims& D, const void* xe, const int32_t* counts,
         const double small = tile_cost((tiles(128, 128) + 1) / 2, 256, 128, 1.15);
         const double narrow = tile_cost(tiles(256, 192), 256, 192, 1.05);
         const double big = tile_cost(tiles(256, 256), 256, 256, 1.0);
-        if (narrow <= small && narrow <= big)
-            launch_bf16<TileNarrow, false, false, EPI_F32>(D, both, rows_m, 2, sched, st);
-        else if (big <= small)
-            launch_bf16<TileBig, false, false, EPI_F32>(D, both, rows_m, 2, sched, st);
-        else
-            launch_bf16<TileSmall, false, false, EPI_F32>(D, both, rows_m, 2, sched, st);
+        // (the gathered input-weight gradient takes the same tiling, so its
+        // results, bias-gradient sums included, are the unfused call's bits)
+        auto go = [&](auto gather) {
+            constexpr int GA = decltype(gather)::value;
+            if (narrow <= small && narrow <= big)
+                launch_bf16<TileNarrow, false, false, EPI_F32, GA>(D, both, rows_m, 2, sched, st);
+            else if (big <= small)
+                launch_bf16<TileBig, false, false, EPI_F32, GA>(D, both, rows_m, 2, sched, st);
+            else
+                launch_bf16<TileSmall, false, false, EPI_F32, GA>(D, both, rows_m, 2, sched, st);
+        };
+        if (row_token != nullptr) go(std::integral_constant<int, 2>{});
+        else go(std::integral_constant<int, 0>{});
     } else {
         launch_gemm<false, false, EPI_F32>(D, w, D.d, 0, st);
         launch_gemm<false, false, EPI_F32>(D, v, D.f, 0, st);

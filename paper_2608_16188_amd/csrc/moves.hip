@@ -284,7 +284,35 @@ RouteMeta meta(const Dims& D, const int32_t* idx, const int32_t* slot, const int
     return RouteMeta{idx, slot, row_base, D.N, D.Ng, D.E, D.k, D.C, D.G};
 }
 
+// The dispatch's permutation without its data: row_token[row(t, j)] = t for
+// every kept assignment (rows no assignment lands on are left as they are).
+// One thread per token, its assignments J at a time.
+template <int J>
+__global__ __launch_bounds__(kBlock) void row_token_kernel(int32_t* __restrict__ row_token,
+                                                           RouteMeta m) {
+    const int t = blockIdx.x * kBlock + threadIdx.x;
+    if (t >= m.N) return;
+    for (int j0 = 0; j0 < m.k; j0 += J) {
+        Rows<J> r;
+        r.fetch(m, t, j0);
+#pragma unroll
+        for (int jj = 0; jj < J; ++jj)
+            if (r.r[jj] >= 0) row_token[r.r[jj]] = t;
+    }
+}
+
 }  // namespace
+
+vmoe_status row_token_launch(const Dims& D, const int32_t* idx, const int32_t* slot,
+                             const int32_t* row_base, int32_t* row_token, hipStream_t st) {
+    if (D.N == 0) return VMOE_OK;
+    const RouteMeta m = meta(D, idx, slot, row_base);
+    if (D.k <= 2)
+        row_token_kernel<2><<<cdiv(D.N, kBlock), kBlock, 0, st>>>(row_token, m);
+    else
+        row_token_kernel<4><<<cdiv(D.N, kBlock), kBlock, 0, st>>>(row_token, m);
+    return launch_status();
+}
 
 vmoe_status dispatch_launch(const Dims& D, const void* x, const int32_t* idx, const int32_t* slot,
                             const int32_t* row_base, void* xe, hipStream_t st) {

@@ -76,6 +76,7 @@ class LayerBuffers:
                                     dtype=torch.uint8, device=dev)
         # expert buffers
         self.xe = torch.empty(E, R, d, dtype=act, device=dev)
+        self.row_token = torch.empty(E, max(R, 1), dtype=i32, device=dev)  # fused path
         self.a = torch.empty(E, R, f, dtype=act, device=dev)       # gelu(H)
         self.a_grad = torch.empty(E, R, f, dtype=act, device=dev)  # gelu'(H)
         self.ye = torch.empty(E, R, d, dtype=act, device=dev)
@@ -102,11 +103,20 @@ class LayerBuffers:
                      self.expert_idx, self.slot, self.gate, self.order, self.counts,
                      self.row_base, self.route_ws, stream)
 
-    def forward(self, logits_in: bool = False, stream=None, quota: bool = False):
+    def forward(self, logits_in: bool = False, stream=None, quota: bool = False,
+                gather: bool = False):
         """quota: the expert MLP through the fill-clamp-refill tile scheduler
-        (vmoe_expert_ffn_fwd_quota; same results)."""
+        (vmoe_expert_ffn_fwd_quota; same results); gather: the dispatch fused
+        into the up-projection's loads (vmoe_dispatch_ffn_fwd; xe unused)."""
         s = self.shape
         self.route(logits_in, stream)
+        if gather:
+            V.vmoe_dispatch_ffn_fwd(s, self.x, self.expert_idx, self.slot, self.row_base,
+                                    self.counts, self.w1, self.b1, self.w2, self.b2,
+                                    self.row_token, self.a, self.a_grad, self.ye, stream)
+            V.vmoe_combine_fwd(s, self.ye, self.expert_idx, self.slot, self.row_base, self.gate,
+                               self.y, stream)
+            return
         V.vmoe_dispatch(s, self.x, self.expert_idx, self.slot, self.row_base, self.xe, stream)
         ffn = V.vmoe_expert_ffn_fwd_quota if quota else V.vmoe_expert_ffn_fwd
         ffn(s, self.xe, self.counts, self.w1, self.b1, self.w2, self.b2, self.a, self.a_grad,
@@ -114,7 +124,8 @@ class LayerBuffers:
         V.vmoe_combine_fwd(s, self.ye, self.expert_idx, self.slot, self.row_base, self.gate,
                            self.y, stream)
 
-    def backward(self, stream=None, fused: bool = True, quota: bool = False):
+    def backward(self, stream=None, fused: bool = True, quota: bool = False,
+                 gather: bool = False):
         """fused: dispatch and router backward in one call (bit-identical to
         vmoe_dispatch_bwd followed by vmoe_route_bwd, which fused=False runs);
         quota: the expert MLP backward through the fill-clamp-refill tile
@@ -122,9 +133,14 @@ class LayerBuffers:
         s = self.shape
         V.vmoe_combine_bwd(s, self.dy, self.ye, self.expert_idx, self.slot, self.row_base,
                            self.gate, self.dye, self.dgate, stream)
-        ffn = V.vmoe_expert_ffn_bwd_quota if quota else V.vmoe_expert_ffn_bwd
-        ffn(s, self.xe, self.counts, self.w1, self.w2, self.a, self.a_grad, self.dye, self.dh,
-            self.dxe, self.dw1, self.db1, self.dw2, self.db2, stream)
+        if gather:
+            V.vmoe_expert_ffn_bwd_gather(s, self.x, self.row_token, self.counts, self.w1,
+                                         self.w2, self.a, self.a_grad, self.dye, self.dh,
+                                         self.dxe, self.dw1, self.db1, self.dw2, self.db2, stream)
+        else:
+            ffn = V.vmoe_expert_ffn_bwd_quota if quota else V.vmoe_expert_ffn_bwd
+            ffn(s, self.xe, self.counts, self.w1, self.w2, self.a, self.a_grad, self.dye,
+                self.dh, self.dxe, self.dw1, self.db1, self.dw2, self.db2, stream)
         if fused:
             V.vmoe_dispatch_route_bwd(s, self.dxe, self.row_base, self.x, self.w_router,
                                       self.probs, self.expert_idx, self.slot, self.dgate, self.dx,
@@ -135,6 +151,6 @@ class LayerBuffers:
         V.vmoe_route_bwd(s, self.x, self.w_router, self.probs, self.expert_idx, self.slot,
                          self.dgate, self.dx, self.dw_router, self.route_bwd_ws, stream)
 
-    def step(self, stream=None, quota: bool = False):
-        self.forward(stream=stream, quota=quota)
-        self.backward(stream=stream, quota=quota)
+    def step(self, stream=None, quota: bool = False, gather: bool = False):
+        self.forward(stream=stream, quota=quota, gather=gather)
+        self.backward(stream=stream, quota=quota, gather=gather)

@@ -67,6 +67,8 @@ def _load():
         "vmoe_dispatch": [S] + [P] * 6,
         "vmoe_expert_ffn_fwd": [S] + [P] * 10,
         "vmoe_expert_ffn_fwd_quota": [S] + [P] * 10,
+        "vmoe_dispatch_ffn_fwd": [S] + [P] * 14,
+        "vmoe_expert_ffn_bwd_gather": [S] + [P] * 15,
         "vmoe_expert_ffn_bwd_quota": [S] + [P] * 14,
         "vmoe_fill_clamp_refill_device": [ctypes.c_int32, P, P, P, ctypes.c_int32, P, P],
         "vmoe_combine_fwd": [S] + [P] * 7,
@@ -167,6 +169,24 @@ def vmoe_expert_ffn_fwd(shape, xe, counts, w1, b1, w2, b2, act, act_grad, ye, st
     _check("vmoe_expert_ffn_fwd", _lib.vmoe_expert_ffn_fwd(
         ctypes.byref(shape), _ptr(xe), _ptr(counts), _ptr(w1), _ptr(b1), _ptr(w2), _ptr(b2),
         _ptr(act), _ptr(act_grad), _ptr(ye), _stream(stream)))
+
+
+def vmoe_dispatch_ffn_fwd(shape, x, expert_idx, slot, row_base, counts, w1, b1, w2, b2,
+                          row_token, act, act_grad, ye, stream=None):
+    """Dispatch fused into the expert MLP forward (no xe); writes row_token."""
+    _check("vmoe_dispatch_ffn_fwd", _lib.vmoe_dispatch_ffn_fwd(
+        ctypes.byref(shape), _ptr(x), _ptr(expert_idx), _ptr(slot), _ptr(row_base),
+        _ptr(counts), _ptr(w1), _ptr(b1), _ptr(w2), _ptr(b2), _ptr(row_token), _ptr(act),
+        _ptr(act_grad), _ptr(ye), _stream(stream)))
+
+
+def vmoe_expert_ffn_bwd_gather(shape, x, row_token, counts, w1, w2, act, act_grad, dye, dh, dxe,
+                               dw1, db1, dw2, db2, stream=None):
+    """Expert MLP backward reading xe's rows from x through row_token."""
+    _check("vmoe_expert_ffn_bwd_gather", _lib.vmoe_expert_ffn_bwd_gather(
+        ctypes.byref(shape), _ptr(x), _ptr(row_token), _ptr(counts), _ptr(w1), _ptr(w2),
+        _ptr(act), _ptr(act_grad), _ptr(dye), _ptr(dh), _ptr(dxe), _ptr(dw1), _ptr(db1),
+        _ptr(dw2), _ptr(db2), _stream(stream)))
 
 
 def vmoe_expert_ffn_fwd_quota(shape, xe, counts, w1, b1, w2, b2, act, act_grad, ye,

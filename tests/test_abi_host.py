@@ -17,7 +17,7 @@ FAKE = 0x10000  # 16-byte aligned, never dereferenced: validation fails first
 
 def test_every_declared_symbol_is_exported():
     declared = V.header_symbols()
-    assert len(declared) == 25, declared
+    assert len(declared) == 27, declared
     out = subprocess.check_output(["nm", "-D", "--defined-only", V.LIB_PATH], text=True)
     exported = {line.split()[-1] for line in out.splitlines() if line.strip()}
     missing = [s for s in declared if s not in exported]
@@ -228,3 +228,20 @@ def test_route_noalloc_validates_before_touching_the_gpu():
         s = V.make_shape(c.n_tokens, c.n_groups, c.d_model, c.d_ff, c.n_experts, c.k,
                          c.capacity_factor, 1)
         assert V.vmoe_route_workspace_bytes(s) <= 16 << 20
+
+
+def test_gathered_expert_mlp_refuses_unsupported_shapes():
+    """The dispatch-fused calls run bf16 layers only, with x within one
+    32-bit buffer range and (backward) at most 6144 rows per expert."""
+    L = V._lib
+    f32 = V.make_shape(64, 1, 64, 128, 8, 2, 1.0, V.VMOE_F32)
+    assert L.vmoe_dispatch_ffn_fwd(ctypes.byref(f32), *([FAKE] * 13), None) == \
+        V.VMOE_ERR_UNSUPPORTED
+    assert L.vmoe_expert_ffn_bwd_gather(ctypes.byref(f32), *([FAKE] * 14), None) == \
+        V.VMOE_ERR_UNSUPPORTED
+    many_rows = V.make_shape(40000, 1, 64, 128, 8, 2, 1.0, V.VMOE_BF16)  # C = 10000
+    assert V.vmoe_capacity(many_rows) > 6144
+    assert L.vmoe_expert_ffn_bwd_gather(ctypes.byref(many_rows), *([FAKE] * 14), None) == \
+        V.VMOE_ERR_UNSUPPORTED
+    assert L.vmoe_dispatch_ffn_fwd(ctypes.byref(_shape()), None, *([FAKE] * 12), None) == \
+        V.VMOE_ERR_INVALID_ARG

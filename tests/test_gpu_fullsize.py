@@ -15,8 +15,10 @@ C ABI, and every output and intermediate is compared with the oracle
   |a - b| <= 2e-2 max(|b|, ||dy_t * ye_row||_2), the second term the size of
   its summands (a wrong element is off by about that much);
 - the router gradient's rows; empty experts' gradients exactly zero.
-The ViT-L/16 layer runs a second time with the expert MLP through the
-fill-clamp-refill tile scheduler (vmoe_expert_ffn_fwd_quota / _bwd_quota).
+The ViT-L/16 layer runs twice more: with the expert MLP through the
+fill-clamp-refill tile scheduler (vmoe_expert_ffn_fwd_quota / _bwd_quota) and
+with the dispatch fused into the expert MLP's loads (vmoe_dispatch_ffn_fwd,
+vmoe_expert_ffn_bwd_gather; xe is then never written and not compared).
 
 With VMOE_PARITY_REPORT_DIR set, each case writes its metrics (per tensor,
 worst row, element-wise) there as JSON.
@@ -35,9 +37,10 @@ from .test_gpu_parity import _compare_routing
 
 pytestmark = pytest.mark.gpu
 
-# (workload, expert MLP through the fill-clamp-refill tile scheduler)
-FULL = [("vitb16_bf16", False), ("vitl16_384_bf16", False), ("vitl16_384_bf16", True),
-        ("wide_e32_bf16", False), ("multitask17_bf16", False)]
+# (workload, variant of the expert MLP calls: "" the default ones, "quota" the
+# fill-clamp-refill tile scheduler, "gather" the dispatch fused into the loads)
+FULL = [("vitb16_bf16", ""), ("vitl16_384_bf16", ""), ("vitl16_384_bf16", "quota"),
+        ("vitl16_384_bf16", "gather"), ("wide_e32_bf16", ""), ("multitask17_bf16", "")]
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -54,13 +57,13 @@ def _rows(t, e, n, dtype):
     return W.to_f64(to_numpy(t[e, :n]), dtype) if n else np.zeros((0, t.shape[2]))
 
 
-@pytest.mark.parametrize("name,quota", FULL,
-                         ids=[n + ("-quota" if q else "") for n, q in FULL])
-def test_layer_full_size_every_element(name, quota):
+@pytest.mark.parametrize("name,variant", FULL,
+                         ids=[n + ("-" + v if v else "") for n, v in FULL])
+def test_layer_full_size_every_element(name, variant):
     cfg, inp = workload_inputs(name)
-    say("full size, every element:", name, "quota scheduler" if quota else "", "GPU step")
+    say("full size, every element:", name, variant, "GPU step")
     L = LayerBuffers(cfg, inp)
-    L.step(quota=quota)
+    L.step(quota=variant == "quota", gather=variant == "gather")
     torch.cuda.synchronize()
     dt, tol = cfg.dtype, TOL[cfg.dtype]
     f = {key: as_f64(inp[key], dt) for key in ("x", "w_router", "w1", "b1", "w2", "b2", "dy")}
@@ -77,12 +80,13 @@ def test_layer_full_size_every_element(name, quota):
                  probs=to_numpy(L.probs), gate=to_numpy(L.gate))
     _compare_routing(got_r, ref, name)
     say(name, "routing bit-exact; comparing expert rows")
-    rep = Report(name + ("-quota" if quota else ""))
+    rep = Report(name + ("-" + variant if variant else ""))
     n_e = ref["n_e"]
     dw1, db1, dw2, db2 = (to_numpy(t) for t in (L.dw1, L.db1, L.dw2, L.db2))
     for e in range(cfg.n_experts):
         n = int(n_e[e])
-        assert np.array_equal(_rows(L.xe, e, n, dt), ref["xe"][e]), f"xe[{e}] not exact"
+        if variant != "gather":  # the fused forward never writes xe
+            assert np.array_equal(_rows(L.xe, e, n, dt), ref["xe"][e]), f"xe[{e}] not exact"
         for key, buf in (("A", L.a), ("Gd", L.a_grad), ("ye", L.ye), ("dye", L.dye),
                          ("dH", L.dh), ("dxe", L.dxe)):
             assert_rows_close(f"{key}", _rows(buf, e, n, dt), ref[key][e], tol, rep)

@@ -3,20 +3,27 @@
 // Pipeline (all on the caller's stream, no host synchronisation):
 //   1. router        logits (bf16: matrix-core product, f32 accumulation;
 //                    f32: double-accumulated in increasing i, rounded once),
-//                    noisy softmax, top-k, 26-bit priority key
-//   2. bin_scan      per group: key range -> 4096 bins spanning it, histogram
-//                    in LDS, exclusive scan -> bin starts; clears the counters
-//   3. bin_scatter   tokens into their bins (atomic fill; order inside a bin
-//                    is irrelevant, ranks are computed exactly next)
+//                    noisy softmax, top-k, 26-bit priority key; each block
+//                    also records its keys' range
+//   2. bin_hist      per 4096 tokens of a group: the group's key range (from
+//                    the router blocks' ranges) -> 4096 bins spanning it,
+//                    the block's bin histogram
+//   3. bin_scatter   the same blocks: bin starts and the block's offset in
+//                    each bin (sums of the group's histograms, scan over the
+//                    bins), then its tokens into their bins (LDS cursors;
+//                    order inside a bin is irrelevant, ranks are exact next)
 //   4. rank          rank of each token = tokens in lower bins + tokens of its
 //                    own bin that precede it by (key, index): a stable
 //                    priority sort without passes; also counts, per chunk of
 //                    256 order positions, the assignments to each expert
-//   5. chunk_scan    per (group, round, expert) exclusive scan over chunks;
-//                    round carries min(C, earlier demand); counts; row_base
+//   5. chunk_scan    one wave per (group, expert): over the rounds, the
+//                    carry min(C, earlier demand) and the exclusive scan over
+//                    chunks; counts; row_base
 //   6. slots         per chunk: rank of each assignment among same-expert
 //                    assignments (wave ballots + cross-wave prefix), slot =
 //                    carry + rank, kept while slot < C
+// A group of at most 8192 tokens may instead run steps 2-6 in one block
+// (local_route), all in LDS.
 // This file must be compiled with -ffp-contract=off: the gate's float
 // arithmetic is specified operation by operation.
 #include <type_traits>
@@ -42,21 +49,33 @@ struct BinMap {
 };
 constexpr int kSlotChunk = 256;              // order positions per slots block
 constexpr int kGateTokens = 32;              // most tokens per f64 router block
+constexpr int kMfmaTokens = 32;              // tokens per bf16 router block
+
+constexpr int kHistTokens = 4096;             // tokens per bin_hist / bin_scatter block
 
 struct RouteWs {
     uint32_t* keys;     // [N]
+    uint2* kpart;       // [G][nkp] (min, max) key of each router block
     BinMap* binmap;     // [G]
     int32_t* bin_start; // [G][kNumBins + 1]
-    int32_t* fill;      // [G][kNumBins]
+    int32_t* bhist;     // [G][nhb][kNumBins] bin counts of each hist block
     uint2* members;     // [N] (key, token) grouped by bin
-    int32_t* ccount;    // [G][nch][k][E]
-    int32_t* cbase;     // [G][nch][k][E]
-    int32_t* demand;    // [G][k][E]
+    int32_t* ccount;    // [G][nch][k][E] (a chunk's counters side by side: rank's atomics)
+    int32_t* cbase;     // [G][k][E][nch]
     int32_t* carry;     // [G][k][E]
     size_t bytes;
 };
 
 size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
+
+// Tokens per f32 router block: one thread per (token, expert).
+int f64_router_tokens(int E) { return kGateTokens < 256 / E ? kGateTokens : 256 / E; }
+
+// Router blocks per group (each records one key range).
+int router_blocks(const Dims& D) {
+    if (D.dtype == VMOE_BF16) return static_cast<int>(cdiv(D.Ng, kMfmaTokens));
+    return static_cast<int>(cdiv(D.Ng, f64_router_tokens(D.E)));
+}
 
 RouteWs route_ws_layout(const Dims& D, void* base) {
     char* p = static_cast<char*>(base);
@@ -67,15 +86,16 @@ RouteWs route_ws_layout(const Dims& D, void* base) {
         return q;
     };
     const size_t nch = cdiv(D.Ng, kSlotChunk);
+    const size_t nhb = cdiv(D.Ng, kHistTokens);
     RouteWs w;
     w.keys = reinterpret_cast<uint32_t*>(take(sizeof(uint32_t) * D.N));
+    w.kpart = reinterpret_cast<uint2*>(take(sizeof(uint2) * D.G * router_blocks(D)));
     w.binmap = reinterpret_cast<BinMap*>(take(sizeof(BinMap) * D.G));
     w.bin_start = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * D.G * (kNumBins + 1)));
-    w.fill = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * D.G * kNumBins));
+    w.bhist = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * D.G * nhb * kNumBins));
     w.members = reinterpret_cast<uint2*>(take(sizeof(uint2) * D.N));
     w.ccount = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * D.G * nch * D.k * D.E));
     w.cbase = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * D.G * nch * D.k * D.E));
-    w.demand = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * D.G * D.k * D.E));
     w.carry = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * D.G * D.k * D.E));
     w.bytes = off;
     return w;
@@ -121,7 +141,7 @@ __device__ __forceinline__ void load8(const float* p, float* v) {
 // Gate of token t from its logits in z[0..E) (LDS; overwritten by the noisy
 // logits): perturb, deterministic softmax, top-k by z (ties to the lower
 // expert), priority key of p[first choice].
-__device__ __forceinline__ void gate_token(float* z, size_t t, const float* __restrict__ bias,
+__device__ __forceinline__ uint32_t gate_token(float* z, size_t t, const float* __restrict__ bias,
                                            const float* __restrict__ noise,
                                            float* __restrict__ probs, int32_t* __restrict__ idx,
                                            uint32_t* __restrict__ keys, int E, int k) {
@@ -146,7 +166,22 @@ __device__ __forceinline__ void gate_token(float* z, size_t t, const float* __re
         idx[t * k + j] = best;
         if (j == 0) first = best;
     }
-    keys[t] = priority_key(__fdiv_rn(exp_spec(z[first] - m), s));
+    const uint32_t key = priority_key(__fdiv_rn(exp_spec(z[first] - m), s));
+    keys[t] = key;
+    return key;
+}
+
+// Wave 0 of a router block (lanes < ntok hold its tokens' keys): the block's
+// key range into kpart.
+__device__ __forceinline__ void key_range(uint32_t key, int ntok, uint2* __restrict__ kpart) {
+    const int lane = threadIdx.x & 63;
+    uint32_t lo = lane < ntok ? key : 0xFFFFFFFFu, hi = lane < ntok ? key : 0u;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        lo = min(lo, static_cast<uint32_t>(__shfl_xor(static_cast<int>(lo), o, 64)));
+        hi = max(hi, static_cast<uint32_t>(__shfl_xor(static_cast<int>(hi), o, 64)));
+    }
+    if (lane == 0) *kpart = make_uint2(lo, hi);
 }
 
 // The gate of a block's tokens, by the same operations in the same order as
@@ -174,7 +209,6 @@ __device__ __forceinline__ void row_to_regs(const float* row, float (&r)[EMAX]) 
 // probabilities — each element by gate_token's operations in its order.
 typedef __bf16 bf16x8_r __attribute__((ext_vector_type(8)));
 typedef float f32x16_r __attribute__((ext_vector_type(16)));
-constexpr int kMfmaTokens = 32;
 
 // Barrier for data exchanged through LDS only: waits for this wave's LDS
 // accesses (lgkmcnt(0)), not for its global stores.
@@ -189,9 +223,11 @@ template <bool WIDE>
 __global__ __launch_bounds__(256) void router_mfma_kernel(
     const uint16_t* __restrict__ x, const uint16_t* __restrict__ wr,
     const float* __restrict__ bias, const float* __restrict__ noise, float* __restrict__ logits,
-    float* __restrict__ probs, int32_t* __restrict__ idx, uint32_t* __restrict__ keys, int Ng,
-    int d, int E, int k, int logits_in) {
-    __shared__ float red[4][kMfmaTokens][kMaxExperts + 1];
+    float* __restrict__ probs, int32_t* __restrict__ idx, uint32_t* __restrict__ keys,
+    uint2* __restrict__ kpart, int Ng, int d, int E, int k, int logits_in) {
+    // partial products, then z and the exp terms: one row per token (padded)
+    constexpr int RW = WIDE ? kMaxExperts + 1 : 33;
+    __shared__ float red[4][kMfmaTokens][RW];
     const int g = blockIdx.y;
     const int t0 = blockIdx.x * kMfmaTokens;
     const int ntok = min(kMfmaTokens, Ng - t0);
@@ -213,8 +249,8 @@ __global__ __launch_bounds__(256) void router_mfma_kernel(
         f32x16_r acc0, acc1;
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc0[r] = acc1[r] = 0.0f;
-        // all of a wave's k-steps in flight at once for d up to 1024 (E <= 32)
-        constexpr int U = WIDE ? 8 : 16;
+        // eight k-steps in flight per round
+        constexpr int U = 8;
         for (int s = s0; s < s1; s += U) {
             uint4 av[U], bv0[U], bv1[U];
 #pragma unroll
@@ -310,6 +346,7 @@ __global__ __launch_bounds__(256) void router_mfma_kernel(
         if (sub < E) red[2][t][sub] = exp_spec(red[1][t][sub] - m_s[t]);
     lds_barrier();
     // 4. per token: s = sum of the terms in expert order; the priority key
+    uint32_t key = 0u;
     auto total = [&](auto emax) {
         constexpr int EM = decltype(emax)::value;
         float q[EM];
@@ -319,7 +356,8 @@ __global__ __launch_bounds__(256) void router_mfma_kernel(
         for (int e = 0; e < EM; ++e)
             if (e < E) sum = sum + q[e];
         s_s[tid] = sum;
-        keys[tok0 + tid] = priority_key(__fdiv_rn(red[2][tid][first_s[tid]], sum));
+        key = priority_key(__fdiv_rn(red[2][tid][first_s[tid]], sum));
+        keys[tok0 + tid] = key;
     };
     if (tid < ntok) {
         if (E <= 8) total(std::integral_constant<int, 8>{});
@@ -327,6 +365,7 @@ __global__ __launch_bounds__(256) void router_mfma_kernel(
         else if (E <= 32 || !WIDE) total(std::integral_constant<int, 32>{});
         else total(std::integral_constant<int, 64>{});
     }
+    if (wave == 0) key_range(key, ntok, kpart + static_cast<size_t>(g) * gridDim.x + blockIdx.x);
     lds_barrier();
     // 5. the probabilities p = q / s (IEEE division)
     for (int t = tg; t < ntok; t += tp)
@@ -347,8 +386,8 @@ constexpr int kGateVecs = 32;  // 16-byte vectors per staged row and round
 __global__ __launch_bounds__(256) void router_f64_kernel(
     const float* __restrict__ x, const float* __restrict__ wr, const float* __restrict__ bias,
     const float* __restrict__ noise, float* __restrict__ logits, float* __restrict__ probs,
-    int32_t* __restrict__ idx, uint32_t* __restrict__ keys, int Ng, int d, int E, int k,
-    int logits_in, int tpb) {
+    int32_t* __restrict__ idx, uint32_t* __restrict__ keys, uint2* __restrict__ kpart, int Ng,
+    int d, int E, int k, int logits_in, int tpb) {
     constexpr int VE = 4;                          // f32 per 16-byte vector
     constexpr int VPR = kGateVecs;                 // vectors per staged row
     constexpr int GC = VPR * VE;                   // columns per round
@@ -424,7 +463,10 @@ __global__ __launch_bounds__(256) void router_f64_kernel(
         lg_store[tt * ld + e] = logits[(tok0 + tt) * E + e];
     }
     __syncthreads();
-    if (tid < ntok) gate_token(lg_store + tid * ld, tok0 + tid, bias, noise, probs, idx, keys, E, k);
+    uint32_t key = 0u;
+    if (tid < ntok)
+        key = gate_token(lg_store + tid * ld, tok0 + tid, bias, noise, probs, idx, keys, E, k);
+    if (tid < 64) key_range(key, ntok, kpart + static_cast<size_t>(g) * gridDim.x + blockIdx.x);
 }
 
 // Exclusive scan of one value per thread over a 1024-thread block.
@@ -455,32 +497,17 @@ __device__ int block_exclusive_scan_1024(int v, int* total) {
     return base + inc - v;
 }
 
-// One block per group: key range -> bin map, bin histogram + scan; clears
-// fill and chunk counters.
-__global__ __launch_bounds__(1024) void bin_scan_kernel(const uint32_t* __restrict__ keys,
-                                                        BinMap* __restrict__ binmap,
-                                                        int32_t* __restrict__ bin_start,
-                                                        int32_t* __restrict__ fill,
-                                                        int32_t* __restrict__ ccount, int Ng,
-                                                        int cc_per_group) {
-    __shared__ int hist[kNumBins];
+// The key range of group g from its router blocks' ranges -> the bin map
+// (every block that needs it computes the same one from the same ranges).
+__device__ BinMap group_binmap(const uint2* __restrict__ kpart, int nkp) {
     __shared__ uint32_t wmin[16], wmax[16];
     __shared__ BinMap map;
-    const int g = blockIdx.x;
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    for (int b = threadIdx.x; b < kNumBins; b += 1024) hist[b] = 0;
-    const uint32_t* kg = keys + static_cast<size_t>(g) * Ng;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
     uint32_t lo = 0xFFFFFFFFu, hi = 0u;
-    // eight keys per thread in flight at a time (clamped indices, repeats are harmless)
-    for (int b0 = 0; b0 < Ng; b0 += 8 * 1024) {
-        uint32_t v[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) v[u] = kg[min(b0 + u * 1024 + static_cast<int>(threadIdx.x), Ng - 1)];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            lo = min(lo, v[u]);
-            hi = max(hi, v[u]);
-        }
+    for (int i = threadIdx.x; i < nkp; i += blockDim.x) {
+        const uint2 v = kpart[i];
+        lo = min(lo, v.x);
+        hi = max(hi, v.y);
     }
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) {
@@ -494,116 +521,198 @@ __global__ __launch_bounds__(1024) void bin_scan_kernel(const uint32_t* __restri
     __syncthreads();
     if (threadIdx.x == 0) {
         uint32_t a = wmin[0], z = wmax[0];
-        for (int q = 1; q < 16; ++q) {
+        for (int q = 1; q < nw; ++q) {
             a = min(a, wmin[q]);
             z = max(z, wmax[q]);
         }
-        if (Ng == 0) a = z = 0u;
         int sh = 0;
         while (((z - a) >> sh) >= static_cast<uint32_t>(kNumBins)) ++sh;
         map = BinMap{a, sh};
-        binmap[g] = map;
     }
     __syncthreads();
-    const BinMap bm = map;
-    for (int b0 = 0; b0 < Ng; b0 += 8 * 1024) {
-        uint32_t v[8];
+    return map;
+}
+
+constexpr int kHistPer = kHistTokens / 1024;  // tokens per thread of a hist block
+
+// This block's kHistTokens tokens of group g (past Ng: not used).
+__device__ __forceinline__ void hist_keys(const uint32_t* __restrict__ keys, int g, int Ng,
+                                          uint32_t (&kv)[kHistPer]) {
+    const size_t t0 = static_cast<size_t>(g) * Ng;
 #pragma unroll
-        for (int u = 0; u < 8; ++u) v[u] = kg[min(b0 + u * 1024 + static_cast<int>(threadIdx.x), Ng - 1)];
-#pragma unroll
-        for (int u = 0; u < 8; ++u)
-            if (b0 + u * 1024 + static_cast<int>(threadIdx.x) < Ng) atomicAdd(&hist[bm(v[u])], 1);
+    for (int u = 0; u < kHistPer; ++u) {
+        const int t = blockIdx.x * kHistTokens + u * 1024 + static_cast<int>(threadIdx.x);
+        kv[u] = t < Ng ? keys[t0 + t] : 0u;
     }
-    __syncthreads();
-    constexpr int per = kNumBins / 1024;
-    int local[per];
-    int sum = 0;
+}
+
+// Block (j, g): the bin histogram of tokens [j kHistTokens, (j + 1) kHistTokens)
+// of group g, into bhist[g][j].
+__global__ __launch_bounds__(1024) void bin_hist_kernel(const uint32_t* __restrict__ keys,
+                                                        const uint2* __restrict__ kpart, int nkp,
+                                                        BinMap* __restrict__ binmap,
+                                                        int32_t* __restrict__ bhist,
+                                                        int32_t* __restrict__ ccount,
+                                                        int cc_per_group, int Ng) {
+    __shared__ int hist[kNumBins];
+    const int g = blockIdx.y, tid = threadIdx.x;
+    uint32_t kv[kHistPer];
+    hist_keys(keys, g, Ng, kv);
+    for (int b = tid; b < kNumBins; b += 1024) hist[b] = 0;
+    const BinMap bm = group_binmap(kpart + static_cast<size_t>(g) * nkp, nkp);
+    if (blockIdx.x == 0 && tid == 0) binmap[g] = bm;
 #pragma unroll
-    for (int q = 0; q < per; ++q) {
-        local[q] = hist[threadIdx.x * per + q];
-        sum += local[q];
+    for (int u = 0; u < kHistPer; ++u)
+        if (static_cast<int>(blockIdx.x) * kHistTokens + u * 1024 + tid < Ng)
+            atomicAdd(&hist[bm(kv[u])], 1);
+    __syncthreads();
+    int32_t* out = bhist + (static_cast<size_t>(g) * gridDim.x + blockIdx.x) * kNumBins;
+    for (int b = tid; b < kNumBins; b += 1024) out[b] = hist[b];
+    // the group's chunk counters, which the rank step adds into, cleared
+    int32_t* cg = ccount + static_cast<size_t>(g) * cc_per_group;
+    for (int q = blockIdx.x * 1024 + tid; q < cc_per_group; q += gridDim.x * 1024) cg[q] = 0;
+}
+
+// Block (j, g): the tokens bin_hist counted into their bins. Bin b starts
+// after the tokens of the bins below it, and this block's tokens of bin b
+// after those of hist blocks j' < j (both from the hist rows of the group:
+// per thread four consecutive bins, summed over the blocks, then a block scan
+// over the bins); cursors in LDS from there. Block 0 stores the bin starts.
+__global__ __launch_bounds__(1024) void bin_scatter_kernel(const uint32_t* __restrict__ keys,
+                                                           const BinMap* __restrict__ binmap,
+                                                           const int32_t* __restrict__ bhist,
+                                                           int32_t* __restrict__ bin_start,
+                                                           uint2* __restrict__ members, int Ng) {
+    static_assert(kNumBins == 4 * 1024, "four consecutive bins per thread");
+    __shared__ int cur[kNumBins];
+    const int g = blockIdx.y, j = blockIdx.x, nhb = gridDim.x, tid = threadIdx.x;
+    uint32_t kv[kHistPer];
+    hist_keys(keys, g, Ng, kv);
+    const int4* hb = reinterpret_cast<const int4*>(bhist + static_cast<size_t>(g) * nhb * kNumBins) + tid;
+    int4 before = make_int4(0, 0, 0, 0), tot = make_int4(0, 0, 0, 0);
+#pragma unroll 8
+    for (int i = 0; i < nhb; ++i) {
+        const int4 v = hb[static_cast<size_t>(i) * (kNumBins / 4)];
+        if (i < j) {
+            before.x += v.x;
+            before.y += v.y;
+            before.z += v.z;
+            before.w += v.w;
+        }
+        tot.x += v.x;
+        tot.y += v.y;
+        tot.z += v.z;
+        tot.w += v.w;
     }
     int total;
-    int run = block_exclusive_scan_1024(sum, &total);
-    int32_t* bs = bin_start + static_cast<size_t>(g) * (kNumBins + 1);
-#pragma unroll
-    for (int q = 0; q < per; ++q) {
-        bs[threadIdx.x * per + q] = run;
-        run += local[q];
+    const int run = block_exclusive_scan_1024(tot.x + tot.y + tot.z + tot.w, &total);
+    const int s0 = run, s1 = s0 + tot.x, s2 = s1 + tot.y, s3 = s2 + tot.z;
+    if (j == 0) {
+        int32_t* bs = bin_start + static_cast<size_t>(g) * (kNumBins + 1);
+        bs[4 * tid] = s0;
+        bs[4 * tid + 1] = s1;
+        bs[4 * tid + 2] = s2;
+        bs[4 * tid + 3] = s3;
+        if (tid == 0) bs[kNumBins] = total;
     }
-    if (threadIdx.x == 0) bs[kNumBins] = total;
-    int32_t* fg = fill + static_cast<size_t>(g) * kNumBins;
-    for (int b = threadIdx.x; b < kNumBins; b += 1024) fg[b] = 0;
-    int32_t* cg = ccount + static_cast<size_t>(g) * cc_per_group;
-    for (int q = threadIdx.x; q < cc_per_group; q += 1024) cg[q] = 0;
-}
-
-__global__ __launch_bounds__(256) void bin_scatter_kernel(const uint32_t* __restrict__ keys,
-                                                          const BinMap* __restrict__ binmap,
-                                                          const int32_t* __restrict__ bin_start,
-                                                          int32_t* __restrict__ fill,
-                                                          uint2* __restrict__ members, int N,
-                                                          int Ng) {
-    const int t = blockIdx.x * 256 + threadIdx.x;
-    if (t >= N) return;
-    const int g = t / Ng;
-    const uint32_t key = keys[t];
-    const int b = binmap[g](key);
-    const int pos = bin_start[static_cast<size_t>(g) * (kNumBins + 1) + b] +
-                    atomicAdd(&fill[static_cast<size_t>(g) * kNumBins + b], 1);
-    members[static_cast<size_t>(g) * Ng + pos] = make_uint2(key, static_cast<uint32_t>(t));
-}
-
-__global__ __launch_bounds__(256) void rank_kernel(
-    const uint32_t* __restrict__ keys, const BinMap* __restrict__ binmap,
-    const int32_t* __restrict__ bin_start,
-    const uint2* __restrict__ members, const int32_t* __restrict__ idx,
-    int32_t* __restrict__ order, int32_t* __restrict__ ccount, int N, int Ng, int E, int k,
-    int nch) {
-    const int t = blockIdx.x * 256 + threadIdx.x;
-    if (t >= N) return;
-    const int g = t / Ng;
-    const uint32_t key = keys[t];
-    const int32_t* bs = bin_start + static_cast<size_t>(g) * (kNumBins + 1);
-    const int b = binmap[g](key);
-    const int lo = bs[b], hi = bs[b + 1];
-    const uint2* mg = members + static_cast<size_t>(g) * Ng;
-    // members carry their keys: four independent loads per round
-    int rank = lo;
-    for (int p = lo; p < hi; p += 4) {
-        uint2 m[4];
+    cur[4 * tid] = s0 + before.x;
+    cur[4 * tid + 1] = s1 + before.y;
+    cur[4 * tid + 2] = s2 + before.z;
+    cur[4 * tid + 3] = s3 + before.w;
+    const BinMap bm = binmap[g];
+    __syncthreads();
+    const size_t t0 = static_cast<size_t>(g) * Ng;
 #pragma unroll
-        for (int u = 0; u < 4; ++u) m[u] = mg[min(p + u, hi - 1)];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const uint32_t k2 = m[u].x, t2 = m[u].y;
-            rank += (p + u < hi && (k2 < key || (k2 == key && t2 < static_cast<uint32_t>(t)))) ? 1 : 0;
+    for (int u = 0; u < kHistPer; ++u) {
+        const int t = j * kHistTokens + u * 1024 + tid;
+        if (t < Ng) {
+            const int pos = atomicAdd(&cur[bm(kv[u])], 1);
+            members[t0 + pos] = make_uint2(kv[u], static_cast<uint32_t>(t0 + t));
         }
     }
-    order[static_cast<size_t>(g) * Ng + rank] = t;
-    const int c = rank / kSlotChunk;
-    int32_t* cc = ccount + (static_cast<size_t>(g) * nch + c) * k * E;
-    for (int r = 0; r < k; ++r) atomicAdd(&cc[r * E + idx[static_cast<size_t>(t) * k + r]], 1);
 }
 
-// Single block: chunk offsets, round carries, counts and row bases.
-__global__ __launch_bounds__(1024) void chunk_scan_kernel(
-    const int32_t* __restrict__ ccount, int32_t* __restrict__ cbase, int32_t* __restrict__ demand,
-    int32_t* __restrict__ carry, int32_t* __restrict__ counts, int32_t* __restrict__ row_base,
-    int G, int E, int k, int C, int nch) {
-    const int kE = k * E;
+// Block (i, g): bin members [256 i, 256 i + 256) of group g, one per thread.
+// A member's rank is its bin's start plus the members of its bin that precede
+// it by (key, token). The bins of a block's members span a contiguous range
+// of members, staged in LDS (up to kRankStage of them from the span's start);
+// a member whose bin reaches past the stage (a bin of thousands) reads the
+// rest of its bin from global memory.
+constexpr int kRankStage = 4096;
+
+__global__ __launch_bounds__(256) void rank_kernel(
+    const BinMap* __restrict__ binmap, const int32_t* __restrict__ bin_start,
+    const uint2* __restrict__ members, const int32_t* __restrict__ idx,
+    int32_t* __restrict__ order, int32_t* __restrict__ ccount, int Ng, int E, int k, int nch) {
+    __shared__ uint2 stage[kRankStage];
+    __shared__ int span[2];
+    const int g = blockIdx.y, tid = threadIdx.x;
+    const int p = blockIdx.x * 256 + tid;
+    const int last = min(256, Ng - static_cast<int>(blockIdx.x) * 256) - 1;
+    const uint2* mg = members + static_cast<size_t>(g) * Ng;
+    const int32_t* bs = bin_start + static_cast<size_t>(g) * (kNumBins + 1);
+    const BinMap bm = binmap[g];
+    const uint2 m = mg[min(p, Ng - 1)];
+    const int b = bm(m.x);
+    const int lo = bs[b], hi = bs[b + 1];
+    if (tid == 0) span[0] = lo;
+    if (tid == last) span[1] = hi;
+    __syncthreads();
+    const int s0 = span[0], s1 = min(span[1], s0 + kRankStage);
+    for (int q = s0 + tid; q < s1; q += 256) stage[q - s0] = mg[q];
+    __syncthreads();
+    if (tid > last) return;
+    const uint32_t key = m.x, t = m.y;
+    auto precedes = [&](uint2 o) { return o.x < key || (o.x == key && o.y < t); };
+    int before = 0;
+    const int hs = max(lo, min(hi, s1));  // [lo, hs) staged, [hs, hi) not
+    for (int q = lo; q < hs; q += 4) {
+        uint2 o[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) o[u] = stage[min(q + u, hs - 1) - s0];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) before += (q + u < hs && precedes(o[u])) ? 1 : 0;
+    }
+    for (int q = hs; q < hi; q += 4) {
+        uint2 o[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) o[u] = mg[min(q + u, hi - 1)];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) before += (q + u < hi && precedes(o[u])) ? 1 : 0;
+    }
+    const int rank = lo + before;
+    order[static_cast<size_t>(g) * Ng + rank] = static_cast<int32_t>(t);
+    const int c = rank / kSlotChunk;
+    for (int r = 0; r < k; ++r)
+        atomicAdd(&ccount[((static_cast<size_t>(g) * nch + c) * k + r) * E +
+                          idx[static_cast<size_t>(t) * k + r]],
+                  1);
+}
+
+// One wave per (group, expert): over the rounds in order, the carry
+// min(C, demand of the earlier rounds) and the exclusive scan of the round's
+// per-chunk counts (64 chunks per step, four steps' loads together); then
+// counts = min(C, total demand) and, for one group, row_base = 0.
+__global__ __launch_bounds__(256) void chunk_scan_kernel(
+    const int32_t* __restrict__ ccount, int32_t* __restrict__ cbase, int32_t* __restrict__ carry,
+    int32_t* __restrict__ counts, int32_t* __restrict__ row_base, int G, int E, int k, int C,
+    int nch) {
     const int lane = threadIdx.x & 63;
-    // one wave per (group, round, expert): exclusive scan over the chunks, 64 at
-    // a time, with the counts of up to four 64-chunk spans requested together
-    for (int q = threadIdx.x >> 6; q < G * kE; q += 16) {
-        const int g = q / kE, re = q % kE;
+    const int q = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (q >= G * E) return;
+    const int g = q / E, e = q % E;
+    int acc = 0;
+    for (int r = 0; r < k; ++r) {
+        if (lane == 0) carry[(g * k + r) * E + e] = min(C, acc);
+        const size_t row = ((static_cast<size_t>(g) * k + r) * E + e) * nch;
+        const int32_t* cc = ccount + static_cast<size_t>(g) * nch * k * E + r * E + e;
         int run = 0;
         for (int c0 = 0; c0 < nch; c0 += 4 * 64) {
             int v[4];
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
                 const int c = c0 + u * 64 + lane;
-                v[u] = c < nch ? ccount[(static_cast<size_t>(g) * nch + c) * kE + re] : 0;
+                v[u] = c < nch ? cc[static_cast<size_t>(c) * k * E] : 0;
             }
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
@@ -614,29 +723,15 @@ __global__ __launch_bounds__(1024) void chunk_scan_kernel(
                     const int w = __shfl_up(inc, o, 64);
                     if (lane >= o) inc += w;
                 }
-                if (c < nch) cbase[(static_cast<size_t>(g) * nch + c) * kE + re] = run + inc - v[u];
+                if (c < nch) cbase[row + c] = run + inc - v[u];
                 run += __shfl(inc, 63, 64);
             }
         }
-        if (lane == 0) demand[q] = run;
+        acc += run;
     }
-    __syncthreads();
-    for (int q = threadIdx.x; q < G * E; q += 1024) {
-        const int g = q / E, e = q % E;
-        int acc = 0;
-        for (int r = 0; r < k; ++r) {
-            carry[(g * k + r) * E + e] = min(C, acc);
-            acc += demand[(g * k + r) * E + e];
-        }
-        counts[q] = min(C, acc);
-    }
-    __syncthreads();
-    for (int e = threadIdx.x; e < E; e += 1024) {
-        int base = 0;
-        for (int g = 0; g < G; ++g) {
-            row_base[g * E + e] = base;
-            base += counts[g * E + e];
-        }
+    if (lane == 0) {
+        counts[g * E + e] = min(C, acc);
+        if (G == 1) row_base[e] = 0;
     }
 }
 
@@ -667,7 +762,7 @@ __global__ __launch_bounds__(kSlotChunk) void slots_kernel(
         if (rank_w == 0) wcnt[w][e] = __popcll(same);
         __syncthreads();
         if (active) {
-            int rank = cbase[(static_cast<size_t>(g) * nch + c) * k * E + r * E + e] + rank_w;
+            int rank = cbase[((static_cast<size_t>(g) * k + r) * E + e) * nch + c] + rank_w;
             for (int w2 = 0; w2 < w; ++w2) rank += wcnt[w2][e];
             const int s = carry[(g * k + r) * E + e] + rank;
             const bool kept = s < C;
@@ -1032,28 +1127,35 @@ __global__ __launch_bounds__(1024) void row_base_kernel(const int32_t* __restric
 
 size_t route_workspace_bytes(const Dims& D) { return route_ws_layout(D, nullptr).bytes; }
 
+// Steps 2-7 in one block per group (local_route) for groups that fit its LDS.
+bool local_route_fits(const Dims& D) {
+    return D.Ng <= kLocalTokens && static_cast<long long>(D.Ng) * D.k <= kLocalAssign;
+}
+
 vmoe_status route_launch(const Dims& D, const void* x, const void* wr, const float* bias,
                          const float* noise, int flags, float* logits, float* probs,
                          int32_t* idx, int32_t* slot, float* gate, int32_t* order, int32_t* counts,
                          int32_t* row_base, void* ws_base, hipStream_t st) {
     RouteWs ws = route_ws_layout(D, ws_base);
     const int nch = static_cast<int>(cdiv(D.Ng, kSlotChunk));
+    const int nkp = router_blocks(D);
     const int logits_in = (flags & VMOE_ROUTE_LOGITS_IN) ? 1 : 0;
     if (D.N > 0) {
         if (D.dtype == VMOE_BF16) {
-            dim3 grid(cdiv(D.Ng, kMfmaTokens), D.G);
+            dim3 grid(nkp, D.G);
             auto kern = D.E > 32 ? router_mfma_kernel<true> : router_mfma_kernel<false>;
             kern<<<grid, 256, 0, st>>>(static_cast<const uint16_t*>(x),
                                        static_cast<const uint16_t*>(wr), bias, noise, logits,
-                                       probs, idx, ws.keys, D.Ng, D.d, D.E, D.k, logits_in);
+                                       probs, idx, ws.keys, ws.kpart, D.Ng, D.d, D.E, D.k,
+                                       logits_in);
         } else {
-            const int tpb = min(kGateTokens, 256 / D.E);
-            dim3 grid(cdiv(D.Ng, tpb), D.G);
+            dim3 grid(nkp, D.G);
             router_f64_kernel<<<grid, 256, 0, st>>>(
                 static_cast<const float*>(x), static_cast<const float*>(wr), bias, noise, logits,
-                probs, idx, ws.keys, D.Ng, D.d, D.E, D.k, logits_in, tpb);
+                probs, idx, ws.keys, ws.kpart, D.Ng, D.d, D.E, D.k, logits_in,
+                f64_router_tokens(D.E));
         }
-        if (D.Ng <= kLocalTokens && static_cast<long long>(D.Ng) * D.k <= kLocalAssign) {
+        if (local_route_fits(D)) {
             auto kern = D.E <= 8 ? local_route_kernel<4>
                       : D.E <= 16 ? local_route_kernel<8> : local_route_kernel<0>;
             kern<<<D.G, 1024, 0, st>>>(ws.keys, idx, probs, order, slot, gate, counts, row_base,
@@ -1061,16 +1163,18 @@ vmoe_status route_launch(const Dims& D, const void* x, const void* wr, const flo
             if (D.G > 1) row_base_kernel<<<1, 1024, 0, st>>>(counts, row_base, D.G, D.E);
             return launch_status();
         }
-        bin_scan_kernel<<<D.G, 1024, 0, st>>>(ws.keys, ws.binmap, ws.bin_start, ws.fill,
-                                               ws.ccount, D.Ng, nch * D.k * D.E);
-        bin_scatter_kernel<<<cdiv(D.N, 256), 256, 0, st>>>(ws.keys, ws.binmap, ws.bin_start,
-                                                            ws.fill, ws.members, D.N, D.Ng);
-        rank_kernel<<<cdiv(D.N, 256), 256, 0, st>>>(ws.keys, ws.binmap, ws.bin_start, ws.members,
-                                                     idx, order, ws.ccount, D.N, D.Ng, D.E, D.k,
-                                                     nch);
+        const int nhb = static_cast<int>(cdiv(D.Ng, kHistTokens));
+        bin_hist_kernel<<<dim3(nhb, D.G), 1024, 0, st>>>(ws.keys, ws.kpart, nkp, ws.binmap,
+                                                          ws.bhist, ws.ccount, nch * D.k * D.E,
+                                                          D.Ng);
+        bin_scatter_kernel<<<dim3(nhb, D.G), 1024, 0, st>>>(ws.keys, ws.binmap, ws.bhist,
+                                                             ws.bin_start, ws.members, D.Ng);
+        rank_kernel<<<dim3(cdiv(D.Ng, 256), D.G), 256, 0, st>>>(
+            ws.binmap, ws.bin_start, ws.members, idx, order, ws.ccount, D.Ng, D.E, D.k, nch);
     }
-    chunk_scan_kernel<<<1, 1024, 0, st>>>(ws.ccount, ws.cbase, ws.demand, ws.carry, counts,
-                                          row_base, D.G, D.E, D.k, D.C, nch);
+    chunk_scan_kernel<<<cdiv(D.G * D.E, 4), 256, 0, st>>>(ws.ccount, ws.cbase, ws.carry, counts,
+                                                         row_base, D.G, D.E, D.k, D.C, nch);
+    if (D.G > 1) row_base_kernel<<<1, 1024, 0, st>>>(counts, row_base, D.G, D.E);
     if (D.N > 0)
         slots_kernel<<<dim3(nch, D.G), kSlotChunk, 0, st>>>(order, idx, probs, ws.cbase, ws.carry,
                                                             slot, gate, D.Ng, D.E, D.k, D.C, nch);

@@ -1,7 +1,7 @@
 """Benchmark: one V-MoE layer forward + backward on one MI355X.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
-                    [--flush-mall]
+                    [--flush-mall] [--no-diagnostics] [--copy-probe]
 
 A step is one pass of the whole layer: routing (router product, noisy top-k,
 batch-prioritized capacity), dispatch, expert MLP forward, combine, and the
@@ -69,7 +69,8 @@ def algorithmic_cost(cfg, A: int, n_noise: bool, n_bias: bool):
     return c
 
 
-TRAFFIC_PROFILE = {"vitb16_bf16": "profiles/vitb16_bf16_hbm_traffic.txt"}
+TRAFFIC_PROFILE = {"vitb16_bf16": "profiles/vitb16_bf16_hbm_traffic.txt",
+                   "vitl16_384_bf16": "profiles/vitl16_384_bf16_hbm_traffic.txt"}
 
 
 def source_digest(path: str) -> str:
@@ -215,6 +216,10 @@ def main():
     ap.add_argument("--flush-mall", action="store_true",
                     help="after the timed region, time every call again with a 512 MiB "
                          "buffer written before each step (the 256 MB MALL holds no inputs)")
+    ap.add_argument("--no-diagnostics", action="store_true",
+                    help="skip the passes after the timed region that run other calls (the "
+                         "quota-scheduled and dispatch-fused steps, the balance losses), so a "
+                         "profiler run sees the step's kernels only")
     ap.add_argument("--copy-probe", action="store_true",
                     help="before warm-up, copy one 256 MiB buffer (a plain copy kernel of known "
                          "size, to calibrate the HBM byte counters of a profiler run)")
@@ -328,7 +333,7 @@ def main():
     # the same step with the expert MLP calls through the fill-clamp-refill
     # tile scheduler, each call bracketed by events (diagnostic)
     quota = None
-    if cfg.dtype == "bf16":
+    if cfg.dtype == "bf16" and not args.no_diagnostics:
         qcalls = [("ffn_fwd_quota" if n == "ffn_fwd" else "ffn_bwd_quota" if n == "ffn_bwd"
                    else n) for n in CALLS]
         evq = [[torch.cuda.Event(enable_timing=True) for _ in range(len(CALLS) + 1)]
@@ -352,7 +357,7 @@ def main():
     # the step with the dispatch fused into the expert MLP's loads: the
     # dispatch call is gone, the forward and backward read x through row_token
     gathered = None
-    if cfg.dtype == "bf16" and L.C * cfg.n_groups <= 6144:
+    if cfg.dtype == "bf16" and L.C * cfg.n_groups <= 6144 and not args.no_diagnostics:
         gcalls = ["route", "dispatch_ffn_fwd", "combine_fwd", "combine_bwd", "ffn_bwd_gather",
                   "dispatch_route_bwd"]
         evg = [[torch.cuda.Event(enable_timing=True) for _ in range(len(gcalls) + 1)]
@@ -390,7 +395,7 @@ def main():
         flushed = {name: float(np.mean([evf[i][c].elapsed_time(evf[i][c + 1])
                                         for i in range(K)])) for c, name in enumerate(CALLS)}
 
-    balance = balance_losses(L, V, stream, K)
+    balance = None if args.no_diagnostics else balance_losses(L, V, stream, K)
 
     counts = L.counts.cpu().numpy()
     A = int(counts.sum())

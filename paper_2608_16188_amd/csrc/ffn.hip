@@ -823,11 +823,12 @@ void gemm_bf16_kernel(GemmBatch batch) {
         const int end = qp.first[lane] + qp.units[lane];
         const int e_b = __popcll(__ballot(end <= b));  // ends never decrease
         if (e_b >= batch.p[0].E) return;              // past every quota
-        qe = e_b;
-        qn = qp.units[e_b];
-        qu = b - qp.first[e_b];
-        qt = qp.tiles[e_b];
-        qne = qp.ne[e_b];
+        // (uniform values read from LDS: kept in scalar registers)
+        qe = __builtin_amdgcn_readfirstlane(e_b);
+        qn = __builtin_amdgcn_readfirstlane(qp.units[e_b]);
+        qu = __builtin_amdgcn_readfirstlane(b - qp.first[e_b]);
+        qt = __builtin_amdgcn_readfirstlane(qp.tiles[e_b]);
+        qne = __builtin_amdgcn_readfirstlane(qp.ne[e_b]);
     }
     for (int it = 0;; ++it) {
     int prob = 0, e, r, ne, tiles_m;

@@ -157,8 +157,13 @@ vmoe_status vmoe_route_noalloc(const vmoe_shape* shape, const void* x, const voi
                                float* gate, int32_t* order, int32_t* counts, int32_t* row_base,
                                void* stream);
 
-/* Dispatch (permutation) of kept tokens into per-expert buffers:
- * xe[row(t, j), :] = x[t, :] for every kept (t, j). x [N, d], xe [E, G*C, d]. */
+/* Dispatch of kept tokens into per-expert buffers (sparse routing sends each
+ * token to its chosen experts, paper Sec. 2.1; a token past an expert's
+ * capacity is dropped, Sec. 2.3): xe[row(t, j), :] = x[t, :] for every kept
+ * (t, j), row(t, j) = e * G*C + row_base[g, e] + slot[t, j] with
+ * e = expert_idx[t, j]. x [N, d], xe [E, G*C, d] (dtype, caller-owned; rows
+ * at or past an expert's n_e are not written). Device pointers, each non-null
+ * and 16-byte aligned; VMOE_ERR_INVALID_ARG otherwise or on a bad shape. */
 vmoe_status vmoe_dispatch(const vmoe_shape* shape, const void* x, const int32_t* expert_idx,
                           const int32_t* slot, const int32_t* row_base, void* xe, void* stream);
 
@@ -176,15 +181,22 @@ vmoe_status vmoe_expert_ffn_fwd(const vmoe_shape* shape, const void* xe, const i
                                 const void* w1, const void* b1, const void* w2, const void* b2,
                                 void* act, void* act_grad, void* ye, void* stream);
 
-/* Gate-weighted combine: y[t] = sum over kept j (in j order, f32 accumulation)
- * of gate[t,j] * ye[row(t,j)]; 0 for a token with no kept assignment. y [N, d]. */
+/* Gate-weighted combine of the experts' outputs (the sparse layer's output
+ * is the gate-weighted sum over the chosen experts, paper Sec. 2.1; dropped
+ * assignments contribute nothing, Sec. 2.3): y[t] = sum over kept j (in j
+ * order, f32 accumulation) of gate[t,j] * ye[row(t,j)]; 0 for a token with no
+ * kept assignment. ye [E, G*C, d], gate [N, k] f32, y [N, d] (dtype,
+ * overwritten). Device pointers; VMOE_ERR_INVALID_ARG on a bad shape. */
 vmoe_status vmoe_combine_fwd(const vmoe_shape* shape, const void* ye, const int32_t* expert_idx,
                              const int32_t* slot, const int32_t* row_base, const float* gate,
                              void* y, void* stream);
 
-/* Backward of the combine: dye[row(t,j)] = gate[t,j] * dy[t];
+/* Backward of the combine (back-propagation through the layer, paper
+ * Sec. 3.1-3.2): dye[row(t,j)] = gate[t,j] * dy[t];
  * dgate[t,j] = <dy[t], ye[row(t,j)]> (f32) for kept j, 0 for dropped j.
- * dy [N, d], dye [E, G*C, d], dgate [N, k] f32. */
+ * dy [N, d], dye [E, G*C, d] (dtype; rows of kept assignments written),
+ * dgate [N, k] f32 (overwritten). Device pointers; VMOE_ERR_INVALID_ARG on a
+ * bad shape. */
 vmoe_status vmoe_combine_bwd(const vmoe_shape* shape, const void* dy, const void* ye,
                              const int32_t* expert_idx, const int32_t* slot,
                              const int32_t* row_base, const float* gate, void* dye, float* dgate,
@@ -260,14 +272,19 @@ vmoe_status vmoe_fill_clamp_refill_device(int32_t n, const int32_t* min_units,
                                           const int32_t* sat_units, const double* coef,
                                           int32_t budget, int32_t* alloc_units, void* stream);
 
-/* Backward of the dispatch: dx[t] = sum over kept j of dxe[row(t,j)]
- * (f32, overwritten; 0 for a token with no kept assignment). dx [N, d] f32. */
+/* Backward of the dispatch (paper Sec. 2.1 routing, back-propagated as in
+ * Sec. 3.1-3.2): dx[t] = sum over kept j of dxe[row(t,j)] (j ascending, f32,
+ * overwritten; 0 for a token with no kept assignment). dxe [E, G*C, d]
+ * (dtype), dx [N, d] f32. Device pointers; VMOE_ERR_INVALID_ARG on a bad
+ * shape. */
 vmoe_status vmoe_dispatch_bwd(const vmoe_shape* shape, const void* dxe,
                               const int32_t* expert_idx, const int32_t* slot,
                               const int32_t* row_base, float* dx, void* stream);
 
-/* Backward through the gate into the router (the top-k choice, capacity and
- * priority order are piecewise constant and pass no gradient):
+/* Backward through the gate into the router (the router is part of the
+ * adapted layer, paper Sec. 3.1-3.2; the top-k choice of Sec. 2.1 and the
+ * capacity and priority order of Sec. 2.3 are piecewise constant and pass
+ * no gradient):
  *   dp[t,e]  = sum of dgate[t,j] over kept j with expert_idx[t,j] = e
  *   dz[t,e]  = probs[t,e] * (dp[t,e] - sum_e' probs[t,e'] dp[t,e'])
  *   dx[t,:] += sum_e dz[t,e] w_router[g,e,:]                    (accumulates)

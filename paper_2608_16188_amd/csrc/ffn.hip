@@ -98,11 +98,12 @@ __device__ __forceinline__ int expert_rows(const int32_t* counts, int G, int E, 
     return n;
 }
 
-// Live tile w of a compact problem (see GemmBatch::compact): lane e of every
-// wave sums expert e's rows (at most `cap`, the rows of its buffer) and its tile count, an inclusive scan over the
-// lanes places the experts' tile ranges end to end, and the expert holding w
-// is the number of ranges that end at or before it. Returns false past the
-// last live tile. Uniform per wave (every wave of a block computes the same).
+// Live tile w of a compact problem: lane e of every wave sums expert e's rows
+// (at most `cap`, the rows of its buffer) and its tile count, an inclusive
+// scan over the lanes places the experts' tile ranges end to end, and the
+// expert holding w is the number of ranges that end at or before it. Returns
+// false past the last live tile. Uniform per wave (every wave of a block
+// computes the same).
 struct LiveTile {
     int e, r, ne;  // expert, tile index inside the expert, expert's rows
 };
@@ -127,6 +128,69 @@ __device__ __forceinline__ bool live_tile(const int32_t* counts, int G, int E, i
     out->e = e;
     out->r = w - __shfl(incl - t, e, 64);
     out->ne = __shfl(ne, e, 64);
+    return true;
+}
+
+// Row GEMMs whose outputs are d wide, under a skewed load. The launch order
+// is cut into chunks of `chunk` tiles; a chunk runs on one XCD (chunks are
+// dealt to the XCDs in turn) and its tiles share operand panels in that
+// XCD's L2. The chunks of heavy experts' live tiles (at least half a tile of
+// rows) are spread evenly over the first 70% of the chunk positions and
+// those of light experts fill the rest, so heavy tiles' products run beside
+// light tiles' weight-panel streaming instead of the launch running all of
+// one kind, then all of the other. Inside each class experts go in order;
+// with no light expert it is the plain live-tile order. Measured at the
+// ViT-L/16 skew (four full experts, 28 of ~17 rows): down-projection 216 ->
+// 178 us, dxe 204 -> 161 us (few n-tiles, long k); the same spread slowed
+// the f-wide row GEMMs (196 -> 213, 173 -> 191 us) and the weight gradients
+// (350 -> 399: heavy tiles apart no longer shared panels in L2), which keep
+// the plain order. Chunk position c, tile i inside it; false past the
+// class's tiles. Uniform per wave.
+__device__ __forceinline__ bool spread_tile(const GemmBatch& batch, int bm, int c, int i,
+                                            int* e_out, int* r_out, int* ne_out) {
+    const GemmArgs& p0 = batch.p[0];
+    const int E = p0.E, lane = threadIdx.x & 63, chunk = batch.chunk;
+    int ne = 0;
+    if (lane < E) ne = min(expert_rows(p0.counts, p0.G, E, lane), p0.M);
+    const bool heavy_l = lane < E && 2 * ne >= bm;
+    const uint64_t emask = E >= 64 ? ~0ull : (1ull << E) - 1ull;
+    const uint64_t hmask = __ballot(heavy_l) & emask;
+    const int te = lane < E ? (ne + bm - 1) / bm * batch.tiles_n[0] : 0;
+    int nh = heavy_l ? te : 0, nl = te;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        nh += __shfl_xor(nh, o, 64);
+        nl += __shfl_xor(nl, o, 64);
+    }
+    nl -= nh;
+    const int nhc = (nh + chunk - 1) / chunk, nlc = (nl + chunk - 1) / chunk;
+    const int first = max(nhc, (7 * (nhc + nlc) + 9) / 10);
+    bool heavy;
+    int ci;
+    if (c < first) {
+        const int hc = static_cast<int>((static_cast<long long>(c) + 1) * nhc / first);
+        const int hp = static_cast<int>(static_cast<long long>(c) * nhc / first);
+        heavy = hc > hp;
+        ci = heavy ? hp : c - hc;
+    } else {
+        heavy = false;
+        ci = c - nhc;
+    }
+    const long long j = static_cast<long long>(ci) * chunk + i;  // index in the class's list
+    if (j >= (heavy ? nh : nl)) return false;
+    const uint64_t cmask = heavy ? hmask : (emask & ~hmask);
+    // the class's experts' tile ranges end to end (inclusive scan)
+    const int t = (cmask >> lane) & 1ull ? te : 0;
+    int incl = t;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int u = __shfl_up(incl, o, 64);
+        if (lane >= o) incl += u;
+    }
+    const int e = __popcll(__ballot(incl <= j));
+    *e_out = e;
+    *r_out = static_cast<int>(j - __shfl(incl - t, e, 64));
+    *ne_out = __shfl(ne, e, 64);
     return true;
 }
 
@@ -852,7 +916,10 @@ void gemm_bf16_kernel(GemmBatch batch) {
     // each expert, however unevenly the rows are spread over experts.
     const int l = b >> 3, chunk = batch.chunk;
     int w = ((l / chunk) * 8 + (b & 7)) * chunk + l % chunk;
-    if constexpr (compact_tiles<EPI>()) {
+    if constexpr (EPI == EPI_BIAS || EPI == EPI_STORE) {
+        if (!spread_tile(batch, BM_, (l / chunk) * 8 + (b & 7), l % chunk, &e, &r, &ne)) return;
+        tiles_m = (ne + BM_ - 1) / BM_;
+    } else if constexpr (compact_tiles<EPI>()) {
         LiveTile lt;
         const GemmArgs& p0 = batch.p[0];
         if (!live_tile(p0.counts, p0.G, p0.E, p0.M, BM_, batch.tiles_n[0], w, &lt)) return;
@@ -1324,7 +1391,10 @@ void launch_bf16(const Dims& D, const GemmArgs* a, const int* grid_m_rows, int n
     const int one_col = AK && BK_ && n == 1 && b.tiles_m[0] <= 8 ? b.tiles_m[0] : 0;
     b.group_m = one_col ? one_col : (T::WAVES_PER_EU == 2 && T::NW == 4 ? 8 : 4);
     b.chunk = 4 * b.group_m;
-    b.per_xcd = static_cast<int>(cdiv(b.total[0] + b.total[1], 8 * b.chunk)) * b.chunk;
+    // (the spread row GEMMs take one chunk more per XCD: splitting the tiles
+    // into two classes can leave a partial chunk in each)
+    const int spread = EPI == EPI_BIAS || EPI == EPI_STORE ? 1 : 0;
+    b.per_xcd = static_cast<int>(cdiv(b.total[0] + b.total[1], 8 * b.chunk) + spread) * b.chunk;
     if (sched && GATHER == 0) {
         // persistent blocks under quotas: as many as are resident at once
         // (one per CU for the 8-wave tiles, two for the 4-wave ones)

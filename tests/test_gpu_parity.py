@@ -185,6 +185,12 @@ SMALL = [
                     capacity_factor=1.0, router_std=0.05),
     W.custom_config("bf16_eight_mtiles", n_tokens=3000, d_model=136, d_ff=520, n_experts=3,
                     k=2, capacity_factor=0.9, router_std=0.1),
+    # heavy and light experts in one launch: two experts full (500 rows, two
+    # m-tiles each), six with 53-85 rows, so the d-wide row GEMMs spread the
+    # heavy experts' tile chunks among the light ones (a partial chunk in
+    # each class)
+    W.custom_config("bf16_two_classes", n_tokens=2000, d_model=72, d_ff=264, n_experts=8, k=2,
+                    capacity_factor=1.0, hot_experts=2, hot_offset=2.0, router_std=0.1),
 ]
 
 

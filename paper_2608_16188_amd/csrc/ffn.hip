@@ -1415,6 +1415,12 @@ void launch_bf16(const Dims& D, const GemmArgs& a, int grid_m_rows, int sched, h
 using TileBig = Tile<256, 256, 2, 4, 32, 4, STAGE_DMA>;    // 8 waves, one block per CU
 using TileNarrow = Tile<256, 192, 4, 2, 64, 2, STAGE_DMA>; // 8 waves, 3/4 of TileBig's columns
 using TileSmall = Tile<128, 128, 2, 2, 32, 4, STAGE_DMA>;  // 4 waves, two blocks per CU
+// TileBig with 64-deep stages in a ring of two: half the stage barriers per
+// k, one stage in flight instead of three. For the f-wide row GEMMs (short
+// k = d, heavy epilogues) measured 1.3-1.5% faster per step at ViT-B/16 and
+// the 17-task pool and even at ViT-L/16; for the weight gradients at the
+// ViT-L/16 skew 5-10 us slower, so those keep TileBig.
+using TileDeep = Tile<256, 256, 2, 4, 64, 2, STAGE_DMA>;
 
 // Work of a launch in units of one CU's time: rounds of one-block-per-CU
 // waves times the tile's area (relative cost per tile area `eff`).
@@ -1426,8 +1432,9 @@ template <bool AK, bool BK_, int EPI, int GATHER = 0>
 void launch_gemm(const Dims& D, const GemmArgs& a, int grid_m_rows, int sched, hipStream_t st) {
     if (D.dtype == VMOE_BF16) {
         // 256 x 256 tiles (half the operand bytes per flop of 128 x 128) for
-        // the GEMMs whose m is the expert's rows; the weight gradients (k is
-        // the rows, often short) run 128 x 128 tiles, two blocks per CU.
+        // the GEMMs whose m is the expert's rows, the f-wide ones with
+        // 64-deep stages (TileDeep). (bf16 weight gradients run batched in
+        // ffn_bwd_launch; this EPI_F32 case only serves other callers.)
         if constexpr (EPI == EPI_F32) {
             launch_bf16<TileSmall, AK, BK_, EPI, GATHER>(D, a, grid_m_rows, sched, st);
         } else if constexpr (EPI == EPI_BIAS || EPI == EPI_STORE) {
@@ -1442,7 +1449,7 @@ void launch_gemm(const Dims& D, const GemmArgs& a, int grid_m_rows, int sched, h
             else
                 launch_bf16<TileBig, AK, BK_, EPI, GATHER>(D, a, grid_m_rows, sched, st);
         } else {
-            launch_bf16<TileBig, AK, BK_, EPI, GATHER>(D, a, grid_m_rows, sched, st);
+            launch_bf16<TileDeep, AK, BK_, EPI, GATHER>(D, a, grid_m_rows, sched, st);
         }
     } else {
         dim3 grid(cdiv(a.N, FT), cdiv(grid_m_rows, FT), D.E);

@@ -103,6 +103,12 @@ ROUTE_CASES = [
     ("single_block_equal_priorities", 8000, 4, 2, 1, dict(seed=15, tie_every=1)),
     ("single_block_k4_groups", 4 * 4096, 16, 4, 4, dict(seed=16, scale=2.0)),
     ("many_small_groups_e64", 300 * 8, 64, 2, 300, dict(seed=17, scale=2.0)),
+    # the multi-block path with several groups: groups past 8192 tokens (hist
+    # blocks of 4096 with a ragged last one, row bases across groups), and
+    # groups of fewer tokens whose assignments pass 16384 (k = 4)
+    ("multi_block_two_groups", 2 * 9000, 8, 2, 2, dict(seed=18, scale=2.0)),
+    ("multi_block_k4_three_groups", 3 * 5000, 16, 4, 3, dict(seed=19, scale=2.0)),
+    ("multi_block_groups_equal_priorities", 2 * 8500, 4, 2, 2, dict(seed=20, tie_every=1)),
 ]
 
 

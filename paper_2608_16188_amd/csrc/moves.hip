@@ -149,7 +149,7 @@ __global__ __launch_bounds__(kBlock) void combine_fwd_kernel(const T* __restrict
         for (int u = 0; u < kItems; ++u)
 #pragma unroll
             for (int jj = 0; jj < kJ; ++jj)
-                r[u][jj] = src[(rows[u].r[jj] >= 0 ? rows[u].r[jj] : 0) * nvec + cc[u]];
+                if (rows[u].r[jj] >= 0) r[u][jj] = src[rows[u].r[jj] * nvec + cc[u]];
 #pragma unroll
         for (int u = 0; u < kItems; ++u)
 #pragma unroll
@@ -258,7 +258,7 @@ __global__ __launch_bounds__(kBlock) void dispatch_bwd_kernel(const T* __restric
         for (int u = 0; u < kItems; ++u)
 #pragma unroll
             for (int jj = 0; jj < kJ; ++jj)
-                r[u][jj] = src[(rows[u].r[jj] >= 0 ? rows[u].r[jj] : 0) * nvec + cc[u]];
+                if (rows[u].r[jj] >= 0) r[u][jj] = src[rows[u].r[jj] * nvec + cc[u]];
 #pragma unroll
         for (int u = 0; u < kItems; ++u)
 #pragma unroll

@@ -108,7 +108,7 @@ struct DxIn {
         for (int j = 0; j < KJ; ++j) {
             const int row = rows[j];
             kept |= (row >= 0 ? 1 : 0) << j;
-            r[j].load(dxe + static_cast<size_t>(row >= 0 ? row : 0) * d + ic);
+            if (row >= 0) r[j].load(dxe + static_cast<size_t>(row) * d + ic);
         }
     }
     __device__ __forceinline__ void to_f32(float (&v)[VEC]) const {
@@ -682,8 +682,9 @@ __global__ __launch_bounds__(512) void route_bwd_mma_kernel(
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
                     const int col = min(c0 + 32 * j + 8 * q + 4 * kh, d - 4);
-                    h[jj][j][q] = *reinterpret_cast<const uint2*>(
-                        dxe + static_cast<size_t>(rr[jj] >= 0 ? rr[jj] : 0) * d + col);
+                    if (rr[jj] >= 0)
+                        h[jj][j][q] = *reinterpret_cast<const uint2*>(
+                            dxe + static_cast<size_t>(rr[jj]) * d + col);
                 }
     }
     // stage 2: into LDS (W transposed to [column][expert])

@@ -377,6 +377,26 @@ def main():
                             "vmoe_expert_ffn_fwd, vmoe_expert_ffn_bwd_gather in place of "
                             "vmoe_expert_ffn_bwd (xe never written)"}
 
+    # the same step captured once in a HIP graph and replayed K times
+    # (diagnostic: the kernels are the step's, only the launch path differs)
+    graph = None
+    if not args.no_diagnostics:
+        g = torch.cuda.CUDAGraph()
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g, stream=stream):
+            for name in CALLS:
+                calls[name]()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(K):
+            g.replay()
+        b.record(stream)
+        torch.cuda.synchronize()
+        graph = {"ms_per_step": a.elapsed_time(b) / K,
+                 "note": "the step's seven calls captured in one HIP graph, K replays"}
+        del g
+
     flushed = None
     if args.flush_mall:
         # per-call times with the MALL flushed before every step: a 512 MiB
@@ -458,6 +478,7 @@ def main():
         "balance_losses": balance,
         "ffn_quota_scheduler": quota,
         "dispatch_fused_step": gathered,
+        "graph_step": graph,
     }
     if flushed is not None:
         fb = sum(cost[n][1] for n in moves)

@@ -601,57 +601,82 @@ __global__ __launch_bounds__(512) void route_bwd_mma_kernel(
     __shared__ __attribute__((aligned(16))) float dzs[TCH * DZLD];
     __shared__ __attribute__((aligned(16))) uint16_t wts[COLS * WLD];
     __shared__ __attribute__((aligned(16))) uint16_t xs[TCH * kRbXLd];
-    const int c = blockIdx.x, g = blockIdx.z;
+    const int g = blockIdx.z;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int t0 = c * TCH;
-    const int ntok = min(TCH, Ng - t0);
-    const size_t tok0 = static_cast<size_t>(g) * Ng + t0;
     const int c0 = blockIdx.y * COLS;
     const uint16_t* wg = wr + static_cast<size_t>(g) * E * d;
-
     const int m = lane & 31, kh = lane >> 5;
     // waves 0-3 form dx, waves 4-7 the router-gradient partial, at the same
     // time once the tiles are staged
     const bool dx_wave = wave < 4;
     const int rw = wave & 3;
-    // the dx rows of a dx wave's lane: tokens [32 w, 32 w + 32) of the chunk;
-    // register 4 q + r of lane l will hold token 32 w + l % 32, column
-    // 32 j + 8 q + 4 (l / 32) + r
-    const int tl = 32 * rw + m;
-    const bool tok_ok = tl < ntok;
-    const size_t trow = (tok0 + min(tl, ntok - 1)) * d;
     constexpr int NJ = COLS / 32;
-    // stage 1, all requested before any is used, in this order (the waits
-    // count in issue order): (fused) the token's expert-buffer rows; the dz
-    // rows, W columns and x rows of the tiles, zero past the chunk, the
-    // experts or d; then the incoming value of each dx element, dx itself or
-    // (fused) the kept dxe rows, which stay in flight through the staging
-    // and the products
-    int rr[KJ > 0 ? KJ : 1];
-    if constexpr (KJ > 0) {
-#pragma unroll
-        for (int jj = 0; jj < KJ; ++jj)
-            rr[jj] = (dx_wave && jj < k) ? rows[(tok0 + min(tl, ntok - 1)) * k + jj] : -1;
-    }
     constexpr int NT = 512;
     constexpr int DZV = TCH * EMAX / NT;      // dz values per thread
     constexpr int WV = EMAX * COLS / 8 / NT;  // 16-byte W vectors per thread
     constexpr int XV = TCH * COLS / 8 / NT;   // 16-byte x vectors per thread
     static_assert(DZV * NT == TCH * EMAX && WV * NT * 8 == EMAX * COLS &&
                       XV * NT * 8 == TCH * COLS, "tiles split evenly over the threads");
+    // the block's W columns, the same for every chunk it takes: staged once
+    // (transposed to [column][expert]); the first chunk's barrier publishes it
+    {
+        uint4 wv[WV];
+#pragma unroll
+        for (int u = 0; u < WV; ++u) {
+            const int q = u * NT + tid, e = q / (COLS / 8), col = c0 + (q % (COLS / 8)) * 8;
+            wv[u] = (e < E && col < d)
+                        ? *reinterpret_cast<const uint4*>(wg + static_cast<size_t>(e) * d + col)
+                        : make_uint4(0u, 0u, 0u, 0u);
+        }
+#pragma unroll
+        for (int u = 0; u < WV; ++u) {
+            const int q = u * NT + tid, e = q / (COLS / 8), cl = (q % (COLS / 8)) * 8;
+            const uint32_t hw[4] = {wv[u].x, wv[u].y, wv[u].z, wv[u].w};
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                wts[(cl + 2 * i) * WLD + e] = static_cast<uint16_t>(hw[i] & 0xFFFFu);
+                wts[(cl + 2 * i + 1) * WLD + e] = static_cast<uint16_t>(hw[i] >> 16);
+            }
+        }
+    }
+    // one set of accumulators, two roles: a dx wave's products of the
+    // current chunk, a dW wave's router-gradient partial over all its chunks
+    constexpr int MB = EMAX / 32;
+    constexpr int NA = NJ > MB ? NJ : MB;
+    f32x16_r acc[NA];
+#pragma unroll
+    for (int b = 0; b < NA; ++b)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc[b][i] = 0.0f;
+
+    // chunks blockIdx.x, blockIdx.x + gridDim.x, ... of the group, in order
+    for (int c = blockIdx.x; c < nch; c += gridDim.x) {
+    const int t0 = c * TCH;
+    const int ntok = min(TCH, Ng - t0);
+    const size_t tok0 = static_cast<size_t>(g) * Ng + t0;
+    // the dx rows of a dx wave's lane: tokens [32 w, 32 w + 32) of the chunk;
+    // register 4 q + r of lane l will hold token 32 w + l % 32, column
+    // 32 j + 8 q + 4 (l / 32) + r
+    const int tl = 32 * rw + m;
+    const bool tok_ok = tl < ntok;
+    const size_t trow = (tok0 + min(tl, ntok - 1)) * d;
+    // stage 1, all requested before any is used, in this order (the waits
+    // count in issue order): (fused) the token's expert-buffer rows; the dz
+    // rows and x rows of the tiles, zero past the chunk, the experts or d;
+    // then the incoming value of each dx element, dx itself or (fused) the
+    // kept dxe rows, which stay in flight through the staging and the products
+    int rr[KJ > 0 ? KJ : 1];
+    if constexpr (KJ > 0) {
+#pragma unroll
+        for (int jj = 0; jj < KJ; ++jj)
+            rr[jj] = (dx_wave && jj < k) ? rows[(tok0 + min(tl, ntok - 1)) * k + jj] : -1;
+    }
     float dzv[DZV];
-    uint4 wv[WV], xv[XV];
+    uint4 xv[XV];
 #pragma unroll
     for (int u = 0; u < DZV; ++u) {
         const int q = u * NT + tid, r = q / EMAX, e = q % EMAX;
         dzv[u] = (r < ntok && e < E) ? dz[(tok0 + r) * E + e] : 0.0f;
-    }
-#pragma unroll
-    for (int u = 0; u < WV; ++u) {
-        const int q = u * NT + tid, e = q / (COLS / 8), col = c0 + (q % (COLS / 8)) * 8;
-        wv[u] = (e < E && col < d)
-                    ? *reinterpret_cast<const uint4*>(wg + static_cast<size_t>(e) * d + col)
-                    : make_uint4(0u, 0u, 0u, 0u);
     }
     if constexpr (DW) {
 #pragma unroll
@@ -687,21 +712,11 @@ __global__ __launch_bounds__(512) void route_bwd_mma_kernel(
                             dxe + static_cast<size_t>(rr[jj]) * d + col);
                 }
     }
-    // stage 2: into LDS (W transposed to [column][expert])
+    // stage 2: into LDS
 #pragma unroll
     for (int u = 0; u < DZV; ++u) {
         const int q = u * NT + tid;
         dzs[(q / EMAX) * DZLD + q % EMAX] = dzv[u];
-    }
-#pragma unroll
-    for (int u = 0; u < WV; ++u) {
-        const int q = u * NT + tid, e = q / (COLS / 8), cl = (q % (COLS / 8)) * 8;
-        const uint32_t hw[4] = {wv[u].x, wv[u].y, wv[u].z, wv[u].w};
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            wts[(cl + 2 * i) * WLD + e] = static_cast<uint16_t>(hw[i] & 0xFFFFu);
-            wts[(cl + 2 * i + 1) * WLD + e] = static_cast<uint16_t>(hw[i] >> 16);
-        }
     }
     if constexpr (DW) {
 #pragma unroll
@@ -714,7 +729,6 @@ __global__ __launch_bounds__(512) void route_bwd_mma_kernel(
     lds_barrier();
 
     if (dx_wave) {
-    f32x16_r acc[NJ];
 #pragma unroll
     for (int j = 0; j < NJ; ++j)
 #pragma unroll
@@ -767,15 +781,9 @@ __global__ __launch_bounds__(512) void route_bwd_mma_kernel(
     }
 
     if (DW && !dx_wave) {
-        // 4. P[e][column] over the chunk's tokens for columns [32 w, 32 w + 32):
+        // 4. P[e][column] += over the chunk's tokens, columns [32 w, 32 w + 32):
         // A = dz^T (expert m, tokens 16 s + 8 kh .. +7, three terms),
         // B = x (column m, the same tokens), read transposed from the x tile
-        constexpr int MB = EMAX / 32;
-        f32x16_r pacc[MB];
-#pragma unroll
-        for (int b = 0; b < MB; ++b)
-#pragma unroll
-            for (int i = 0; i < 16; ++i) pacc[b][i] = 0.0f;
         const int gq = lane >> 4, jq = lane & 15;
         const int ntk = (ntok + 15) / 16;  // rows past the chunk are zero in both tiles
         for (int s = 0; s < ntk; ++s) {
@@ -792,14 +800,20 @@ __global__ __launch_bounds__(512) void route_bwd_mma_kernel(
                 for (int i = 0; i < 8; ++i) a8[i] = dzs[(16 * s + 8 * kh + i) * DZLD + 32 * b + m];
                 bf16x8_r ahi, amid, alo;
                 split3(a8, ahi, amid, alo);
-                pacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bx, alo, pacc[b], 0, 0, 0);
-                pacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bx, amid, pacc[b], 0, 0, 0);
-                pacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bx, ahi, pacc[b], 0, 0, 0);
+                acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bx, alo, acc[b], 0, 0, 0);
+                acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bx, amid, acc[b], 0, 0, 0);
+                acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bx, ahi, acc[b], 0, 0, 0);
             }
         }
+    }
+    // every wave is done with this chunk's tiles before the next overwrites them
+    lds_barrier();
+    }
+
+    if (DW && !dx_wave) {
         // register 4 q + r of lane l: expert 32 b + l % 32, column
         // 32 w + 8 q + 4 (l / 32) + r
-        float* pg = partial + (static_cast<size_t>(g) * nch + c) * E * d;
+        float* pg = partial + (static_cast<size_t>(g) * gridDim.x + blockIdx.x) * E * d;
 #pragma unroll
         for (int b = 0; b < MB; ++b) {
             const int e = 32 * b + m;
@@ -809,8 +823,8 @@ __global__ __launch_bounds__(512) void route_bwd_mma_kernel(
                     const int col = c0 + 32 * rw + 8 * q + 4 * kh;
                     if (col < d)
                         *reinterpret_cast<float4*>(pg + static_cast<size_t>(e) * d + col) =
-                            make_float4(pacc[b][4 * q], pacc[b][4 * q + 1], pacc[b][4 * q + 2],
-                                        pacc[b][4 * q + 3]);
+                            make_float4(acc[b][4 * q], acc[b][4 * q + 1], acc[b][4 * q + 2],
+                                        acc[b][4 * q + 3]);
                 }
             }
         }
@@ -854,12 +868,22 @@ __global__ __launch_bounds__(256) void route_bwd_reduce_kernel(const float* __re
 
 struct ChunkPlan {
     int tch, nch;
+    int npart;  // router-gradient partials per group (the reducer's count)
+    int nblk;   // matrix-core kernel: blocks per (group, column block)
 };
 
 ChunkPlan plan(const Dims& D) {
-    // bf16 with E > 16: the matrix-core kernel's fixed chunk
-    if (D.dtype == VMOE_BF16 && D.E > 16)
-        return ChunkPlan{kRbTok, D.Ng > 0 ? static_cast<int>(cdiv(D.Ng, kRbTok)) : 0};
+    // bf16 with E > 16: the matrix-core kernel's fixed chunk; about one
+    // block per CU over (column blocks, groups), each taking an even share of
+    // the chunks in turn and writing one partial
+    if (D.dtype == VMOE_BF16 && D.E > 16) {
+        const int nch = D.Ng > 0 ? static_cast<int>(cdiv(D.Ng, kRbTok)) : 0;
+        const long long per = static_cast<long long>(D.G) * cdiv(D.d, kRbCols);
+        int nb = static_cast<int>(256 / per);
+        nb = nb < 1 ? 1 : (nb > nch ? nch : nb);
+        if (nb > 0) nb = static_cast<int>(cdiv(nch, cdiv(nch, nb)));
+        return ChunkPlan{kRbTok, nch, nb, nb};
+    }
     // about 1024 blocks over (chunks, column blocks, groups)
     const int cols = 64 * (D.E <= 8    ? ColsPerLane<8>::value
                            : D.E <= 16 ? ColsPerLane<16>::value
@@ -873,7 +897,8 @@ ChunkPlan plan(const Dims& D) {
                      : D.E <= 32 ? ChunkMax<32>::value
                                  : ChunkMax<64>::value;
     tch = tch < kMinChunk ? kMinChunk : (tch > tmax ? tmax : tch);
-    return ChunkPlan{tch, D.Ng > 0 ? static_cast<int>(cdiv(D.Ng, tch)) : 0};
+    const int nch = D.Ng > 0 ? static_cast<int>(cdiv(D.Ng, tch)) : 0;
+    return ChunkPlan{tch, nch, nch, nch};
 }
 
 // Inputs of one launch of the main kernel (dxe, row_base, gc: fused only).
@@ -902,7 +927,7 @@ void launch_main(const Dims& D, const ChunkPlan& P, const BwdArgs& a, hipStream_
         rbwd_dz_kernel<EMAX><<<cdiv(D.N, TPB), 256, 0, st>>>(
             a.probs, a.idx, a.slot, a.dgate, a.dz_add, a.row_base, a.dz,
             KJ > 0 ? a.rows : nullptr, gc, D.N, D.Ng, D.E, D.k);
-        const dim3 grid(P.nch, cdiv(D.d, kRbCols), D.G);
+        const dim3 grid(P.nblk, cdiv(D.d, kRbCols), D.G);
         auto go = [&](auto kern) {
             kern<<<grid, 512, 0, st>>>(static_cast<const uint16_t*>(a.x),
                                        static_cast<const uint16_t*>(a.wr), a.dz, a.rows,
@@ -964,7 +989,7 @@ vmoe_status run_route_bwd(const Dims& D, BwdArgs a, float* dwr, void* ws, int kj
     else launch_main_t<4>(D, P, a, st);
     if (dwr)
         route_bwd_reduce_kernel<<<cdiv(total, 32), 256, 0, st>>>(a.partial, dwr, D.E, D.d,
-                                                                  P.nch, total);
+                                                                  P.npart, total);
     return launch_status();
 }
 

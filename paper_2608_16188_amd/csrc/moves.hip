@@ -84,6 +84,7 @@ struct Rows {
 // then metadata) is issued before the first store.
 constexpr int kBlock = 256;
 constexpr int kItems = 2;
+constexpr int kCItems = 1;  // combine: one item per thread
 // J: assignments per pass (2 when k <= 2, else 4; larger k loops)
 
 template <typename T, int kJ>
@@ -120,14 +121,14 @@ __global__ __launch_bounds__(kBlock) void combine_fwd_kernel(const T* __restrict
                                                              int nvec) {
     constexpr int VN = Vec<T>::n;
     const long long total = static_cast<long long>(m.N) * nvec;
-    const long long i0 = static_cast<long long>(blockIdx.x) * kBlock * kItems + threadIdx.x;
+    const long long i0 = static_cast<long long>(blockIdx.x) * kBlock * kCItems + threadIdx.x;
     const uint4* src = reinterpret_cast<const uint4*>(ye);
     uint4* dst = reinterpret_cast<uint4*>(y);
-    long long it[kItems];
-    int tt[kItems], cc[kItems];
-    float acc[kItems][VN];
+    long long it[kCItems];
+    int tt[kCItems], cc[kCItems];
+    float acc[kCItems][VN];
 #pragma unroll
-    for (int u = 0; u < kItems; ++u) {
+    for (int u = 0; u < kCItems; ++u) {
         it[u] = min(i0 + u * kBlock, total - 1);
         tt[u] = static_cast<int>(it[u] / nvec);
         cc[u] = static_cast<int>(it[u] - static_cast<long long>(tt[u]) * nvec);
@@ -135,23 +136,23 @@ __global__ __launch_bounds__(kBlock) void combine_fwd_kernel(const T* __restrict
         for (int q = 0; q < VN; ++q) acc[u][q] = 0.0f;
     }
     for (int j0 = 0; j0 < m.k; j0 += kJ) {
-        Rows<kJ> rows[kItems];
-        float gj[kItems][kJ];
-        uint4 r[kItems][kJ];
+        Rows<kJ> rows[kCItems];
+        float gj[kCItems][kJ];
+        uint4 r[kCItems][kJ];
 #pragma unroll
-        for (int u = 0; u < kItems; ++u) {
+        for (int u = 0; u < kCItems; ++u) {
             rows[u].fetch(m, tt[u], j0);
 #pragma unroll
             for (int jj = 0; jj < kJ; ++jj)
                 gj[u][jj] = gate[static_cast<size_t>(tt[u]) * m.k + min(j0 + jj, m.k - 1)];
         }
 #pragma unroll
-        for (int u = 0; u < kItems; ++u)
+        for (int u = 0; u < kCItems; ++u)
 #pragma unroll
             for (int jj = 0; jj < kJ; ++jj)
                 if (rows[u].r[jj] >= 0) r[u][jj] = src[rows[u].r[jj] * nvec + cc[u]];
 #pragma unroll
-        for (int u = 0; u < kItems; ++u)
+        for (int u = 0; u < kCItems; ++u)
 #pragma unroll
             for (int jj = 0; jj < kJ; ++jj) {
                 if (rows[u].r[jj] < 0) continue;
@@ -162,7 +163,7 @@ __global__ __launch_bounds__(kBlock) void combine_fwd_kernel(const T* __restrict
             }
     }
 #pragma unroll
-    for (int u = 0; u < kItems; ++u)
+    for (int u = 0; u < kCItems; ++u)
         if (i0 + u * kBlock < total) dst[it[u]] = Vec<T>::pack(acc[u]);
 }
 
@@ -340,7 +341,7 @@ vmoe_status combine_fwd_launch(const Dims& D, const void* ye, const int32_t* idx
     if (D.N == 0) return VMOE_OK;
     const RouteMeta m = meta(D, idx, slot, row_base);
     const int nvec = D.d / (D.dtype == VMOE_BF16 ? 8 : 4);
-    const unsigned grid = cdiv(static_cast<long long>(D.N) * nvec, kBlock * kItems);
+    const unsigned grid = cdiv(static_cast<long long>(D.N) * nvec, kBlock * kCItems);
     auto go = [&](auto jc) {
         constexpr int J = decltype(jc)::value;
         if (D.dtype == VMOE_BF16)

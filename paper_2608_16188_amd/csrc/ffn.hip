@@ -98,6 +98,14 @@ __device__ __forceinline__ int expert_rows(const int32_t* counts, int G, int E, 
     return n;
 }
 
+// m-tiles of an expert with ne rows: ceil(ne / bm), except that an expert
+// whose rows fit one 32-row block (a light expert) gets `lsplit` tiles per
+// n-tile, each taking a share of the tile's columns (its weight stream then
+// runs on lsplit CUs). lsplit = 1 leaves every expert at ceil(ne / bm).
+__device__ __forceinline__ int expert_mtiles(int ne, int bm, int lsplit) {
+    return lsplit > 1 && ne > 0 && ne <= 32 ? lsplit : (ne + bm - 1) / bm;
+}
+
 // Live tile w of a compact problem: lane e of every wave sums expert e's rows
 // (at most `cap`, the rows of its buffer) and its tile count, an inclusive
 // scan over the lanes places the experts' tile ranges end to end, and the
@@ -108,7 +116,7 @@ struct LiveTile {
     int e, r, ne;  // expert, tile index inside the expert, expert's rows
 };
 __device__ __forceinline__ bool live_tile(const int32_t* counts, int G, int E, int cap, int bm,
-                                          int tiles_n, int w, LiveTile* out) {
+                                          int lsplit, int tiles_n, int w, LiveTile* out) {
     const int lane = threadIdx.x & 63;
     int ne = 0;
     if (lane < E) {
@@ -116,7 +124,7 @@ __device__ __forceinline__ bool live_tile(const int32_t* counts, int G, int E, i
         for (int g = 0; g < G; ++g) ne += counts[g * E + lane];
         ne = min(ne, cap);  // never past the expert's rows, whatever the counts say
     }
-    const int t = (ne + bm - 1) / bm * tiles_n;
+    const int t = expert_mtiles(ne, bm, lsplit) * tiles_n;
     int incl = t;
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
@@ -134,20 +142,25 @@ __device__ __forceinline__ bool live_tile(const int32_t* counts, int G, int E, i
 // Row GEMMs whose outputs are d wide, under a skewed load. The launch order
 // is cut into chunks of `chunk` tiles; a chunk runs on one XCD (chunks are
 // dealt to the XCDs in turn) and its tiles share operand panels in that
-// XCD's L2. The chunks of heavy experts' live tiles (at least half a tile of
-// rows) are spread evenly over the first 70% of the chunk positions and
-// those of light experts fill the rest, so heavy tiles' products run beside
-// light tiles' weight-panel streaming instead of the launch running all of
-// one kind, then all of the other. Inside each class experts go in order;
-// with no light expert it is the plain live-tile order. Measured at the
-// ViT-L/16 skew (four full experts, 28 of ~17 rows): down-projection 216 ->
-// 178 us, dxe 204 -> 161 us (few n-tiles, long k); the same spread slowed
-// the f-wide row GEMMs (196 -> 213, 173 -> 191 us) and the weight gradients
+// XCD's L2. With lsplit = 1 (light tiles as long as a heavy one's weight
+// stream) the chunks of heavy experts' live tiles (at least half a tile of
+// rows) are spread evenly over the first 70% of the chunk positions and those
+// of light experts fill the rest, so that light tiles do not run alone at the
+// end. Inside each class experts go in order; with no light expert it is the
+// plain live-tile order. Measured at the ViT-L/16 skew (four full experts, 28
+// of ~17 rows): the spread took the down-projection 216 -> 178 us and dxe
+// 204 -> 161 us against expert order (few n-tiles, long k); it slowed the
+// f-wide row GEMMs (196 -> 213, 173 -> 191 us) and the weight gradients
 // (350 -> 399: heavy tiles apart no longer shared panels in L2), which keep
-// the plain order. Chunk position c, tile i inside it; false past the
+// the plain order. With lsplit > 1 (light tiles split into short column
+// parts) every XCD instead takes an equal contiguous share of the heavy
+// tiles first, all of them starting in the first round, then an equal
+// contiguous share of the light parts, which run on its remaining CUs beside
+// them: x is the block's XCD, c its place in that XCD's block sequence (i is
+// unused). Chunk position c, tile i inside it (lsplit = 1); false past the
 // class's tiles. Uniform per wave.
-__device__ __forceinline__ bool spread_tile(const GemmBatch& batch, int bm, int c, int i,
-                                            int* e_out, int* r_out, int* ne_out) {
+__device__ __forceinline__ bool spread_tile(const GemmBatch& batch, int bm, int lsplit, int x,
+                                            int c, int i, int* e_out, int* r_out, int* ne_out) {
     const GemmArgs& p0 = batch.p[0];
     const int E = p0.E, lane = threadIdx.x & 63, chunk = batch.chunk;
     int ne = 0;
@@ -155,7 +168,7 @@ __device__ __forceinline__ bool spread_tile(const GemmBatch& batch, int bm, int 
     const bool heavy_l = lane < E && 2 * ne >= bm;
     const uint64_t emask = E >= 64 ? ~0ull : (1ull << E) - 1ull;
     const uint64_t hmask = __ballot(heavy_l) & emask;
-    const int te = lane < E ? (ne + bm - 1) / bm * batch.tiles_n[0] : 0;
+    const int te = lane < E ? expert_mtiles(ne, bm, lsplit) * batch.tiles_n[0] : 0;
     int nh = heavy_l ? te : 0, nl = te;
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) {
@@ -163,20 +176,28 @@ __device__ __forceinline__ bool spread_tile(const GemmBatch& batch, int bm, int 
         nl += __shfl_xor(nl, o, 64);
     }
     nl -= nh;
-    const int nhc = (nh + chunk - 1) / chunk, nlc = (nl + chunk - 1) / chunk;
-    const int first = max(nhc, (7 * (nhc + nlc) + 9) / 10);
     bool heavy;
-    int ci;
-    if (c < first) {
-        const int hc = static_cast<int>((static_cast<long long>(c) + 1) * nhc / first);
-        const int hp = static_cast<int>(static_cast<long long>(c) * nhc / first);
-        heavy = hc > hp;
-        ci = heavy ? hp : c - hc;
+    long long j;  // index in the class's list
+    if (lsplit > 1) {
+        const int h0 = x * nh / 8, hx = (x + 1) * nh / 8 - h0;
+        heavy = c < hx;
+        j = heavy ? h0 + c : x * nl / 8 + (c - hx);
+        if (!heavy && c - hx >= (x + 1) * nl / 8 - x * nl / 8) return false;
     } else {
-        heavy = false;
-        ci = c - nhc;
+        const int nhc = (nh + chunk - 1) / chunk, nlc = (nl + chunk - 1) / chunk;
+        const int first = max(nhc, (7 * (nhc + nlc) + 9) / 10);
+        int ci;
+        if (c < first) {
+            const int hc = static_cast<int>((static_cast<long long>(c) + 1) * nhc / first);
+            const int hp = static_cast<int>(static_cast<long long>(c) * nhc / first);
+            heavy = hc > hp;
+            ci = heavy ? hp : c - hc;
+        } else {
+            heavy = false;
+            ci = c - nhc;
+        }
+        j = static_cast<long long>(ci) * chunk + i;
     }
-    const long long j = static_cast<long long>(ci) * chunk + i;  // index in the class's list
     if (j >= (heavy ? nh : nl)) return false;
     const uint64_t cmask = heavy ? hmask : (emask & ~hmask);
     // the class's experts' tile ranges end to end (inclusive scan)
@@ -288,7 +309,8 @@ constexpr bool compact_epi(int epi) { return epi != EPI_F32; }
 // of one block when it has tiles, and the fill-clamp-refill split of the
 // launch's blocks; experts own consecutive block ranges in expert order.
 template <int EPI>
-__device__ void build_quota_plan(const GemmBatch& batch, int bm, int budget, QuotaPlan* qp) {
+__device__ void build_quota_plan(const GemmBatch& batch, int bm, int lsplit, int budget,
+                                 QuotaPlan* qp) {
     const int lane = threadIdx.x & 63;
     const GemmArgs& p0 = batch.p[0];
     const int E = p0.E;
@@ -299,7 +321,7 @@ __device__ void build_quota_plan(const GemmBatch& batch, int bm, int budget, Quo
     if (lane < E) {
         if constexpr (compact_epi(EPI)) {
             ne = min(ne, p0.M);
-            tiles = (ne + bm - 1) / bm * batch.tiles_n[0];
+            tiles = expert_mtiles(ne, bm, lsplit) * batch.tiles_n[0];
         } else {
             tiles = batch.tiles_m[0] * batch.tiles_n[0] +
                     (batch.total[1] > 0 ? batch.tiles_m[1] * batch.tiles_n[1] : 0);
@@ -829,6 +851,221 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& p, f32x16 (&acc)[T
     }
 }
 
+// Light tiles. A tile whose live rows fit one 32-row block (an expert with a
+// handful of rows under a skewed load) streams a BN-column weight panel over
+// the whole k range for a few products, so its time is that stream, and the
+// stage ring keeps only NS - 1 stages of it in flight. Such a tile skips the
+// ring: each wave streams its own share in 64-deep k groups, two groups in
+// flight in registers, every load a coalesced 128-byte piece of a row; a
+// group passes through a small LDS block of the wave's own to be read back
+// as fragments. The waves of the block split the tile's columns (whole wave
+// columns) and its k groups between them, and the waves of k slice 0 add the
+// other slices' sums in slice order (a fixed order) before the usual
+// epilogue of their one live row block.
+constexpr int kLightGroups = 2;  // 64-deep k groups in flight per wave
+
+// LDS-typed views of the stage buffers for the light path (a pointer selected
+// among the buffers at run time would otherwise become a flat pointer, whose
+// accesses wait on the vector-memory counter too)
+typedef __attribute__((address_space(3))) uint16_t lds_u16;
+typedef __attribute__((address_space(3))) v4i32 lds_v4;
+typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
+typedef __attribute__((address_space(3))) float lds_f32;
+
+template <class T, bool A_KMAJOR, bool B_KMAJOR, int EPI>
+constexpr bool light_ok() {
+    return A_KMAJOR && EPI != EPI_F32 && T::WN == 64;
+}
+
+// A light expert's tiles split into this many column parts (whole wave
+// columns each): one HBM stream per CU runs at a fraction of a CU's share of
+// the chip's bandwidth, so a light tile's weight panel is spread over CUs.
+template <class T>
+constexpr int light_parts() {
+    return T::WGN % 4 == 0 ? 4 : (T::WGN % 2 == 0 ? 2 : 1);
+}
+
+template <class T, class CFG, bool B_KMAJOR, int EPI, int GS>
+__device__ __forceinline__ void light_tile(const GemmArgs& p, __amdgpu_buffer_rsrc_t ra_rs,
+                                           __amdgpu_buffer_rsrc_t rb_rs, int e, int M, int N,
+                                           int K, int m0, int n0, int part, int nparts,
+                                           uint16_t* buf0, uint16_t* buf1, uint16_t* buf2,
+                                           uint16_t* buf3, uint16_t* buf4) {
+    constexpr int FM = T::FM, FN = T::FN, WN = T::WN, WGN = T::WGN, NS = T::NS;
+    constexpr int U = kLightGroups;
+    constexpr int LD = 64 + 8;          // LDS row: 64 elements + 16 bytes (rows on other banks)
+    constexpr int A_EL = 32 * LD;       // A block: 32 rows x 64 k
+    constexpr int B_EL = 64 * LD;       // B block: 64 n x 64 k (k-major) or 64 k x 64 n
+    constexpr int W_EL = A_EL + B_EL;   // one wave's LDS block
+    constexpr int WPB = (T::NW + NS - 1) / NS;  // waves per stage buffer
+    constexpr int PB = FN * 16 * 64;    // floats of one wave's partial sums
+    static_assert(WN == 64 && FN == 2, "light tiles: 64-column wave tiles");
+    static_assert(WPB * W_EL * 2 <= CFG::BUF_BYTES, "wave LDS blocks fit the stage buffers");
+    static_assert((T::NW - 1 + NS - 1) / NS * PB * 4 <= CFG::BUF_BYTES,
+                  "partial sums fit the stage buffers");
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    // the part's columns are `cols` wave columns; wave w takes column c and k
+    // slice sl of ks (slice 0 holds the sums)
+    const int cols = WGN / nparts, ks = T::NW / cols;
+    const int c = wave % cols, sl = wave / cols;
+    const int nb = n0 + (part * cols + c) * WN;  // the wave's first column
+    // the epilogue places wave w's columns at n0 + (w mod WGN) WN
+    const int wn = wave % WGN, n0w = nb - wn * WN;
+    // slice sl takes the 64-deep k groups [g0, g1); loads past klim read zeros
+    const int ng = (K + 63) / 64;
+    const int g0 = ng * sl / ks, g1 = ng * (sl + 1) / ks;
+    const int klim = min(K, g1 * 64);
+    // load i of a group: row (k-major) or k row (mn-major) 8 i + lane / 8,
+    // elements 8 (lane % 8) .. + 7 of its 64
+    const int lr = lane >> 3, lc = 8 * (lane & 7);
+    int arow[4];  // element offsets of the lane's A rows, -1 past M
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int mr = m0 + 8 * i + lr;
+        if constexpr (GS == 1) arow[i] = mr < M ? p.tok[e * p.tok_estride + mr] * p.a.ld : -1;
+        else arow[i] = mr < M ? mr * p.a.ld : -1;
+    }
+
+    uint4 ra[U][4], rb[U][8];
+    auto load = [&](int u, int g) {
+        const int k = g * 64 + lc;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            ra[u][i] = buf_load16(ra_rs, arow[i] >= 0 && k < klim
+                                             ? static_cast<uint32_t>(arow[i] + k) * 2u
+                                             : kOutOfRange);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            if constexpr (B_KMAJOR)
+                rb[u][i] = buf_load16(rb_rs, vec_off<true>(p.b.ld, nb + 8 * i + lr, N, k, klim));
+            else
+                rb[u][i] = buf_load16(rb_rs, vec_off<false>(p.b.ld, nb + lc, N, g * 64 + 8 * i + lr,
+                                                            klim));
+        }
+    };
+
+    BiasRegs<T, EPI> bias;
+    bias.load(p, e, N, n0w, wn, lane);
+    f32x16 lacc[FN];
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            float b4[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+            if constexpr (BiasRegs<T, EPI>::USED) {
+                if (sl == 0) {
+                    const uint2 bb = bias.v[j * 4 + q];
+                    b4[0] = bf16_to_f32(bb.x & 0xFFFFu);
+                    b4[1] = bf16_to_f32(bb.x >> 16);
+                    b4[2] = bf16_to_f32(bb.y & 0xFFFFu);
+                    b4[3] = bf16_to_f32(bb.y >> 16);
+                }
+            }
+#pragma unroll
+            for (int r = 0; r < 4; ++r) lacc[j][4 * q + r] = b4[r];
+        }
+
+    auto lds_buf = [&](int i) -> lds_u16* {
+        uint16_t* const b = i == 0 ? buf0 : i == 1 ? buf1 : i == 2 ? buf2 : i == 3 ? buf3 : buf4;
+        return (lds_u16*)(b);
+    };
+    // wave w's LDS block: stage buffer w mod NS, slot w / NS
+    lds_u16* const as = lds_buf(wave % NS) + (wave / NS) * W_EL;
+    lds_u16* const bs = as + A_EL;
+    // (group by group, as the loop refills them: each group then waits for its
+    // own loads only, also on the loop's first trip)
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        load(u, g0 + u);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    for (int g = g0; g < g1; g += U) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            // the group into the wave's LDS block (one wave's LDS accesses run
+            // in order: the previous group's fragment reads are done first)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                *reinterpret_cast<lds_v4*>(as + (8 * i + lr) * LD + lc) =
+                    __builtin_bit_cast(v4i32, ra[u][i]);
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+                *reinterpret_cast<lds_v4*>(bs + (8 * i + lr) * LD + lc) =
+                    __builtin_bit_cast(v4i32, rb[u][i]);
+            __builtin_amdgcn_sched_barrier(0);
+            // its registers refill with group g + u + U (past g1: out of range,
+            // no traffic), so U groups stay in flight
+            load(u, g + u + U);
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                const int kk = 16 * s + 8 * (lane >> 5);
+                const bf16x8 a = *reinterpret_cast<const lds_bf16x8*>(as + (lane & 31) * LD + kk);
+                bf16x8 b[FN];
+#pragma unroll
+                for (int j = 0; j < FN; ++j) {
+                    if constexpr (B_KMAJOR) {
+                        b[j] = *reinterpret_cast<const lds_bf16x8*>(bs + (32 * j + (lane & 31)) * LD +
+                                                                    kk);
+                    } else {
+                        // transposing reads of the [k][n] block: lane gets column
+                        // 32 j + lane % 32, k rows 16 s + 8 (lane / 32) + 0..7
+                        const int gq = lane >> 4, jj = lane & 15;
+                        const int kr = 16 * s + 8 * (gq >> 1) + (jj >> 2);
+                        const int n = 32 * j + 16 * (gq & 1) + 4 * (jj & 3);
+                        typedef __attribute__((address_space(3))) s16x4* lds_s16x4;
+                        const s16x4 lo =
+                            __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4)(bs + kr * LD + n));
+                        const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                            (lds_s16x4)(bs + (kr + 4) * LD + n));
+                        b[j] = __builtin_bit_cast(
+                            bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+                    }
+                }
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+                    lacc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[j], a, lacc[j], 0, 0, 0);
+            }
+        }
+    }
+
+    // slices 1.. park their sums (slot s = (sl - 1) cols + c: stage buffer s
+    // mod NS); every wave is past its LDS block first
+    auto slot = [&](int s) -> lds_f32* {
+        return reinterpret_cast<lds_f32*>(lds_buf(s % NS)) + (s / NS) * PB;
+    };
+    __syncthreads();
+    if (sl > 0) {
+        lds_f32* const dst = slot((sl - 1) * cols + c);
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) dst[(j * 16 + r) * 64 + lane] = lacc[j][r];
+    }
+    __syncthreads();
+    f32x16 acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+    if (sl == 0) {
+        for (int s = 1; s < ks; ++s) {
+            const lds_f32* const src = slot((s - 1) * cols + c);
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) lacc[j][r] += src[(j * 16 + r) * 64 + lane];
+        }
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[0][j] = lacc[j];
+    }
+    __syncthreads();  // the sums are read before the epilogue stages outputs over them
+    uint16_t* const ep = (uint16_t*)(lds_buf(wave % NS));  // (an LDS pointer, seen as such)
+    gemm_epilogue<T, CFG, EPI>(p, acc, buf0, ep, 0.0f, false, e, M, N, m0, n0w, sl == 0 ? 1 : 0);
+}
+
 // One BM x BN output tile of expert e per block of WGM x WGN waves, each
 // (BM/WGM) x (BN/WGN) as 32 x 32 MFMA blocks; tiles are dealt to the 8 XCDs
 // in chunks of neighbouring tiles (shared operand panels in each XCD's L2).
@@ -878,10 +1115,18 @@ void gemm_bf16_kernel(GemmBatch batch) {
     __shared__ uint32_t tok_s[GATHER == 2 ? kGatherRows + 2 * NS * KB : 1];
 
     const int b = blockIdx.x;
+    // column parts of a light expert's tiles: at most the expert's m-tile
+    // slots of the grid (ceil(capacity / BM)), so the live tiles still fit it
+    // (the d-wide row GEMMs: a few long tiles per expert; the f-wide ones have
+    // many short light tiles already)
+    const int lsplit = light_ok<T, A_KMAJOR, B_KMAJOR, EPI>() && (EPI == EPI_BIAS || EPI == EPI_STORE)
+                           ? min(light_parts<T>(), (batch.p[0].M + BM_ - 1) / BM_)
+                           : 1;
     int qe = 0, qu = 0, qn = 0, qt = 0, qne = 0;  // quota: expert, rank, units, tiles, rows
     if constexpr (SCHED == 1) {
         __shared__ QuotaPlan qp;
-        if (threadIdx.x < 64) build_quota_plan<EPI>(batch, BM_, static_cast<int>(gridDim.x), &qp);
+        if (threadIdx.x < 64)
+            build_quota_plan<EPI>(batch, BM_, lsplit, static_cast<int>(gridDim.x), &qp);
         __syncthreads();
         const int lane = threadIdx.x & 63;
         const int end = qp.first[lane] + qp.units[lane];
@@ -902,7 +1147,7 @@ void gemm_bf16_kernel(GemmBatch batch) {
         e = qe;
         ne = qne;
         if constexpr (compact_tiles<EPI>()) {
-            tiles_m = (ne + BM_ - 1) / BM_;
+            tiles_m = expert_mtiles(ne, BM_, lsplit);
         } else {
             const int t0 = batch.tiles_m[0] * batch.tiles_n[0];
             prob = r >= t0 ? 1 : 0;
@@ -917,16 +1162,20 @@ void gemm_bf16_kernel(GemmBatch batch) {
     const int l = b >> 3, chunk = batch.chunk;
     int w = ((l / chunk) * 8 + (b & 7)) * chunk + l % chunk;
     if constexpr (EPI == EPI_BIAS || EPI == EPI_STORE) {
-        if (!spread_tile(batch, BM_, (l / chunk) * 8 + (b & 7), l % chunk, &e, &r, &ne)) return;
-        tiles_m = (ne + BM_ - 1) / BM_;
+        const bool in = lsplit > 1
+                            ? spread_tile(batch, BM_, lsplit, b & 7, l, 0, &e, &r, &ne)
+                            : spread_tile(batch, BM_, lsplit, b & 7, (l / chunk) * 8 + (b & 7),
+                                          l % chunk, &e, &r, &ne);
+        if (!in) return;
+        tiles_m = expert_mtiles(ne, BM_, lsplit);
     } else if constexpr (compact_tiles<EPI>()) {
         LiveTile lt;
         const GemmArgs& p0 = batch.p[0];
-        if (!live_tile(p0.counts, p0.G, p0.E, p0.M, BM_, batch.tiles_n[0], w, &lt)) return;
+        if (!live_tile(p0.counts, p0.G, p0.E, p0.M, BM_, lsplit, batch.tiles_n[0], w, &lt)) return;
         e = lt.e;
         r = lt.r;
         ne = lt.ne;
-        tiles_m = (ne + BM_ - 1) / BM_;
+        tiles_m = expert_mtiles(ne, BM_, lsplit);
     } else {
         if (w >= batch.total[0] + batch.total[1]) return;
         prob = w >= batch.total[0] ? 1 : 0;  // uniform per block
@@ -959,7 +1208,9 @@ void gemm_bf16_kernel(GemmBatch batch) {
     const int M = p.var_k ? p.M : min(ne, p.M);
     const int K = p.var_k ? ne : p.K;
     const int N = p.N;
-    const int m0 = tm * BM_, n0 = tn * BN_;
+    // a light expert's m-tile index is its column part
+    const bool parts = lsplit > 1 && !p.var_k && ne > 0 && ne <= 32;
+    const int m0 = parts ? 0 : tm * BM_, n0 = tn * BN_;
     if (m0 >= M) return false;
 
     static_assert(GS == 0 || (GS == 1 && A_KMAJOR) || (GS == 2 && !B_KMAJOR),
@@ -973,6 +1224,14 @@ void gemm_bf16_kernel(GemmBatch batch) {
         GS == 2 ? make_rsrc(p.b.base, p.gather_bytes)
            : make_rsrc(static_cast<const uint16_t*>(p.b.base) + e * p.b.estride,
                        p.b.estride * 2);
+    if constexpr (light_ok<T, A_KMAJOR, B_KMAJOR, EPI>()) {
+        if (!p.var_k && __builtin_amdgcn_readfirstlane(M - m0) <= 32) {
+            light_tile<T, CFG, B_KMAJOR, EPI, GS>(p, ra_rs, rb_rs, e, M, N, K, m0, n0,
+                                                   parts ? tm : 0, parts ? lsplit : 1, buf0,
+                                                   buf1, buf2, buf3, buf4);
+            return true;
+        }
+    }
     // Gathered A rows (the tile's rows, fixed over the k loop): each lane's
     // row offsets in x, read once. Gathered B k rows (new ones every stage):
     // the expert's token list in LDS, each lane's offsets for the next

@@ -77,6 +77,15 @@ struct Rows {
     }
 };
 
+// Whether token t keeps any of its k assignments (a dropped one has slot -1).
+// Under a skewed load most tokens keep none: the moves then skip their rows.
+__device__ __forceinline__ bool keeps_any(const RouteMeta& m, int t) {
+    const int32_t* s = m.slot + static_cast<size_t>(t) * m.k;
+    bool any = false;
+    for (int j = 0; j < m.k; ++j) any = any || s[j] >= 0;
+    return any;
+}
+
 // Flat element-wise mapping for the row moves without a reduction: item i is
 // 16-byte vector v = i mod nvec of token t = i / nvec, so consecutive lanes
 // touch consecutive bytes of a row and every lane is busy whatever d is. Each
@@ -97,10 +106,13 @@ __global__ __launch_bounds__(kBlock) void dispatch_kernel(const T* __restrict__ 
     uint4* dst = reinterpret_cast<uint4*>(xe);
     static_assert(kItems == 2, "two items per thread");
     const long long ia = min(i0, total - 1), ib = min(i0 + kBlock, total - 1);
-    const uint4 va = src[ia], vb = src[ib];
     const int ta = static_cast<int>(ia / nvec), tb = static_cast<int>(ib / nvec);
     const int ca = static_cast<int>(ia - static_cast<long long>(ta) * nvec);
     const int cb = static_cast<int>(ib - static_cast<long long>(tb) * nvec);
+    // the row of x is read only when some assignment of its token is kept
+    uint4 va = make_uint4(0u, 0u, 0u, 0u), vb = va;
+    if (keeps_any(m, ta)) va = src[ia];
+    if (keeps_any(m, tb)) vb = src[ib];
     for (int j0 = 0; j0 < m.k; j0 += kJ) {
         Rows<kJ> ra, rb;
         ra.fetch(m, ta, j0);
@@ -176,9 +188,15 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void combine_bwd_kernel(
     T* __restrict__ dye, float* __restrict__ dgate, RouteMeta m, int nvec) {
     constexpr int VN = Vec<T>::n;
     constexpr int NV = 2;  // vectors per lane per pass: rows up to 128 vectors in one pass
-    const int t = blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+    const int t = blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
     if (t >= m.N) return;
+    // a token that keeps no assignment has zero gate gradients and no dye
+    // rows: its dy row is not read
+    if (!keeps_any(m, t)) {
+        for (int j = lane; j < m.k; j += 64) dgate[static_cast<size_t>(t) * m.k + j] = 0.0f;
+        return;
+    }
     const uint4* g_dy = reinterpret_cast<const uint4*>(dy) + static_cast<size_t>(t) * nvec;
     for (int v0 = 0; v0 < nvec; v0 += 64 * NV) {
         uint4 a[NV];

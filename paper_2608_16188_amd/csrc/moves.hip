@@ -93,7 +93,6 @@ __device__ __forceinline__ bool keeps_any(const RouteMeta& m, int t) {
 // then metadata) is issued before the first store.
 constexpr int kBlock = 256;
 constexpr int kItems = 2;
-constexpr int kCItems = 1;  // combine: one item per thread
 // J: assignments per pass (2 when k <= 2, else 4; larger k loops)
 
 template <typename T, int kJ>
@@ -126,57 +125,59 @@ __global__ __launch_bounds__(kBlock) void dispatch_kernel(const T* __restrict__ 
 }
 
 // y[t] = sum over kept j (ascending) of gate[t, j] ye[row(t, j)], f32 sums.
+// One wave per token: its routing metadata is read once per wave, and a
+// token that keeps no assignment (most of them under a skewed load) writes
+// its zero row right after that.
 template <typename T, int kJ>
-__global__ __launch_bounds__(kBlock) void combine_fwd_kernel(const T* __restrict__ ye,
-                                                             const float* __restrict__ gate,
-                                                             T* __restrict__ y, RouteMeta m,
-                                                             int nvec) {
+__global__ __launch_bounds__(64 * kWavesPerBlock) void combine_fwd_kernel(
+    const T* __restrict__ ye, const float* __restrict__ gate, T* __restrict__ y, RouteMeta m,
+    int nvec) {
     constexpr int VN = Vec<T>::n;
-    const long long total = static_cast<long long>(m.N) * nvec;
-    const long long i0 = static_cast<long long>(blockIdx.x) * kBlock * kCItems + threadIdx.x;
+    constexpr int NV = 2;  // vectors per lane per pass: rows up to 128 vectors in one pass
+    const int t = blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    if (t >= m.N) return;
     const uint4* src = reinterpret_cast<const uint4*>(ye);
-    uint4* dst = reinterpret_cast<uint4*>(y);
-    long long it[kCItems];
-    int tt[kCItems], cc[kCItems];
-    float acc[kCItems][VN];
+    uint4* g_y = reinterpret_cast<uint4*>(y) + static_cast<size_t>(t) * nvec;
+    for (int v0 = 0; v0 < nvec; v0 += 64 * NV) {
+        float acc[NV][VN];
 #pragma unroll
-    for (int u = 0; u < kCItems; ++u) {
-        it[u] = min(i0 + u * kBlock, total - 1);
-        tt[u] = static_cast<int>(it[u] / nvec);
-        cc[u] = static_cast<int>(it[u] - static_cast<long long>(tt[u]) * nvec);
+        for (int q = 0; q < NV; ++q)
 #pragma unroll
-        for (int q = 0; q < VN; ++q) acc[u][q] = 0.0f;
-    }
-    for (int j0 = 0; j0 < m.k; j0 += kJ) {
-        Rows<kJ> rows[kCItems];
-        float gj[kCItems][kJ];
-        uint4 r[kCItems][kJ];
-#pragma unroll
-        for (int u = 0; u < kCItems; ++u) {
-            rows[u].fetch(m, tt[u], j0);
-#pragma unroll
-            for (int jj = 0; jj < kJ; ++jj)
-                gj[u][jj] = gate[static_cast<size_t>(tt[u]) * m.k + min(j0 + jj, m.k - 1)];
-        }
-#pragma unroll
-        for (int u = 0; u < kCItems; ++u)
-#pragma unroll
-            for (int jj = 0; jj < kJ; ++jj)
-                if (rows[u].r[jj] >= 0) r[u][jj] = src[rows[u].r[jj] * nvec + cc[u]];
-#pragma unroll
-        for (int u = 0; u < kCItems; ++u)
+            for (int i = 0; i < VN; ++i) acc[q][i] = 0.0f;
+        for (int j0 = 0; j0 < m.k; j0 += kJ) {
+            Rows<kJ> rows;
+            rows.fetch(m, t, j0);
+            float gj[kJ];
+            uint4 r[kJ][NV];
 #pragma unroll
             for (int jj = 0; jj < kJ; ++jj) {
-                if (rows[u].r[jj] < 0) continue;
-                float f[VN];
-                Vec<T>::unpack(r[u][jj], f);
+                gj[jj] = gate[static_cast<size_t>(t) * m.k + min(j0 + jj, m.k - 1)];
+                if (rows.r[jj] >= 0)
 #pragma unroll
-                for (int q = 0; q < VN; ++q) acc[u][q] = __builtin_fmaf(gj[u][jj], f[q], acc[u][q]);
+                    for (int q = 0; q < NV; ++q) {
+                        const int v = v0 + lane + 64 * q;
+                        if (v < nvec) r[jj][q] = src[rows.r[jj] * nvec + v];
+                    }
             }
-    }
 #pragma unroll
-    for (int u = 0; u < kCItems; ++u)
-        if (i0 + u * kBlock < total) dst[it[u]] = Vec<T>::pack(acc[u]);
+            for (int jj = 0; jj < kJ; ++jj) {
+                if (rows.r[jj] < 0) continue;
+#pragma unroll
+                for (int q = 0; q < NV; ++q) {
+                    float f[VN];
+                    Vec<T>::unpack(r[jj][q], f);
+#pragma unroll
+                    for (int i = 0; i < VN; ++i) acc[q][i] = __builtin_fmaf(gj[jj], f[i], acc[q][i]);
+                }
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < NV; ++q) {
+            const int v = v0 + lane + 64 * q;
+            if (v < nvec) g_y[v] = Vec<T>::pack(acc[q]);
+        }
+    }
 }
 
 // One wave per token (the dot products reduce across the row): the token's dy
@@ -359,14 +360,14 @@ vmoe_status combine_fwd_launch(const Dims& D, const void* ye, const int32_t* idx
     if (D.N == 0) return VMOE_OK;
     const RouteMeta m = meta(D, idx, slot, row_base);
     const int nvec = D.d / (D.dtype == VMOE_BF16 ? 8 : 4);
-    const unsigned grid = cdiv(static_cast<long long>(D.N) * nvec, kBlock * kCItems);
+    const unsigned grid = cdiv(D.N, kWavesPerBlock);  // one wave per token
     auto go = [&](auto jc) {
         constexpr int J = decltype(jc)::value;
         if (D.dtype == VMOE_BF16)
-            combine_fwd_kernel<uint16_t, J><<<grid, kBlock, 0, st>>>(
+            combine_fwd_kernel<uint16_t, J><<<grid, 64 * kWavesPerBlock, 0, st>>>(
                 static_cast<const uint16_t*>(ye), gate, static_cast<uint16_t*>(y), m, nvec);
         else
-            combine_fwd_kernel<float, J><<<grid, kBlock, 0, st>>>(
+            combine_fwd_kernel<float, J><<<grid, 64 * kWavesPerBlock, 0, st>>>(
                 static_cast<const float*>(ye), gate, static_cast<float*>(y), m, nvec);
     };
     if (D.k <= 2) go(std::integral_constant<int, 2>{});

@@ -36,6 +36,8 @@ CASES = [
                     capacity_factor=1.0, n_groups=2, router_std=0.3),
     W.custom_config("bf16_ten_mtiles_g", n_tokens=2400, d_model=72, d_ff=264, n_experts=2, k=2,
                     capacity_factor=1.0, router_std=0.05),
+    W.custom_config("bf16_light_tails_g", n_tokens=2240, d_model=200, d_ff=520, n_experts=16,
+                    k=2, capacity_factor=1.0, hot_experts=2, hot_offset=0.8),
 ]
 OUTS = ("a", "a_grad", "ye", "y", "dye", "dgate", "dh", "dxe", "dw1", "db1", "dw2", "db2", "dx",
         "dw_router")

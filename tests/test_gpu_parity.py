@@ -197,6 +197,12 @@ SMALL = [
     # each class)
     W.custom_config("bf16_two_classes", n_tokens=2000, d_model=72, d_ff=264, n_experts=8, k=2,
                     capacity_factor=1.0, hot_experts=2, hot_offset=2.0, router_std=0.1),
+    # light experts: two experts full at 280 rows (a 24-row last m-tile), the
+    # other 14 with 15-47 rows (most within one 32-row block), so the light
+    # tiles' register-streamed path runs, with its column parts in the d-wide
+    # GEMMs, beside the stage ring; k and n ragged (d 200, f 520)
+    W.custom_config("bf16_light_tails", n_tokens=2240, d_model=200, d_ff=520, n_experts=16, k=2,
+                    capacity_factor=1.0, hot_experts=2, hot_offset=0.8),
 ]
 
 

@@ -872,6 +872,19 @@ typedef __attribute__((address_space(3))) v4i32 lds_v4;
 typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
 typedef __attribute__((address_space(3))) float lds_f32;
 
+// Stage buffer i of NS as an LDS pointer (a select over values: a closure or
+// array of the buffers' addresses would sit in scratch memory)
+template <int NS>
+__device__ __forceinline__ lds_u16* pick_lds(int i, uint16_t* b0, uint16_t* b1, uint16_t* b2,
+                                             uint16_t* b3, uint16_t* b4) {
+    uint16_t* b = b0;
+    if (NS > 1 && i == 1) b = b1;
+    if (NS > 2 && i == 2) b = b2;
+    if (NS > 3 && i == 3) b = b3;
+    if (NS > 4 && i == 4) b = b4;
+    return (lds_u16*)(b);
+}
+
 template <class T, bool A_KMAJOR, bool B_KMAJOR, int EPI>
 constexpr bool light_ok() {
     return A_KMAJOR && EPI != EPI_F32 && T::WN == 64;
@@ -965,10 +978,7 @@ __device__ __forceinline__ void light_tile(const GemmArgs& p, __amdgpu_buffer_rs
             for (int r = 0; r < 4; ++r) lacc[j][4 * q + r] = b4[r];
         }
 
-    auto lds_buf = [&](int i) -> lds_u16* {
-        uint16_t* const b = i == 0 ? buf0 : i == 1 ? buf1 : i == 2 ? buf2 : i == 3 ? buf3 : buf4;
-        return (lds_u16*)(b);
-    };
+    auto lds_buf = [=](int i) { return pick_lds<NS>(i, buf0, buf1, buf2, buf3, buf4); };
     // wave w's LDS block: stage buffer w mod NS, slot w / NS
     lds_u16* const as = lds_buf(wave % NS) + (wave / NS) * W_EL;
     lds_u16* const bs = as + A_EL;

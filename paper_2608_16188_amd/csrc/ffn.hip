@@ -327,7 +327,9 @@ __device__ void build_quota_plan(const GemmBatch& batch, int bm, int lsplit, int
                     (batch.total[1] > 0 ? batch.tiles_m[1] * batch.tiles_n[1] : 0);
         }
     }
-    const double coef = static_cast<double>(tiles) * tile_work<EPI>(ne, bm);
+    // (a light expert's column parts each carry a share of one tile's stream)
+    const bool parts = lsplit > 1 && ne > 0 && ne <= 32;
+    const double coef = static_cast<double>(tiles) * tile_work<EPI>(ne, bm) / (parts ? lsplit : 1);
     const int units = fill_clamp_refill_wave(E, tiles > 0 ? 1 : 0, tiles, coef, budget);
     int incl = units;
 #pragma unroll

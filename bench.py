@@ -41,23 +41,26 @@ CALLS = ["route", "dispatch", "ffn_fwd", "combine_fwd", "combine_bwd", "ffn_bwd"
          "dispatch_route_bwd"]
 
 
-def algorithmic_cost(cfg, A: int, n_noise: bool, n_bias: bool):
+def algorithmic_cost(cfg, A: int, n_noise: bool, n_bias: bool, NK: int = -1):
     """Per-call algorithmic (flops, bytes): only what the definition must touch.
 
-    A = kept assignments. Bytes count each tensor once at its storage width;
+    A = kept assignments, NK = tokens that keep at least one (their rows of
+    x and dy are the only ones dispatch and combine backward need; default
+    every token). Bytes count each tensor once at its storage width;
     workspace, sort passes and re-reads are overhead, not algorithmic.
     """
     N, d, f, E, k, G = cfg.n_tokens, cfg.d_model, cfg.d_ff, cfg.n_experts, cfg.k, cfg.n_groups
     B = 2 if cfg.dtype == "bf16" else 4
+    NK = N if NK < 0 else NK
     meta = N * k * 4 * 2 + G * E * 4  # idx + slot, row_base
     c = {}
     c["route"] = (2 * N * d * E, N * d * B + G * E * d * B + N * E * 4 * (2 + (1 if n_noise else 0))
                   + N * k * 12 + N * 4 + G * E * 8)
-    c["dispatch"] = (0, N * d * B + A * d * B + meta)
+    c["dispatch"] = (0, NK * d * B + A * d * B + meta)
     c["ffn_fwd"] = (4 * A * d * f, 2 * E * d * f * B + E * (d + f) * B + A * d * B + 2 * A * f * B
                     + A * d * B)
     c["combine_fwd"] = (2 * A * d, A * d * B + N * d * B + meta + N * k * 4)
-    c["combine_bwd"] = (2 * A * d, N * d * B + 2 * A * d * B + meta + N * k * 8)
+    c["combine_bwd"] = (2 * A * d, NK * d * B + 2 * A * d * B + meta + N * k * 8)
     c["ffn_bwd"] = (8 * A * d * f, 2 * E * d * f * B + A * d * B + 2 * A * f * B + A * d * B
                     + A * f * B + A * d * B + E * (2 * d * f + d + f) * 4)
     c["dispatch_bwd"] = (0, A * d * B + N * d * 4 + meta)
@@ -419,7 +422,8 @@ def main():
 
     counts = L.counts.cpu().numpy()
     A = int(counts.sum())
-    cost = algorithmic_cost(cfg, A, L.noise is not None, L.logit_bias is not None)
+    NK = int((L.slot.view(cfg.n_tokens, cfg.k) >= 0).any(dim=1).sum().item())
+    cost = algorithmic_cost(cfg, A, L.noise is not None, L.logit_bias is not None, NK)
     peak_mfma = PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_F32_TFLOPS
     fl, by = cost[dom]
     ach = fl / (dom_ms * 1e-3) / 1e12

@@ -639,8 +639,11 @@ struct GemmCfg {
     // Epilogue staging: wave w parks its outputs in stage buffer w mod NS; IPP
     // of its FM 32-row blocks per pass, all outputs of those rows at once when
     // they fit (a second output pass would recompute the activation).
-    static constexpr int EP_LD = T::WN + 4;
+    // staged rows padded by 16 bytes: 16-byte aligned for the row reads (a
+    // 136-byte bf16 row left every other row's reads misaligned, which the
+    // LDS serves with stalls) and off the banks of the row above
     static constexpr int ELEM = F32_OUT ? 4 : 2;
+    static constexpr int EP_LD = T::WN + 16 / ELEM;
     static constexpr int EP_ROWBLK = 32 * EP_LD * ELEM;
     static constexpr int WAVES_PER_BUF = (T::NW + T::NS - 1) / T::NS;
     static constexpr bool fits(int outs, int blocks) {

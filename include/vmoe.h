@@ -351,9 +351,9 @@ size_t vmoe_balance_loss_workspace_bytes(const vmoe_shape* shape);
  *   losses [G, 2], dlogits [N, E] f32 out; importance, load [G, E] f32 out
  *   or NULL; workspace: vmoe_balance_loss_workspace_bytes(shape) bytes.
  * Sums over tokens are f32 within a chunk of tokens and double across chunks
- * in chunk order (deterministic); the chunk is 256 tokens for E <= 16, 128
- * for E <= 32 and 64 for E <= 64. VMOE_ERR_INVALID_ARG for a non-positive or
- * non-finite noise_std or non-finite weights. */
+ * in chunk order (deterministic); the chunk is 256 tokens for E <= 8, 64 for
+ * E <= 16, 32 for E <= 32 and 16 for E <= 64. VMOE_ERR_INVALID_ARG for a
+ * non-positive or non-finite noise_std or non-finite weights. */
 vmoe_status vmoe_balance_loss(const vmoe_shape* shape, const float* logits,
                               const float* logit_bias, const float* noise, const float* probs,
                               float noise_std, float w_importance, float w_load, float* losses,

@@ -227,7 +227,7 @@ __global__ __launch_bounds__(256) void router_mfma_kernel(
     uint2* __restrict__ kpart, int Ng, int d, int E, int k, int logits_in) {
     // partial products, then z and the exp terms: one row per token (padded)
     constexpr int RW = WIDE ? kMaxExperts + 1 : 33;
-    __shared__ float red[4][kMfmaTokens][RW];
+    __shared__ __attribute__((aligned(16))) float red[4][kMfmaTokens][RW];
     const int g = blockIdx.y;
     const int t0 = blockIdx.x * kMfmaTokens;
     const int ntok = min(kMfmaTokens, Ng - t0);
@@ -242,36 +242,66 @@ __global__ __launch_bounds__(256) void router_mfma_kernel(
         const int per = (ksteps + 3) / 4;
         const int s0 = wave * per, s1 = min(ksteps, s0 + per);
         const int m = lane & 31, kh = (lane >> 5) * 8;
-        // 16-byte vector (row r, columns k..k+7), zero outside the rows / past d
-        auto off = [&](int r, int rows, int kk) {
-            return (r < rows && kk < d) ? static_cast<uint32_t>(r * d + kk) * 2u : kOutOfRange;
-        };
         f32x16_r acc0, acc1;
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc0[r] = acc1[r] = 0.0f;
-        // eight k-steps in flight per round
+        // eight k-steps in flight per round. The tokens' x rows arrive as
+        // coalesced 128-byte pieces (load i: row 8 i + lane / 8, elements
+        // 8 (lane % 8) .. + 7 of a 64-deep group) and pass through this wave's
+        // slice of `red` (free until the products are done; 16-byte chunks
+        // XOR-swizzled by row so the fragment reads miss no bank) to become
+        // the same fragments a direct load would give; the router rows are
+        // read straight into fragments (few, and shared by every block in L2).
+        const int klim = min(d, s1 * 16);
+        // 16-byte vector (row r, columns kk..kk+7), zero outside the rows or
+        // past this wave's k range
+        auto offk = [&](int r, int rows, int kk) {
+            return (r < rows && kk < klim) ? static_cast<uint32_t>(r * d + kk) * 2u : kOutOfRange;
+        };
+        typedef __attribute__((address_space(3))) v4i32 lds_v4;
+        lds_v4* const stage = (lds_v4*)(&red[wave][0][0]);  // 32 rows x 8 chunks of 16 bytes
+        static_assert(kMfmaTokens * 64 * 2 <= kMfmaTokens * RW * 4, "a row group fits the slice");
         constexpr int U = 8;
         for (int s = s0; s < s1; s += U) {
-            uint4 av[U], bv0[U], bv1[U];
+            uint4 ax[2][4], bv0[U], bv1[U];
+#pragma unroll
+            for (int gi = 0; gi < 2; ++gi)
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    ax[gi][i] = buf_load16(rx, offk(8 * i + (lane >> 3), ntok,
+                                                    (s + 4 * gi) * 16 + 8 * (lane & 7)));
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 const int kk = (s + u) * 16 + kh;
-                const bool live = s + u < s1;
-                av[u] = buf_load16(rx, live ? off(m, ntok, kk) : kOutOfRange);
-                bv0[u] = buf_load16(rw, live ? off(m, E, kk) : kOutOfRange);
-                if constexpr (WIDE) bv1[u] = buf_load16(rw, live ? off(32 + m, E, kk) : kOutOfRange);
+                bv0[u] = buf_load16(rw, offk(m, E, kk));
+                if constexpr (WIDE) bv1[u] = buf_load16(rw, offk(32 + m, E, kk));
             }
             // keep every load of the round ahead of the first MFMA (the
             // scheduler would otherwise interleave them, two loads in flight)
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const bf16x8_r a = __builtin_bit_cast(bf16x8_r, av[u]);
-                acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                    __builtin_bit_cast(bf16x8_r, bv0[u]), a, acc0, 0, 0, 0);
-                if constexpr (WIDE)
-                    acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                        __builtin_bit_cast(bf16x8_r, bv1[u]), a, acc1, 0, 0, 0);
+            for (int gi = 0; gi < 2; ++gi) {
+                // one wave's LDS accesses run in order: the previous group's
+                // fragment reads are done before these writes
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int r = 8 * i + (lane >> 3);
+                    stage[r * 8 + ((lane & 7) ^ (r & 7))] = __builtin_bit_cast(v4i32, ax[gi][i]);
+                }
+                bf16x8_r af[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int c = 2 * q + (lane >> 5);
+                    af[q] = __builtin_bit_cast(bf16x8_r, stage[m * 8 + (c ^ (m & 7))]);
+                }
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                        __builtin_bit_cast(bf16x8_r, bv0[4 * gi + q]), af[q], acc0, 0, 0, 0);
+                    if constexpr (WIDE)
+                        acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                            __builtin_bit_cast(bf16x8_r, bv1[4 * gi + q]), af[q], acc1, 0, 0, 0);
+                }
             }
         }
         // register 4q + r of lane l: token l % 32, expert 8q + 4 (l / 32) + r (+ 32)

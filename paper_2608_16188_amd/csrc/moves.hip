@@ -110,8 +110,12 @@ __global__ __launch_bounds__(kBlock) void dispatch_kernel(const T* __restrict__ 
     const int cb = static_cast<int>(ib - static_cast<long long>(tb) * nvec);
     // the row of x is read only when some assignment of its token is kept
     uint4 va = make_uint4(0u, 0u, 0u, 0u), vb = va;
-    if (keeps_any(m, ta)) va = src[ia];
-    if (keeps_any(m, tb)) vb = src[ib];
+    const bool ka = keeps_any(m, ta), kb = keeps_any(m, tb);
+    if (ka) va = src[ia];
+    if (kb) vb = src[ib];
+    // neither token keeps an assignment: no row to write, so no second round
+    // of routing loads (expert, row base) either
+    if (!ka && !kb) return;
     for (int j0 = 0; j0 < m.k; j0 += kJ) {
         Rows<kJ> ra, rb;
         ra.fetch(m, ta, j0);

@@ -595,7 +595,7 @@ __global__ __launch_bounds__(512) void route_bwd_mma_kernel(
     const uint16_t* __restrict__ x, const uint16_t* __restrict__ wr,
     const float* __restrict__ dz, const int32_t* __restrict__ rows,
     const uint16_t* __restrict__ dxe, float* __restrict__ dx, float* __restrict__ partial,
-    int Ng, int d, int E, int k, int nch) {
+    int Ng, int d, int E, int k, int nch, int has_rows) {
     constexpr int TCH = kRbTok, COLS = kRbCols, DZLD = EMAX + 1, WLD = EMAX + 8;
     constexpr int KS = EMAX / 16;  // k-steps of the dx product
     __shared__ __attribute__((aligned(16))) float dzs[TCH * DZLD];
@@ -612,11 +612,15 @@ __global__ __launch_bounds__(512) void route_bwd_mma_kernel(
     const int rw = wave & 3;
     constexpr int NJ = COLS / 32;
     constexpr int NT = 512;
-    constexpr int DZV = TCH * EMAX / NT;      // dz values per thread
+    // the per-chunk dz and x tiles are loaded and staged by the 256 threads
+    // of the router-gradient waves (the dx waves' registers hold their
+    // products and incoming dxe rows)
+    constexpr int NTT = 256;
+    constexpr int DZV = TCH * EMAX / NTT;     // dz values per loading thread
     constexpr int WV = EMAX * COLS / 8 / NT;  // 16-byte W vectors per thread
-    constexpr int XV = TCH * COLS / 8 / NT;   // 16-byte x vectors per thread
-    static_assert(DZV * NT == TCH * EMAX && WV * NT * 8 == EMAX * COLS &&
-                      XV * NT * 8 == TCH * COLS, "tiles split evenly over the threads");
+    constexpr int XV = TCH * COLS / 8 / NTT;  // 16-byte x vectors per loading thread
+    static_assert(DZV * NTT == TCH * EMAX && WV * NT * 8 == EMAX * COLS &&
+                      XV * NTT * 8 == TCH * COLS, "tiles split evenly over the threads");
     // the block's W columns, the same for every chunk it takes: staged once
     // (transposed to [column][expert]); the first chunk's barrier publishes it
     {
@@ -639,178 +643,249 @@ __global__ __launch_bounds__(512) void route_bwd_mma_kernel(
             }
         }
     }
-    // one set of accumulators, two roles: a dx wave's products of the
-    // current chunk, a dW wave's router-gradient partial over all its chunks
+    // The token chunks blockIdx.x, blockIdx.x + gridDim.x, ... of the group,
+    // in order, software-pipelined: the next chunk's dz and x tiles (and the
+    // fused call's row indices) are requested before this chunk's products,
+    // the dx waves' incoming values right after this chunk's dx rows are
+    // written, so a chunk's load latency hides behind the previous chunk's
+    // work. Every load and store in the loops is unconditional (clamped
+    // addresses with the value selected afterwards, buffer stores that drop
+    // out-of-range offsets; the last chunk's prefetch repeats it), so the
+    // compiler's wait counts are exact and leave the prefetched loads in
+    // flight. Waves 0-3 form dx; waves 4-7 load and stage the tiles and form
+    // the router-gradient partial; each role runs a loop of its own with the
+    // same two LDS barriers per chunk.
     constexpr int MB = EMAX / 32;
-    constexpr int NA = NJ > MB ? NJ : MB;
-    f32x16_r acc[NA];
-#pragma unroll
-    for (int b = 0; b < NA; ++b)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) acc[b][i] = 0.0f;
-
-    // chunks blockIdx.x, blockIdx.x + gridDim.x, ... of the group, in order
-    for (int c = blockIdx.x; c < nch; c += gridDim.x) {
-    const int t0 = c * TCH;
-    const int ntok = min(TCH, Ng - t0);
-    const size_t tok0 = static_cast<size_t>(g) * Ng + t0;
-    // the dx rows of a dx wave's lane: tokens [32 w, 32 w + 32) of the chunk;
-    // register 4 q + r of lane l will hold token 32 w + l % 32, column
-    // 32 j + 8 q + 4 (l / 32) + r
-    const int tl = 32 * rw + m;
-    const bool tok_ok = tl < ntok;
-    const size_t trow = (tok0 + min(tl, ntok - 1)) * d;
-    // stage 1, all requested before any is used, in this order (the waits
-    // count in issue order): (fused) the token's expert-buffer rows; the dz
-    // rows and x rows of the tiles, zero past the chunk, the experts or d;
-    // then the incoming value of each dx element, dx itself or (fused) the
-    // kept dxe rows, which stay in flight through the staging and the products
-    int rr[KJ > 0 ? KJ : 1];
-    if constexpr (KJ > 0) {
-#pragma unroll
-        for (int jj = 0; jj < KJ; ++jj)
-            rr[jj] = (dx_wave && jj < k) ? rows[(tok0 + min(tl, ntok - 1)) * k + jj] : -1;
-    }
+    const int tt = tid - NTT;  // a router-gradient wave's thread: 0 .. 255
     float dzv[DZV];
     uint4 xv[XV];
+    // stage 1 of chunk c (router-gradient waves): this thread's share of the
+    // dz and x tiles, zero past the chunk, the experts or d (buffer loads over
+    // the chunk's rows: rows past it, and offsets set out of range for
+    // experts past E or columns past d, read zeros)
+    auto load_tiles = [&](int c) {
+        const int t0 = c * TCH;
+        const int ntok = min(TCH, Ng - t0);
+        const size_t tok0 = static_cast<size_t>(g) * Ng + t0;
+        const __amdgpu_buffer_rsrc_t rz =
+            make_rsrc(dz + tok0 * E, static_cast<long long>(ntok) * E * 4);
 #pragma unroll
-    for (int u = 0; u < DZV; ++u) {
-        const int q = u * NT + tid, r = q / EMAX, e = q % EMAX;
-        dzv[u] = (r < ntok && e < E) ? dz[(tok0 + r) * E + e] : 0.0f;
-    }
-    if constexpr (DW) {
-#pragma unroll
-        for (int u = 0; u < XV; ++u) {
-            const int q = u * NT + tid, r = q / (COLS / 8), col = c0 + (q % (COLS / 8)) * 8;
-            xv[u] = (r < ntok && col < d)
-                        ? *reinterpret_cast<const uint4*>(x + (tok0 + r) * d + col)
-                        : make_uint4(0u, 0u, 0u, 0u);
+        for (int u = 0; u < DZV; ++u) {
+            const int q = u * NTT + tt, r = q / EMAX, e = q % EMAX;
+            const uint32_t off = e < E ? static_cast<uint32_t>(r * E + e) * 4u : kOutOfRange;
+            dzv[u] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rz, off, 0, 0));
         }
-    }
-    float4 dxin[KJ == 0 ? NJ : 1][4];
-    uint2 h[KJ > 0 ? KJ : 1][NJ][4];
-    if constexpr (KJ == 0) {
+        if constexpr (DW) {
+            const __amdgpu_buffer_rsrc_t rx =
+                make_rsrc(x + tok0 * d, static_cast<long long>(ntok) * d * 2);
 #pragma unroll
-        for (int j = 0; j < NJ; ++j)
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int col = c0 + 32 * j + 8 * q + 4 * kh;  // d is a multiple of 8
-                dxin[j][q] = (dx_wave && tok_ok && col < d)
-                                 ? *reinterpret_cast<const float4*>(dx + trow + col)
-                                 : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+            for (int u = 0; u < XV; ++u) {
+                const int q = u * NTT + tt, r = q / (COLS / 8), col = c0 + (q % (COLS / 8)) * 8;
+                const uint32_t off =
+                    col < d ? static_cast<uint32_t>(r * d + col) * 2u : kOutOfRange;
+                xv[u] = buf_load16(rx, off);
             }
-    } else if (dx_wave) {
+        }
+    };
+    // stage 2: into LDS
+    auto stage_tiles = [&]() {
 #pragma unroll
-        for (int jj = 0; jj < KJ; ++jj)
+        for (int u = 0; u < DZV; ++u) {
+            const int q = u * NTT + tt;
+            dzs[(q / EMAX) * DZLD + q % EMAX] = dzv[u];
+        }
+        if constexpr (DW) {
+#pragma unroll
+            for (int u = 0; u < XV; ++u) {
+                const int q = u * NTT + tt, r = q / (COLS / 8), v = q % (COLS / 8);
+                *reinterpret_cast<uint4*>(xs + r * kRbXLd + v * 8) = xv[u];
+            }
+        }
+    };
+    const bool any_chunk = static_cast<int>(blockIdx.x) < nch;  // uniform per block
+
+    if (dx_wave) {
+        // the dx rows of the lane: token tl of the chunk; register 4 q + r of
+        // lane l holds token 32 w + l % 32, column 32 j + 8 q + 4 (l / 32) + r
+        const int tl = 32 * rw + m;
+        int rn[KJ > 0 ? KJ : 1];
+        bool keep[KJ > 0 ? KJ : 1];
+        float4 dxin[KJ == 0 ? NJ : 1][4];
+        uint2 h[KJ > 0 ? KJ : 1][NJ][4];
+        // (fused) the expert-buffer rows of the token's assignments, -1 dropped
+        auto load_rows = [&](int c) {
+            if constexpr (KJ > 0) {
+                const int t0 = c * TCH;
+                const int ntok = min(TCH, Ng - t0);
+                const size_t tok0 = static_cast<size_t>(g) * Ng + t0;
+#pragma unroll
+                for (int jj = 0; jj < KJ; ++jj) {
+                    const int v = rows[(tok0 + min(tl, ntok - 1)) * k + min(jj, k - 1)];
+                    rn[jj] = jj < k ? v : -1;
+                }
+            }
+        };
+        // the incoming value of each dx element of chunk c: dx itself, or
+        // (fused) the kept dxe rows of the row indices in rn; a dropped
+        // assignment reads the first row of the expert buffers (of x when
+        // they are empty) and its value is discarded
+        auto load_in = [&](int c) {
+            if constexpr (KJ == 0) {
+                const int t0 = c * TCH;
+                const int ntok = min(TCH, Ng - t0);
+                const __amdgpu_buffer_rsrc_t rdx =
+                    make_rsrc(dx + (static_cast<size_t>(g) * Ng + t0) * d,
+                              static_cast<long long>(ntok) * d * 4);
+#pragma unroll
+                for (int j = 0; j < NJ; ++j)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const int col = c0 + 32 * j + 8 * q + 4 * kh;
+                        const uint32_t off =
+                            col < d ? static_cast<uint32_t>(tl * d + col) * 4u : kOutOfRange;
+                        const v4i32 v = __builtin_amdgcn_raw_buffer_load_b128(rdx, off, 0, 0);
+                        dxin[j][q] = __builtin_bit_cast(float4, v);
+                    }
+            } else {
+#pragma unroll
+                for (int jj = 0; jj < KJ; ++jj) {
+                    keep[jj] = rn[jj] >= 0;
+                    const uint16_t* src = keep[jj] ? dxe + static_cast<size_t>(rn[jj]) * d
+                                                   : (has_rows ? dxe : x);
+#pragma unroll
+                    for (int j = 0; j < NJ; ++j)
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            const int col = min(c0 + 32 * j + 8 * q + 4 * kh, d - 4);
+                            h[jj][j][q] = *reinterpret_cast<const uint2*>(src + col);
+                        }
+                }
+            }
+        };
+        f32x16_r acc[NJ];
+        if (any_chunk) {
+            load_rows(blockIdx.x);
+            load_in(blockIdx.x);
+        }
+        for (int c = blockIdx.x; c < nch; c += gridDim.x) {
+            const int cn = min(c + static_cast<int>(gridDim.x), nch - 1);
+            // the tiles of chunk c are staged; LDS only: the dx inputs stay in flight
+            lds_barrier();
+            load_rows(cn);
+#pragma unroll
+            for (int j = 0; j < NJ; ++j)
+#pragma unroll
+                for (int i = 0; i < 16; ++i) acc[j][i] = 0.0f;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                // A: dz[token m][e = 16 ks + 8 kh .. +7] as three bf16 terms
+                float a8[8];
+#pragma unroll
+                for (int i = 0; i < 8; ++i) a8[i] = dzs[tl * DZLD + 16 * ks + 8 * kh + i];
+                bf16x8_r ahi, amid, alo;
+                split3(a8, ahi, amid, alo);
+#pragma unroll
+                for (int j = 0; j < NJ; ++j) {
+                    // B: W[e][column 32 j + m], from the transposed tile
+                    const bf16x8_r b = *reinterpret_cast<const bf16x8_r*>(
+                        wts + (32 * j + m) * WLD + 16 * ks + 8 * kh);
+                    acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, alo, acc[j], 0, 0, 0);
+                    acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, amid, acc[j], 0, 0, 0);
+                    acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, ahi, acc[j], 0, 0, 0);
+                }
+            }
+            // dx rows of the chunk: rows past the chunk and columns past d are
+            // out of the store buffer's range
+            const int t0 = c * TCH;
+            const int ntok = min(TCH, Ng - t0);
+            const __amdgpu_buffer_rsrc_t rdx =
+                make_rsrc(dx + (static_cast<size_t>(g) * Ng + t0) * d,
+                          static_cast<long long>(ntok) * d * 4);
 #pragma unroll
             for (int j = 0; j < NJ; ++j)
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
-                    const int col = min(c0 + 32 * j + 8 * q + 4 * kh, d - 4);
-                    if (rr[jj] >= 0)
-                        h[jj][j][q] = *reinterpret_cast<const uint2*>(
-                            dxe + static_cast<size_t>(rr[jj]) * d + col);
-                }
-    }
-    // stage 2: into LDS
+                    float4 din;
+                    if constexpr (KJ == 0) {
+                        din = dxin[j][q];
+                    } else {
+                        float v[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-    for (int u = 0; u < DZV; ++u) {
-        const int q = u * NT + tid;
-        dzs[(q / EMAX) * DZLD + q % EMAX] = dzv[u];
-    }
-    if constexpr (DW) {
-#pragma unroll
-        for (int u = 0; u < XV; ++u) {
-            const int q = u * NT + tid, r = q / (COLS / 8), v = q % (COLS / 8);
-            *reinterpret_cast<uint4*>(xs + r * kRbXLd + v * 8) = xv[u];
-        }
-    }
-    // LDS only: the dx inputs stay in flight
-    lds_barrier();
-
-    if (dx_wave) {
-#pragma unroll
-    for (int j = 0; j < NJ; ++j)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) acc[j][i] = 0.0f;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-        // A: dz[token m][e = 16 ks + 8 kh .. +7] as three bf16 terms
-        float a8[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) a8[i] = dzs[tl * DZLD + 16 * ks + 8 * kh + i];
-        bf16x8_r ahi, amid, alo;
-        split3(a8, ahi, amid, alo);
-#pragma unroll
-        for (int j = 0; j < NJ; ++j) {
-            // B: W[e][column 32 j + m], from the transposed tile
-            const bf16x8_r b = *reinterpret_cast<const bf16x8_r*>(
-                wts + (32 * j + m) * WLD + 16 * ks + 8 * kh);
-            acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, alo, acc[j], 0, 0, 0);
-            acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, amid, acc[j], 0, 0, 0);
-            acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b, ahi, acc[j], 0, 0, 0);
-        }
-    }
-    if (tok_ok) {
-#pragma unroll
-        for (int j = 0; j < NJ; ++j)
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                float4 din;
-                if constexpr (KJ == 0) {
-                    din = dxin[j][q];
-                } else {
-                    float v[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-                    for (int jj = 0; jj < KJ; ++jj) {
-                        if (rr[jj] < 0) continue;
-                        v[0] += bf16_to_f32(static_cast<uint16_t>(h[jj][j][q].x & 0xFFFFu));
-                        v[1] += bf16_to_f32(static_cast<uint16_t>(h[jj][j][q].x >> 16));
-                        v[2] += bf16_to_f32(static_cast<uint16_t>(h[jj][j][q].y & 0xFFFFu));
-                        v[3] += bf16_to_f32(static_cast<uint16_t>(h[jj][j][q].y >> 16));
+                        for (int jj = 0; jj < KJ; ++jj) {
+                            // a dropped assignment adds nothing (not even a signed zero)
+                            const uint2 hv = h[jj][j][q];
+                            const float h0 = bf16_to_f32(static_cast<uint16_t>(hv.x & 0xFFFFu));
+                            const float h1 = bf16_to_f32(static_cast<uint16_t>(hv.x >> 16));
+                            const float h2 = bf16_to_f32(static_cast<uint16_t>(hv.y & 0xFFFFu));
+                            const float h3 = bf16_to_f32(static_cast<uint16_t>(hv.y >> 16));
+                            v[0] = keep[jj] ? v[0] + h0 : v[0];
+                            v[1] = keep[jj] ? v[1] + h1 : v[1];
+                            v[2] = keep[jj] ? v[2] + h2 : v[2];
+                            v[3] = keep[jj] ? v[3] + h3 : v[3];
+                        }
+                        din = make_float4(v[0], v[1], v[2], v[3]);
                     }
-                    din = make_float4(v[0], v[1], v[2], v[3]);
-                }
-                const int col = c0 + 32 * j + 8 * q + 4 * kh;
-                if (col < d)
-                    *reinterpret_cast<float4*>(dx + trow + col) =
+                    const int col = c0 + 32 * j + 8 * q + 4 * kh;
+                    const uint32_t off =
+                        col < d ? static_cast<uint32_t>(tl * d + col) * 4u : kOutOfRange;
+                    const float4 o =
                         make_float4(din.x + acc[j][4 * q], din.y + acc[j][4 * q + 1],
                                     din.z + acc[j][4 * q + 2], din.w + acc[j][4 * q + 3]);
-            }
-    }
+                    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4i32, o), rdx, off,
+                                                           0, 0);
+                }
+            // the next chunk's incoming values, now that this chunk's are used
+            load_in(cn);
+            // every wave is done with this chunk's tiles before the next overwrites them
+            lds_barrier();
+        }
+        return;
     }
 
-    if (DW && !dx_wave) {
-        // 4. P[e][column] += over the chunk's tokens, columns [32 w, 32 w + 32):
-        // A = dz^T (expert m, tokens 16 s + 8 kh .. +7, three terms),
-        // B = x (column m, the same tokens), read transposed from the x tile
-        const int gq = lane >> 4, jq = lane & 15;
-        const int ntk = (ntok + 15) / 16;  // rows past the chunk are zero in both tiles
-        for (int s = 0; s < ntk; ++s) {
-            const int kt = 16 * s + 8 * (gq >> 1) + (jq >> 2);
-            const int mn = 32 * rw + 16 * (gq & 1) + 4 * (jq & 3);
-            const s16x4_r lo4 = rb_read_tr(xs + kt * kRbXLd + mn);
-            const s16x4_r hi4 = rb_read_tr(xs + (kt + 4) * kRbXLd + mn);
-            const bf16x8_r bx = __builtin_bit_cast(
-                bf16x8_r, __builtin_shufflevector(lo4, hi4, 0, 1, 2, 3, 4, 5, 6, 7));
+    // router-gradient waves: P[e][column] += over the chunk's tokens, columns
+    // [32 w, 32 w + 32): A = dz^T (expert m, tokens 16 s + 8 kh .. +7, three
+    // terms), B = x (column m, the same tokens), read transposed from the x tile
+    f32x16_r acc[MB];
 #pragma unroll
-            for (int b = 0; b < MB; ++b) {
-                float a8[8];
+    for (int b = 0; b < MB; ++b)
 #pragma unroll
-                for (int i = 0; i < 8; ++i) a8[i] = dzs[(16 * s + 8 * kh + i) * DZLD + 32 * b + m];
-                bf16x8_r ahi, amid, alo;
-                split3(a8, ahi, amid, alo);
-                acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bx, alo, acc[b], 0, 0, 0);
-                acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bx, amid, acc[b], 0, 0, 0);
-                acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bx, ahi, acc[b], 0, 0, 0);
+        for (int i = 0; i < 16; ++i) acc[b][i] = 0.0f;
+    if (any_chunk) load_tiles(blockIdx.x);
+    for (int c = blockIdx.x; c < nch; c += gridDim.x) {
+        const int cn = min(c + static_cast<int>(gridDim.x), nch - 1);
+        stage_tiles();
+        lds_barrier();
+        load_tiles(cn);
+        if constexpr (DW) {
+            const int ntok = min(TCH, Ng - c * TCH);
+            const int gq = lane >> 4, jq = lane & 15;
+            const int ntk = (ntok + 15) / 16;  // rows past the chunk are zero in both tiles
+            for (int s = 0; s < ntk; ++s) {
+                const int kt = 16 * s + 8 * (gq >> 1) + (jq >> 2);
+                const int mn = 32 * rw + 16 * (gq & 1) + 4 * (jq & 3);
+                const s16x4_r lo4 = rb_read_tr(xs + kt * kRbXLd + mn);
+                const s16x4_r hi4 = rb_read_tr(xs + (kt + 4) * kRbXLd + mn);
+                const bf16x8_r bx = __builtin_bit_cast(
+                    bf16x8_r, __builtin_shufflevector(lo4, hi4, 0, 1, 2, 3, 4, 5, 6, 7));
+#pragma unroll
+                for (int b = 0; b < MB; ++b) {
+                    float a8[8];
+#pragma unroll
+                    for (int i = 0; i < 8; ++i)
+                        a8[i] = dzs[(16 * s + 8 * kh + i) * DZLD + 32 * b + m];
+                    bf16x8_r ahi, amid, alo;
+                    split3(a8, ahi, amid, alo);
+                    acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bx, alo, acc[b], 0, 0, 0);
+                    acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bx, amid, acc[b], 0, 0, 0);
+                    acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bx, ahi, acc[b], 0, 0, 0);
+                }
             }
         }
-    }
-    // every wave is done with this chunk's tiles before the next overwrites them
-    lds_barrier();
+        // every wave is done with this chunk's tiles before the next overwrites them
+        lds_barrier();
     }
 
-    if (DW && !dx_wave) {
+    if constexpr (DW) {
         // register 4 q + r of lane l: expert 32 b + l % 32, column
         // 32 w + 8 q + 4 (l / 32) + r
         float* pg = partial + (static_cast<size_t>(g) * gridDim.x + blockIdx.x) * E * d;
@@ -932,7 +1007,7 @@ void launch_main(const Dims& D, const ChunkPlan& P, const BwdArgs& a, hipStream_
             kern<<<grid, 512, 0, st>>>(static_cast<const uint16_t*>(a.x),
                                        static_cast<const uint16_t*>(a.wr), a.dz, a.rows,
                                        static_cast<const uint16_t*>(a.dxe), a.dx, a.partial,
-                                       D.Ng, D.d, D.E, D.k, P.nch);
+                                       D.Ng, D.d, D.E, D.k, P.nch, gc > 0 ? 1 : 0);
         };
         if (a.partial) go(route_bwd_mma_kernel<EMAX, true, KJ>);
         else go(route_bwd_mma_kernel<EMAX, false, KJ>);

@@ -467,14 +467,16 @@ typedef short s16x8_r __attribute__((ext_vector_type(8)));
 // summed over the kept experts in ascending e with fused multiply-adds (the
 // order the fused kernel of fewer experts uses). With rows != null also the
 // expert-buffer row of each kept assignment, rows [N, k] (-1 = dropped).
-template <int EL>
+// KB: assignments read per pass (2, 4 or 8: the least that holds k when k
+// <= 8, so a top-2 layer issues 6 loads per lane for them rather than 24).
+template <int EL, int KB>
 __global__ __launch_bounds__(256) void rbwd_dz_kernel(
     const float* __restrict__ probs, const int32_t* __restrict__ idx,
     const int32_t* __restrict__ slot, const float* __restrict__ dgate,
     const float* __restrict__ dz_add, const int32_t* __restrict__ row_base,
     float* __restrict__ dz, int32_t* __restrict__ rows, long long gc, int N, int Ng, int E,
     int k) {
-    constexpr int TPB = 256 / EL, KB = 8;
+    constexpr int TPB = 256 / EL;
     const int sub = threadIdx.x % EL;
     const int t = blockIdx.x * TPB + static_cast<int>(threadIdx.x) / EL;
     if (t >= N) return;  // uniform per group of EL lanes (EL divides 64)
@@ -999,9 +1001,14 @@ void launch_main(const Dims& D, const ChunkPlan& P, const BwdArgs& a, hipStream_
     if constexpr (std::is_same<T, uint16_t>::value && EMAX >= 32) {
         const long long gc = static_cast<long long>(D.G) * D.C;
         constexpr int TPB = 256 / EMAX;
-        rbwd_dz_kernel<EMAX><<<cdiv(D.N, TPB), 256, 0, st>>>(
-            a.probs, a.idx, a.slot, a.dgate, a.dz_add, a.row_base, a.dz,
-            KJ > 0 ? a.rows : nullptr, gc, D.N, D.Ng, D.E, D.k);
+        auto dz_pass = [&](auto kern) {
+            kern<<<cdiv(D.N, TPB), 256, 0, st>>>(a.probs, a.idx, a.slot, a.dgate, a.dz_add,
+                                                 a.row_base, a.dz, KJ > 0 ? a.rows : nullptr, gc,
+                                                 D.N, D.Ng, D.E, D.k);
+        };
+        if (D.k <= 2) dz_pass(rbwd_dz_kernel<EMAX, 2>);
+        else if (D.k <= 4) dz_pass(rbwd_dz_kernel<EMAX, 4>);
+        else dz_pass(rbwd_dz_kernel<EMAX, 8>);
         const dim3 grid(P.nblk, cdiv(D.d, kRbCols), D.G);
         auto go = [&](auto kern) {
             kern<<<grid, 512, 0, st>>>(static_cast<const uint16_t*>(a.x),

@@ -25,10 +25,16 @@
  *
  * Conventions shared by every entry point
  * - All tensor pointers are DEVICE pointers owned by the caller, row-major and
- *   contiguous, 16-byte aligned. The library allocates nothing, keeps no
- *   state, never synchronises and never reads device data on the host.
+ *   contiguous, 16-byte aligned. The library allocates no device memory,
+ *   never synchronises and never reads device data on the host. Its only
+ *   state is per GPU: the static scratch of vmoe_route_noalloc, and a side
+ *   stream with two events that the bf16 expert-MLP backward creates on its
+ *   first call (kept until the process ends).
  * - `stream` is a hipStream_t passed as void* (NULL = the null stream). Work
- *   is enqueued asynchronously on it, in call order.
+ *   is enqueued asynchronously on it, in call order (a call that also uses
+ *   the side stream forks it from `stream` and joins it back before
+ *   returning, so its work still starts after, and completes before, the
+ *   neighbouring work on `stream`).
  * - Activations and weights use shape.dtype (VMOE_F32 or VMOE_BF16; bf16 is
  *   stored as raw 16-bit patterns). Gating tensors (logits, probs, gate,
  *   dgate, noise, bias) and all weight / router / input gradients are f32.
@@ -208,7 +214,10 @@ vmoe_status vmoe_combine_bwd(const vmoe_shape* shape, const void* dy, const void
  *   dW2 = dye^T act, db2 = sum_rows dye  dw2 [E, d, f], db2 [E, d]  f32 out
  *   dW1 = dH^T xe,  db1 = sum_rows dH    dw1 [E, f, d], db1 [E, f]  f32 out
  * act and act_grad are the forward's saved tensors. Experts with n_e = 0 get
- * zero weight gradients. */
+ * zero weight gradients. With 16 or more bf16 experts, dxe runs on the
+ * library's side stream beside the weight gradients (forked after dH and
+ * joined before the call returns); concurrent calls on one GPU from several
+ * host threads serialise their dxe launches on that stream. */
 vmoe_status vmoe_expert_ffn_bwd(const vmoe_shape* shape, const void* xe, const int32_t* counts,
                                 const void* w1, const void* w2, const void* act,
                                 const void* act_grad, const void* dye, void* dh, void* dxe,

@@ -29,6 +29,7 @@
 // f32 path: 64 x 64 tiles on the f32 matrix cores (v_mfma_f32_32x32x2f32, one
 // 32 x 32 block per wave) with coalesced operand staging through LDS and the
 // same operand and epilogue description (the accuracy path).
+#include <mutex>
 #include <type_traits>
 
 #include "common.h"
@@ -1741,6 +1742,44 @@ GemmArgs base_args(const Dims& D, const int32_t* counts) {
 
 size_t esize(const Dims& D) { return D.dtype == VMOE_BF16 ? 2 : 4; }
 
+// A second stream per GPU (default priority, non-blocking) and two events,
+// made on first use, for launches that may run beside the caller's stream:
+// the caller's stream records `fork`, the side stream waits for it, takes
+// its launches and records `join`, which the caller's stream waits for, so
+// the call still completes in its stream's order (and a captured stream
+// captures the side stream's work as a branch of its graph).
+struct SideStream {
+    hipStream_t s = nullptr;
+    hipEvent_t fork = nullptr, join = nullptr;
+};
+constexpr int kMaxSideDevices = 64;
+std::mutex side_mu;
+SideStream side_tab[kMaxSideDevices];
+// held by a call from its fork to its join, so calls from several host
+// threads never interleave their event records and waits
+std::mutex side_seq_mu;
+
+// The current GPU's side stream, or null fields on a HIP error (the caller
+// then runs everything on its own stream).
+SideStream side_stream() {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxSideDevices) return {};
+    std::lock_guard<std::mutex> lock(side_mu);
+    SideStream& t = side_tab[dev];
+    if (t.s == nullptr) {
+        SideStream n;
+        if (hipStreamCreateWithFlags(&n.s, hipStreamNonBlocking) != hipSuccess) return {};
+        if (hipEventCreateWithFlags(&n.fork, hipEventDisableTiming) != hipSuccess ||
+            hipEventCreateWithFlags(&n.join, hipEventDisableTiming) != hipSuccess) {
+            if (n.fork) (void)hipEventDestroy(n.fork);
+            (void)hipStreamDestroy(n.s);
+            return {};
+        }
+        t = n;
+    }
+    return t;
+}
+
 // One wave: the device fill-clamp-refill of n experts (the routine the
 // quota-scheduled GEMMs run), for comparison with the host routine.
 __global__ __launch_bounds__(64) void fcr_kernel(int n, const int32_t* __restrict__ mn,
@@ -1812,6 +1851,8 @@ vmoe_status ffn_bwd_launch(const Dims& D, const void* xe, const int32_t* counts,
                            int sched, const int32_t* row_token, hipStream_t st) {
     const long long rows = D.rows_per_expert();
     if (D.E == 0) return VMOE_OK;
+    SideStream side;  // set when dxe runs beside the weight gradients
+    std::unique_lock<std::mutex> seq;
     if (rows > 0) {
         // dH = (dye W2) * A': W2 [d, f] read with k = d strided (mn-major)
         GemmArgs g = base_args(D, counts);
@@ -1835,7 +1876,22 @@ vmoe_status ffn_bwd_launch(const Dims& D, const void* xe, const int32_t* counts,
         x.out = dxe;
         x.out_estride = rows * D.d;
         x.ldo = D.d;
-        launch_gemm<true, false, EPI_STORE>(D, x, static_cast<int>(rows), sched, st);
+        // dxe and the weight gradients both read only dH and the layer's saved
+        // tensors: dxe runs on the side stream beside them, so the weight-
+        // gradient blocks take the CUs that its partly filled tiles and last
+        // round leave idle (bf16, one-tile-per-block schedule, 16 or more
+        // experts: measured 0.90 -> 0.81 ms on the 17-task pool, 1.18 -> 1.14
+        // at E = 32; with 8 evenly loaded experts every tile is full and the
+        // two launches only contend, 0.33 -> 0.34 ms at ViT-B/16)
+        if (D.dtype == VMOE_BF16 && sched == 0 && D.E >= 16) {
+            seq = std::unique_lock<std::mutex>(side_seq_mu);
+            side = side_stream();
+            if (side.s != nullptr && (hipEventRecord(side.fork, st) != hipSuccess ||
+                                      hipStreamWaitEvent(side.s, side.fork, 0) != hipSuccess))
+                side = SideStream{};
+        }
+        launch_gemm<true, false, EPI_STORE>(D, x, static_cast<int>(rows), sched,
+                                            side.s != nullptr ? side.s : st);
     }
     // dW2 [d, f] = dye^T A, reduced over the n_e rows (k = row, strided)
     GemmArgs w = base_args(D, counts);
@@ -1897,6 +1953,14 @@ vmoe_status ffn_bwd_launch(const Dims& D, const void* xe, const int32_t* counts,
     } else {
         launch_gemm<false, false, EPI_F32>(D, w, D.d, 0, st);
         launch_gemm<false, false, EPI_F32>(D, v, D.f, 0, st);
+    }
+    if (side.s != nullptr) {
+        // the call ends in its stream's order: after the side stream's dxe
+        const vmoe_status ls = launch_status();
+        if (hipEventRecord(side.join, side.s) != hipSuccess ||
+            hipStreamWaitEvent(st, side.join, 0) != hipSuccess)
+            return VMOE_ERR_HIP;
+        if (ls != VMOE_OK) return ls;
     }
     // bias gradients (the bf16 path sums them inside the dW GEMMs)
     if (D.dtype == VMOE_F32) {

@@ -40,10 +40,15 @@ def _bits(t):
     return t.clone()
 
 
+# (20 experts: the expert-MLP backward forks its dxe onto the library's side
+# stream and joins it back, which the capture must record as a branch)
+_E20 = W.custom_config("bf16_e20_graph", n_tokens=400, d_model=96, d_ff=160, n_experts=20, k=2,
+                       capacity_factor=1.0, n_groups=2, router_std=0.3)
 CASES = [("vitb16_bf16", False), ("vitb16_bf16", True), ("tiny_fp32", False),
          (W.custom_config("bf16_ragged_graph", n_tokens=300, d_model=72, d_ff=200, n_experts=5,
                           k=2, capacity_factor=0.8, n_groups=3, router_std=0.2,
-                          noise_var=0.1), False)]
+                          noise_var=0.1), False),
+         (_E20, False), (_E20, True)]
 
 
 @pytest.mark.parametrize("case,gather", CASES,

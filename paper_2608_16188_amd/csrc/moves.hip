@@ -86,6 +86,53 @@ __device__ __forceinline__ bool keeps_any(const RouteMeta& m, int t) {
     return any;
 }
 
+// The slots and experts of assignments j0 .. j0 + J - 1 of token t, clamped
+// to k - 1 (all requested at once, no branch), and whether any of them with
+// j < k is kept.
+template <int J>
+struct Assign {
+    int s[J], e[J];
+    __device__ __forceinline__ void fetch(const RouteMeta& m, int t, int j0) {
+        const size_t a0 = static_cast<size_t>(t) * m.k;
+#pragma unroll
+        for (int jj = 0; jj < J; ++jj) {
+            const int j = min(j0 + jj, m.k - 1);
+            s[jj] = m.slot[a0 + j];
+            e[jj] = m.idx[a0 + j];  // a valid expert for every assignment
+        }
+    }
+    __device__ __forceinline__ bool any_kept(const RouteMeta& m, int j0) const {
+        bool any = false;
+#pragma unroll
+        for (int jj = 0; jj < J; ++jj) any = any || (j0 + jj < m.k && s[jj] >= 0);
+        return any;
+    }
+    // the row bases of the experts in t's group (requested, not yet used)
+    __device__ __forceinline__ void row_bases(const RouteMeta& m, int t, int (&rb)[J]) const {
+        const int g = t / m.Ng;
+#pragma unroll
+        for (int jj = 0; jj < J; ++jj) rb[jj] = m.row_base[g * m.E + e[jj]];
+    }
+    // expert-buffer rows (-1: dropped or past k)
+    __device__ __forceinline__ void rows(const RouteMeta& m, int j0, const int (&rb)[J],
+                                         long long (&r)[J]) const {
+#pragma unroll
+        for (int jj = 0; jj < J; ++jj)
+            r[jj] = (j0 + jj < m.k && s[jj] >= 0)
+                        ? static_cast<long long>(e[jj]) * m.G * m.C + rb[jj] + s[jj]
+                        : -1;
+    }
+};
+
+// Marks values as used here, so the loads that produce them stay where they
+// were issued (all of a round together) instead of moving into the branches
+// that consume them, where each would wait for its own round trip.
+template <int J>
+__device__ __forceinline__ void keep_issued(int (&v)[J]) {
+#pragma unroll
+    for (int i = 0; i < J; ++i) asm volatile("" : "+v"(v[i]));
+}
+
 // Flat element-wise mapping for the row moves without a reduction: item i is
 // 16-byte vector v = i mod nvec of token t = i / nvec, so consecutive lanes
 // touch consecutive bytes of a row and every lane is busy whatever d is. Each
@@ -95,35 +142,59 @@ constexpr int kBlock = 256;
 constexpr int kItems = 2;
 // J: assignments per pass (2 when k <= 2, else 4; larger k loops)
 
+// Three rounds of straight-line loads: the slots and experts of both items'
+// tokens; then their x rows (buffer loads whose offset is out of range for a
+// token that keeps nothing, which read no memory) beside the row bases; then
+// the stores. A thread neither of whose tokens keeps anything stops after the
+// first round.
 template <typename T, int kJ>
 __global__ __launch_bounds__(kBlock) void dispatch_kernel(const T* __restrict__ x,
                                                           T* __restrict__ xe, RouteMeta m,
                                                           int nvec) {
     const long long total = static_cast<long long>(m.N) * nvec;
-    const long long i0 = static_cast<long long>(blockIdx.x) * kBlock * kItems + threadIdx.x;
-    const uint4* src = reinterpret_cast<const uint4*>(x);
+    const long long b0 = static_cast<long long>(blockIdx.x) * kBlock * kItems;
+    const long long i0 = b0 + threadIdx.x;
     uint4* dst = reinterpret_cast<uint4*>(xe);
     static_assert(kItems == 2, "two items per thread");
     const long long ia = min(i0, total - 1), ib = min(i0 + kBlock, total - 1);
     const int ta = static_cast<int>(ia / nvec), tb = static_cast<int>(ib / nvec);
     const int ca = static_cast<int>(ia - static_cast<long long>(ta) * nvec);
     const int cb = static_cast<int>(ib - static_cast<long long>(tb) * nvec);
-    // the row of x is read only when some assignment of its token is kept
-    uint4 va = make_uint4(0u, 0u, 0u, 0u), vb = va;
-    const bool ka = keeps_any(m, ta), kb = keeps_any(m, tb);
-    if (ka) va = src[ia];
-    if (kb) vb = src[ib];
-    // neither token keeps an assignment: no row to write, so no second round
-    // of routing loads (expert, row base) either
+    Assign<kJ> aa, ab;
+    aa.fetch(m, ta, 0);
+    ab.fetch(m, tb, 0);
+    bool ka, kb;
+    if (m.k <= kJ) {
+        ka = aa.any_kept(m, 0);
+        kb = ab.any_kept(m, 0);
+    } else {
+        ka = keeps_any(m, ta);
+        kb = keeps_any(m, tb);
+    }
     if (!ka && !kb) return;
+    // the block's items of x as one buffer (the row of x is read only when
+    // some assignment of its token is kept)
+    const long long nb = min(static_cast<long long>(kBlock) * kItems, total - b0);
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(reinterpret_cast<const uint4*>(x) + b0, nb * 16);
+    const uint4 va = buf_load16(rx, ka ? static_cast<uint32_t>(ia - b0) * 16u : kOutOfRange);
+    const uint4 vb = buf_load16(rx, kb ? static_cast<uint32_t>(ib - b0) * 16u : kOutOfRange);
     for (int j0 = 0; j0 < m.k; j0 += kJ) {
-        Rows<kJ> ra, rb;
-        ra.fetch(m, ta, j0);
-        rb.fetch(m, tb, j0);
+        if (j0 > 0) {
+            aa.fetch(m, ta, j0);
+            ab.fetch(m, tb, j0);
+        }
+        int ba[kJ], bb[kJ];
+        aa.row_bases(m, ta, ba);
+        ab.row_bases(m, tb, bb);
+        keep_issued(ba);
+        keep_issued(bb);
+        long long ra[kJ], rb[kJ];
+        aa.rows(m, j0, ba, ra);
+        ab.rows(m, j0, bb, rb);
 #pragma unroll
         for (int jj = 0; jj < kJ; ++jj) {
-            if (i0 < total && ra.r[jj] >= 0) dst[ra.r[jj] * nvec + ca] = va;
-            if (i0 + kBlock < total && rb.r[jj] >= 0) dst[rb.r[jj] * nvec + cb] = vb;
+            if (i0 < total && ra[jj] >= 0) dst[ra[jj] * nvec + ca] = va;
+            if (i0 + kBlock < total && rb[jj] >= 0) dst[rb[jj] * nvec + cb] = vb;
         }
     }
 }

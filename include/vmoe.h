@@ -50,8 +50,9 @@
  *   multiple of 8, a non-positive capacity factor, an unknown dtype or
  *   misaligned pointer -> VMOE_ERR_INVALID_ARG; a shape beyond the kernels'
  *   32-bit addressing (one expert's [G*C, d or f] operand or [f, d] weight of
- *   2 GiB or more, or 2^31 or more elements in the pooled expert buffers or
- *   the token-major tensors) -> VMOE_ERR_UNSUPPORTED (vmoe_capacity returns
+ *   2 GiB or more, 2^31 or more elements in the pooled expert buffers or
+ *   the token-major tensors, or d >= 2^22, where 128 f32 rows of width d
+ *   reach 2 GiB) -> VMOE_ERR_UNSUPPORTED (vmoe_capacity returns
  *   -1 for it); a too-small workspace -> VMOE_ERR_WORKSPACE; a failed kernel
  *   launch -> VMOE_ERR_HIP. Required
  *   pointers are checked whatever the sizes: with N = 0 they still point to

@@ -90,7 +90,9 @@ vmoe_status make_dims(const vmoe_shape* s, Dims* out) {
     //   offsets >= 2^31 (the tail-mask offset), so every per-expert operand
     //   ([G*C, d or f] activations, [f, d] weights) stays below 2^31 bytes;
     // - expert-buffer rows (E*G*C) and element indices into the expert buffers
-    //   and the token-major tensors ([N, d], [N, E]) are 32-bit integers.
+    //   and the token-major tensors ([N, d], [N, E]) are 32-bit integers;
+    // - the router backward addresses a chunk of 128 token rows of dx (f32)
+    //   with 32-bit byte offsets, so d < 2^22.
     const long long lim = 0x7FFFFFFFLL;
     const long long elem = D.dtype == VMOE_BF16 ? 2 : 4;
     const long long rows = static_cast<long long>(D.G) * D.C;
@@ -98,7 +100,8 @@ vmoe_status make_dims(const vmoe_shape* s, Dims* out) {
     const long long er = rows * D.E;
     if (rows * wide * elem > lim || static_cast<long long>(D.f) * D.d * elem > lim ||
         er > lim || er * wide > lim ||
-        static_cast<long long>(D.N) * (wide > D.E ? wide : D.E) > lim)
+        static_cast<long long>(D.N) * (wide > D.E ? wide : D.E) > lim ||
+        128LL * D.d * 4 > lim)
         return VMOE_ERR_UNSUPPORTED;
     *out = D;
     return VMOE_OK;

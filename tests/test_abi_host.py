@@ -187,6 +187,9 @@ def test_workspace_sizes_are_modest_for_workloads():
     dict(n_tokens=100_000, d_model=8, d_ff=4096, n_experts=64, k=8, capacity_factor=1.0),
     # one expert's [f, d] weight passes 2 GiB
     dict(n_tokens=64, d_model=32768, d_ff=32768, n_experts=2, k=1, capacity_factor=1.0),
+    # every per-expert operand fits, but a 128-token f32 chunk of dx (the
+    # router backward's unit) passes 2 GiB: d = 2^22
+    dict(n_tokens=4, d_model=1 << 22, d_ff=8, n_experts=17, k=1, capacity_factor=1.0),
 ])
 def test_shapes_beyond_32bit_addressing_unsupported(kw):
     """Shapes the kernels' 32-bit buffer offsets cannot address are refused

@@ -449,11 +449,13 @@ __global__ __launch_bounds__(256) void route_bwd_kernel(
 // product dz W or dz x is formed as three exact bf16 products summed in f32.
 //
 // dz is formed first, once per token, by its own kernel (rbwd_dz_kernel) into
-// the workspace, so the product kernel starts streaming at once: a block =
-// kRbTok tokens x kRbCols columns of one group, four waves; dz rows (f32), W
-// columns (transposed to [column][expert] bf16) and x rows are staged in LDS,
-// wave w computes dx for tokens [32 w, 32 w + 32) over the block's columns and
-// the partial P for columns [32 w, 32 w + 32) over all experts.
+// the workspace, so the product kernel starts streaming at once: a block takes
+// kRbCols columns of one group and walks chunks of kRbTok tokens, eight waves;
+// W columns (transposed to [column][expert] bf16) are staged in LDS once, the
+// chunk's dz rows (f32) and x rows by waves 4-7 one chunk ahead; dx wave w
+// (0-3) computes dx for tokens [32 w, 32 w + 32) over the block's columns, and
+// wave 4 + w the partial P for columns [32 w, 32 w + 32) over all experts,
+// summed over the block's chunks.
 constexpr int kRbTok = 128, kRbCols = 128;
 constexpr int kRbXLd = kRbCols + 16;  // bf16 per staged x row (rows 32 bytes apart in banks)
 
@@ -608,8 +610,8 @@ __global__ __launch_bounds__(512) void route_bwd_mma_kernel(
     const int c0 = blockIdx.y * COLS;
     const uint16_t* wg = wr + static_cast<size_t>(g) * E * d;
     const int m = lane & 31, kh = lane >> 5;
-    // waves 0-3 form dx, waves 4-7 the router-gradient partial, at the same
-    // time once the tiles are staged
+    // waves 0-3 form dx, waves 4-7 stage the tiles and form the router-
+    // gradient partial
     const bool dx_wave = wave < 4;
     const int rw = wave & 3;
     constexpr int NJ = COLS / 32;

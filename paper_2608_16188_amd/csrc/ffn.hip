@@ -1693,8 +1693,10 @@ using TileSmall = Tile<128, 128, 2, 2, 32, 4, STAGE_DMA>;  // 4 waves, two block
 // TileBig with 64-deep stages in a ring of two: half the stage barriers per
 // k, one stage in flight instead of three. For the f-wide row GEMMs (short
 // k = d, heavy epilogues) measured 1.3-1.5% faster per step at ViT-B/16 and
-// the 17-task pool and even at ViT-L/16; for the weight gradients at the
-// ViT-L/16 skew 5-10 us slower, so those keep TileBig.
+// the 17-task pool and even at ViT-L/16; for the d-wide ones (k = f) the
+// forward 0.743 -> 0.722 ms at wide E = 32 and 0.312 -> 0.307 at ViT-L/16;
+// for the weight gradients at the ViT-L/16 skew 5-10 us slower, so those
+// keep TileBig.
 using TileDeep = Tile<256, 256, 2, 4, 64, 2, STAGE_DMA>;
 
 // Work of a launch in units of one CU's time: rounds of one-block-per-CU
@@ -1706,10 +1708,10 @@ double tile_cost(long long tiles, int bm, int bn, double eff) {
 template <bool AK, bool BK_, int EPI, int GATHER = 0>
 void launch_gemm(const Dims& D, const GemmArgs& a, int grid_m_rows, int sched, hipStream_t st) {
     if (D.dtype == VMOE_BF16) {
-        // 256 x 256 tiles (half the operand bytes per flop of 128 x 128) for
-        // the GEMMs whose m is the expert's rows, the f-wide ones with
-        // 64-deep stages (TileDeep). (bf16 weight gradients run batched in
-        // ffn_bwd_launch; this EPI_F32 case only serves other callers.)
+        // 256 x 256 tiles (half the operand bytes per flop of 128 x 128) with
+        // 64-deep stages (TileDeep) for the GEMMs whose m is the expert's rows.
+        // (bf16 weight gradients run batched in ffn_bwd_launch; this EPI_F32
+        // case only serves other callers.)
         if constexpr (EPI == EPI_F32) {
             launch_bf16<TileSmall, AK, BK_, EPI, GATHER>(D, a, grid_m_rows, sched, st);
         } else if constexpr (EPI == EPI_BIAS || EPI == EPI_STORE) {
@@ -1722,7 +1724,7 @@ void launch_gemm(const Dims& D, const GemmArgs& a, int grid_m_rows, int sched, h
             if (narrow < big)
                 launch_bf16<TileNarrow, AK, BK_, EPI, GATHER>(D, a, grid_m_rows, sched, st);
             else
-                launch_bf16<TileBig, AK, BK_, EPI, GATHER>(D, a, grid_m_rows, sched, st);
+                launch_bf16<TileDeep, AK, BK_, EPI, GATHER>(D, a, grid_m_rows, sched, st);
         } else {
             launch_bf16<TileDeep, AK, BK_, EPI, GATHER>(D, a, grid_m_rows, sched, st);
         }

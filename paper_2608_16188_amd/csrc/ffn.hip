@@ -1695,8 +1695,10 @@ using TileSmall = Tile<128, 128, 2, 2, 32, 4, STAGE_DMA>;  // 4 waves, two block
 // k = d, heavy epilogues) measured 1.3-1.5% faster per step at ViT-B/16 and
 // the 17-task pool and even at ViT-L/16; for the d-wide ones (k = f) the
 // forward 0.743 -> 0.722 ms at wide E = 32 and 0.312 -> 0.307 at ViT-L/16;
-// for the weight gradients at the ViT-L/16 skew 5-10 us slower, so those
-// keep TileBig.
+// for the batched weight gradients the backward 0.629 -> 0.625 ms at
+// ViT-L/16 (no spill, against one with TileBig), the other workloads
+// unchanged. So every 256 x 256 launch takes TileDeep; TileBig (the 32-deep
+// ring of four) is the baseline these measurements and TileNarrow refer to.
 using TileDeep = Tile<256, 256, 2, 4, 64, 2, STAGE_DMA>;
 
 // Work of a launch in units of one CU's time: rounds of one-block-per-CU
@@ -1946,7 +1948,7 @@ vmoe_status ffn_bwd_launch(const Dims& D, const void* xe, const int32_t* counts,
             if (narrow <= small && narrow <= big)
                 launch_bf16<TileNarrow, false, false, EPI_F32, GA>(D, both, rows_m, 2, sched, st);
             else if (big <= small)
-                launch_bf16<TileBig, false, false, EPI_F32, GA>(D, both, rows_m, 2, sched, st);
+                launch_bf16<TileDeep, false, false, EPI_F32, GA>(D, both, rows_m, 2, sched, st);
             else
                 launch_bf16<TileSmall, false, false, EPI_F32, GA>(D, both, rows_m, 2, sched, st);
         };
